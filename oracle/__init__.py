@@ -1,0 +1,196 @@
+"""SegBlocks CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow CPU implementation of the SegBlocks block modules (arXiv
+2011.12025, Method section "Block modules": BlockSample, BlockPad,
+BlockCombine) and of the block convolution that runs the same 3x3 filters on
+the high- and the low-resolution block stacks.  The arithmetic lives in
+``segblocks_oracle.c`` (plain C, built with gcc ``-O2 -ffp-contract=off``);
+this module only marshals numpy arrays.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the GPU path
+(``paper_2011_12025_amd``) and neither imports the other.
+
+All arrays are float32 in logical N,C,H,W order and hold values exactly
+representable in the storage type ``dtype`` ("f32", "f16" or "bf16").
+``mask[n, gy, gx] != 0`` marks a high-resolution block.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "segblocks_oracle.c")
+_LIB = os.path.join(_HERE, "_liboracle.so")
+_DT = {"f32": 0, "f16": 1, "bf16": 2}
+
+_fp = ctypes.POINTER(ctypes.c_float)
+_dp = ctypes.POINTER(ctypes.c_double)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle's C source into ``_liboracle.so`` (gcc, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math",
+                               "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        lib.orc_round.restype = ctypes.c_double
+        lib.orc_round.argtypes = [ctypes.c_double, ctypes.c_int]
+        lib.orc_round_array.argtypes = [_dp, _fp, ctypes.c_long, ctypes.c_int]
+        lib.orc_avg4.restype = ctypes.c_float
+        lib.orc_avg4.argtypes = [ctypes.c_float] * 4 + [ctypes.c_int]
+        lib.orc_plan.argtypes = [_u8p, ctypes.c_long, _i32p, _i32p, _i32p, _i32p]
+        lib.orc_split.argtypes = [_fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp, _fp]
+        lib.orc_pad.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp, _fp]
+        lib.orc_conv3x3_valid.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, _fp, _fp,
+                                          ctypes.c_int, _dp]
+        lib.orc_combine.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, _fp]
+        _lib = lib
+    return _lib
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _ptr(a, t):
+    return a.ctypes.data_as(t)
+
+
+def _check_shape(mask, N, H, W, bs):
+    if bs < 2 or bs % 2 or H % bs or W % bs:
+        raise ValueError("block size must be even and divide H and W")
+    if mask.shape != (N, H // bs, W // bs):
+        raise ValueError("mask must have shape [N, H/bs, W/bs]")
+
+
+# --------------------------------------------------------------------------
+# rounding and the 2x2 average
+# --------------------------------------------------------------------------
+
+def round_to(a, dtype: str) -> np.ndarray:
+    """Round float64 values to the storage type (round-to-nearest-even), as float32."""
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    out = np.empty(a.shape, np.float32)
+    _L().orc_round_array(_ptr(a, _dp), _ptr(out, _fp), a.size, _DT[dtype])
+    return out
+
+
+def round_scalar(v: float, dtype: str) -> float:
+    return _L().orc_round(float(v), _DT[dtype])
+
+
+def avg4(a: float, b: float, c: float, d: float, dtype: str) -> float:
+    return _L().orc_avg4(a, b, c, d, _DT[dtype])
+
+
+# --------------------------------------------------------------------------
+# the block modules
+# --------------------------------------------------------------------------
+
+def plan(mask):
+    """Slot of each block within its class, plus the inverse tables and counts."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8).reshape(-1)
+    B = m.size
+    slot = np.empty(max(B, 1), np.int32)
+    inv_hi = np.empty(max(B, 1), np.int32)
+    inv_lo = np.empty(max(B, 1), np.int32)
+    counts = np.zeros(2, np.int32)
+    _L().orc_plan(_ptr(m, _u8p), B, _ptr(slot, _i32p), _ptr(inv_hi, _i32p), _ptr(inv_lo, _i32p),
+                  _ptr(counts, _i32p))
+    nh, nl = int(counts[0]), int(counts[1])
+    return slot[:B], inv_hi[:nh], inv_lo[:nl], nh, nl
+
+
+def split(x, mask, bs: int, dtype: str):
+    """BlockSample: x[N,C,H,W] -> (hi[nh,C,bs,bs], lo[nl,C,bs/2,bs/2])."""
+    x = _f32(x)
+    N, C, H, W = x.shape
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    _check_shape(mask, N, H, W, bs)
+    _, _, _, nh, nl = plan(mask)
+    hi = np.zeros((nh, C, bs, bs), np.float32)
+    lo = np.zeros((nl, C, bs // 2, bs // 2), np.float32)
+    _L().orc_split(_ptr(x, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
+                   _ptr(hi, _fp), _ptr(lo, _fp))
+    return hi, lo
+
+
+def pad(hi, lo, mask, bs: int, H: int, W: int, dtype: str):
+    """BlockPad: (hi, lo) -> (hi_pad[nh,C,bs+2,bs+2], lo_pad[nl,C,bs/2+2,bs/2+2])."""
+    hi, lo = _f32(hi), _f32(lo)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    N = mask.shape[0]
+    _check_shape(mask, N, H, W, bs)
+    C = hi.shape[1] if hi.shape[0] else lo.shape[1]
+    nh, nl = hi.shape[0], lo.shape[0]
+    hp = np.zeros((nh, C, bs + 2, bs + 2), np.float32)
+    lp = np.zeros((nl, C, bs // 2 + 2, bs // 2 + 2), np.float32)
+    _L().orc_pad(_ptr(hi, _fp), _ptr(lo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
+                 _ptr(hp, _fp), _ptr(lp, _fp))
+    return hp, lp
+
+
+def conv3x3_valid(P, w, b=None):
+    """3x3 valid convolution of a stack of padded blocks, fp64 result (unrounded)."""
+    P, w = _f32(P), _f32(w)
+    S, Cin, pe, pe2 = P.shape
+    assert pe == pe2 and pe >= 3
+    Cout = w.shape[0]
+    assert w.shape == (Cout, Cin, 3, 3)
+    E = pe - 2
+    out = np.zeros((S, Cout, E, E), np.float64)
+    bp = None
+    if b is not None:
+        b = _f32(b)
+        assert b.shape == (Cout,)
+        bp = _ptr(b, _fp)
+    if S:
+        _L().orc_conv3x3_valid(_ptr(P, _fp), S, Cin, E, _ptr(w, _fp), bp, Cout, _ptr(out, _dp))
+    return out
+
+
+def conv3x3(hp, lp, w, b, dtype: str):
+    """Block convolution of both padded stacks, rounded to the storage type."""
+    return (round_to(conv3x3_valid(hp, w, b), dtype),
+            round_to(conv3x3_valid(lp, w, b), dtype))
+
+
+def combine(hi, lo, mask, bs: int, H: int, W: int):
+    """BlockCombine: (hi, lo) -> y[N,C,H,W], low blocks nearest-upsampled."""
+    hi, lo = _f32(hi), _f32(lo)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    N = mask.shape[0]
+    _check_shape(mask, N, H, W, bs)
+    C = hi.shape[1] if hi.shape[0] else lo.shape[1]
+    y = np.zeros((N, C, H, W), np.float32)
+    _L().orc_combine(_ptr(hi, _fp), _ptr(lo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _ptr(y, _fp))
+    return y
+
+
+def layer(x, mask, bs: int, w, b, dtype: str):
+    """One block-conv layer: combine(conv3x3(pad(split(x)))), rounding to the
+    storage type wherever a stage stores its result."""
+    x = _f32(x)
+    N, C, H, W = x.shape
+    hi, lo = split(x, mask, bs, dtype)
+    hp, lp = pad(hi, lo, mask, bs, H, W, dtype)
+    ho, lo_o = conv3x3(hp, lp, w, b, dtype)
+    return combine(ho, lo_o, mask, bs, H, W)

@@ -1,0 +1,265 @@
+/*
+ * SegBlocks CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously-correct C implementation of the block modules of
+ * SegBlocks (Verelst & Tuytelaars, "SegBlocks: Block-Based Dynamic Resolution
+ * Networks for Real-Time Segmentation", arXiv 2011.12025), written from the
+ * paper's Method section ("Block modules": BlockSample, BlockPad,
+ * BlockCombine) and its description of the block convolution (the same
+ * filters applied to the high- and the low-resolution block stacks).
+ *
+ * Only the test suite, the smoke check and the CPU-baseline leg of the
+ * benchmark may load this file's library.  The GPU product path never links,
+ * imports or calls it, and the two share no code, headers or tables.
+ *
+ * Conventions
+ *   - Every tensor is a float array in logical N,C,H,W order (row-major).
+ *     For fp16/bf16 runs the arrays hold values that are exactly
+ *     representable in that type (the wrapper converts bit-exactly).
+ *   - dtype: 0 = fp32, 1 = fp16, 2 = bf16.
+ *   - mask[n][gy][gx] != 0 means the block is processed at HIGH resolution
+ *     (the paper's action a_b = 1).
+ *   - Blocks are packed into each stack in row-major (n, gy, gx) order
+ *     (stable compaction); the paper leaves the order open.
+ *
+ * Build: gcc -O2 -ffp-contract=off (no fast-math) so that the fp32
+ * arithmetic below is performed exactly as written.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_F32 0
+#define ORC_F16 1
+#define ORC_BF16 2
+
+/* ------------------------------------------------------------------------ */
+/* Rounding to the storage type, from the IEEE-754 definition.               */
+/* ------------------------------------------------------------------------ */
+
+/* Round v to the nearest value of a binary format with p significand bits
+ * (implicit bit included), minimum normal exponent emin and maximum exponent
+ * emax; ties go to the even significand; overflow goes to +-inf.  The
+ * quantum inside a binade is 2^(E-(p-1)); below the normal range it is fixed
+ * at 2^(emin-(p-1)) (gradual underflow). */
+static double round_binary(double v, int p, int emin, int emax)
+{
+    if (v != v || v == 0.0 || isinf(v)) return v;
+    double a = fabs(v);
+    int e2;
+    frexp(a, &e2);          /* a = m * 2^e2, 0.5 <= m < 1 */
+    int E = e2 - 1;         /* a = 1.f * 2^E              */
+    if (E < emin) E = emin;
+    double q = ldexp(1.0, E - (p - 1));
+    double r = nearbyint(a / q) * q;     /* a/q is exact: scaling by 2^k */
+    double maxf = ldexp(2.0 - ldexp(1.0, 1 - p), emax);
+    if (r > maxf) r = INFINITY;
+    return copysign(r, v);
+}
+
+double orc_round(double v, int dtype)
+{
+    switch (dtype) {
+    case ORC_F16:  return round_binary(v, 11, -14, 15);
+    case ORC_BF16: return round_binary(v, 8, -126, 127);
+    default:       return round_binary(v, 24, -126, 127);
+    }
+}
+
+void orc_round_array(const double* in, float* out, long n, int dtype)
+{
+    for (long i = 0; i < n; ++i) out[i] = (float)orc_round(in[i], dtype);
+}
+
+/* 2x2 average used by BlockSample's downsampling and by BlockPad's average
+ * sampling.  The paper specifies average pooling but not its arithmetic;
+ * this implementation fixes it as fp32 ((a+b)+(c+d)) * 0.25, rounded once
+ * to the storage type.  a,b are the top-left/top-right and c,d the
+ * bottom-left/bottom-right pixels of the 2x2 cell. */
+float orc_avg4(float a, float b, float c, float d, int dtype)
+{
+    float s = (a + b) + (c + d);
+    float m = s * 0.25f;
+    return (float)orc_round((double)m, dtype);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block plan: class and slot of every block.                                */
+/* ------------------------------------------------------------------------ */
+
+/* For each block k (row-major over n, gy, gx): slot[k] = number of earlier
+ * blocks of the same class.  inv_hi[s] / inv_lo[s] give the block id of the
+ * s-th high / low block.  counts[0] = #high, counts[1] = #low. */
+void orc_plan(const uint8_t* mask, long B, int32_t* slot, int32_t* inv_hi,
+              int32_t* inv_lo, int32_t* counts)
+{
+    int32_t nh = 0, nl = 0;
+    for (long k = 0; k < B; ++k) {
+        if (mask[k]) { slot[k] = nh; if (inv_hi) inv_hi[nh] = (int32_t)k; ++nh; }
+        else         { slot[k] = nl; if (inv_lo) inv_lo[nl] = (int32_t)k; ++nl; }
+    }
+    counts[0] = nh;
+    counts[1] = nl;
+}
+
+/* ------------------------------------------------------------------------ */
+/* BlockSample: split into blocks, 2x average-pool the low-resolution ones.  */
+/* ------------------------------------------------------------------------ */
+
+/* x[N][C][H][W] -> hi[nh][C][bs][bs], lo[nl][C][bs/2][bs/2]. */
+void orc_split(const float* x, int N, int C, int H, int W, const uint8_t* mask,
+               int bs, int dtype, float* hi, float* lo)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    long nh = 0, nl = 0;
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        for (int c = 0; c < C; ++c) {
+            const float* img = x + ((long)n * C + c) * H * W;
+            if (mask[k]) {
+                float* dst = hi + (nh * C + c) * (long)bs * bs;
+                for (int i = 0; i < bs; ++i)
+                    for (int j = 0; j < bs; ++j)
+                        dst[i * bs + j] = img[(long)(gy * bs + i) * W + gx * bs + j];
+            } else {
+                float* dst = lo + (nl * C + c) * (long)lb * lb;
+                for (int i = 0; i < lb; ++i)
+                    for (int j = 0; j < lb; ++j) {
+                        const long r0 = (long)(gy * bs + 2 * i) * W + gx * bs + 2 * j;
+                        dst[i * lb + j] = orc_avg4(img[r0], img[r0 + 1],
+                                                   img[r0 + W], img[r0 + W + 1], dtype);
+                    }
+            }
+        }
+        if (mask[k]) ++nh; else ++nl;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* BlockPad: one-pixel halo filled from the neighbouring blocks.             */
+/* ------------------------------------------------------------------------ */
+
+/* hi[nh][C][bs][bs], lo[nl][C][lb][lb] -> hp[nh][C][bs+2][bs+2],
+ * lp[nl][C][lb+2][lb+2].  For a halo pixel the neighbour is the block in
+ * the direction of the pixel (diagonal blocks for the corners):
+ *   outside the image                 -> 0
+ *   neighbour at the same resolution  -> copy
+ *   high block, low neighbour         -> nearest-upsampled neighbour value
+ *   low block, high neighbour         -> 2x2 average of the neighbour       */
+void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
+             const uint8_t* mask, int bs, int dtype, float* hp, float* lp)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    const long B = (long)N * GH * GW;
+    int32_t* slot = (int32_t*)malloc(sizeof(int32_t) * (size_t)(B > 0 ? B : 1));
+    int32_t counts[2];
+    orc_plan(mask, B, slot, NULL, NULL, counts);
+
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        const int high = mask[k] != 0;
+        const int e = high ? bs : lb;          /* own extent */
+        const int pe = e + 2;                  /* padded extent */
+        const float* own = high ? hi + (long)slot[k] * C * bs * bs
+                                : lo + (long)slot[k] * C * lb * lb;
+        float* out = high ? hp + (long)slot[k] * C * pe * pe
+                          : lp + (long)slot[k] * C * pe * pe;
+        for (int c = 0; c < C; ++c)
+        for (int u = -1; u <= e; ++u)
+        for (int v = -1; v <= e; ++v) {
+            const int dy = u < 0 ? -1 : (u >= e ? 1 : 0);
+            const int dx = v < 0 ? -1 : (v >= e ? 1 : 0);
+            float val;
+            if (dy == 0 && dx == 0) {
+                val = own[((long)c * e + u) * e + v];
+            } else {
+                const int ny = gy + dy, nx = gx + dx;
+                if (ny < 0 || ny >= GH || nx < 0 || nx >= GW) {
+                    val = 0.0f;
+                } else {
+                    const long nk = ((long)n * GH + ny) * GW + nx;
+                    const int nhigh = mask[nk] != 0;
+                    const int u2 = u - dy * e, v2 = v - dx * e; /* coords in neighbour */
+                    if (nhigh && high) {
+                        val = hi[(((long)slot[nk] * C + c) * bs + u2) * bs + v2];
+                    } else if (!nhigh && !high) {
+                        val = lo[(((long)slot[nk] * C + c) * lb + u2) * lb + v2];
+                    } else if (high) { /* low neighbour: nearest upsampling */
+                        val = lo[(((long)slot[nk] * C + c) * lb + (u2 >> 1)) * lb + (v2 >> 1)];
+                    } else {           /* high neighbour: average sampling */
+                        const float* q = hi + ((long)slot[nk] * C + c) * bs * bs;
+                        const int r = 2 * u2, s = 2 * v2;
+                        val = orc_avg4(q[r * bs + s], q[r * bs + s + 1],
+                                       q[(r + 1) * bs + s], q[(r + 1) * bs + s + 1], dtype);
+                    }
+                }
+            }
+            out[((long)c * pe + (u + 1)) * pe + (v + 1)] = val;
+        }
+    }
+    free(slot);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block convolution: 3x3 "valid" convolution of every padded block.        */
+/* ------------------------------------------------------------------------ */
+
+/* P[S][Cin][E+2][E+2], w[Cout][Cin][3][3], bias[Cout] (or NULL)
+ * -> out[S][Cout][E][E] in fp64:
+ *    out = bias[co] + sum_ci sum_ky sum_kx w[co][ci][ky][kx] * P[ci][i+ky][j+kx]
+ * (cross-correlation, as in every CNN framework), accumulated in fp64 in
+ * the fixed order ci, ky, kx.  The products of fp16/bf16/fp32 operands are
+ * exact in fp64. */
+void orc_conv3x3_valid(const float* P, long S, int Cin, int E, const float* w,
+                       const float* bias, int Cout, double* out)
+{
+    const int pe = E + 2;
+    for (long s = 0; s < S; ++s)
+    for (int co = 0; co < Cout; ++co)
+    for (int i = 0; i < E; ++i)
+    for (int j = 0; j < E; ++j) {
+        double acc = 0.0;
+        for (int ci = 0; ci < Cin; ++ci) {
+            const float* p = P + ((s * Cin + ci) * pe) * (long)pe;
+            const float* wk = w + ((long)co * Cin + ci) * 9;
+            for (int ky = 0; ky < 3; ++ky)
+                for (int kx = 0; kx < 3; ++kx)
+                    acc += (double)wk[ky * 3 + kx] * (double)p[(i + ky) * pe + (j + kx)];
+        }
+        if (bias) acc += (double)bias[co];
+        out[((s * Cout + co) * E + i) * (long)E + j] = acc;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* BlockCombine: nearest-upsample the low blocks and reassemble the map.     */
+/* ------------------------------------------------------------------------ */
+
+/* hi[nh][C][bs][bs], lo[nl][C][lb][lb] -> y[N][C][H][W]. */
+void orc_combine(const float* hi, const float* lo, int N, int C, int H, int W,
+                 const uint8_t* mask, int bs, float* y)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    long nh = 0, nl = 0;
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        for (int c = 0; c < C; ++c) {
+            float* img = y + ((long)n * C + c) * H * W;
+            for (int i = 0; i < bs; ++i)
+                for (int j = 0; j < bs; ++j) {
+                    float v;
+                    if (mask[k]) v = hi[((nh * C + c) * bs + i) * (long)bs + j];
+                    else         v = lo[((nl * C + c) * lb + (i >> 1)) * (long)lb + (j >> 1)];
+                    img[(long)(gy * bs + i) * W + gx * bs + j] = v;
+                }
+        }
+        if (mask[k]) ++nh; else ++nl;
+    }
+}

@@ -1,0 +1,350 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+library routines, exact identities of the block modules, closed forms, a
+hand-worked example and exhaustive enumeration of small masks.
+
+Paper: SegBlocks (arXiv 2011.12025), Method > Block modules (BlockSample,
+BlockPad, BlockCombine) and the statement that a network evaluated with only
+high-resolution blocks equals ordinary processing without blocks.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from oracle_closed_forms import (conv_pad1_f64, layer_closed_form, pad_closed_form, pixel_mask,
+                                 pool_f32, to_type, up2)
+from paper_2011_12025_amd import inputs
+
+DTYPES = ["f32", "f16", "bf16"]
+
+
+def _ulp(v, dtype):
+    """Spacing of the storage type at |v| (fixed below the normal range)."""
+    f = np.spacing(np.abs(np.asarray(v, np.float32)))
+    if dtype == "f16":
+        return np.maximum(f * 2.0 ** 13, 2.0 ** -24)
+    if dtype == "bf16":
+        return np.maximum(f * 2.0 ** 16, 2.0 ** -133)
+    return f
+
+
+def _x(seed, N, C, H, W, dtype):
+    return inputs.feature_map(seed, N, C, H, W, dtype).float().numpy()
+
+
+def _w(seed, Co, Ci, dtype):
+    return inputs.conv_weight(seed, Co, Ci, 3, dtype).float().numpy()
+
+
+def _b(seed, Co, Ci, dtype):
+    return inputs.conv_bias(seed, Co, 9 * Ci, dtype).float().numpy()
+
+
+# ---------------------------------------------------------------------------
+# rounding to the storage type (IEEE-754 round-to-nearest-even)
+# ---------------------------------------------------------------------------
+
+def _special_values():
+    v = [0.0, -0.0, 1.0, -1.0, 65504.0, 65519.99, 65520.0, -65520.0, 2.0 ** -24, 2.0 ** -25,
+         3 * 2.0 ** -26, 2.0 ** -14, 2.0 ** -14 - 2.0 ** -25, 1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11,
+         1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, 3.0e38, 3.4028235e38, 1e-40, 2.0 ** -133, 2.0 ** -134,
+         3 * 2.0 ** -135, 1e-45]
+    return np.array(v, np.float64)
+
+
+def test_round_f16_matches_numpy_cast():
+    g = np.random.default_rng(123)
+    v = np.concatenate([_special_values(),
+                        g.standard_normal(200000) * np.exp2(g.integers(-30, 18, 200000)),
+                        # exact ties between adjacent fp16 values
+                        (g.integers(-2048, 2048, 20000) + 0.5) * np.exp2(g.integers(-24, 5, 20000))])
+    with np.errstate(over="ignore"):
+        ref = v.astype(np.float16).astype(np.float64)
+    got = oracle.round_to(v, "f16").astype(np.float64)
+    np.testing.assert_array_equal(got, ref)
+    assert np.array_equal(np.signbit(got), np.signbit(ref))
+
+
+def test_round_bf16_matches_torch_cast():
+    g = np.random.default_rng(7)
+    v32 = np.concatenate([_special_values().astype(np.float32),
+                          (g.standard_normal(200000) * np.exp2(g.integers(-130, 120, 200000))).astype(np.float32),
+                          ((g.integers(-256, 256, 20000) + 0.5) * np.exp2(g.integers(-120, 100, 20000))).astype(np.float32)])
+    v32 = v32[np.isfinite(v32)]
+    ref = torch.from_numpy(v32).to(torch.bfloat16).float().numpy()
+    got = oracle.round_to(v32.astype(np.float64), "bf16")
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_round_f32_matches_c_cast():
+    g = np.random.default_rng(11)
+    v = np.concatenate([_special_values(), g.standard_normal(100000) * np.exp2(g.integers(-140, 120, 100000))])
+    with np.errstate(over="ignore"):
+        ref = v.astype(np.float32)
+    got = oracle.round_to(v, "f32")
+    np.testing.assert_array_equal(got, ref)
+
+
+# ---------------------------------------------------------------------------
+# the 2x2 average (BlockSample's pooling and BlockPad's average sampling)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_avg4_constant_cell_is_identity(dtype):
+    for v in to_type(np.random.default_rng(5).standard_normal(500).astype(np.float32) * 100, dtype):
+        assert oracle.avg4(v, v, v, v, dtype) == v
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_avg4_within_one_ulp_of_exact_mean(dtype):
+    """Against the exact mean (fp64 holds the sum of four values of similar
+    magnitude exactly), rounded once by a library cast.  Error bound of the fp32
+    arithmetic: two additions contribute at most 2^-24 * (|a|+|b|+|c|+|d|)/2 to
+    the mean, the final rounding half a storage ulp, the reference another half."""
+    g = np.random.default_rng(9)
+    a = to_type(g.standard_normal((4, 4000)).astype(np.float32), dtype)
+    exact = (a[0].astype(np.float64) + a[1] + a[2] + a[3]) / 4.0
+    ref = to_type(exact.astype(np.float32), dtype) if dtype != "f32" else exact.astype(np.float32)
+    got = np.array([oracle.avg4(*a[:, i], dtype) for i in range(a.shape[1])], np.float32)
+    bound = _ulp(ref, dtype) + 2.0 ** -24 * np.abs(a).astype(np.float64).sum(axis=0) / 2
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= bound)
+    if dtype != "f32":      # fp32 intermediates are far finer than the storage type
+        assert np.mean(got == ref) > 0.99
+    assert oracle.avg4(1.0, 2.0, 3.0, 4.0, dtype) == 2.5
+
+
+# ---------------------------------------------------------------------------
+# block plan: stable row-major compaction
+# ---------------------------------------------------------------------------
+
+def test_plan_matches_flatnonzero_ranks():
+    g = np.random.default_rng(3)
+    for B in [1, 7, 64, 65, 1000, 2048]:
+        m = (g.random(B) < 0.4).astype(np.uint8) * g.integers(1, 256, B).astype(np.uint8)
+        slot, inv_hi, inv_lo, nh, nl = oracle.plan(m)
+        hi_ids, lo_ids = np.flatnonzero(m != 0), np.flatnonzero(m == 0)
+        assert (nh, nl) == (hi_ids.size, lo_ids.size)
+        np.testing.assert_array_equal(inv_hi, hi_ids)
+        np.testing.assert_array_equal(inv_lo, lo_ids)
+        np.testing.assert_array_equal(slot[hi_ids], np.arange(nh))
+        np.testing.assert_array_equal(slot[lo_ids], np.arange(nl))
+
+
+# ---------------------------------------------------------------------------
+# hand-worked example (values derived by hand from the module definitions)
+# ---------------------------------------------------------------------------
+
+def test_hand_worked_two_block_example():
+    """1x2 block grid, bs=2, C=1; left block high, right block low.
+
+        x = [[1 2 3 4]      split: hi = [[1 2],[5 6]], lo = [[(3+4+7+8)/4]] = [[5.5]]
+             [5 6 7 8]]
+
+    BlockPad: the high block's right halo is the low neighbour nearest-upsampled
+    (5.5, 5.5); the low block's left halo is the 2x2 average of the high
+    neighbour ((1+2+5+6)/4 = 3.5); everything outside the image is 0.
+    An all-ones 3x3 kernel then gives the high outputs [[14 25],[14 25]] and the
+    low output 3.5 + 5.5 = 9, which BlockCombine writes 2x2."""
+    x = np.array([[[[1, 2, 3, 4], [5, 6, 7, 8]]]], np.float32)
+    mask = np.array([[[1, 0]]], np.uint8)
+    hi, lo = oracle.split(x, mask, 2, "f32")
+    np.testing.assert_array_equal(hi, [[[[1, 2], [5, 6]]]])
+    np.testing.assert_array_equal(lo, [[[[5.5]]]])
+    hp, lp = oracle.pad(hi, lo, mask, 2, 2, 4, "f32")
+    np.testing.assert_array_equal(hp[0, 0], [[0, 0, 0, 0], [0, 1, 2, 5.5], [0, 5, 6, 5.5], [0, 0, 0, 0]])
+    np.testing.assert_array_equal(lp[0, 0], [[0, 0, 0], [3.5, 5.5, 0], [0, 0, 0]])
+    w = np.ones((1, 1, 3, 3), np.float32)
+    y = oracle.layer(x, mask, 2, w, None, "f32")
+    np.testing.assert_array_equal(y[0, 0], [[14, 25, 9, 9], [14, 25, 9, 9]])
+
+
+def test_hand_worked_corner_from_diagonal_neighbour():
+    """2x2 grid, bs=2: only the bottom-right block is high.  The top-left (low)
+    block's bottom-right corner halo pixel comes from its diagonal neighbour,
+    which is high, so it is that neighbour's 2x2 average; the bottom-right (high)
+    block's top-left corner comes from the low diagonal neighbour, nearest."""
+    x = np.arange(16, dtype=np.float32).reshape(1, 1, 4, 4)
+    mask = np.array([[[0, 0], [0, 1]]], np.uint8)
+    hi, lo = oracle.split(x, mask, 2, "f32")
+    hp, lp = oracle.pad(hi, lo, mask, 2, 4, 4, "f32")
+    # high block = x[2:4, 2:4] = [[10 11],[14 15]], average 12.5
+    assert lp[0, 0, 2, 2] == 12.5
+    # low block (0,0) = mean(x[0:2,0:2]) = 2.5
+    assert hp[0, 0, 0, 0] == 2.5
+    # low block (0,1) covers x[0:2, 2:4] -> mean 4.5, nearest into the high block's top halo
+    np.testing.assert_array_equal(hp[0, 0, 0, 1:3], [4.5, 4.5])
+
+
+# ---------------------------------------------------------------------------
+# invariants from the paper's definitions
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_split_combine_roundtrip_exact(dtype):
+    """split(combine(hi, lo)) = (hi, lo) for every mask (BlockSample undoes
+    BlockCombine: nearest-upsampling then 2x2 averaging returns each value)."""
+    g = np.random.default_rng(21)
+    N, C, bs, GH, GW = 2, 3, 6, 3, 4
+    mask = (g.random((N, GH, GW)) < 0.5).astype(np.uint8)
+    nh = int(mask.sum()); nl = mask.size - nh
+    hi = to_type(g.standard_normal((nh, C, bs, bs)).astype(np.float32), dtype)
+    lo = to_type(g.standard_normal((nl, C, bs // 2, bs // 2)).astype(np.float32), dtype)
+    y = oracle.combine(hi, lo, mask, bs, GH * bs, GW * bs)
+    hi2, lo2 = oracle.split(y, mask, bs, dtype)
+    np.testing.assert_array_equal(hi2, hi)
+    np.testing.assert_array_equal(lo2, lo)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_combine_split_closed_form(dtype):
+    """combine(split(x)) = M*x + (1-M)*up2(pool(x)); the identity for an all-high mask."""
+    N, C, bs, H, W = 2, 4, 8, 32, 48
+    x = _x(1, N, C, H, W, dtype)
+    mask = inputs.mask_bernoulli(2, N, H // bs, W // bs, 0.5)
+    y = oracle.combine(*oracle.split(x, mask, bs, dtype), mask, bs, H, W)
+    M = pixel_mask(mask, bs)
+    np.testing.assert_array_equal(y, M * x + (1 - M) * up2(pool_f32(x, dtype)))
+    ones = np.ones_like(mask)
+    np.testing.assert_array_equal(oracle.combine(*oracle.split(x, ones, bs, dtype), ones, bs, H, W), x)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_split_low_blocks_match_library_avg_pool(dtype):
+    N, C, bs, H, W = 1, 5, 4, 16, 16
+    x = _x(4, N, C, H, W, dtype)
+    mask = np.zeros((N, H // bs, W // bs), np.uint8)
+    _, lo = oracle.split(x, mask, bs, dtype)
+    ref = F.avg_pool2d(torch.from_numpy(x).double(), 2).numpy()          # exact-ish mean
+    ref_t = to_type(ref.astype(np.float32), dtype)
+    got = lo.reshape(H // bs, W // bs, C, bs // 2, bs // 2).transpose(2, 0, 3, 1, 4).reshape(1, C, H // 2, W // 2)
+    # same error bound as the 2x2 average itself: one storage ulp plus the two
+    # fp32 additions (2^-24 * sum|cell| / 2 = 2^-23 * mean|cell|)
+    mean_abs = F.avg_pool2d(torch.from_numpy(np.abs(x)).double(), 2).numpy()
+    assert np.all(np.abs(got - ref_t) <= _ulp(ref_t, dtype) + 2.0 ** -23 * mean_abs)
+    if dtype != "f32":
+        assert np.mean(got == ref_t) > 0.99
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("bs", [2, 4, 6, 8])
+def test_pad_closed_form_random_masks(dtype, bs):
+    """BlockPad equals windows of the zero-padded combined map (high blocks) and of
+    its 2x2-pooled version (low blocks), bit for bit."""
+    N, C, GH, GW = 2, 3, 3, 5
+    H, W = GH * bs, GW * bs
+    x = _x(5, N, C, H, W, dtype)
+    for p in [0.0, 0.3, 0.7, 1.0]:
+        mask = inputs.mask_bernoulli(6, N, GH, GW, p)
+        hi, lo = oracle.split(x, mask, bs, dtype)
+        hp, lp = oracle.pad(hi, lo, mask, bs, H, W, dtype)
+        Z = oracle.combine(hi, lo, mask, bs, H, W)
+        rhp, rlp = pad_closed_form(Z, mask, bs, dtype)
+        np.testing.assert_array_equal(hp, rhp)
+        np.testing.assert_array_equal(lp, rlp)
+
+
+def test_conv3x3_valid_matches_library():
+    g = np.random.default_rng(8)
+    P = g.standard_normal((3, 5, 7, 7)).astype(np.float32)
+    w = g.standard_normal((4, 5, 3, 3)).astype(np.float32)
+    b = g.standard_normal(4).astype(np.float32)
+    got = oracle.conv3x3_valid(P, w, b)
+    ref = F.conv2d(torch.from_numpy(P).double(), torch.from_numpy(w).double(),
+                   torch.from_numpy(b).double()).numpy()
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_all_high_layer_is_plain_conv(dtype):
+    """With every block at high resolution the layer is an ordinary zero-padded
+    3x3 convolution (the paper's equivalence with processing without blocks)."""
+    N, C, Co, bs, H, W = 1, 6, 5, 8, 24, 32
+    x = _x(10, N, C, H, W, dtype)
+    w, b = _w(11, Co, C, dtype), _b(12, Co, C, dtype)
+    mask = np.ones((N, H // bs, W // bs), np.uint8)
+    y = oracle.layer(x, mask, bs, w, b, dtype)
+    ref = conv_pad1_f64(x, w, b)
+    tol = {"f32": 1e-6, "f16": 1e-3, "bf16": 8e-3}[dtype]
+    assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_all_low_layer_is_pooled_conv_upsampled(dtype):
+    """All blocks low: up2(conv_pad1(avgpool2(x))) with library ops in float64."""
+    N, C, Co, bs, H, W = 2, 4, 3, 4, 16, 24
+    x = _x(13, N, C, H, W, dtype)
+    w, b = _w(14, Co, C, dtype), _b(15, Co, C, dtype)
+    mask = np.zeros((N, H // bs, W // bs), np.uint8)
+    y = oracle.layer(x, mask, bs, w, b, dtype)
+    xt = torch.from_numpy(x).double()
+    ref = F.interpolate(F.conv2d(F.avg_pool2d(xt, 2), torch.from_numpy(w).double(),
+                                 torch.from_numpy(b).double(), padding=1),
+                        scale_factor=2, mode="nearest").numpy()
+    tol = {"f32": 1e-5, "f16": 4e-3, "bf16": 3e-2}[dtype]
+    assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_layer_closed_form_random_masks(dtype):
+    N, C, Co, bs, GH, GW = 2, 5, 4, 6, 3, 4
+    x = _x(16, N, C, GH * bs, GW * bs, dtype)
+    w, b = _w(17, Co, C, dtype), _b(18, Co, C, dtype)
+    for p in [0.25, 0.5, 0.75]:
+        mask = inputs.mask_bernoulli(19, N, GH, GW, p)
+        y = oracle.layer(x, mask, bs, w, b, dtype)
+        ref = layer_closed_form(x, mask, bs, w, b, dtype)
+        # the oracle rounds once per stored stage; the closed form does not round its output
+        tol = {"f32": 2e-6, "f16": 1e-3, "bf16": 8e-3}[dtype]
+        assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
+
+
+def test_locality_of_mask_flip():
+    """Flipping one block's resolution changes the layer output only inside that
+    block and its 8 neighbours (the halo is one pixel wide)."""
+    N, C, Co, bs, GH, GW = 1, 3, 2, 4, 5, 6
+    H, W = GH * bs, GW * bs
+    x = _x(20, N, C, H, W, "f32")
+    w, b = _w(21, Co, C, "f32"), _b(22, Co, C, "f32")
+    mask = inputs.mask_bernoulli(23, N, GH, GW, 0.5)
+    y0 = oracle.layer(x, mask, bs, w, b, "f32")
+    for gy, gx in [(0, 0), (2, 3), (4, 5), (1, 0)]:
+        m2 = mask.copy()
+        m2[0, gy, gx] ^= 1
+        y1 = oracle.layer(x, m2, bs, w, b, "f32")
+        diff = np.abs(y1 - y0).max(axis=(0, 1)).reshape(GH, bs, GW, bs).max(axis=(1, 3)) > 0
+        allowed = np.zeros((GH, GW), bool)
+        allowed[max(gy - 1, 0):gy + 2, max(gx - 1, 0):gx + 2] = True
+        assert not np.any(diff & ~allowed)
+        assert diff[gy, gx]
+
+
+# ---------------------------------------------------------------------------
+# exhaustive: every mask of a 4x4 block grid
+# ---------------------------------------------------------------------------
+
+def test_bruteforce_all_masks_4x4_grid():
+    """All 2^16 masks of a 4x4 grid (bs=4, 16x16 map, one channel, fp32), one
+    mask per image of a single batch: the plan against flatnonzero, BlockPad
+    against its closed form (exact), and the layer against its float64 closed
+    form."""
+    B = 1 << 16
+    bits = (np.arange(B)[:, None] >> np.arange(16)[None, :]) & 1
+    mask = bits.astype(np.uint8).reshape(B, 4, 4)
+    x1 = _x(30, 1, 1, 16, 16, "f32")
+    x = np.ascontiguousarray(np.broadcast_to(x1, (B, 1, 16, 16)))
+    slot, inv_hi, _, nh, nl = oracle.plan(mask)
+    np.testing.assert_array_equal(inv_hi, np.flatnonzero(mask.reshape(-1)))
+    hi, lo = oracle.split(x, mask, 4, "f32")
+    hp, lp = oracle.pad(hi, lo, mask, 4, 16, 16, "f32")
+    Z = oracle.combine(hi, lo, mask, 4, 16, 16)
+    rhp, rlp = pad_closed_form(Z, mask, 4, "f32")
+    np.testing.assert_array_equal(hp, rhp)
+    np.testing.assert_array_equal(lp, rlp)
+    del hp, lp, rhp, rlp, Z
+    w, b = _w(31, 1, 1, "f32"), _b(32, 1, 1, "f32")
+    y = oracle.layer(x, mask, 4, w, b, "f32")
+    ref = layer_closed_form(x, mask, 4, w, b, "f32")
+    assert np.max(np.abs(y - ref)) <= 2e-6 * np.max(np.abs(ref))
