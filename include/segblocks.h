@@ -1,0 +1,153 @@
+/*
+ * segblocks.h -- C ABI of libsegblocks.so, block-based dynamic-resolution
+ * convolution for AMD Instinct MI355X (gfx950).
+ *
+ * Method: SegBlocks (Verelst & Tuytelaars, arXiv 2011.12025), Method section,
+ * "Block modules".  A feature map is cut into a grid of bs x bs blocks; a
+ * per-block mask selects high or low resolution for every block; low blocks
+ * are 2x average-pooled (BlockSample), every block gets a one-pixel halo
+ * taken from its neighbours (BlockPad), the same 3x3 filters run on both
+ * block stacks, and the results are reassembled into a full-resolution map
+ * with the low blocks nearest-upsampled (BlockCombine).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are DEVICE pointers unless stated otherwise.  The caller owns
+ *    every buffer; the library allocates no device memory.
+ *  - Logical dimensions are always N, C, H, W.  `layout` selects the memory
+ *    format of every feature tensor of the call (input, stacks and output):
+ *      SB_NCHW  contiguous [N][C][H][W]          (PyTorch default)
+ *      SB_NHWC  contiguous [N][H][W][C]          (PyTorch channels_last)
+ *    A block stack with S blocks of extent e is a tensor of logical shape
+ *    [S, C, e, e] in the same memory format.
+ *  - dtype is the storage type of every feature tensor, weight and bias of
+ *    the call: SB_F32, SB_F16 or SB_BF16.  Arithmetic is fp32.
+ *  - mask is uint8 [N][H/bs][W/bs] (row-major).  mask != 0 selects HIGH
+ *    resolution for that block (the paper's action a_b = 1).  Block id
+ *    k = (n*GH + gy)*GW + gx with GH = H/bs, GW = W/bs.
+ *  - Blocks are packed into the high stack and into the low stack in
+ *    increasing block id (stable compaction): the slot of block k is the
+ *    number of blocks before k with the same resolution.  nh = number of
+ *    high blocks, nl = number of low blocks.
+ *  - Stack capacities hi_cap / lo_cap are the number of blocks each stack
+ *    buffer can hold.  The kernels read the true nh / nl from the mask on
+ *    the device; a block whose slot is >= the capacity of its stack is
+ *    skipped (not read, not written; BlockPad reads it as zeros; BlockCombine
+ *    writes zeros for it).  Allocate nh / nl blocks after segblocks_count, or
+ *    N*GH*GW blocks for each stack to avoid the synchronisation.
+ *  - bs must be even and >= 2, and divide H and W.  Low blocks have extent
+ *    lb = bs/2.
+ *  - Every call except segblocks_count is asynchronous on `stream` and
+ *    performs no host synchronisation.  Arguments are validated on the host
+ *    before anything is launched; on failure nothing is launched, the call
+ *    returns a negative sb_status and segblocks_last_error() describes it.
+ *    Device faults surface at the caller's next synchronisation.
+ *  - Output buffers must not overlap input buffers.
+ *
+ * Arithmetic
+ *  - The 2x2 average (BlockSample's pooling and BlockPad's average sampling)
+ *    is computed in fp32 as ((a + b) + (c + d)) * 0.25 with a, b the top
+ *    and c, d the bottom pixels of the cell, then rounded to nearest-even.
+ *    Split, pad and combine are therefore bit-exact and deterministic.
+ *  - Convolutions accumulate in fp32 (MFMA), add the bias in fp32 and round
+ *    once to the storage type (nearest-even).
+ */
+#ifndef SEGBLOCKS_H
+#define SEGBLOCKS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SB_F32 = 0, SB_F16 = 1, SB_BF16 = 2 } sb_dtype;
+typedef enum { SB_NCHW = 0, SB_NHWC = 1 } sb_layout;
+typedef enum {
+    SB_OK = 0,
+    SB_EINVAL = -1, /* null pointer, bad enum, non-positive size, aliasing   */
+    SB_ESHAPE = -2, /* bs odd or < 2, bs does not divide H or W, too large   */
+    SB_EHIP = -3    /* a HIP runtime call failed (message from the runtime)  */
+} sb_status;
+
+/* Flags of segblocks_block_conv3x3. */
+#define SB_FLAG_RELU 1 /* max(0, .) after bias (and residual) */
+
+/* Number of high (mask != 0) and low blocks of a mask.  BLOCKING: copies the
+ * mask to the host on `stream` and waits for it.  n_high / n_low are HOST
+ * pointers.  Not needed on the hot path (see the capacity convention). */
+int segblocks_count(const uint8_t* mask, int N, int GH, int GW,
+                    int* n_high, int* n_low, hipStream_t stream);
+
+/* BlockSample (paper: Method > Block modules > BlockSample).
+ * x [N,C,H,W] -> hi [nh,C,bs,bs] (block copied) and lo [nl,C,bs/2,bs/2]
+ * (2x2 average of the block). */
+int segblocks_split(const void* x, int dtype, int layout, int N, int C, int H, int W,
+                    const uint8_t* mask, int bs,
+                    void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t stream);
+
+/* BlockPad with average sampling (paper: Method > Block modules > BlockPad).
+ * hi [nh,C,bs,bs], lo [nl,C,lb,lb] -> hi_pad [nh,C,bs+2,bs+2],
+ * lo_pad [nl,C,lb+2,lb+2].  Interior: the block itself.  A halo pixel is
+ * taken from the neighbouring block in its direction (the diagonal block for
+ * corners): same resolution -> copied; low neighbour of a high block ->
+ * nearest-upsampled; high neighbour of a low block -> 2x2 average; outside
+ * the image -> 0.  hi/hi_pad hold hi_cap blocks, lo/lo_pad lo_cap blocks. */
+int segblocks_pad(const void* hi, const void* lo, int dtype, int layout,
+                  int N, int C, int H, int W, const uint8_t* mask, int bs,
+                  void* hi_pad, void* lo_pad, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* Block convolution on padded stacks (paper: Method -- the same filters are
+ * applied to the high- and the low-resolution blocks).  3x3, stride 1,
+ * "valid" on every padded block:
+ *   out[s,co,i,j] = bias[co] + sum_{ci,ky,kx} w[co,ci,ky,kx] * pad[s,ci,i+ky,j+kx]
+ * hi_pad [nh,C_in,bs+2,bs+2], lo_pad [nl,C_in,lb+2,lb+2]
+ *   -> hi_out [nh,C_out,bs,bs], lo_out [nl,C_out,lb,lb].
+ * weight: OIHW [C_out][C_in][3][3] contiguous (any layout); bias [C_out] or
+ * NULL.  Both in `dtype`. */
+int segblocks_conv3x3(const void* hi_pad, const void* lo_pad, int dtype, int layout,
+                      int N, int C_in, int H, int W, const uint8_t* mask, int bs,
+                      const void* weight, const void* bias, int C_out,
+                      void* hi_out, void* lo_out, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* BlockCombine (paper: Method > Block modules > BlockCombine).
+ * hi [nh,C,bs,bs], lo [nl,C,lb,lb] -> y [N,C,H,W]; a low block is written
+ * nearest-upsampled (each value covers 2x2 output pixels). */
+int segblocks_combine(const void* hi, const void* lo, int dtype, int layout,
+                      int N, int C, int H, int W, const uint8_t* mask, int bs,
+                      int hi_cap, int lo_cap, void* y, hipStream_t stream);
+
+/* Block convolution with BlockPad fused into the tile load: packed stacks in,
+ * packed stacks out, no padded stacks in memory.  Equal to
+ * segblocks_conv3x3(segblocks_pad(hi, lo)) followed by the optional epilogue
+ *   out = act(conv + bias + residual)
+ * with residual_hi / residual_lo stacks shaped like the outputs (or both
+ * NULL) and act = ReLU when flags & SB_FLAG_RELU.  hi/hi_out/residual_hi hold
+ * hi_cap blocks, lo/lo_out/residual_lo lo_cap blocks. */
+int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layout,
+                            int N, int C_in, int H, int W, const uint8_t* mask, int bs,
+                            const void* weight, const void* bias, int C_out, int flags,
+                            const void* residual_hi, const void* residual_lo,
+                            void* hi_out, void* lo_out, int hi_cap, int lo_cap,
+                            hipStream_t stream);
+
+/* One complete block-conv layer, fused into a single kernel:
+ *   y = combine(conv3x3(pad(split(x))))
+ * x [N,C_in,H,W] -> y [N,C_out,H,W]; weight/bias as in segblocks_conv3x3.
+ * Intermediate values are rounded to `dtype` exactly where the four-call
+ * chain stores them, so the result equals that chain's up to the order of
+ * the fp32 accumulation. */
+int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W,
+                    const uint8_t* mask, int bs, const void* weight, const void* bias,
+                    int C_out, void* y, hipStream_t stream);
+
+/* Description of the last failure on the calling thread ("" if none).  The
+ * string stays valid until the next call on the same thread. */
+const char* segblocks_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEGBLOCKS_H */

@@ -1,0 +1,184 @@
+"""SegBlocks block-based dynamic-resolution convolution on MI355X (gfx950).
+
+Python face of ``libsegblocks.so``.  Tensors are torch CUDA(HIP) tensors with
+logical shape [N, C, H, W] (stacks: [S, C, e, e]) in either the default
+contiguous (NCHW) or the channels_last (NHWC) memory format; all tensors of
+one call share the dtype (float32, float16 or bfloat16) and the memory format.
+``mask`` is a uint8 [N, H/bs, W/bs] tensor, non-zero = high resolution.
+
+Paper: Verelst & Tuytelaars, SegBlocks (arXiv 2011.12025), Method section,
+"Block modules" (BlockSample, BlockPad, BlockCombine) and the block
+convolution that applies the same filters to both block stacks.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _binding as _b
+
+__all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "layer", "layout_of"]
+
+_DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
+
+
+def layout_of(t: torch.Tensor) -> int:
+    """SB_NCHW for a contiguous tensor, SB_NHWC for a channels_last one."""
+    if t.dim() != 4:
+        raise ValueError("expected a 4-d tensor")
+    if t.is_contiguous():
+        return _b.SB_NCHW
+    if t.is_contiguous(memory_format=torch.channels_last):
+        return _b.SB_NHWC
+    raise ValueError("tensor must be contiguous or channels_last")
+
+
+def _fmt(layout: int):
+    return torch.channels_last if layout == _b.SB_NHWC else torch.contiguous_format
+
+
+def _empty(shape, like: torch.Tensor, layout: int) -> torch.Tensor:
+    return torch.empty(shape, dtype=like.dtype, device=like.device, memory_format=_fmt(layout))
+
+
+def _check_layout(layout: int, *ts):
+    for t in ts:
+        if t is None or t.numel() == 0:
+            continue
+        ok = t.is_contiguous(memory_format=_fmt(layout))
+        if not ok:
+            raise ValueError("all feature tensors of a call must share the memory format")
+
+
+def _dt(t: torch.Tensor) -> int:
+    try:
+        return _DT[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}") from None
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _mask(mask: torch.Tensor) -> torch.Tensor:
+    if mask.dtype != torch.uint8 or mask.dim() != 3 or not mask.is_contiguous():
+        raise ValueError("mask must be a contiguous uint8 tensor [N, GH, GW]")
+    return mask
+
+
+def count(mask: torch.Tensor):
+    """(n_high, n_low) of a device mask.  Blocks on the current stream."""
+    mask = _mask(mask)
+    nh, nl = ctypes.c_int(0), ctypes.c_int(0)
+    N, GH, GW = mask.shape
+    _b.call("segblocks_count", _ptr(mask), N, GH, GW, ctypes.byref(nh), ctypes.byref(nl), _stream(mask))
+    return nh.value, nl.value
+
+
+def split(x: torch.Tensor, mask: torch.Tensor, bs: int, counts=None, layout=None):
+    """BlockSample: returns (hi [nh,C,bs,bs], lo [nl,C,bs/2,bs/2]).
+
+    ``counts`` = (n_high, n_low) sizes the stacks; without it they are counted
+    (one host synchronisation)."""
+    mask = _mask(mask)
+    layout = layout_of(x) if layout is None else layout
+    _check_layout(layout, x)
+    N, C, H, W = x.shape
+    nh, nl = counts if counts is not None else count(mask)
+    hi = _empty((nh, C, bs, bs), x, layout)
+    lo = _empty((nl, C, bs // 2, bs // 2), x, layout)
+    _b.call("segblocks_split", _ptr(x), _dt(x), layout, N, C, H, W, _ptr(mask), bs, _ptr(hi), nh, _ptr(lo), nl,
+            _stream(x))
+    return hi, lo
+
+
+def pad(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None):
+    """BlockPad: returns (hi_pad [nh,C,bs+2,bs+2], lo_pad [nl,C,bs/2+2,bs/2+2])."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hi, lo)
+    C = ref.shape[1]
+    N = mask.shape[0]
+    hp = _empty((hi.shape[0], C, bs + 2, bs + 2), ref, layout)
+    lp = _empty((lo.shape[0], C, bs // 2 + 2, bs // 2 + 2), ref, layout)
+    _b.call("segblocks_pad", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, _ptr(hp), _ptr(lp),
+            hi.shape[0], lo.shape[0], _stream(ref))
+    return hp, lp
+
+
+def conv3x3(hp: torch.Tensor, lp: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
+            weight: torch.Tensor, bias=None, layout=None):
+    """3x3 valid convolution of both padded stacks: returns (hi_out, lo_out)."""
+    mask = _mask(mask)
+    ref = hp if hp.shape[0] else lp
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hp, lp)
+    C_in = ref.shape[1]
+    C_out = weight.shape[0]
+    N = mask.shape[0]
+    weight = weight.contiguous()
+    bias = None if bias is None else bias.contiguous()
+    ho = _empty((hp.shape[0], C_out, bs, bs), ref, layout)
+    lo = _empty((lp.shape[0], C_out, bs // 2, bs // 2), ref, layout)
+    _b.call("segblocks_conv3x3", _ptr(hp), _ptr(lp), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
+            _ptr(weight), _ptr(bias), C_out, _ptr(ho), _ptr(lo), hp.shape[0], lp.shape[0], _stream(ref))
+    return ho, lo
+
+
+def combine(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None,
+            out=None):
+    """BlockCombine: returns y [N,C,H,W] with the low blocks nearest-upsampled."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hi, lo)
+    N, C = mask.shape[0], ref.shape[1]
+    y = _empty((N, C, H, W), ref, layout) if out is None else out
+    _b.call("segblocks_combine", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, hi.shape[0],
+            lo.shape[0], _ptr(y), _stream(ref))
+    return y
+
+
+def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
+                  weight: torch.Tensor, bias=None, relu: bool = False, residual=None, layout=None, out=None):
+    """3x3 block convolution with BlockPad fused into the tile load (packed in,
+    packed out); optional epilogue act(conv + bias + residual)."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hi, lo)
+    C_in, C_out, N = ref.shape[1], weight.shape[0], mask.shape[0]
+    weight = weight.contiguous()
+    bias = None if bias is None else bias.contiguous()
+    if out is None:
+        ho = _empty((hi.shape[0], C_out, bs, bs), ref, layout)
+        lo_o = _empty((lo.shape[0], C_out, bs // 2, bs // 2), ref, layout)
+    else:
+        ho, lo_o = out
+    rh, rl = (None, None) if residual is None else residual
+    _b.call("segblocks_block_conv3x3", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
+            _ptr(weight), _ptr(bias), C_out, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl), _ptr(ho),
+            _ptr(lo_o), hi.shape[0], lo.shape[0], _stream(ref))
+    return ho, lo_o
+
+
+def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bias=None, layout=None, out=None):
+    """One fused block-conv layer: combine(conv3x3(pad(split(x)))) in one kernel."""
+    mask = _mask(mask)
+    layout = layout_of(x) if layout is None else layout
+    _check_layout(layout, x)
+    N, C_in, H, W = x.shape
+    C_out = weight.shape[0]
+    weight = weight.contiguous()
+    bias = None if bias is None else bias.contiguous()
+    y = _empty((N, C_out, H, W), x, layout) if out is None else out
+    _b.call("segblocks_layer", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(mask), bs, _ptr(weight), _ptr(bias),
+            C_out, _ptr(y), _stream(x))
+    return y

@@ -1,0 +1,245 @@
+// C ABI of libsegblocks.so (declared in include/segblocks.h): host-side
+// argument validation, then one kernel launch on the caller's stream.
+// Nothing here allocates device memory and nothing touches the GPU before
+// every argument has been checked.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+#include <vector>
+
+#include "segblocks.h"
+#include "sb_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fn, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = std::string(fn) + ": " + buf;
+    return code;
+}
+
+int hip_status(const char* fn, hipError_t e) {
+    if (e == hipSuccess) {
+        g_err.clear();
+        return SB_OK;
+    }
+    return fail(SB_EHIP, fn, "HIP error %d (%s)", (int)e, hipGetErrorString(e));
+}
+
+int esize(int dtype) { return dtype == SB_F32 ? 4 : 2; }
+
+struct Range {
+    const void* p;
+    long long bytes;
+};
+
+bool overlap(Range a, Range b) {
+    if (!a.p || !b.p || a.bytes <= 0 || b.bytes <= 0) return false;
+    const char* a0 = (const char*)a.p;
+    const char* b0 = (const char*)b.p;
+    return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// Checks dtype, layout, sizes, block size and the mask pointer; fills g.
+int check_geo(const char* fn, int dtype, int layout, int N, int C, int H, int W, const uint8_t* mask, int bs,
+              sb::Geo& g) {
+    if (dtype != SB_F32 && dtype != SB_F16 && dtype != SB_BF16) return fail(SB_EINVAL, fn, "bad dtype %d", dtype);
+    if (layout != SB_NCHW && layout != SB_NHWC) return fail(SB_EINVAL, fn, "bad layout %d", layout);
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
+        return fail(SB_EINVAL, fn, "N, C, H, W must be positive (got %d, %d, %d, %d)", N, C, H, W);
+    if (!mask) return fail(SB_EINVAL, fn, "mask is NULL");
+    if (bs < 2 || (bs & 1)) return fail(SB_ESHAPE, fn, "block size must be even and >= 2 (got %d)", bs);
+    if (H % bs || W % bs) return fail(SB_ESHAPE, fn, "block size %d does not divide H=%d and W=%d", bs, H, W);
+    g.N = N; g.C = C; g.H = H; g.W = W; g.bs = bs;
+    g.GH = H / bs; g.GW = W / bs;
+    g.B = (long long)N * g.GH * g.GW;
+    const long long elems = (long long)N * C * H * W;
+    if (elems > (1LL << 40) || g.B * (bs + 2) >= (1LL << 31))
+        return fail(SB_ESHAPE, fn, "problem too large (N*C*H*W = %lld, blocks = %lld)", elems, g.B);
+    return SB_OK;
+}
+
+int check_caps(const char* fn, int hi_cap, int lo_cap) {
+    if (hi_cap < 0 || lo_cap < 0) return fail(SB_EINVAL, fn, "capacities must be >= 0");
+    return SB_OK;
+}
+
+// a stack pointer may be NULL only when its capacity is 0
+int check_stack(const char* fn, const char* name, const void* p, int cap) {
+    if (!p && cap > 0) return fail(SB_EINVAL, fn, "%s is NULL with capacity %d", name, cap);
+    return SB_OK;
+}
+
+int check_conv_shape(const char* fn, int C_in, int C_out, int bs, const void* weight) {
+    if (C_in <= 0 || C_out <= 0) return fail(SB_EINVAL, fn, "C_in and C_out must be positive");
+    if (!weight) return fail(SB_EINVAL, fn, "weight is NULL");
+    if (bs > 256) return fail(SB_ESHAPE, fn, "convolution supports block sizes up to 256 (got %d)", bs);
+    return SB_OK;
+}
+
+bool any_overlap(const std::vector<Range>& outs, const std::vector<Range>& ins) {
+    for (size_t i = 0; i < outs.size(); ++i) {
+        for (const Range& r : ins)
+            if (overlap(outs[i], r)) return true;
+        for (size_t j = i + 1; j < outs.size(); ++j)
+            if (overlap(outs[i], outs[j])) return true;
+    }
+    return false;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* segblocks_last_error(void) { return g_err.c_str(); }
+
+int segblocks_count(const uint8_t* mask, int N, int GH, int GW, int* n_high, int* n_low, hipStream_t stream) {
+    const char* fn = "segblocks_count";
+    if (!mask || !n_high || !n_low) return fail(SB_EINVAL, fn, "NULL pointer argument");
+    if (N <= 0 || GH <= 0 || GW <= 0) return fail(SB_EINVAL, fn, "N, GH, GW must be positive");
+    const long long B = (long long)N * GH * GW;
+    if (B >= (1LL << 31)) return fail(SB_ESHAPE, fn, "too many blocks (%lld)", B);
+    std::vector<uint8_t> host((size_t)B);
+    hipError_t e = hipMemcpyAsync(host.data(), mask, (size_t)B, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_status(fn, e);
+    long long nh = 0;
+    for (long long k = 0; k < B; ++k) nh += host[(size_t)k] != 0;
+    *n_high = (int)nh;
+    *n_low = (int)(B - nh);
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_split(const void* x, int dtype, int layout, int N, int C, int H, int W, const uint8_t* mask, int bs,
+                    void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_split";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (!x) return fail(SB_EINVAL, fn, "x is NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rx{x, (long long)N * C * H * W * es}, rm{mask, g.B};
+    const Range rh{hi, hi_cap * (long long)C * bs * bs * es}, rl{lo, lo_cap * (long long)C * lb * lb * es};
+    if (any_overlap({rh, rl}, {rx, rm})) return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_split(dtype, layout, g, x, mask, hi, hi_cap, lo, lo_cap, stream));
+}
+
+int segblocks_pad(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+                  const uint8_t* mask, int bs, void* hi_pad, void* lo_pad, int hi_cap, int lo_cap,
+                  hipStream_t stream) {
+    const char* fn = "segblocks_pad";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
+        (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rh{hi, hi_cap * (long long)C * bs * bs * es}, rl{lo, lo_cap * (long long)C * lb * lb * es};
+    const Range rhp{hi_pad, hi_cap * (long long)C * (bs + 2) * (bs + 2) * es};
+    const Range rlp{lo_pad, lo_cap * (long long)C * (lb + 2) * (lb + 2) * es};
+    if (any_overlap({rhp, rlp}, {rh, rl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_pad(dtype, layout, g, hi, lo, mask, hi_pad, lo_pad, hi_cap, lo_cap, stream));
+}
+
+int segblocks_conv3x3(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C_in, int H, int W,
+                      const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, void* hi_out,
+                      void* lo_out, int hi_cap, int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_conv3x3";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
+        (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rhp{hi_pad, hi_cap * (long long)C_in * (bs + 2) * (bs + 2) * es};
+    const Range rlp{lo_pad, lo_cap * (long long)C_in * (lb + 2) * (lb + 2) * es};
+    const Range rw{weight, (long long)C_out * C_in * 9 * es}, rb{bias, bias ? C_out * es : 0};
+    const Range rho{hi_out, hi_cap * (long long)C_out * bs * bs * es};
+    const Range rlo{lo_out, lo_cap * (long long)C_out * lb * lb * es};
+    if (any_overlap({rho, rlo}, {rhp, rlp, rw, rb, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    sb::ConvArgs a{hi_pad, lo_pad, weight, bias, nullptr, nullptr, hi_out, lo_out, C_in, C_out, 0, hi_cap, lo_cap};
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PADDED, sb::DST_PACKED, g, mask, a, stream));
+}
+
+int segblocks_combine(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+                      const uint8_t* mask, int bs, int hi_cap, int lo_cap, void* y, hipStream_t stream) {
+    const char* fn = "segblocks_combine";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (!y) return fail(SB_EINVAL, fn, "y is NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rh{hi, hi_cap * (long long)C * bs * bs * es}, rl{lo, lo_cap * (long long)C * lb * lb * es};
+    const Range ry{y, (long long)N * C * H * W * es};
+    if (any_overlap({ry}, {rh, rl, Range{mask, g.B}})) return fail(SB_EINVAL, fn, "y overlaps an input");
+    return hip_status(fn, sb::launch_combine(dtype, layout, g, hi, lo, mask, hi_cap, lo_cap, y, stream));
+}
+
+int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
+                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int flags,
+                            const void* residual_hi, const void* residual_lo, void* hi_out, void* lo_out,
+                            int hi_cap, int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_block_conv3x3";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
+        return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
+    const Range rw{weight, (long long)C_out * C_in * 9 * es}, rb{bias, bias ? C_out * es : 0};
+    const Range rho{hi_out, hi_cap * (long long)C_out * bs * bs * es};
+    const Range rlo{lo_out, lo_cap * (long long)C_out * lb * lb * es};
+    // the residual may be read at exactly the output location it feeds (in-place add is not allowed either)
+    const Range rrh{residual_hi, hi_cap * (long long)C_out * bs * bs * es};
+    const Range rrl{residual_lo, lo_cap * (long long)C_out * lb * lb * es};
+    if (any_overlap({rho, rlo}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, mask, a, stream));
+}
+
+int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const uint8_t* mask,
+                    int bs, const void* weight, const void* bias, int C_out, void* y, hipStream_t stream) {
+    const char* fn = "segblocks_layer";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if (!x || !y) return fail(SB_EINVAL, fn, "x or y is NULL");
+    const long long es = esize(dtype);
+    const Range rx{x, (long long)N * C_in * H * W * es}, ry{y, (long long)N * C_out * H * W * es};
+    const Range rw{weight, (long long)C_out * C_in * 9 * es}, rb{bias, bias ? C_out * es : 0};
+    if (any_overlap({ry}, {rx, rw, rb, Range{mask, g.B}})) return fail(SB_EINVAL, fn, "y overlaps an input");
+    sb::ConvArgs a{x, nullptr, weight, bias, nullptr, nullptr, y, nullptr, C_in, C_out, 0, 0, 0};
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, mask, a, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,40 @@
+// Internal launcher interface between the C ABI (sb_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sb {
+
+// Geometry of one call: logical N, C, H, W; block size; block grid.
+struct Geo {
+    int N, C, H, W, bs, GH, GW;
+    long long B;  // N * GH * GW
+};
+
+enum ConvSrc { SRC_PADDED = 0, SRC_PACKED = 1, SRC_DENSE = 2 };
+enum ConvDst { DST_PACKED = 0, DST_DENSE = 1 };
+
+struct ConvArgs {
+    const void* in_hi;   // padded or packed high stack, or the dense map
+    const void* in_lo;   // padded or packed low stack (unused for dense input)
+    const void* weight;  // OIHW [C_out][C_in][3][3]
+    const void* bias;    // [C_out] or nullptr
+    const void* res_hi;  // residual stacks (packed output only) or nullptr
+    const void* res_lo;
+    void* out_hi;        // packed output stacks, or the dense output map
+    void* out_lo;
+    int C_in, C_out, flags, hi_cap, lo_cap;
+};
+
+hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask,
+                        void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t st);
+hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
+                      const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, hipStream_t st);
+hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
+                          const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st);
+// g.C is ignored by the convolution launcher (C_in / C_out are in ConvArgs).
+hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g,
+                       const uint8_t* mask, const ConvArgs& a, hipStream_t st);
+
+}  // namespace sb
