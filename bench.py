@@ -92,7 +92,7 @@ def main():
     cl = torch.channels_last
     mask = torch.from_numpy(mask_np).to(dev)
     ones = torch.ones_like(mask)
-    wd, bd = w0.to(dev).contiguous(), b0.to(dev).contiguous()
+    wd, bd = w0.to(dev).contiguous(memory_format=cl), b0.to(dev).contiguous()  # OHWI for channels_last calls
     x_first = x0.to(dev).contiguous(memory_format=cl)
 
     map_bytes = N * C * H * W * es

@@ -15,7 +15,8 @@
  *  - Pointers are DEVICE pointers unless stated otherwise.  The caller owns
  *    every buffer; the library allocates no device memory.
  *  - Logical dimensions are always N, C, H, W.  `layout` selects the memory
- *    format of every feature tensor of the call (input, stacks and output):
+ *    format of every 4-d tensor of the call (input, stacks, output and the
+ *    convolution weight):
  *      SB_NCHW  contiguous [N][C][H][W]          (PyTorch default)
  *      SB_NHWC  contiguous [N][H][W][C]          (PyTorch channels_last)
  *    A block stack with S blocks of extent e is a tensor of logical shape
@@ -104,8 +105,9 @@ int segblocks_pad(const void* hi, const void* lo, int dtype, int layout,
  *   out[s,co,i,j] = bias[co] + sum_{ci,ky,kx} w[co,ci,ky,kx] * pad[s,ci,i+ky,j+kx]
  * hi_pad [nh,C_in,bs+2,bs+2], lo_pad [nl,C_in,lb+2,lb+2]
  *   -> hi_out [nh,C_out,bs,bs], lo_out [nl,C_out,lb,lb].
- * weight: OIHW [C_out][C_in][3][3] contiguous (any layout); bias [C_out] or
- * NULL.  Both in `dtype`. */
+ * weight: logical [C_out][C_in][3][3] in the call's memory format: OIHW
+ * memory for SB_NCHW, OHWI memory ([C_out][3][3][C_in], a channels_last
+ * weight tensor) for SB_NHWC.  bias [C_out] or NULL.  Both in `dtype`. */
 int segblocks_conv3x3(const void* hi_pad, const void* lo_pad, int dtype, int layout,
                       int N, int C_in, int H, int W, const uint8_t* mask, int bs,
                       const void* weight, const void* bias, int C_out,

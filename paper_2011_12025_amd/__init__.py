@@ -66,6 +66,13 @@ def _stream(t: torch.Tensor):
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
 
+def _weight(weight: torch.Tensor, layout: int) -> torch.Tensor:
+    """The weight in the call's memory format (OHWI memory for channels_last)."""
+    if weight.dim() != 4 or tuple(weight.shape[2:]) != (3, 3):
+        raise ValueError("weight must be [C_out, C_in, 3, 3]")
+    return weight.contiguous(memory_format=_fmt(layout))
+
+
 def _mask(mask: torch.Tensor) -> torch.Tensor:
     if mask.dtype != torch.uint8 or mask.dim() != 3 or not mask.is_contiguous():
         raise ValueError("mask must be a contiguous uint8 tensor [N, GH, GW]")
@@ -123,7 +130,7 @@ def conv3x3(hp: torch.Tensor, lp: torch.Tensor, mask: torch.Tensor, bs: int, H: 
     C_in = ref.shape[1]
     C_out = weight.shape[0]
     N = mask.shape[0]
-    weight = weight.contiguous()
+    weight = _weight(weight, layout)
     bias = None if bias is None else bias.contiguous()
     ho = _empty((hp.shape[0], C_out, bs, bs), ref, layout)
     lo = _empty((lp.shape[0], C_out, bs // 2, bs // 2), ref, layout)
@@ -155,7 +162,7 @@ def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
     layout = layout_of(ref) if layout is None else layout
     _check_layout(layout, hi, lo)
     C_in, C_out, N = ref.shape[1], weight.shape[0], mask.shape[0]
-    weight = weight.contiguous()
+    weight = _weight(weight, layout)
     bias = None if bias is None else bias.contiguous()
     if out is None:
         ho = _empty((hi.shape[0], C_out, bs, bs), ref, layout)
@@ -176,7 +183,7 @@ def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bi
     _check_layout(layout, x)
     N, C_in, H, W = x.shape
     C_out = weight.shape[0]
-    weight = weight.contiguous()
+    weight = _weight(weight, layout)
     bias = None if bias is None else bias.contiguous()
     y = _empty((N, C_out, H, W), x, layout) if out is None else out
     _b.call("segblocks_layer", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(mask), bs, _ptr(weight), _ptr(bias),

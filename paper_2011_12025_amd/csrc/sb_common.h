@@ -80,6 +80,25 @@ __device__ __forceinline__ void vstore(T* p, const Vec<T, V>& v) {
     }
 }
 
+// Streaming (non-temporal) 16-byte loads and stores.  Data that is read or
+// written once per kernel goes through these: on MI355X ordinary loads of
+// streamed data reached about a third of the bandwidth of the non-temporal
+// form (measured: ~1.9 vs ~5.8 TB/s into LDS).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_nt16(const void* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return uint4{v.x, v.y, v.z, v.w};
+}
+__device__ __forceinline__ void st_nt16(void* p, uint4 v) {
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
+}
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void st_nt8(void* p, uint2 v) {
+    const u32x2_t w = {v.x, v.y};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x2_t*>(p));
+}
+
 template <typename T, int V>
 __device__ __forceinline__ Vec<T, V> vzero() {
     Vec<T, V> v;
@@ -98,15 +117,15 @@ __device__ __forceinline__ Vec<T, V> vavg4(const Vec<T, V>& a, const Vec<T, V>& 
 }
 
 // ---------------------------------------------------------------------------
-// Wavefront primitives
+// Wavefront primitives and the block plan
+//
+// The plan (class and slot of a block, the block of a slot) is computed by
+// every wave from the mask itself: each lane loads 16 mask bytes per
+// 1024-block stride with one vector load, and the cross-lane sums use
+// ballots (scalar bit counts of bit planes) and v_mbcnt (lanes below), so no
+// LDS traffic and no barrier is involved and the results are wave-uniform.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
-
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
 
 // Bit b (0..15) set iff byte b of the 16-byte word is non-zero.
 __device__ __forceinline__ uint32_t nonzero_bytes16(uint4 w) {
@@ -122,77 +141,161 @@ __device__ __forceinline__ uint32_t nonzero_bytes16(uint4 w) {
     return r;
 }
 
-// Block plan by wavefront counting.  For each of NT target block ids t[i]
-// (0 <= t[i] <= B) returns, uniformly across the wave, the number of high
-// blocks (mask != 0) among ids [0, t[i]).  Every lane covers 16 mask bytes per
-// 1024-block stride with one vector load; partial counts are summed across
-// the wave.  All 64 lanes of the wave must call it.
-template <int NT>
-__device__ __forceinline__ void wave_count_high(const uint8_t* __restrict__ mask, long long B,
-                                                const long long (&t)[NT], int (&out)[NT]) {
-    long long tmax = 0;
+// Wave-wide sum of per-lane values in [0, 31]: bit plane b contributes
+// popcount(ballot(bit b)) << b.
+__device__ __forceinline__ int wave_sum5(int v) {
+    int s = 0;
 #pragma unroll
-    for (int i = 0; i < NT; ++i) tmax = t[i] > tmax ? t[i] : tmax;
-    const bool aligned = (reinterpret_cast<uintptr_t>(mask) & 15) == 0;
-    int cnt[NT];
-#pragma unroll
-    for (int i = 0; i < NT; ++i) cnt[i] = 0;
-    for (long long base = (long long)lane_id() * 16; base < tmax; base += 1024) {
-        uint32_t bits = 0;
-        if (aligned && base + 16 <= B) {
-            bits = nonzero_bytes16(*reinterpret_cast<const uint4*>(mask + base));
-        } else {
-            for (int b = 0; b < 16; ++b)
-                if (base + b < B && mask[base + b]) bits |= 1u << b;
-        }
-#pragma unroll
-        for (int i = 0; i < NT; ++i) {
-            const long long n = t[i] - base;
-            if (n > 0) cnt[i] += __popc(bits & (n >= 16 ? 0xFFFFu : ((1u << n) - 1u)));
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < NT; ++i) out[i] = wave_sum(cnt[i]);
+    for (int b = 0; b < 5; ++b) s += __popcll(__ballot((v >> b) & 1)) << b;
+    return s;
 }
 
+// Sum of the values in [0, 31] of the lanes below this one.
+__device__ __forceinline__ int wave_excl5(int v) {
+    int s = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const unsigned long long m = __ballot((v >> b) & 1);
+        s += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << b;
+    }
+    return s;
+}
+
+// The mask as seen by one wave: a mask of B bytes (block ids 0..B-1, mask
+// != 0 = high), read in strides of 1024 blocks, lane l holding the non-zero
+// flags of bytes [stride + 16 l, stride + 16 l + 16) as bits 0..15.  For the
+// first stride every lane also keeps the number of high blocks in the lanes
+// below it, so that a class, a slot or the block of a slot inside the first
+// stride costs a few scalar operations (v_readlane, s_bcnt1).  Block ids
+// beyond the first stride are answered by rescanning the later strides;
+// ONE = true promises B <= 1024 and compiles that code out.  All 64 lanes of
+// the wave must take part in every call.
+template <bool ONE>
+struct WaveMaskT {
+    const uint8_t* __restrict__ mask;
+    int B;
+    bool aligned;
+    uint32_t first;  // this lane's bits of the first stride
+    int pre;         // high blocks in the first stride's lanes below this one
+    int tot;         // high blocks in the first stride
+
+    __device__ __forceinline__ uint32_t load(int stride) const {
+        const int b0 = stride + 16 * lane_id();
+        if (b0 >= B) return 0;
+        if (aligned && b0 + 16 <= B) return nonzero_bytes16(*reinterpret_cast<const uint4*>(mask + b0));
+        // the mask's final partial chunk: one byte at a time, all issued together
+        uint8_t v[16];
+#pragma unroll
+        for (int b = 0; b < 16; ++b) v[b] = (b0 + b < B) ? mask[b0 + b] : (uint8_t)0;
+        uint32_t r = 0;
+#pragma unroll
+        for (int b = 0; b < 16; ++b) r |= (uint32_t)(v[b] != 0) << b;
+        return r;
+    }
+    __device__ __forceinline__ void init(const uint8_t* m, int nbytes) {
+        mask = m;
+        B = nbytes;
+        aligned = (reinterpret_cast<uintptr_t>(m) & 15) == 0;
+        first = load(0);
+        const int c = __popc(first);
+        pre = wave_excl5(c);
+        tot = wave_sum5(c);
+    }
+    // valid-byte bits of this lane's chunk of a stride
+    __device__ __forceinline__ uint32_t inside(int stride) const {
+        const int b0 = stride + 16 * lane_id();
+        return b0 >= B ? 0u : (b0 + 16 <= B ? 0xFFFFu : ((1u << (B - b0)) - 1u));
+    }
+
+    // Is block t (0 <= t < B, wave-uniform) high?
+    __device__ __forceinline__ bool high(int t) const {
+        const int stride = ONE ? 0 : (t & ~1023);
+        const uint32_t b = stride == 0 ? first : load(stride);
+        const int w = __builtin_amdgcn_readlane((int)b, (t - stride) >> 4);
+        return (w >> ((t - stride) & 15)) & 1;
+    }
+    // Number of high blocks among ids [0, t) (0 <= t <= B, wave-uniform).
+    __device__ __forceinline__ int count_high(int t) const {
+        if (ONE || t < 1024) {
+            if (t == 0) return 0;
+            const int l = (t - 1) >> 4;  // lane holding block t - 1
+            const int n = t - 16 * l;    // 1..16 bits of that lane below t
+            const uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)first, l);
+            return __builtin_amdgcn_readlane(pre, l) + __popc(w & (n >= 16 ? 0xFFFFu : ((1u << n) - 1u)));
+        }
+        int cnt = tot;
+        for (int stride = 1024; stride < t; stride += 1024) {
+            const int n = t - (stride + 16 * lane_id());
+            const uint32_t b = load(stride);
+            cnt += wave_sum5(n <= 0 ? 0 : __popc(b & (n >= 16 ? 0xFFFFu : ((1u << n) - 1u))));
+        }
+        return cnt;
+    }
+    // Slot of block t: its rank among the earlier blocks of its class.
+    __device__ __forceinline__ int slot(int t, bool is_high) const {
+        const int c = count_high(t);
+        return is_high ? c : t - c;
+    }
+    // Block id of the s-th block (0-based, wave-uniform) of the class
+    // `want_high`, or -1 if the mask has no more than s blocks of that class.
+    __device__ __forceinline__ int find_nth(int s, bool want_high) const {
+        int before = 0;
+        for (int stride = 0; stride < (ONE ? 1 : B); stride += 1024) {
+            const uint32_t b = stride == 0 ? first : load(stride);
+            const uint32_t cls = want_high ? b : (~b & inside(stride));
+            const int cnt = __popc(cls);
+            int excl, total;
+            if (stride == 0) {
+                const int below = min(16 * lane_id(), B);  // mask bytes in the lanes below
+                excl = want_high ? pre : below - pre;
+                total = want_high ? tot : min(B, 1024) - tot;
+            } else {
+                excl = wave_excl5(cnt);
+                total = wave_sum5(cnt);
+            }
+            if (before + total > s) {
+                excl += before;
+                const bool mine = s >= excl && s < excl + cnt;
+                const int src = __ffsll((unsigned long long)__ballot(mine)) - 1;
+                uint32_t m = cls;
+                for (int i = excl; mine && i < s; ++i) m &= m - 1;
+                const int pos = __builtin_amdgcn_readlane(__ffs(m) - 1, src);
+                return stride + 16 * src + pos;
+            }
+            before += total;
+        }
+        return -1;
+    }
+};
+typedef WaveMaskT<false> WaveMask;
+
 // Class and slot of a block and of its 8 neighbours.  Neighbour index
-// d = (dy+1)*3 + (dx+1); d = 4 is the block itself.  Lives in LDS so that
-// every thread of the workgroup can index it with a run-time d.
+// d = (dy+1)*3 + (dx+1); d = 4 is the block itself.
 struct Neigh {
     uint32_t valid;  // bit d: neighbour d lies inside the block grid
     uint32_t high;   // bit d: neighbour d is high resolution
     int slot[9];     // slot of neighbour d in its class's stack
 };
 
-// Fills *out (in LDS) with the neighbourhood of block (n, gy, gx): classes and,
-// when WITH_SLOTS, slots from one wavefront count over the image's mask
-// prefix.  Must be called by one whole wave; lane 0 writes.  The caller
-// synchronises the workgroup before other waves read *out.
-template <bool WITH_SLOTS>
-__device__ __forceinline__ void block_neighbourhood(const uint8_t* __restrict__ mask, int GH, int GW,
-                                                    int n, int gy, int gx, Neigh* out) {
-    long long t[9];
-    uint32_t valid = 0, high = 0;
+// Neighbourhood of block (n, gy, gx): classes and, when WITH_SLOTS, slots.
+// Wave-uniform; all 64 lanes of the wave must call it.
+template <bool WITH_SLOTS, bool ONE>
+__device__ __forceinline__ Neigh wave_neighbourhood(const WaveMaskT<ONE>& wm, int GH, int GW, int n, int gy, int gx) {
+    int t[9];
+    Neigh r;
+    r.valid = 0;
+    r.high = 0;
 #pragma unroll
     for (int d = 0; d < 9; ++d) {
         const int ny = gy + d / 3 - 1, nx = gx + d % 3 - 1;
         const bool v = (ny >= 0 && ny < GH && nx >= 0 && nx < GW);
-        const long long k = ((long long)n * GH + (v ? ny : gy)) * GW + (v ? nx : gx);
-        t[d] = k;
-        valid |= (uint32_t)v << d;
-        high |= (uint32_t)(mask[k] != 0) << d;
+        t[d] = (n * GH + (v ? ny : gy)) * GW + (v ? nx : gx);
+        r.valid |= (uint32_t)v << d;
+        r.high |= (uint32_t)wm.high(t[d]) << d;
     }
-    int c[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-    if constexpr (WITH_SLOTS) {
-        wave_count_high<9>(mask, ((long long)n + 1) * GH * GW, t, c);
-    }
-    if (lane_id() == 0) {
-        out->valid = valid;
-        out->high = high;
 #pragma unroll
-        for (int d = 0; d < 9; ++d)
-            out->slot[d] = WITH_SLOTS ? (((high >> d) & 1) ? c[d] : (int)(t[d] - c[d])) : 0;
-    }
+    for (int d = 0; d < 9; ++d) r.slot[d] = WITH_SLOTS ? wm.slot(t[d], (r.high >> d) & 1) : 0;
+    return r;
 }
 
 }  // namespace sb

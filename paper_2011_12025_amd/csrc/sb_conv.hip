@@ -1,21 +1,36 @@
 // 3x3 block convolution as an MFMA implicit GEMM for gfx950.
 //
-// GEMM view per block: M = output pixels of the block (e x e), N = output
-// channels, K = 9 taps x C_in.  One workgroup (4 waves) computes a tile of
-// up to 256 output pixels (whole rows of one block) x 64 output channels.
-// K is walked in chunks of 64 bytes of channels (32 fp16/bf16 or 16 fp32):
-// the padded input rows of the tile and the chunk's weights are staged in
-// LDS with an XOR swizzle of the 16-byte sub-chunks, then every tap reads
-// its A fragments at a constant pixel offset from the same LDS tile.
-// MFMA: v_mfma_f32_16x16x32_{f16,bf16} (8 K-values per lane) or
-// v_mfma_f32_16x16x4_f32.  Each wave owns up to four 16-row M sub-tiles and
-// all four 16-column N sub-tiles (64 fp32 accumulators per lane).
+// GEMM view per block: output pixels x output channels, K = 9 taps x C_in.
+// One workgroup (4 waves) computes a tile of up to 256 output pixels (whole
+// rows of one block) x 64 output channels.  K is walked in chunks of 64
+// bytes of input channels (32 fp16/bf16 or 16 fp32): the padded input rows
+// of the tile and the chunk's weights are staged in LDS with an XOR swizzle
+// of the 16-byte sub-chunks, and every tap reads its pixel fragments at a
+// constant offset from the same LDS tile.
+//
+// MFMA: v_mfma_f32_16x16x32_{f16,bf16} (8 K values per lane) or
+// v_mfma_f32_16x16x4_f32, with the weights as the A operand (16 output
+// channels) and the pixels as the B operand (16 pixels).  A lane's result is
+// then 4 consecutive output channels of one pixel, which the epilogue stores
+// directly (8 bytes for fp16/bf16) without a trip through LDS.  Each wave
+// owns up to four 16-pixel sub-tiles and all four 16-channel sub-tiles (64
+// fp32 accumulators per lane).
+//
+// Staging is batched: every thread computes the sources of several 16-byte
+// vectors, issues all their loads, then writes LDS.  While the MFMAs of
+// chunk kc run, the weights and the first input batch of chunk kc+1 are
+// already being loaded into registers.  LDS use (58.6 KiB for 32-pixel
+// blocks) allows two workgroups per CU, so one workgroup's loads overlap
+// the other's MFMAs.
 //
 // The tile loader is where the block modules live:
 //   SRC_PADDED : reads padded stacks (plain conv of segblocks_conv3x3)
 //   SRC_PACKED : BlockPad fused (neighbour lookup into the packed stacks)
 //   SRC_DENSE  : BlockSample + BlockPad fused (reads the dense input map)
 // and the store is either a packed stack or BlockCombine into a dense map.
+//
+// Weights: channels-last calls take OHWI memory ([C_out][3][3][C_in], the
+// memory of a channels_last [C_out, C_in, 3, 3] tensor), NCHW calls OIHW.
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -54,249 +69,359 @@ template <> struct MF<float> {
 constexpr int NT = 64;     // output channels per workgroup
 constexpr int ROWB = 64;   // LDS bytes per tile pixel / weight row (one K chunk)
 constexpr int MT = 256;    // target output pixels per workgroup
-constexpr int SROW = NT + 4;  // fp32 staging row (padded against bank conflicts)
 constexpr int W_BYTES = 9 * NT * ROWB;
+// Input-tile vectors per thread per batch (UI), and prefetched during the
+// MFMAs (UP).  A fused-pad source may need four loads per vector (2x2
+// average), so its batches are smaller and only its weights are prefetched,
+// to stay within 256 VGPRs (the next chunk's input pixels share cache lines
+// with the current chunk's and come from L2).
+template <int SRC> struct Batches { static constexpr int UI = 2, UP = 0; };
+template <> struct Batches<SRC_PADDED> { static constexpr int UI = 4, UP = 2; };
+constexpr int UW = 9 * NT * (ROWB / 16) / WG;  // weight vectors per thread per chunk
+static_assert(UW * WG == 9 * NT * (ROWB / 16), "weight staging covers the chunk exactly");
 
 // byte offset of 16-byte sub-chunk q of LDS row `row`: sub-chunks are XOR-
 // swizzled with bits 1..2 of the row so that 8 consecutive rows read at the
 // same sub-chunk hit 8 distinct 16-byte bank groups.
 __device__ __forceinline__ int swz(int row, int q) { return row * ROWB + ((q ^ ((row >> 1) & 3)) << 4); }
 
-template <typename T, int L, int SRC, int V>
-__device__ __forceinline__ Vec<T, V> tile_pixel(const Geo& g, const ConvArgs& a, const Neigh& nb, int n, int gy,
-                                                int gx, int slot, bool high, int pe, int u, int v, int c) {
+// Geometry of one workgroup's tile (uniform across the workgroup).
+struct Tile {
+    int n, gy, gx, slot, high, e, pe, r0, rows, M, in_px;
+};
+
+// Source of the tile pixel p (padded-tile coordinates, row-major over
+// (rows + 2) x pe) for channels starting at c.
+template <typename T, int L, int SRC>
+__device__ __forceinline__ Src<T> tile_src(const Geo& g, const ConvArgs& a, const Neigh& nb, const Tile& t, int p,
+                                           int c) {
+    const int pu = p / t.pe, pv = p - pu * t.pe;
+    const int u = t.r0 + pu;
     if constexpr (SRC == SRC_PADDED) {
-        const T* base = (const T*)(high ? a.in_hi : a.in_lo);
-        return vload<T, V>(stack_at<T, L>(base, slot, a.C_in, pe, u, v, c));
+        return src_copy<T>(stack_at<T, L>((const T*)(t.high ? a.in_hi : a.in_lo), t.slot, a.C_in, t.pe, u, pv, c));
     } else if constexpr (SRC == SRC_PACKED) {
-        return packed_pixel<T, L, V>((const T*)a.in_hi, (const T*)a.in_lo, a.C_in, g.bs, nb, a.hi_cap, a.lo_cap,
-                                     u - 1, v - 1, c);
+        return packed_src<T, L>((const T*)a.in_hi, (const T*)a.in_lo, a.C_in, g.bs, nb, a.hi_cap, a.lo_cap, u - 1,
+                                pv - 1, c);
     } else {
-        return dense_pixel<T, L, V>((const T*)a.in_hi, n, a.C_in, g.H, g.W, g.bs, gy, gx, nb, u - 1, v - 1, c);
+        return dense_src<T, L>((const T*)a.in_hi, t.n, a.C_in, g.H, g.W, g.bs, t.gy, t.gx, nb, u - 1, pv - 1, c);
     }
 }
 
-template <typename T, int L, int SRC, int DST>
-__global__ __launch_bounds__(WG) void k_conv(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int Rh, int Rl,
-                                             int G, int w_off, int vec_in, int vec_out) {
+// One batch of UI 16-byte input vectors (channels-last, C_in % 8 (fp16) or
+// % 4 (fp32) == 0): item it -> pixel it/4, sub-chunk it%4.
+template <typename T, int L, int SRC, int U>
+struct InBatch {
+    static constexpr int KC = ROWB / (int)sizeof(T);
+    static constexpr int VQ = 16 / (int)sizeof(T);
+    SrcBatch<T, VQ, U> b;
+
+    __device__ __forceinline__ void issue(const Geo& g, const ConvArgs& a, const Neigh& nb, const Tile& t,
+                                          int base, int kc) {
+        const int items = t.in_px * 4;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it = base + u * WG + (int)threadIdx.x;
+            Src<T> s = src_zero<T>();
+            if (it < items) {
+                const int c0 = kc * KC + (it & 3) * VQ;
+                if (c0 < a.C_in) s = tile_src<T, L, SRC>(g, a, nb, t, it >> 2, c0);
+            }
+            b.issue(u, s);
+        }
+    }
+    __device__ __forceinline__ void commit(unsigned char* s_in, const Tile& t, int base) const {
+        const int items = t.in_px * 4;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it = base + u * WG + (int)threadIdx.x;
+            if (it < items) *reinterpret_cast<uint4*>(s_in + swz(it >> 2, it & 3)) = b.value(u).raw;
+        }
+    }
+};
+
+// The weights of one K chunk as 16-byte vectors of OHWI memory, stored in LDS
+// as rows [tap][co] of 64 bytes (the chunk's input channels).
+template <typename T>
+struct WBatch {
+    static constexpr int KC = ROWB / (int)sizeof(T);
+    static constexpr int VQ = 16 / (int)sizeof(T);
+    Vec<T, VQ> w[UW];
+
+    __device__ __forceinline__ void issue(const ConvArgs& a, int co0, int kc) {
+        const T* __restrict__ wgt = (const T*)a.weight;
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+            const int v = u * WG + (int)threadIdx.x;
+            const int col = v / 36, rem = v - col * 36;
+            const int tap = rem >> 2, q = rem & 3;
+            const int co = co0 + col, ci = kc * KC + q * VQ;
+            if (co < a.C_out && ci < a.C_in) w[u] = vload<T, VQ>(wgt + ((size_t)co * 9 + tap) * a.C_in + ci);
+            else                             w[u] = vzero<T, VQ>();
+        }
+    }
+    __device__ __forceinline__ void commit(unsigned char* s_w) const {
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+            const int v = u * WG + (int)threadIdx.x;
+            const int col = v / 36, rem = v - col * 36;
+            const int tap = rem >> 2, q = rem & 3;
+            *reinterpret_cast<uint4*>(s_w + swz(tap * NT + col, q)) = w[u].raw;
+        }
+    }
+};
+
+// Element-wise staging of one K chunk (any layout and channel count): the
+// input tile and the weights (OIHW for NCHW calls, OHWI for NHWC calls).
+template <typename T, int L, int SRC>
+__device__ __forceinline__ void stage_scalar(const Geo& g, const ConvArgs& a, const Neigh& nb, const Tile& t,
+                                             int co0, int kc, unsigned char* s_in, unsigned char* s_w) {
+    constexpr int KC = ROWB / (int)sizeof(T);
+    constexpr int VQ = 16 / (int)sizeof(T);
+    const int tid = threadIdx.x;
+    for (int it = tid; it < t.in_px * 4; it += WG) {
+        const int p = it >> 2, q = it & 3;
+        const int c0 = kc * KC + q * VQ;
+        Vec<T, VQ> val;
+#pragma unroll
+        for (int e = 0; e < VQ; ++e) {
+            const int c = c0 + e;
+            T v = from_f32<T>(0.0f);
+            if (c < a.C_in) {
+                const Src<T> s = tile_src<T, L, SRC>(g, a, nb, t, p, c);
+                if (s.p) v = s.avg ? avg4(s.p[0], s.p[s.d1], s.p[s.d2], s.p[s.d2 + s.d1]) : s.p[0];
+            }
+            val.e[e] = v;
+        }
+        *reinterpret_cast<uint4*>(s_in + swz(p, q)) = val.raw;
+    }
+    const T* __restrict__ wgt = (const T*)a.weight;
+    for (int it = tid; it < NT * KC; it += WG) {
+        const int col = it / KC, cil = it - col * KC;
+        const int co = co0 + col, ci = kc * KC + cil;
+        const bool ok = co < a.C_out && ci < a.C_in;
+        const int byte = cil * (int)sizeof(T);
+#pragma unroll
+        for (int tap = 0; tap < 9; ++tap) {
+            T wv = from_f32<T>(0.0f);
+            if (ok) {
+                if constexpr (L == NHWC) wv = wgt[((size_t)co * 9 + tap) * a.C_in + ci];
+                else                     wv = wgt[((size_t)co * a.C_in + ci) * 9 + tap];
+            }
+            *reinterpret_cast<T*>(s_w + swz(tap * NT + col, byte >> 4) + (byte & 15)) = wv;
+        }
+    }
+}
+
+template <typename T, int L, int SRC, int DST, bool VEC>
+__global__ __launch_bounds__(WG, 2) void k_conv(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int Rh,
+                                                int Rl, int G, int w_off, int vec_out) {
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ Neigh s_nb;
     typedef MF<T> mf;
     constexpr int KC = ROWB / (int)sizeof(T);  // channels per K chunk
-    constexpr int VQ = 16 / (int)sizeof(T);    // channels per 16-byte sub-chunk
     constexpr bool NEED_SLOTS = !(SRC == SRC_DENSE && DST == DST_DENSE);
 
-    const long long k = blockIdx.x / G;
-    const int grp = (int)(blockIdx.x - k * G);
+    const int k = (int)blockIdx.x / G;
+    const int grp = (int)blockIdx.x - k * G;
     const int co0 = blockIdx.y * NT;
-    const long long per = (long long)g.GH * g.GW;
-    const int n = (int)(k / per);
-    const int rem = (int)(k - (long long)n * per);
-    const int gy = rem / g.GW, gx = rem - gy * g.GW;
-
-    if (threadIdx.x < 64) block_neighbourhood<NEED_SLOTS>(mask, g.GH, g.GW, n, gy, gx, &s_nb);
-    __syncthreads();
-    const bool high = (s_nb.high >> 4) & 1;
-    const int slot = s_nb.slot[4];
-    if (NEED_SLOTS && slot >= (high ? a.hi_cap : a.lo_cap)) return;
-    const int e = high ? g.bs : (g.bs >> 1);
-    const int R = high ? Rh : Rl;
-    const int r0 = grp * R;
-    if (r0 >= e) return;
-    const int rows = min(R, e - r0);
-    const int M = rows * e;
-    const int pe = e + 2;
-    const int in_px = (rows + 2) * pe;
+    Tile t;
+    {
+        const int per = g.GH * g.GW;
+        t.n = k / per;
+        const int rem = k - t.n * per;
+        t.gy = rem / g.GW;
+        t.gx = rem - t.gy * g.GW;
+    }
+    WaveMask wm;
+    wm.init(mask, (int)g.B);
+    const Neigh nb = wave_neighbourhood<NEED_SLOTS>(wm, g.GH, g.GW, t.n, t.gy, t.gx);
+    t.high = (nb.high >> 4) & 1;
+    t.slot = nb.slot[4];
+    if (NEED_SLOTS && t.slot >= (t.high ? a.hi_cap : a.lo_cap)) return;
+    t.e = t.high ? g.bs : (g.bs >> 1);
+    const int R = t.high ? Rh : Rl;
+    t.r0 = grp * R;
+    if (t.r0 >= t.e) return;
+    t.rows = min(R, t.e - t.r0);
+    t.M = t.rows * t.e;
+    t.pe = t.e + 2;
+    t.in_px = (t.rows + 2) * t.pe;
 
     unsigned char* s_in = smem;
     unsigned char* s_w = smem + w_off;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, kg = lane >> 4;
 
-    const int nst = (M + 15) >> 4;  // 16-row M sub-tiles
+    const int nst = (t.M + 15) >> 4;  // 16-pixel sub-tiles
     int pbase[4];
 #pragma unroll
     for (int ms = 0; ms < 4; ++ms) {
-        const int m = min((wave + 4 * ms) * 16 + l16, M - 1);
-        const int i = m / e, j = m - i * e;
-        pbase[ms] = i * pe + j;
+        const int m = min((wave + 4 * ms) * 16 + l16, t.M - 1);
+        const int i = m / t.e, j = m - i * t.e;
+        pbase[ms] = i * t.pe + j;
     }
+    const int nchunks = (a.C_in + KC - 1) / KC;
+    const int in_items = t.in_px * 4;
+    constexpr int UI = Batches<SRC>::UI, UP = Batches<SRC>::UP;
+
+    // -- chunk 0
+    if constexpr (VEC) {
+        {
+            WBatch<T> wb;
+            InBatch<T, L, SRC, UI> ib;
+            wb.issue(a, co0, 0);
+            ib.issue(g, a, nb, t, 0, 0);
+            wb.commit(s_w);
+            ib.commit(s_in, t, 0);
+        }
+        for (int base = WG * UI; base < in_items; base += WG * UI) {
+            InBatch<T, L, SRC, UI> ib;
+            ib.issue(g, a, nb, t, base, 0);
+            ib.commit(s_in, t, base);
+        }
+    } else {
+        stage_scalar<T, L, SRC>(g, a, nb, t, co0, 0, s_in, s_w);
+    }
+    __syncthreads();
+
     floatx4 acc[4][4];
 #pragma unroll
     for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
         for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    const T* __restrict__ wgt = (const T*)a.weight;
-    const int nchunks = (a.C_in + KC - 1) / KC;
     for (int kc = 0; kc < nchunks; ++kc) {
-        // -- stage the padded input rows of the tile for channels [kc*KC, kc*KC + KC)
-        for (int it = tid; it < in_px * 4; it += WG) {
-            const int p = it >> 2, q = it & 3;
-            const int pu = p / pe, pv = p - pu * pe;
-            const int c0 = kc * KC + q * VQ;
-            Vec<T, VQ> val;
-            if (c0 >= a.C_in) {
-                val = vzero<T, VQ>();
-            } else if (L == NHWC && vec_in) {
-                val = tile_pixel<T, L, SRC, VQ>(g, a, s_nb, n, gy, gx, slot, high, pe, r0 + pu, pv, c0);
-            } else {
-#pragma unroll
-                for (int t = 0; t < VQ; ++t)
-                    val.e[t] = (c0 + t < a.C_in)
-                                   ? tile_pixel<T, L, SRC, 1>(g, a, s_nb, n, gy, gx, slot, high, pe, r0 + pu, pv,
-                                                              c0 + t).e[0]
-                                   : from_f32<T>(0.0f);
-            }
-            *reinterpret_cast<uint4*>(s_in + swz(p, q)) = val.raw;
-        }
-        // -- stage the chunk's weights as [tap][co][ci]
-        for (int it = tid; it < NT * KC; it += WG) {
-            const int col = it / KC, cil = it - col * KC;
-            const int co = co0 + col, ci = kc * KC + cil;
-            T wv[9];
-            if (co < a.C_out && ci < a.C_in) {
-                const T* src = wgt + ((size_t)co * a.C_in + ci) * 9;
-#pragma unroll
-                for (int t = 0; t < 9; ++t) wv[t] = src[t];
-            } else {
-#pragma unroll
-                for (int t = 0; t < 9; ++t) wv[t] = from_f32<T>(0.0f);
-            }
-            const int byte = cil * (int)sizeof(T);
-#pragma unroll
-            for (int t = 0; t < 9; ++t) {
-                const int row = t * NT + col;
-                *reinterpret_cast<T*>(s_w + swz(row, byte >> 4) + (byte & 15)) = wv[t];
+        const bool more = kc + 1 < nchunks;
+        // -- prefetch the next chunk's weights and first input batch
+        WBatch<T> wb;
+        InBatch<T, L, SRC, (UP > 0 ? UP : 1)> ib;
+        if constexpr (VEC) {
+            if (more) {
+                wb.issue(a, co0, kc + 1);
+                if constexpr (UP > 0) ib.issue(g, a, nb, t, 0, kc + 1);
             }
         }
-        __syncthreads();
         // -- MFMA over the 9 taps of this chunk
-#pragma unroll
+#pragma unroll 1
         for (int tap = 0; tap < 9; ++tap) {
-            const int toff = (tap / 3) * pe + (tap % 3);
+            const int toff = (tap / 3) * t.pe + (tap % 3);
 #pragma unroll
             for (int ks = 0; ks < KC / mf::KS; ++ks) {
                 const int byte = (ks * mf::KS + kg * mf::EL) * (int)sizeof(T);
-                typename mf::frag b[4];
+                typename mf::frag wf[4];
 #pragma unroll
                 for (int ns = 0; ns < 4; ++ns) {
                     const int row = tap * NT + ns * 16 + l16;
-                    b[ns] = *reinterpret_cast<const typename mf::frag*>(s_w + swz(row, byte >> 4) + (byte & 15));
+                    wf[ns] = *reinterpret_cast<const typename mf::frag*>(s_w + swz(row, byte >> 4) + (byte & 15));
                 }
 #pragma unroll
                 for (int ms = 0; ms < 4; ++ms) {
                     if (wave + 4 * ms < nst) {
                         const int p = pbase[ms] + toff;
-                        const typename mf::frag av =
+                        const typename mf::frag pf =
                             *reinterpret_cast<const typename mf::frag*>(s_in + swz(p, byte >> 4) + (byte & 15));
 #pragma unroll
-                        for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = mf::mma(av, b[ns], acc[ms][ns]);
+                        for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = mf::mma(wf[ns], pf, acc[ms][ns]);
                     }
                 }
             }
         }
         __syncthreads();
-    }
-
-    // -- epilogue: stage fp32 accumulators as [m][co], then store vectors
-    float* s_st = reinterpret_cast<float*>(smem);
-#pragma unroll
-    for (int ms = 0; ms < 4; ++ms) {
-        if (wave + 4 * ms < nst) {
-#pragma unroll
-            for (int ns = 0; ns < 4; ++ns)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = (wave + 4 * ms) * 16 + kg * 4 + r;
-                    if (m < M) s_st[m * SROW + ns * 16 + l16] = acc[ms][ns][r];
+        if (more) {
+            if constexpr (VEC) {
+                wb.commit(s_w);
+                if constexpr (UP > 0) ib.commit(s_in, t, 0);
+                for (int base = WG * UP; base < in_items; base += WG * UI) {
+                    InBatch<T, L, SRC, UI> ib2;
+                    ib2.issue(g, a, nb, t, base, kc + 1);
+                    ib2.commit(s_in, t, base);
                 }
+            } else {
+                stage_scalar<T, L, SRC>(g, a, nb, t, co0, kc + 1, s_in, s_w);
+            }
+            __syncthreads();
         }
     }
-    __syncthreads();
 
+    // -- epilogue: lane holds channels co0 + ns*16 + kg*4 + {0..3} of pixel (wave + 4*ms)*16 + l16
     const T* __restrict__ bias = (const T*)a.bias;
     const bool relu = (a.flags & 1) != 0;
-    if constexpr (L == NHWC) {
-        constexpr int VS = 16 / (int)sizeof(T);
-        const int items = M * (NT / VS);
-        for (int it = tid; it < items; it += WG) {
-            const int m = it / (NT / VS), nq = (it - m * (NT / VS)) * VS;
-            const int co = co0 + nq;
+    float bv[4][4];
+#pragma unroll
+    for (int ns = 0; ns < 4; ++ns)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = co0 + ns * 16 + kg * 4 + r;
+            bv[ns][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
+        }
+    const T* res_base = (const T*)(t.high ? a.res_hi : a.res_lo);
+    T* out_base = (T*)((DST == DST_DENSE || t.high) ? a.out_hi : a.out_lo);
+#pragma unroll
+    for (int ms = 0; ms < 4; ++ms) {
+        if (wave + 4 * ms >= nst) continue;
+        const int m = (wave + 4 * ms) * 16 + l16;
+        if (m >= t.M) continue;
+        const int i = t.r0 + m / t.e, j = m % t.e;
+#pragma unroll
+        for (int ns = 0; ns < 4; ++ns) {
+            const int co = co0 + ns * 16 + kg * 4;
             if (co >= a.C_out) continue;
-            const int i = r0 + m / e, j = m % e;
-            float f[VS];
+            float f[4];
 #pragma unroll
-            for (int t = 0; t < VS; ++t) {
-                f[t] = s_st[m * SROW + nq + t];
-                if (bias && co + t < a.C_out) f[t] += to_f32(bias[co + t]);
-            }
-            size_t off = 0;
-            T* out;
+            for (int r = 0; r < 4; ++r) f[r] = acc[ms][ns][r] + bv[ns][r];
+            const bool full = vec_out && co + 4 <= a.C_out;
             if constexpr (DST == DST_PACKED) {
-                off = (((size_t)slot * e + i) * e + j) * a.C_out + co;
-                out = (T*)(high ? a.out_hi : a.out_lo);
-                const T* res = (const T*)(high ? a.res_hi : a.res_lo);
-                if (res) {
+                // packed stack element (slot, co + r, i, j)
+                size_t off[4];
 #pragma unroll
-                    for (int t = 0; t < VS; ++t)
-                        if (co + t < a.C_out) f[t] += to_f32(res[off + t]);
+                for (int r = 0; r < 4; ++r) {
+                    if constexpr (L == NHWC) off[r] = (((size_t)t.slot * t.e + i) * t.e + j) * a.C_out + co + r;
+                    else off[r] = (((size_t)t.slot * a.C_out + co + r) * t.e + i) * t.e + j;
                 }
-            } else {
-                out = (T*)a.out_hi;
-            }
-            Vec<T, VS> o;
+                if (res_base) {
+                    if (L == NHWC && full) {
+                        const Vec<T, 4> rv = vload<T, 4>(res_base + off[0]);
 #pragma unroll
-            for (int t = 0; t < VS; ++t) o.e[t] = from_f32<T>(relu ? fmaxf(f[t], 0.0f) : f[t]);
-            if constexpr (DST == DST_PACKED) {
-                if (vec_out) {
-                    vstore<T, VS>(out + off, o);
+                        for (int r = 0; r < 4; ++r) f[r] += to_f32(rv.e[r]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (co + r < a.C_out) f[r] += to_f32(res_base[off[r]]);
+                    }
+                }
+                Vec<T, 4> o;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o.e[r] = from_f32<T>(relu ? fmaxf(f[r], 0.0f) : f[r]);
+                if (L == NHWC && full) {
+                    vstore<T, 4>(out_base + off[0], o);
                 } else {
 #pragma unroll
-                    for (int t = 0; t < VS; ++t)
-                        if (co + t < a.C_out) out[off + t] = o.e[t];
+                    for (int r = 0; r < 4; ++r)
+                        if (co + r < a.C_out) out_base[off[r]] = o.e[r];
                 }
             } else {
-                const int reps = high ? 1 : 2;
+                Vec<T, 4> o;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o.e[r] = from_f32<T>(relu ? fmaxf(f[r], 0.0f) : f[r]);
+                const int reps = t.high ? 1 : 2;
                 for (int dy = 0; dy < reps; ++dy)
                     for (int dx = 0; dx < reps; ++dx) {
-                        const int Y = gy * g.bs + (high ? i : 2 * i + dy);
-                        const int X = gx * g.bs + (high ? j : 2 * j + dx);
-                        const size_t doff = (((size_t)n * g.H + Y) * g.W + X) * a.C_out + co;
-                        if (vec_out) {
-                            vstore<T, VS>(out + doff, o);
+                        const int Y = t.gy * g.bs + (t.high ? i : 2 * i + dy);
+                        const int X = t.gx * g.bs + (t.high ? j : 2 * j + dx);
+                        if constexpr (L == NHWC) {
+                            T* p = out_base + (((size_t)t.n * g.H + Y) * g.W + X) * a.C_out + co;
+                            if (full) {
+                                vstore<T, 4>(p, o);
+                            } else {
+#pragma unroll
+                                for (int r = 0; r < 4; ++r)
+                                    if (co + r < a.C_out) p[r] = o.e[r];
+                            }
                         } else {
 #pragma unroll
-                            for (int t = 0; t < VS; ++t)
-                                if (co + t < a.C_out) out[doff + t] = o.e[t];
+                            for (int r = 0; r < 4; ++r)
+                                if (co + r < a.C_out)
+                                    out_base[(((size_t)t.n * a.C_out + co + r) * g.H + Y) * g.W + X] = o.e[r];
                         }
-                    }
-            }
-        }
-    } else {
-        const int items = NT * M;
-        for (int it = tid; it < items; it += WG) {
-            const int nn = it / M, m = it - nn * M;
-            const int co = co0 + nn;
-            if (co >= a.C_out) continue;
-            const int i = r0 + m / e, j = m % e;
-            float f = s_st[m * SROW + nn];
-            if (bias) f += to_f32(bias[co]);
-            if constexpr (DST == DST_PACKED) {
-                const size_t off = (((size_t)slot * a.C_out + co) * e + i) * e + j;
-                const T* res = (const T*)(high ? a.res_hi : a.res_lo);
-                if (res) f += to_f32(res[off]);
-                T* out = (T*)(high ? a.out_hi : a.out_lo);
-                out[off] = from_f32<T>(relu ? fmaxf(f, 0.0f) : f);
-            } else {
-                T* out = (T*)a.out_hi;
-                const T o = from_f32<T>(relu ? fmaxf(f, 0.0f) : f);
-                const int reps = high ? 1 : 2;
-                for (int dy = 0; dy < reps; ++dy)
-                    for (int dx = 0; dx < reps; ++dx) {
-                        const int Y = gy * g.bs + (high ? i : 2 * i + dy);
-                        const int X = gx * g.bs + (high ? j : 2 * j + dx);
-                        out[(((size_t)n * a.C_out + co) * g.H + Y) * g.W + X] = o;
                     }
             }
         }
@@ -304,41 +429,43 @@ __global__ __launch_bounds__(WG) void k_conv(Geo g, const uint8_t* __restrict__ 
 }
 
 inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
-inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+inline bool aligned(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; }
 
-template <typename T, int L, int SRC, int DST>
+template <typename T, int L, int SRC, int DST, bool VEC>
 hipError_t run_conv(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
     const int eh = g.bs, el = g.bs / 2;
     const int Rh = clampi(MT / eh, 1, eh), Rl = clampi(MT / el, 1, el);
     const int G = (((eh + Rh - 1) / Rh) > ((el + Rl - 1) / Rl)) ? (eh + Rh - 1) / Rh : (el + Rl - 1) / Rl;
     const int in_px = ((Rh + 2) * (eh + 2) > (Rl + 2) * (el + 2)) ? (Rh + 2) * (eh + 2) : (Rl + 2) * (el + 2);
     const int w_off = in_px * ROWB;
-    const int m_max = (Rh * eh > Rl * el) ? Rh * eh : Rl * el;
-    const int stage = m_max * SROW * 4;
-    const int smem = (w_off + W_BYTES > stage) ? w_off + W_BYTES : stage;
-    const int vec_in = (L == NHWC) && (a.C_in % (16 / (int)sizeof(T)) == 0) && aligned16(a.in_hi) &&
-                       (SRC == SRC_DENSE || aligned16(a.in_lo));
-    constexpr int VS = 16 / (int)sizeof(T);
-    const int vec_out = (a.C_out % VS == 0) && aligned16(a.out_hi) && (DST == DST_DENSE || aligned16(a.out_lo)) &&
-                        aligned16(a.res_hi) && aligned16(a.res_lo);
+    const int smem = w_off + W_BYTES;
+    const int ob = 4 * (int)sizeof(T);  // one epilogue vector: 4 channels
+    const int vec_out = (a.C_out % 4 == 0) && aligned(a.out_hi, ob) && aligned(a.out_lo, ob) &&
+                        aligned(a.res_hi, ob) && aligned(a.res_lo, ob);
     // raise the kernel's dynamic-LDS limit to what this launch needs (kept per instantiation)
     static int attr_bytes = 0;
     if (smem > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_conv<T, L, SRC, DST>,
+        hipError_t e = hipFuncSetAttribute((const void*)k_conv<T, L, SRC, DST, VEC>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return e;
         attr_bytes = smem;
     }
     const dim3 grid((unsigned)(g.B * G), (unsigned)((a.C_out + NT - 1) / NT));
-    hipLaunchKernelGGL((k_conv<T, L, SRC, DST>), grid, dim3(WG), smem, st, g, mask, a, Rh, Rl, G, w_off, vec_in,
+    hipLaunchKernelGGL((k_conv<T, L, SRC, DST, VEC>), grid, dim3(WG), smem, st, g, mask, a, Rh, Rl, G, w_off,
                        vec_out);
     return hipGetLastError();
 }
 
 template <typename T, int SRC, int DST>
 hipError_t conv_l(int layout, const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
-    if (layout == NHWC) return run_conv<T, NHWC, SRC, DST>(g, mask, a, st);
-    return run_conv<T, NCHW, SRC, DST>(g, mask, a, st);
+    constexpr int VQ = 16 / (int)sizeof(T);
+    if (layout == NHWC) {
+        const bool vec = (a.C_in % VQ == 0) && aligned(a.in_hi, 16) && aligned(a.in_lo, 16) &&
+                         aligned(a.weight, 16);
+        if (vec) return run_conv<T, NHWC, SRC, DST, true>(g, mask, a, st);
+        return run_conv<T, NHWC, SRC, DST, false>(g, mask, a, st);
+    }
+    return run_conv<T, NCHW, SRC, DST, false>(g, mask, a, st);
 }
 
 template <typename T>
@@ -354,6 +481,7 @@ hipError_t conv_t(int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint
 
 hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
                        const ConvArgs& a, hipStream_t st) {
+    if (conv_res_fits(dtype, layout, g, a)) return launch_conv_res(dtype, src, dst, g, mask, a, st);
     switch (dtype) {
     case 0: return conv_t<float>(layout, src, dst, g, mask, a, st);
     case 1: return conv_t<f16>(layout, src, dst, g, mask, a, st);

@@ -1,11 +1,24 @@
 // BlockSample (split), BlockPad (pad) and BlockCombine (combine) as
 // gather/scatter kernels for gfx950.
 //
-// Work decomposition: one workgroup per (block k, group of rows of that
-// block); block k's resolution comes from its mask byte and its slot from a
-// wavefront count of the high blocks before it.  Every thread moves one
-// vector of V elements per item (16 bytes in the channels-last layout, along
-// the channel axis), so a wave covers 1 KiB of contiguous memory per access.
+// Work decomposition: every workgroup writes one piece of 256 output vectors
+// (4 KiB for 16-byte vectors) of one block, one vector per thread, so that a
+// launch has thousands of small workgroups and the memory system always has
+// both loads and stores of many workgroups in flight.  (Fewer, larger
+// workgroups whose threads first load several vectors and then store them
+// measured about half the bandwidth on MI355X.)
+//
+//   split   : grid over the output stacks: (class, slot, piece); the block
+//             of a slot is found from the mask by a wavefront scan.
+//   pad     : grid over the padded stacks: (class, slot, piece), plus the
+//             slots of the 8 neighbours.
+//   combine : grid over the dense output: (block, piece); the block's slot
+//             comes from a wavefront count of the mask prefix.
+//
+// Every wave computes the plan it needs by itself (no LDS, no barrier).
+// Items are numbered in the memory order of the output, so consecutive
+// threads write consecutive vectors: along the channels for channels-last
+// (NHWC) tensors, along the rows for NCHW tensors.
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -14,20 +27,14 @@ namespace sb {
 
 namespace {
 
-__device__ __forceinline__ void block_coords(long long k, int GH, int GW, int& n, int& gy, int& gx) {
-    const long long per = (long long)GH * GW;
-    n = (int)(k / per);
-    const int rem = (int)(k - (long long)n * per);
+constexpr int PIECE = WG;  // output vectors per workgroup
+
+__device__ __forceinline__ void block_coords(int k, int GH, int GW, int& n, int& gy, int& gx) {
+    const int per = GH * GW;
+    n = k / per;
+    const int rem = k - n * per;
     gy = rem / GW;
     gx = rem - gy * GW;
-}
-
-// slot of block k within its class (uniform across the wave)
-__device__ __forceinline__ int block_slot(const uint8_t* __restrict__ mask, long long k, bool high) {
-    long long t[1] = {k};
-    int c[1];
-    wave_count_high<1>(mask, k + 1, t, c);
-    return high ? c[0] : (int)(k - c[0]);
 }
 
 // Picks element `idx` of the concatenation of two vectors.
@@ -36,228 +43,204 @@ __device__ __forceinline__ T pick2(const Vec<T, V>& a, const Vec<T, V>& b, int i
     return idx < V ? a.e[idx] : b.e[idx - V];
 }
 
+// Coordinates of output vector `it` of a block of extent e with C channels,
+// items in memory order: NHWC (r, j, c0) with V channels, NCHW (c, r, j0)
+// with V pixels along the row.
+template <int L, int V>
+__device__ __forceinline__ void item_coords(int it, int e, int C, int& r, int& j, int& c) {
+    if constexpr (L == NHWC) {
+        const int cv = C / V;
+        const int pix = it / cv;
+        c = (it - pix * cv) * V;
+        r = pix / e;
+        j = pix - r * e;
+    } else {
+        const int rv = e / V;
+        const int row = it / rv;
+        j = (it - row * rv) * V;
+        c = row / e;
+        r = row - c * e;
+    }
+}
+
+// Decodes a workgroup of a (class, slot, piece) grid: high slots first.
+__device__ __forceinline__ bool slot_piece(int w, int hi_cap, int Gh, int Gl, bool& high, int& slot, int& piece) {
+    if (w < hi_cap * Gh) {
+        high = true;
+        slot = w / Gh;
+        piece = w - slot * Gh;
+        return true;
+    }
+    w -= hi_cap * Gh;
+    high = false;
+    slot = w / Gl;
+    piece = w - slot * Gl;
+    return true;
+}
+
 // ---------------------------------------------------------------------------
 // split: x[N,C,H,W] -> hi[nh,C,bs,bs], lo[nl,C,lb,lb]
-// R = high rows per workgroup (even); a low block's workgroup produces R/2
-// low rows from the same R input rows.
 // ---------------------------------------------------------------------------
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, int H, int W,
-                                              const uint8_t* __restrict__ mask, int bs, int R, int groups,
+                                              const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
                                               T* __restrict__ hi, int hi_cap, T* __restrict__ lo, int lo_cap) {
+    bool high;
+    int slot, piece;
+    slot_piece((int)blockIdx.x, hi_cap, Gh, Gl, high, slot, piece);
+    WaveMask wm;
+    wm.init(mask, B);
+    const int k = wm.find_nth(slot, high);
+    if (k < 0) return;
     const int GH = H / bs, GW = W / bs, lb = bs >> 1;
-    const long long k = blockIdx.x / groups;
-    const int g = (int)(blockIdx.x - k * groups);
     int n, gy, gx;
     block_coords(k, GH, GW, n, gy, gx);
-    const bool high = mask[k] != 0;
-    const int slot = block_slot(mask, k, high);
-    if (slot >= (high ? hi_cap : lo_cap)) return;
-    const int tid = threadIdx.x;
+    const int e = high ? bs : lb;
+    const int items = e * e * C / V;
+    const int it = piece * PIECE + (int)threadIdx.x;
+    if (it >= items) return;
+    int r, j, c;
+    item_coords<L, V>(it, e, C, r, j, c);
+    T* dst = (high ? hi : lo) + (size_t)slot * C * e * e + (size_t)it * V;
     if (high) {
-        const int r0 = g * R, r1 = min(bs, r0 + R);
-        if (r0 >= r1) return;
-        if constexpr (L == NHWC) {
-            const int rowv = bs * C / V;
-            const int items = (r1 - r0) * rowv;
-            for (int it = tid; it < items; it += WG) {
-                const int r = r0 + it / rowv, o = (it % rowv) * V;
-                const T* src = x + ((size_t)((long long)n * H + gy * bs + r) * W + (size_t)gx * bs) * C + o;
-                T* dst = hi + ((size_t)slot * bs + r) * (size_t)bs * C + o;
-                vstore<T, V>(dst, vload<T, V>(src));
-            }
-        } else {
-            const int rowv = bs / V, per_c = (r1 - r0) * rowv;
-            const int items = C * per_c;
-            for (int it = tid; it < items; it += WG) {
-                const int c = it / per_c, q = it - c * per_c;
-                const int r = r0 + q / rowv, j = (q % rowv) * V;
-                const T* src = x + (((size_t)n * C + c) * H + gy * bs + r) * (size_t)W + (size_t)gx * bs + j;
-                T* dst = hi + (((size_t)slot * C + c) * bs + r) * (size_t)bs + j;
-                vstore<T, V>(dst, vload<T, V>(src));
-            }
-        }
+        vstore<T, V>(dst, vload<T, V>(map_at<T, L>(x, n, C, H, W, gy * bs + r, gx * bs + j, c)));
+        return;
+    }
+    const int Y = gy * bs + 2 * r, X = gx * bs + 2 * j;
+    if constexpr (L == NHWC) {
+        const T* p = map_at<T, L>(x, n, C, H, W, Y, X, c);
+        const size_t down = (size_t)W * C;
+        vstore<T, V>(dst, vavg4<T, V>(vload<T, V>(p), vload<T, V>(p + C), vload<T, V>(p + down),
+                                      vload<T, V>(p + down + C)));
     } else {
-        const int r0 = (g * R) >> 1, r1 = min(lb, (g * R + R) >> 1);
-        if (r0 >= r1) return;
-        if constexpr (L == NHWC) {
-            const int cv = C / V, rowv = lb * cv;
-            const int items = (r1 - r0) * rowv;
-            for (int it = tid; it < items; it += WG) {
-                const int r = r0 + it / rowv, q = it % rowv;
-                const int j = q / cv, c = (q % cv) * V;
-                const T* p = x + ((size_t)((long long)n * H + gy * bs + 2 * r) * W + (size_t)gx * bs + 2 * j) * C + c;
-                const size_t down = (size_t)W * C;
-                const Vec<T, V> a = vload<T, V>(p), b = vload<T, V>(p + C);
-                const Vec<T, V> cc = vload<T, V>(p + down), d = vload<T, V>(p + down + C);
-                vstore<T, V>(lo + (((size_t)slot * lb + r) * lb + j) * C + c, vavg4<T, V>(a, b, cc, d));
-            }
-        } else {
-            const int rowv = lb / V, per_c = (r1 - r0) * rowv;
-            const int items = C * per_c;
-            for (int it = tid; it < items; it += WG) {
-                const int c = it / per_c, q = it - c * per_c;
-                const int r = r0 + q / rowv, j = (q % rowv) * V;
-                const T* p = x + (((size_t)n * C + c) * H + gy * bs + 2 * r) * (size_t)W + (size_t)gx * bs + 2 * j;
-                const Vec<T, V> t0 = vload<T, V>(p), t1 = vload<T, V>(p + V);
-                const Vec<T, V> b0 = vload<T, V>(p + W), b1 = vload<T, V>(p + W + V);
-                Vec<T, V> o;
+        // V low pixels along the row come from 2V input pixels of two rows
+        const T* p = map_at<T, L>(x, n, C, H, W, Y, X, c);
+        const Vec<T, V> t0 = vload<T, V>(p), t1 = vload<T, V>(p + V);
+        const Vec<T, V> b0 = vload<T, V>(p + W), b1 = vload<T, V>(p + W + V);
+        Vec<T, V> o;
 #pragma unroll
-                for (int e = 0; e < V; ++e)
-                    o.e[e] = avg4(pick2(t0, t1, 2 * e), pick2(t0, t1, 2 * e + 1),
-                                  pick2(b0, b1, 2 * e), pick2(b0, b1, 2 * e + 1));
-                vstore<T, V>(lo + (((size_t)slot * C + c) * lb + r) * (size_t)lb + j, o);
-            }
-        }
+        for (int q = 0; q < V; ++q)
+            o.e[q] = avg4(pick2(t0, t1, 2 * q), pick2(t0, t1, 2 * q + 1), pick2(b0, b1, 2 * q),
+                          pick2(b0, b1, 2 * q + 1));
+        vstore<T, V>(dst, o);
     }
 }
 
 // ---------------------------------------------------------------------------
 // pad: hi, lo -> hp[nh,C,bs+2,bs+2], lp[nl,C,lb+2,lb+2]
-// R = padded rows per workgroup.
 // ---------------------------------------------------------------------------
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* __restrict__ lo, int C, int H, int W,
-                                            const uint8_t* __restrict__ mask, int bs, int R, int groups,
+                                            const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
                                             T* __restrict__ hp, T* __restrict__ lp, int hi_cap, int lo_cap) {
-    __shared__ Neigh s_nb;
+    bool high;
+    int slot, piece;
+    slot_piece((int)blockIdx.x, hi_cap, Gh, Gl, high, slot, piece);
+    WaveMask wm;
+    wm.init(mask, B);
+    const int k = wm.find_nth(slot, high);
+    if (k < 0) return;
     const int GH = H / bs, GW = W / bs, lb = bs >> 1;
-    const long long k = blockIdx.x / groups;
-    const int g = (int)(blockIdx.x - k * groups);
     int n, gy, gx;
     block_coords(k, GH, GW, n, gy, gx);
-    if (threadIdx.x < 64) block_neighbourhood<true>(mask, GH, GW, n, gy, gx, &s_nb);
-    __syncthreads();
-    const bool high = (s_nb.high >> 4) & 1;
-    const int slot = s_nb.slot[4];
-    if (slot >= (high ? hi_cap : lo_cap)) return;
     const int e = high ? bs : lb, pe = e + 2;
-    const int r0 = g * R, r1 = min(pe, r0 + R);
-    if (r0 >= r1) return;
-    T* out = high ? hp : lp;
-    const int tid = threadIdx.x;
-    if constexpr (L == NHWC) {
-        const int cv = C / V, rowv = pe * cv;
-        const int items = (r1 - r0) * rowv;
-        for (int it = tid; it < items; it += WG) {
-            const int u = r0 + it / rowv, q = it % rowv;
-            const int v = q / cv, c = (q % cv) * V;
-            const Vec<T, V> val = packed_pixel<T, L, V>(hi, lo, C, bs, s_nb, hi_cap, lo_cap, u - 1, v - 1, c);
-            vstore<T, V>(out + (((size_t)slot * pe + u) * pe + v) * C + c, val);
-        }
+    const int items = pe * pe * C / V;
+    const int it = piece * PIECE + (int)threadIdx.x;
+    const Neigh nb = wave_neighbourhood<true>(wm, GH, GW, n, gy, gx);
+    if (it >= items) return;
+    int u, v, c;
+    item_coords<L, V>(it, pe, C, u, v, c);
+    T* dst = (high ? hp : lp) + (size_t)slot * C * pe * pe + (size_t)it * V;
+    if constexpr (L == NHWC || V == 1) {
+        const Src<T> s = packed_src<T, L>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, v - 1, c);
+        SrcBatch<T, V, 1> b;
+        b.issue(0, s);
+        vstore<T, V>(dst, b.value(0));
     } else {
-        static_assert(L == NHWC || V == 1, "NCHW pad is scalar");
-        const int per_c = (r1 - r0) * pe;
-        const int items = C * per_c;
-        for (int it = tid; it < items; it += WG) {
-            const int c = it / per_c, q = it - c * per_c;
-            const int u = r0 + q / pe, v = q % pe;
-            const Vec<T, 1> val = packed_pixel<T, L, 1>(hi, lo, C, bs, s_nb, hi_cap, lo_cap, u - 1, v - 1, c);
-            vstore<T, 1>(out + (((size_t)slot * C + c) * pe + u) * pe + v, val);
-        }
+        static_assert(L == NHWC || V == 1, "NCHW pad moves single elements");
     }
 }
 
 // ---------------------------------------------------------------------------
 // combine: hi, lo -> y[N,C,H,W]
-// R = output rows per workgroup.
 // ---------------------------------------------------------------------------
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_combine(const T* __restrict__ hi, const T* __restrict__ lo, int C, int H,
-                                                int W, const uint8_t* __restrict__ mask, int bs, int R, int groups,
+                                                int W, const uint8_t* __restrict__ mask, int bs, int B, int G,
                                                 int hi_cap, int lo_cap, T* __restrict__ y) {
+    const int k = (int)blockIdx.x / G;
+    const int piece = (int)blockIdx.x - k * G;
     const int GH = H / bs, GW = W / bs, lb = bs >> 1;
-    const long long k = blockIdx.x / groups;
-    const int g = (int)(blockIdx.x - k * groups);
     int n, gy, gx;
     block_coords(k, GH, GW, n, gy, gx);
-    const bool high = mask[k] != 0;
-    const int slot = block_slot(mask, k, high);
+    WaveMask wm;
+    wm.init(mask, B);
+    const bool high = wm.high(k);
+    const int slot = wm.slot(k, high);
     const bool skip = slot >= (high ? hi_cap : lo_cap);
-    const int r0 = g * R, r1 = min(bs, r0 + R);
-    if (r0 >= r1) return;
-    const int tid = threadIdx.x;
-    if constexpr (L == NHWC) {
-        const int cv = C / V, rowv = bs * cv;
-        const int items = (r1 - r0) * rowv;
-        for (int it = tid; it < items; it += WG) {
-            const int i = r0 + it / rowv, q = it % rowv;
-            const int j = q / cv, c = (q % cv) * V;
-            Vec<T, V> val;
-            if (skip)      val = vzero<T, V>();
-            else if (high) val = vload<T, V>(hi + (((size_t)slot * bs + i) * bs + j) * C + c);
-            else           val = vload<T, V>(lo + (((size_t)slot * lb + (i >> 1)) * lb + (j >> 1)) * C + c);
-            vstore<T, V>(y + ((size_t)((long long)n * H + gy * bs + i) * W + (size_t)gx * bs + j) * C + c, val);
-        }
+    const int items = bs * bs * C / V;
+    const int it = piece * PIECE + (int)threadIdx.x;
+    if (it >= items) return;
+    int r, j, c;
+    item_coords<L, V>(it, bs, C, r, j, c);
+    Vec<T, V> val;
+    if (skip) {
+        val = vzero<T, V>();
+    } else if (high) {
+        val = vload<T, V>(hi + (size_t)slot * C * bs * bs + (size_t)it * V);
+    } else if constexpr (L == NHWC) {
+        val = vload<T, V>(stack_at<T, L>(lo, slot, C, lb, r >> 1, j >> 1, c));
+    } else if constexpr (V == 1) {
+        val = vload<T, 1>(stack_at<T, L>(lo, slot, C, lb, r >> 1, j >> 1, c));
     } else {
-        const int rowv = bs / V, per_c = (r1 - r0) * rowv;
-        const int items = C * per_c;
-        for (int it = tid; it < items; it += WG) {
-            const int c = it / per_c, q = it - c * per_c;
-            const int i = r0 + q / rowv, j = (q % rowv) * V;
-            Vec<T, V> val;
-            if (skip) {
-                val = vzero<T, V>();
-            } else if (high) {
-                val = vload<T, V>(hi + (((size_t)slot * C + c) * bs + i) * (size_t)bs + j);
-            } else {
-                const T* src = lo + (((size_t)slot * C + c) * lb + (i >> 1)) * (size_t)lb + (j >> 1);
-                if constexpr (V == 1) {
-                    val = vload<T, 1>(src);
-                } else {
-                    const Vec<T, V / 2> h = vload<T, V / 2>(src);
+        // V output pixels along the row repeat V/2 low pixels
+        const Vec<T, V / 2> h = vload<T, V / 2>(stack_at<T, L>(lo, slot, C, lb, r >> 1, j >> 1, c));
 #pragma unroll
-                    for (int e = 0; e < V; ++e) val.e[e] = h.e[e >> 1];
-                }
-            }
-            vstore<T, V>(y + (((size_t)n * C + c) * H + gy * bs + i) * (size_t)W + (size_t)gx * bs + j, val);
-        }
+        for (int q = 0; q < V; ++q) val.e[q] = h.e[q >> 1];
     }
+    T* dst;
+    if constexpr (L == NHWC) dst = y + (((size_t)n * H + gy * bs + r) * W + (size_t)gx * bs + j) * C + c;
+    else                     dst = y + (((size_t)n * C + c) * H + gy * bs + r) * (size_t)W + (size_t)gx * bs + j;
+    vstore<T, V>(dst, val);
 }
 
 // ---------------------------------------------------------------------------
 // host-side launch helpers
 // ---------------------------------------------------------------------------
-constexpr int kTargetBytes = 32768;  // bytes moved per workgroup (approx.)
-
-inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
-
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+inline int pieces(long long vectors) { return (int)((vectors + PIECE - 1) / PIECE); }
 
 template <typename T, int L, int V>
 hipError_t run_split(const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap, void* lo,
                      int lo_cap, hipStream_t st) {
-    const int row_bytes = g.bs * g.C * (int)sizeof(T);
-    int R = clampi(kTargetBytes / (row_bytes > 0 ? row_bytes : 1), 2, g.bs) & ~1;
-    const int groups = (g.bs + R - 1) / R;
-    const long long blocks = g.B * groups;
+    const int lb = g.bs / 2;
+    const int Gh = pieces((long long)g.bs * g.bs * g.C / V), Gl = pieces((long long)lb * lb * g.C / V);
+    const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
+    if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((k_split<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)x, g.C, g.H, g.W,
-                       mask, g.bs, R, groups, (T*)hi, hi_cap, (T*)lo, lo_cap);
+                       mask, g.bs, (int)g.B, Gh, Gl, (T*)hi, hi_cap, (T*)lo, lo_cap);
     return hipGetLastError();
 }
 
 template <typename T, int L, int V>
 hipError_t run_pad(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
                    int hi_cap, int lo_cap, hipStream_t st) {
-    const int pe = g.bs + 2;
-    const int row_bytes = pe * g.C * (int)sizeof(T);
-    const int R = clampi(kTargetBytes / (row_bytes > 0 ? row_bytes : 1), 1, pe);
-    const int groups = (pe + R - 1) / R;
-    const long long blocks = g.B * groups;
+    const int ph = g.bs + 2, pl = g.bs / 2 + 2;
+    const int Gh = pieces((long long)ph * ph * g.C / V), Gl = pieces((long long)pl * pl * g.C / V);
+    const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
+    if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((k_pad<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)hi, (const T*)lo, g.C,
-                       g.H, g.W, mask, g.bs, R, groups, (T*)hp, (T*)lp, hi_cap, lo_cap);
+                       g.H, g.W, mask, g.bs, (int)g.B, Gh, Gl, (T*)hp, (T*)lp, hi_cap, lo_cap);
     return hipGetLastError();
 }
 
 template <typename T, int L, int V>
 hipError_t run_combine(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, int hi_cap, int lo_cap,
                        void* y, hipStream_t st) {
-    const int row_bytes = g.bs * g.C * (int)sizeof(T);
-    const int R = clampi(kTargetBytes / (row_bytes > 0 ? row_bytes : 1), 1, g.bs);
-    const int groups = (g.bs + R - 1) / R;
-    const long long blocks = g.B * groups;
+    const int G = pieces((long long)g.bs * g.bs * g.C / V);
+    const long long blocks = g.B * G;
     hipLaunchKernelGGL((k_combine<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)hi, (const T*)lo,
-                       g.C, g.H, g.W, mask, g.bs, R, groups, hi_cap, lo_cap, (T*)y);
+                       g.C, g.H, g.W, mask, g.bs, (int)g.B, G, hi_cap, lo_cap, (T*)y);
     return hipGetLastError();
 }
 

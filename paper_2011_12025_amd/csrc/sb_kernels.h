@@ -37,4 +37,10 @@ hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, c
 hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g,
                        const uint8_t* mask, const ConvArgs& a, hipStream_t st);
 
+// Persistent convolution with LDS-resident weights (channels-last fp16/bf16,
+// C_in <= 64, 16 <= bs <= 64); conv_res_fits tells whether it applies.
+bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
+hipError_t launch_conv_res(int dtype, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
+                           const ConvArgs& a, hipStream_t st);
+
 }  // namespace sb

@@ -1,11 +1,36 @@
-// Source of one padded-tile pixel (a vector of V channels starting at c) for
-// BlockPad and for the convolutions that fuse BlockPad / BlockSample into
-// their tile load.
+// Where one padded-tile pixel comes from, for BlockPad and for the
+// convolutions that fuse BlockPad (and BlockSample) into their tile load.
+//
+// A source is either nothing (the pixel is zero), one location (a copy), or
+// the 2x2 cell p, p + d1, p + d2, p + d2 + d1 whose average is the value.
+// Kernels first compute the sources of a batch of pixels, then issue every
+// load of the batch, then combine: the loads of a batch are in flight
+// together instead of one dependent round trip per pixel.
 #pragma once
 
 #include "sb_common.h"
 
 namespace sb {
+
+template <typename T>
+struct Src {
+    const T* p;  // nullptr -> zero
+    int avg;     // 1 -> average of the 2x2 cell at p
+    int d1, d2;  // element offsets of the right and of the lower pixel of the cell
+};
+
+template <typename T>
+__device__ __forceinline__ Src<T> src_zero() {
+    return Src<T>{nullptr, 0, 0, 0};
+}
+template <typename T>
+__device__ __forceinline__ Src<T> src_copy(const T* p) {
+    return Src<T>{p, 0, 0, 0};
+}
+template <typename T>
+__device__ __forceinline__ Src<T> src_avg(const T* p, int d1, int d2) {
+    return Src<T>{p, 1, d1, d2};
+}
 
 // Element (s, c, y, x) of a block stack of extent `ext` with C channels.
 template <typename T, int L>
@@ -24,70 +49,86 @@ __device__ __forceinline__ const T* map_at(const T* base, int n, int C, int H, i
 // BlockPad from packed stacks.  (uu, vv) in [-1, e] are coordinates in the
 // block's own grid (e = bs for a high block, bs/2 for a low one); the value
 // is the block's own pixel inside, else the neighbour's pixel in that
-// direction: copied at equal resolution, nearest-upsampled from a low
-// neighbour into a high block, 2x2-averaged from a high neighbour into a low
-// block, zero outside the image or for a neighbour beyond the stack capacity.
-// For NCHW, V must be 1.
-template <typename T, int L, int V>
-__device__ __forceinline__ Vec<T, V> packed_pixel(const T* __restrict__ hi, const T* __restrict__ lo, int C, int bs,
-                                                  const Neigh& nb, int hi_cap, int lo_cap, int uu, int vv, int c) {
+// direction (the diagonal neighbour for a corner): copied at equal
+// resolution, nearest-upsampled from a low neighbour into a high block,
+// 2x2-averaged from a high neighbour into a low block, zero outside the
+// image or for a neighbour beyond its stack's capacity.
+template <typename T, int L>
+__device__ __forceinline__ Src<T> packed_src(const T* __restrict__ hi, const T* __restrict__ lo, int C, int bs,
+                                             const Neigh& nb, int hi_cap, int lo_cap, int uu, int vv, int c) {
     const int own_high = (nb.high >> 4) & 1;
     const int lb = bs >> 1, e = own_high ? bs : lb;
     const int dy = uu < 0 ? -1 : (uu >= e ? 1 : 0);
     const int dx = vv < 0 ? -1 : (vv >= e ? 1 : 0);
     const int d = (dy + 1) * 3 + (dx + 1);
-    if (!((nb.valid >> d) & 1)) return vzero<T, V>();
+    if (!((nb.valid >> d) & 1)) return src_zero<T>();
     const int nhigh = (nb.high >> d) & 1;
-    const int ns = nb.slot[d];
-    if (ns >= (nhigh ? hi_cap : lo_cap)) return vzero<T, V>();
+    int ns = nb.slot[0];  // nb.slot[d] with constant indices, so nb stays in registers
+#pragma unroll
+    for (int i = 1; i < 9; ++i)
+        if (d == i) ns = nb.slot[i];
+    if (ns >= (nhigh ? hi_cap : lo_cap)) return src_zero<T>();
     const int u2 = uu - dy * e, v2 = vv - dx * e;
-    if (nhigh == own_high)
-        return vload<T, V>(stack_at<T, L>(nhigh ? hi : lo, ns, C, e, u2, v2, c));
-    if (own_high)  // low neighbour: nearest upsampling
-        return vload<T, V>(stack_at<T, L>(lo, ns, C, lb, u2 >> 1, v2 >> 1, c));
-    // high neighbour of a low block: average sampling over the 2x2 cell
-    const int r = 2 * u2, s = 2 * v2;
-    const Vec<T, V> a = vload<T, V>(stack_at<T, L>(hi, ns, C, bs, r, s, c));
-    const Vec<T, V> b = vload<T, V>(stack_at<T, L>(hi, ns, C, bs, r, s + 1, c));
-    const Vec<T, V> cc = vload<T, V>(stack_at<T, L>(hi, ns, C, bs, r + 1, s, c));
-    const Vec<T, V> dd = vload<T, V>(stack_at<T, L>(hi, ns, C, bs, r + 1, s + 1, c));
-    return vavg4<T, V>(a, b, cc, dd);
+    if (nhigh == own_high) return src_copy<T>(stack_at<T, L>(nhigh ? hi : lo, ns, C, e, u2, v2, c));
+    if (own_high) return src_copy<T>(stack_at<T, L>(lo, ns, C, lb, u2 >> 1, v2 >> 1, c));
+    const int px = (L == NHWC) ? C : 1;
+    return src_avg<T>(stack_at<T, L>(hi, ns, C, bs, 2 * u2, 2 * v2, c), px, px * bs);
 }
 
 // BlockSample + BlockPad straight from the dense map x (block (n, gy, gx)).
-// High block: the image pixel if its block is high, else the 2x2 average of
-// the image cell containing it (= the low neighbour's value, nearest-
-// upsampled).  Low block: the 2x2 average of the image cell at twice the
-// low-resolution coordinate, whatever the neighbour's resolution (a high
+// High block: the image pixel when the block it lies in is high, else the
+// 2x2 average of the image cell containing it (= the low neighbour's value,
+// nearest-upsampled).  Low block: the 2x2 average of the image cell at twice
+// the low-resolution coordinate, whatever the neighbour's resolution (a high
 // neighbour's 2x2 average and a low neighbour's own value are both that
-// cell's average).  Zero outside the image.  For NCHW, V must be 1.
-template <typename T, int L, int V>
-__device__ __forceinline__ Vec<T, V> dense_pixel(const T* __restrict__ x, int n, int C, int H, int W, int bs,
-                                                 int gy, int gx, const Neigh& nb, int uu, int vv, int c) {
+// cell's average).  Zero outside the image.
+template <typename T, int L>
+__device__ __forceinline__ Src<T> dense_src(const T* __restrict__ x, int n, int C, int H, int W, int bs, int gy,
+                                            int gx, const Neigh& nb, int uu, int vv, int c) {
     const int own_high = (nb.high >> 4) & 1;
+    const int px = (L == NHWC) ? C : 1;
+    const int row = px * W;
     if (own_high) {
         const int Y = gy * bs + uu, X = gx * bs + vv;
-        if (Y < 0 || Y >= H || X < 0 || X >= W) return vzero<T, V>();
+        if (Y < 0 || Y >= H || X < 0 || X >= W) return src_zero<T>();
         const int dy = uu < 0 ? -1 : (uu >= bs ? 1 : 0);
         const int dx = vv < 0 ? -1 : (vv >= bs ? 1 : 0);
         const int d = (dy + 1) * 3 + (dx + 1);
-        if ((nb.high >> d) & 1) return vload<T, V>(map_at<T, L>(x, n, C, H, W, Y, X, c));
-        const int Y0 = Y & ~1, X0 = X & ~1;
-        const Vec<T, V> a = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0, X0, c));
-        const Vec<T, V> b = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0, X0 + 1, c));
-        const Vec<T, V> cc = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0 + 1, X0, c));
-        const Vec<T, V> dd = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0 + 1, X0 + 1, c));
-        return vavg4<T, V>(a, b, cc, dd);
+        if ((nb.high >> d) & 1) return src_copy<T>(map_at<T, L>(x, n, C, H, W, Y, X, c));
+        return src_avg<T>(map_at<T, L>(x, n, C, H, W, Y & ~1, X & ~1, c), px, row);
     }
     const int lb = bs >> 1;
     const int Yl = gy * lb + uu, Xl = gx * lb + vv;
-    if (Yl < 0 || 2 * Yl >= H || Xl < 0 || 2 * Xl >= W) return vzero<T, V>();
-    const int Y0 = 2 * Yl, X0 = 2 * Xl;
-    const Vec<T, V> a = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0, X0, c));
-    const Vec<T, V> b = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0, X0 + 1, c));
-    const Vec<T, V> cc = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0 + 1, X0, c));
-    const Vec<T, V> dd = vload<T, V>(map_at<T, L>(x, n, C, H, W, Y0 + 1, X0 + 1, c));
-    return vavg4<T, V>(a, b, cc, dd);
+    if (Yl < 0 || 2 * Yl >= H || Xl < 0 || 2 * Xl >= W) return src_zero<T>();
+    return src_avg<T>(map_at<T, L>(x, n, C, H, W, 2 * Yl, 2 * Xl, c), px, row);
 }
+
+// A batch of U vectors of V elements: sources first, then every load, then
+// the combination.  Lanes whose item is past the end use a zero source.
+template <typename T, int V, int U>
+struct SrcBatch {
+    Vec<T, V> v[U][4];
+    int mode[U];  // 0 zero, 1 copy, 2 average
+
+    __device__ __forceinline__ void issue(int u, const Src<T>& s) {
+        if (!s.p) {
+            mode[u] = 0;
+        } else if (!s.avg) {
+            mode[u] = 1;
+            v[u][0] = vload<T, V>(s.p);
+        } else {
+            mode[u] = 2;
+            v[u][0] = vload<T, V>(s.p);
+            v[u][1] = vload<T, V>(s.p + s.d1);
+            v[u][2] = vload<T, V>(s.p + s.d2);
+            v[u][3] = vload<T, V>(s.p + s.d2 + s.d1);
+        }
+    }
+    __device__ __forceinline__ Vec<T, V> value(int u) const {
+        if (mode[u] == 0) return vzero<T, V>();
+        if (mode[u] == 1) return v[u][0];
+        return vavg4<T, V>(v[u][0], v[u][1], v[u][2], v[u][3]);
+    }
+};
 
 }  // namespace sb
