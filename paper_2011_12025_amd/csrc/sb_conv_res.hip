@@ -2,29 +2,34 @@
 // channels-last fp16/bf16 layers with up to 64 input channels (the early,
 // bandwidth-bound layers of the network).
 //
-// One workgroup per CU (4 waves) loads its 64-output-channel slice of the
-// weights into LDS once and then walks a static list of tiles.  A tile is a
-// group of R image rows of one block: R rows of a high block, R/2 rows of a
-// low block, so every tile covers the same image area and moves about the
-// same number of bytes.  The padded input tile (all input channels, 128
-// bytes per pixel) is double-buffered in LDS:
+// One 12-wave workgroup per CU keeps its 64-output-channel slice of the
+// weights in LDS and walks a static list of tiles.  A tile is a group of R
+// image rows of one block: R rows of a high block, R/2 rows of a low block,
+// so every tile covers the same image area and moves about the same number of
+// bytes.  The padded input tile (all input channels, 128 bytes per pixel) is
+// double-buffered in LDS, and the waves are specialised:
 //
+//   waves 0-7  (consumers): MFMA over tile j from one buffer, then the
+//              epilogue (bias, residual, ReLU, rounding) stored directly to
+//              global memory;
+//   waves 8-11 (producers): stage tile j+1 into the other buffer.
+//
+// Staging issues every load of the tile before waiting once:
 //   - pixels that are plain copies (interior, same-resolution halo,
 //     nearest-upsampled halo) go straight from global memory to LDS with
-//     global_load_lds_dwordx4 (gfx950), which needs no registers, so a whole
-//     tile is in flight at once;
+//     global_load_lds_dwordx4 (gfx950);
 //   - pixels that are 2x2 averages (a low tile read from the dense map, or a
-//     halo pixel across a resolution boundary) are loaded into registers,
-//     averaged and written to LDS;
+//     halo pixel across a resolution boundary) are loaded into registers
+//     with non-temporal loads, averaged and written to LDS;
 //   - pixels outside the image are written as zeros.
-//
-// The next tile is requested before the current tile's MFMAs start, so its
-// loads overlap the MFMAs and the epilogue stores of the current tile.
+// One barrier per tile hands the buffer from the producers to the consumers.
+// The barrier carries no memory fence, so the consumers' epilogue stores stay
+// in flight while the next tile is computed.
 //
 // MFMA v_mfma_f32_16x16x32_{f16,bf16}: weights are the A operand (16 output
-// channels), pixels the B operand (16 pixels).  Each wave owns up to four
-// 16-pixel sub-tiles and the four 16-channel sub-tiles; a lane's result is
-// 4 consecutive output channels of one pixel, stored directly.
+// channels), pixels the B operand (16 pixels).  Consumer wave w owns the
+// 16-pixel sub-tiles w, w + 8 (of up to 16) and all four 16-channel
+// sub-tiles; a lane's result is 4 consecutive output channels of one pixel.
 //
 // LDS rows (a weight row [tap][co] or a tile pixel) are 128 bytes = 8
 // sub-chunks of 16 bytes; sub-chunk q of row r lives at position q ^ (r & 7)
@@ -61,10 +66,12 @@ constexpr int RROW = 128;         // LDS bytes per row: 64 channels of 16 bits
 constexpr int RSUB = RROW / 16;   // 16-byte sub-chunks per row
 constexpr int RW_BYTES = 9 * RNT * RROW;
 constexpr int RMT = 256;          // most output pixels of one tile
+constexpr int NCW = 8;            // consumer waves
+constexpr int NPW = 4;            // producer waves
+constexpr int RWG = 64 * (NCW + NPW);
+constexpr int PT = 64 * NPW;      // producer threads
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
-
-__device__ __forceinline__ int rswz(int row, int q) { return row * RROW + ((q ^ (row & 7)) << 4); }
 
 // One 16-byte global -> LDS copy per active lane; the wave's 64 lanes fill
 // the 64 consecutive 16-byte slots starting at `window`.
@@ -72,24 +79,24 @@ __device__ __forceinline__ void dma16(const void* g, unsigned char* window) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr)window, 16, 0, 0);
 }
 
-struct RTile {
-    int k, n, gy, gx, high, slot, e, pe, r0, rows, M, in_px;
-    float inv_pe, inv_e;  // exact quotients p / pe, m / e for the tile's small p, m (see res_div)
-};
-
 // q = p / d for 0 <= p < 4096 and 1 <= d <= 128: (p + 0.5) / d in fp32 is at
 // least 0.5 / d away from an integer and its rounding error is below 2^-11,
 // so truncation gives the exact quotient.
 __device__ __forceinline__ int res_div(int p, float inv_d) { return (int)(((float)p + 0.5f) * inv_d); }
 
+struct RTile {
+    int n, gy, gx, high, slot, e, pe, r0, rows, M, in_px;
+    float inv_e;
+};
+
 template <int SRC, int DST, bool ONE>
 __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const WaveMaskT<ONE>& wm, int R, int G,
                                          int tile, RTile& t, Neigh& nb) {
-    t.k = tile / G;
-    const int grp = tile - t.k * G;
+    const int k = tile / G;
+    const int grp = tile - k * G;
     const int per = g.GH * g.GW;
-    t.n = t.k / per;
-    const int rem = t.k - t.n * per;
+    t.n = k / per;
+    const int rem = k - t.n * per;
     t.gy = rem / g.GW;
     t.gx = rem - t.gy * g.GW;
     constexpr bool NEED_SLOTS = !(SRC == SRC_DENSE && DST == DST_DENSE);
@@ -105,24 +112,23 @@ __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const 
     t.M = t.rows * t.e;
     t.pe = t.e + 2;
     t.in_px = (t.rows + 2) * t.pe;
-    t.inv_pe = 1.0f / (float)t.pe;
     t.inv_e = 1.0f / (float)t.e;
     return true;
 }
 
-// Where the value of tile slot (pixel p, channels c..c+7) comes from, as a
-// 32-bit element offset from one of two per-call bases (0: the input map or
-// the high / own stack, 1: the low stack): mode 0 = zero, 1 = copy,
-// 2 = average of the 2x2 cell at off, off + C, off + row, off + row + C.
+// Where the value of tile pixel (u, v) (row u of the padded tile, column v),
+// channels c..c+7, comes from: a 32-bit element offset from one of two
+// per-tile bases (0: the tile's image or the high / own stack, 1: the low
+// stack); mode 0 = zero, 1 = copy, 2 = average of the 2x2 cell at off,
+// off + C, off + row, off + row + C.
 struct RLoc {
     int off, mode, which, row;
 };
 
 template <int SRC>
-__device__ __forceinline__ RLoc res_loc(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t, int p,
-                                        int c) {
+__device__ __forceinline__ RLoc res_loc(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t, int u,
+                                        int v, int c) {
     RLoc L{0, 0, 0, 0};
-    const int u = res_div(p, t.inv_pe), v = p - u * t.pe;
     const int C = a.C_in;
     if constexpr (SRC == SRC_PADDED) {
         L.off = ((t.slot * t.pe + t.r0 + u) * t.pe + v) * C + c;
@@ -182,8 +188,8 @@ __device__ __forceinline__ RLoc res_loc(const Geo& g, const ConvArgs& a, const N
     }
 }
 
-// The two bases of a tile's source offsets (uniform): the image of the
-// tile for the dense map, else the high and the low stack.
+// The two bases of a tile's source offsets (uniform): the tile's image for
+// the dense map, else the high and the low stack.
 template <typename T, int SRC>
 __device__ __forceinline__ void res_bases(const Geo& g, const ConvArgs& a, const RTile& t, const T*& b0,
                                           const T*& b1) {
@@ -196,29 +202,6 @@ __device__ __forceinline__ void res_bases(const Geo& g, const ConvArgs& a, const
     }
 }
 
-// Issues the copy part of a tile (DMA) and writes its zero slots.  Slots
-// whose value is a 2x2 average are left to the average pass.
-template <typename T, int SRC>
-__device__ __forceinline__ void res_stage_copies(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
-                                                 const T* base0, const T* base1, unsigned char* buf, int ptid) {
-    const int lane = lane_id(), pwave = ptid >> 6;
-    const int slots = t.in_px * RSUB;
-    for (int w0 = pwave * 64; w0 < slots; w0 += WG) {
-        const int s = w0 + lane;
-        const int p = s >> 3, q = (s & 7) ^ (p & 7);
-        const int c = q * 8;
-        RLoc L{0, 0, 0, 0};
-        if (s < slots && c < a.C_in) L = res_loc<SRC>(g, a, nb, t, p, c);
-        if (s < slots && L.mode == 1) dma16((L.which ? base1 : base0) + L.off, buf + w0 * 16);
-        if (s < slots && L.mode == 0) *reinterpret_cast<uint4*>(buf + s * 16) = uint4{0u, 0u, 0u, 0u};
-    }
-}
-
-// Average pass: the slots of a tile whose value is a 2x2 average.  For a
-// low tile read from the dense map that is every pixel; otherwise only halo
-// pixels can be averages.  Up to AV items per thread, loaded together.
-constexpr int AV = 4;
-
 // 2x2 average of four raw 16-byte vectors of 8 elements.
 template <typename T>
 __device__ __forceinline__ uint4 avg4_raw(uint4 a, uint4 b, uint4 c, uint4 d) {
@@ -230,26 +213,35 @@ __device__ __forceinline__ uint4 avg4_raw(uint4 a, uint4 b, uint4 c, uint4 d) {
     return vavg4<T, 8>(va, vb, vc, vd).raw;
 }
 
+// Average pass: the slots of a tile whose value is a 2x2 average.  For a
+// low tile read from the dense map that is every pixel; otherwise only halo
+// pixels can be averages.  Up to AV items per producer thread per batch.
+constexpr int AV = 4;
+
 template <typename T, int SRC>
 struct ResAvg {
     uint4 v[AV][4];  // raw loaded data (kept packed until the average is taken)
     int slot[AV];    // LDS slot, -1 = none
 
-    // item -> tile pixel: all pixels, or the halo ring
-    __device__ __forceinline__ static int item_pixel(const RTile& t, bool all, int h) {
-        if (all) return h;
+    // item h -> tile pixel (u, v): every pixel, or the halo ring
+    __device__ __forceinline__ static bool item_pixel(const RTile& t, bool all, int h, int& u, int& v) {
+        if (all) {
+            u = res_div(h, 1.0f / (float)t.pe);
+            v = h - u * t.pe;
+            return true;
+        }
         const int side = t.rows + 2;
-        if (h < side) return h * t.pe;                      // left column
+        if (h < side) { u = h; v = 0; return true; }                  // left column
         h -= side;
-        if (h < side) return h * t.pe + t.pe - 1;           // right column
+        if (h < side) { u = h; v = t.pe - 1; return true; }           // right column
         h -= side;
-        if (h < t.e) return t.r0 == 0 ? 1 + h : -1;         // top row
+        if (h < t.e) { u = 0; v = 1 + h; return t.r0 == 0; }          // top row
         h -= t.e;
-        return (t.r0 + t.rows == t.e) ? (t.rows + 1) * t.pe + 1 + h : -1;  // bottom row
+        u = t.rows + 1;                                               // bottom row
+        v = 1 + h;
+        return t.r0 + t.rows == t.e;
     }
-    __device__ __forceinline__ static bool all_avg(const RTile& t) {
-        return SRC == SRC_DENSE && !t.high;
-    }
+    __device__ __forceinline__ static bool all_avg(const RTile& t) { return SRC == SRC_DENSE && !t.high; }
     __device__ __forceinline__ static int n_items(const RTile& t) {
         if constexpr (SRC == SRC_PADDED) return 0;
         if constexpr (SRC == SRC_PACKED) {
@@ -263,21 +255,22 @@ struct ResAvg {
         const bool all = all_avg(t);
         const int items = n_items(t);
 #pragma unroll
-        for (int u = 0; u < AV; ++u) {
-            slot[u] = -1;
-            const int it = base + u * WG + ptid;
-            if (it < items) {
+        for (int i = 0; i < AV; ++i) {
+            slot[i] = -1;
+            const int it = base + i * PT + ptid;
+            int u, w;
+            if (it < items && item_pixel(t, all, it >> 3, u, w)) {
                 const int q = it & 7;
-                const int p = item_pixel(t, all, it >> 3);
-                if (p >= 0 && q * 8 < a.C_in) {
-                    const RLoc L = res_loc<SRC>(g, a, nb, t, p, q * 8);
+                if (q * 8 < a.C_in) {
+                    const RLoc L = res_loc<SRC>(g, a, nb, t, u, w, q * 8);
                     if (L.mode == 2) {
                         const T* p0 = (L.which ? base1 : base0) + L.off;
-                        slot[u] = p * RSUB + (q ^ (p & 7));
-                        v[u][0] = ld_nt16(p0);
-                        v[u][1] = ld_nt16(p0 + a.C_in);
-                        v[u][2] = ld_nt16(p0 + L.row);
-                        v[u][3] = ld_nt16(p0 + L.row + a.C_in);
+                        const int p = u * t.pe + w;
+                        slot[i] = p * RSUB + (q ^ (p & 7));
+                        v[i][0] = ld_nt16(p0);
+                        v[i][1] = ld_nt16(p0 + a.C_in);
+                        v[i][2] = ld_nt16(p0 + L.row);
+                        v[i][3] = ld_nt16(p0 + L.row + a.C_in);
                     }
                 }
             }
@@ -285,28 +278,62 @@ struct ResAvg {
     }
     __device__ __forceinline__ void commit(unsigned char* buf) const {
 #pragma unroll
-        for (int u = 0; u < AV; ++u)
-            if (slot[u] >= 0)
-                *reinterpret_cast<uint4*>(buf + slot[u] * 16) = avg4_raw<T>(v[u][0], v[u][1], v[u][2], v[u][3]);
+        for (int i = 0; i < AV; ++i)
+            if (slot[i] >= 0)
+                *reinterpret_cast<uint4*>(buf + slot[i] * 16) = avg4_raw<T>(v[i][0], v[i][1], v[i][2], v[i][3]);
     }
 };
 
-// MFMA over one tile and its epilogue, for a wave owning NMS 16-pixel
-// sub-tiles (pixels (wave + 4 ms) * 16 + l16) and NKS 32-channel K-steps per
-// tap.  Fully unrolled; the fragments of the next K-step are read from LDS
-// while the MFMAs of the current one run.
+// Stages tile t completely into `buf` (producer waves, ptid = 0..PT-1):
+// every copy by DMA, every zero slot, and the first batch of averages are
+// issued before a single wait; returns with every write to `buf` complete.
+template <typename T, int SRC>
+__device__ __forceinline__ void res_stage(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
+                                          unsigned char* buf, int ptid) {
+    const T *b0, *b1;
+    res_bases<T, SRC>(g, a, t, b0, b1);
+    const int lane = lane_id(), pwave = ptid >> 6;
+    const int nwin = (t.in_px * RSUB + 63) >> 6;  // 64-slot windows = 8 pixels each
+    for (int w = pwave; w < nwin; w += NPW) {
+        const int pw = w * 8;                       // first pixel of the window (uniform)
+        const int u0 = pw / t.pe, v0 = pw - u0 * t.pe;
+        int u = u0, v = v0 + (lane >> 3);
+        if (v >= t.pe) {                            // a window spans at most two rows (pe >= 10)
+            v -= t.pe;
+            ++u;
+        }
+        const int p = pw + (lane >> 3);
+        const int q = (lane & 7) ^ (lane >> 3);     // p & 7 == lane >> 3 inside a window
+        RLoc L{0, 0, 0, 0};
+        const bool in = p < t.in_px;
+        if (in && q * 8 < a.C_in) L = res_loc<SRC>(g, a, nb, t, u, v, q * 8);
+        if (in && L.mode == 1) dma16((L.which ? b1 : b0) + L.off, buf + w * 1024);
+        if (in && L.mode == 0) *reinterpret_cast<uint4*>(buf + w * 1024 + lane * 16) = uint4{0u, 0u, 0u, 0u};
+    }
+    const int navg = ResAvg<T, SRC>::n_items(t);
+    for (int base = 0; base < navg; base += PT * AV) {
+        ResAvg<T, SRC> av;
+        av.issue(g, a, nb, t, b0, b1, base, ptid);
+        av.commit(buf);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // DMA (vmcnt) and LDS writes (lgkmcnt) done
+}
+
+// MFMA over one tile and its epilogue, for a consumer wave cw owning NMS
+// 16-pixel sub-tiles (pixels (cw + NCW * ms) * 16 + l16) and NKS 32-channel
+// K-steps per tap.  Fully unrolled; the fragments of the next K-step are
+// read from LDS while the MFMAs of the current one run.
 template <typename T, int DST, int NMS, int NKS>
-__device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, const RTile& t,
+__device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, const RTile& t, int cw,
                                             const unsigned char* s_w, const unsigned char* buf,
                                             const float (&bv)[4][4], int co0, int vec_out, bool relu) {
     typedef MFR<T> mf;
     typedef typename mf::frag frag;
     const int lane = lane_id(), l16 = lane & 15, kg = lane >> 4;
-    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     int pbase[NMS];
 #pragma unroll
     for (int ms = 0; ms < NMS; ++ms) {
-        const int m = min((wave + 4 * ms) * 16 + l16, t.M - 1);
+        const int m = min((cw + NCW * ms) * 16 + l16, t.M - 1);
         const int mi = res_div(m, t.inv_e);
         pbase[ms] = mi * t.pe + (m - mi * t.e);
     }
@@ -321,12 +348,13 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
 #pragma unroll
         for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    constexpr int S = 9 * NKS;
+    constexpr int S = 9 * NKS;  // K-steps (even: 18, or 9 with one odd step left)
     frag wf[2][4], pf[2][NMS];
     auto load = [&](int step, int b) {
-        const int tap = step / NKS, ks = step - tap * NKS;
+        const int tap = NKS == 2 ? (step >> 1) : step, ks = NKS == 2 ? (step & 1) : 0;
+        const int ky = tap >= 6 ? 2 : (tap >= 3 ? 1 : 0);
+        const int toff = ky * t.pe + (tap - 3 * ky);
         const int q = ks * 4 + kg;
-        const int toff = (tap / 3) * t.pe + (tap % 3);
 #pragma unroll
         for (int ns = 0; ns < 4; ++ns)
             wf[b][ns] = *reinterpret_cast<const frag*>(s_w + wbase[ks] + (tap * RNT + ns * 16) * RROW);
@@ -336,17 +364,23 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
             pf[b][ms] = *reinterpret_cast<const frag*>(buf + r * RROW + ((q ^ (r & 7)) << 4));
         }
     };
-    load(0, 0);
-#pragma unroll
-    for (int step = 0; step < S; ++step) {
-        if (step + 1 < S) load(step + 1, (step + 1) & 1);
+    auto mma = [&](int b) {
 #pragma unroll
         for (int ms = 0; ms < NMS; ++ms)
 #pragma unroll
-            for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = mf::mma(wf[step & 1][ns], pf[step & 1][ms], acc[ms][ns]);
+            for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = mf::mma(wf[b][ns], pf[b][ms], acc[ms][ns]);
+    };
+    load(0, 0);
+#pragma unroll 1
+    for (int step = 0; step + 1 < S; step += 2) {
+        load(step + 1, 1);
+        mma(0);
+        if (step + 2 < S) load(step + 2, 0);
+        mma(1);
     }
+    if (S & 1) mma(0);
 
-    // -- epilogue: channels co0 + ns*16 + kg*4 + {0..3} of pixel (wave + 4*ms)*16 + l16
+    // -- epilogue: channels co0 + ns*16 + kg*4 + {0..3} of pixel (cw + NCW*ms)*16 + l16
     const int Co = a.C_out;
     T* obase;  // the tile's block in its output stack, or the tile's image
     const T* rbase = nullptr;
@@ -360,7 +394,7 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
     }
 #pragma unroll
     for (int ms = 0; ms < NMS; ++ms) {
-        const int m = (wave + 4 * ms) * 16 + l16;
+        const int m = (cw + NCW * ms) * 16 + l16;
         if (m >= t.M) continue;
         const int mi = res_div(m, t.inv_e);
         const int i = t.r0 + mi, j = m - mi * t.e;
@@ -400,8 +434,7 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
                 for (int dx = 0; dx < reps; ++dx) {
                     T* q = obase + off + dy * down + dx * Co + co;
                     if (full) {
-                        if constexpr (sizeof(T) == 2) st_nt8(q, o.raw);
-                        else vstore<T, 4>(q, o);
+                        st_nt8(q, o.raw);
                     } else {
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
@@ -410,23 +443,6 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
                 }
         }
     }
-}
-
-// Stages tile t completely into `buf`: copies by DMA, zeros, then the 2x2
-// averages; returns with every write to `buf` complete.  Producer waves only
-// (ptid = 0..255).
-template <typename T, int SRC>
-__device__ __forceinline__ void res_stage(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
-                                          unsigned char* buf, int ptid) {
-    const T *b0, *b1;
-    res_bases<T, SRC>(g, a, t, b0, b1);
-    res_stage_copies<T, SRC>(g, a, nb, t, b0, b1, buf, ptid);
-    for (int base = 0; base < ResAvg<T, SRC>::n_items(t); base += WG * AV) {
-        ResAvg<T, SRC> av;
-        av.issue(g, a, nb, t, b0, b1, base, ptid);
-        av.commit(buf);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // DMA (vmcnt) and LDS writes (lgkmcnt) done
 }
 
 // Workgroup barrier without the memory fences of __syncthreads: consumer
@@ -438,34 +454,23 @@ __device__ __forceinline__ void res_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// 8 waves: waves 0-3 compute (MFMA + epilogue) tile j from buffer j & 1 while
-// waves 4-7 stage tile j + 1 into the other buffer; one barrier per tile.
-template <typename T, int SRC, int DST, bool ONE>
-__global__ __launch_bounds__(2 * WG, 2) void k_conv_res(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int R,
-                                                        int G, int ntiles, int buf_bytes, int vec_out) {
+template <typename T, int SRC, int DST, bool ONE, int NKS>
+__global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int R,
+                                                     int G, int ntiles, int buf_bytes, int vec_out) {
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* s_w = smem;
     unsigned char* s_buf0 = smem + RW_BYTES;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-    const bool producer = wave >= 4;
-    const int ptid = (int)threadIdx.x - WG;
+    const bool producer = wave >= NCW;
+    const int ptid = (int)threadIdx.x - 64 * NCW;
     const int lane = lane_id(), kg = lane >> 4;
     const int co0 = blockIdx.y * RNT;
 
-    WaveMaskT<ONE> wm;
-    wm.init(mask, (int)g.B);
-
-    // the tile sequence of this workgroup (every wave walks it identically)
-    int tile = blockIdx.x;
-    RTile t;
-    Neigh nb;
-    bool have = false;
-    while (tile < ntiles && !(have = res_tile<SRC, DST, ONE>(g, a, wm, R, G, tile, t, nb))) tile += gridDim.x;
-
     if (producer) {
-        // weights of this workgroup's output channels: rows [tap][co], 64 channels each
+        // weights of this workgroup's output channels first (they do not depend on the
+        // mask): rows [tap][co], 64 channels each
         const T* __restrict__ wgt = (const T*)a.weight;
-        for (int w0 = (wave - 4) * 64; w0 < 9 * RNT * RSUB; w0 += WG) {
+        for (int w0 = (wave - NCW) * 64; w0 < 9 * RNT * RSUB; w0 += PT) {
             const int s = w0 + lane;
             const int row = s >> 3, q = (s & 7) ^ (row & 7);
             const int tap = row / RNT, col = row - tap * RNT;
@@ -473,10 +478,10 @@ __global__ __launch_bounds__(2 * WG, 2) void k_conv_res(Geo g, const uint8_t* __
             if (co < a.C_out && ci < a.C_in) dma16(wgt + ((size_t)co * 9 + tap) * a.C_in + ci, s_w + w0 * 16);
             else *reinterpret_cast<uint4*>(s_w + s * 16) = uint4{0u, 0u, 0u, 0u};
         }
-        if (have) res_stage<T, SRC>(g, a, nb, t, s_buf0, ptid);
-        __builtin_amdgcn_s_waitcnt(0);
     }
-    res_barrier();
+
+    WaveMaskT<ONE> wm;
+    wm.init(mask, (int)g.B);
 
     const T* __restrict__ bias = (const T*)a.bias;
     const bool relu = (a.flags & 1) != 0;
@@ -489,40 +494,35 @@ __global__ __launch_bounds__(2 * WG, 2) void k_conv_res(Geo g, const uint8_t* __
             bv[ns][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
         }
 
-    int cur = 0;
-    while (have) {
-        unsigned char* buf = s_buf0 + cur * buf_bytes;
-        unsigned char* nbuf = s_buf0 + (cur ^ 1) * buf_bytes;
-        int ntile = tile + gridDim.x;
+    // Step i: the producers stage tile i of this workgroup's sequence into buffer i & 1
+    // while the consumers compute tile i - 1 from the other buffer.  Every wave walks
+    // the sequence identically, so all of them leave the loop together.
+    int tile = blockIdx.x;
+    RTile t;            // the tile the consumers compute in this step
+    bool have = false;  // ... if any
+    for (int it = 0;; ++it) {
         RTile t2;
         Neigh nb2;
         bool have2 = false;
-        while (ntile < ntiles && !(have2 = res_tile<SRC, DST, ONE>(g, a, wm, R, G, ntile, t2, nb2)))
-            ntile += gridDim.x;
+        while (tile < ntiles && !(have2 = res_tile<SRC, DST, ONE>(g, a, wm, R, G, tile, t2, nb2))) tile += gridDim.x;
+        tile += gridDim.x;
+        if (!have && !have2) break;
+        unsigned char* sbuf = s_buf0 + (it & 1) * buf_bytes;
+        unsigned char* cbuf = s_buf0 + ((it & 1) ^ 1) * buf_bytes;
         if (producer) {
-            if (have2) res_stage<T, SRC>(g, a, nb2, t2, nbuf, ptid);
-        } else {
+            // the staging wait also covers the weight copies of the first step
+            if (have2) res_stage<T, SRC>(g, a, nb2, t2, sbuf, ptid);
+            __builtin_amdgcn_s_waitcnt(0);
+        } else if (have) {
             const int nst = (t.M + 15) >> 4;
-            const int nms = nst > wave ? min(4, (nst - wave + 3) >> 2) : 0;
-            if (a.C_in > 32) {
-                if (nms == 4) res_compute<T, DST, 4, 2>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 3) res_compute<T, DST, 3, 2>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 2) res_compute<T, DST, 2, 2>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 1) res_compute<T, DST, 1, 2>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-            } else {
-                if (nms == 4) res_compute<T, DST, 4, 1>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 3) res_compute<T, DST, 3, 1>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 2) res_compute<T, DST, 2, 1>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-                else if (nms == 1) res_compute<T, DST, 1, 1>(g, a, t, s_w, buf, bv, co0, vec_out, relu);
-            }
+            const int nms = nst > wave ? min(2, (nst - wave + NCW - 1) / NCW) : 0;
+            if (nms == 2) res_compute<T, DST, 2, NKS>(g, a, t, wave, s_w, cbuf, bv, co0, vec_out, relu);
+            else if (nms == 1) res_compute<T, DST, 1, NKS>(g, a, t, wave, s_w, cbuf, bv, co0, vec_out, relu);
             __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this tile's LDS reads are done
         }
         res_barrier();
-        have = have2;
         t = t2;
-        nb = nb2;
-        tile = ntile;
-        cur ^= 1;
+        have = have2;
     }
 }
 
@@ -539,7 +539,7 @@ int cu_count() {
 
 inline bool aligned_to(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; }
 
-template <typename T, int SRC, int DST, bool ONE>
+template <typename T, int SRC, int DST, bool ONE, int NKS>
 hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, hipStream_t st) {
     const int G = (g.bs + R - 1) / R;
     const long long ntiles = g.B * G;
@@ -552,15 +552,15 @@ hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, 
                         aligned_to(a.res_hi, ob) && aligned_to(a.res_lo, ob);
     static int attr_bytes = 0;
     if (smem > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_conv_res<T, SRC, DST, ONE>,
+        hipError_t e = hipFuncSetAttribute((const void*)k_conv_res<T, SRC, DST, ONE, NKS>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return e;
         attr_bytes = smem;
     }
     const int nwg = (int)(ntiles < cu_count() ? ntiles : cu_count());
     const dim3 grid((unsigned)nwg, (unsigned)((a.C_out + RNT - 1) / RNT));
-    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE>), grid, dim3(2 * WG), smem, st, g, mask, a, R, G, (int)ntiles, buf_bytes,
-                       vec_out);
+    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, G, (int)ntiles,
+                       buf_bytes, vec_out);
     return hipGetLastError();
 }
 
@@ -577,13 +577,19 @@ int res_rows(int bs) {
     return best;
 }
 
+template <typename T, bool ONE, int NKS>
+hipError_t res_k(ConvSrc src, const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, hipStream_t st) {
+    if (src == SRC_PADDED) return run_res<T, SRC_PADDED, DST_PACKED, ONE, NKS>(g, mask, a, R, st);
+    if (src == SRC_PACKED) return run_res<T, SRC_PACKED, DST_PACKED, ONE, NKS>(g, mask, a, R, st);
+    return run_res<T, SRC_DENSE, DST_DENSE, ONE, NKS>(g, mask, a, R, st);
+}
+
 template <typename T, bool ONE>
 hipError_t res_t(ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask, const ConvArgs& a, int R,
                  hipStream_t st) {
-    if (src == SRC_PADDED) return run_res<T, SRC_PADDED, DST_PACKED, ONE>(g, mask, a, R, st);
-    if (src == SRC_PACKED) return run_res<T, SRC_PACKED, DST_PACKED, ONE>(g, mask, a, R, st);
     (void)dst;
-    return run_res<T, SRC_DENSE, DST_DENSE, ONE>(g, mask, a, R, st);
+    if (a.C_in > 32) return res_k<T, ONE, 2>(src, g, mask, a, R, st);
+    return res_k<T, ONE, 1>(src, g, mask, a, R, st);
 }
 
 }  // namespace
@@ -604,7 +610,8 @@ hipError_t launch_conv_res(int dtype, ConvSrc src, ConvDst dst, const Geo& g, co
                            hipStream_t st) {
     const int R = res_rows(g.bs);
     const bool one = g.B <= 1024;
-    if (dtype == 1) return one ? res_t<f16, true>(src, dst, g, mask, a, R, st) : res_t<f16, false>(src, dst, g, mask, a, R, st);
+    if (dtype == 1)
+        return one ? res_t<f16, true>(src, dst, g, mask, a, R, st) : res_t<f16, false>(src, dst, g, mask, a, R, st);
     return one ? res_t<bf16, true>(src, dst, g, mask, a, R, st) : res_t<bf16, false>(src, dst, g, mask, a, R, st);
 }
 
