@@ -1,40 +1,49 @@
-// Persistent 3x3 block convolution with LDS-resident weights, for the
-// channels-last fp16/bf16 layers with up to 64 input channels (the early,
-// bandwidth-bound layers of the network).
+// Persistent 3x3 block convolution with register-resident weights, for the
+// channels-last fp16/bf16 layers with up to 64 input channels and block sides
+// 32 or 64 (the early, bandwidth-bound layers of the network).
 //
-// One 12-wave workgroup per CU keeps its 64-output-channel slice of the
-// weights in LDS and walks a static list of tiles.  A tile is a group of R
-// image rows of one block: R rows of a high block, R/2 rows of a low block,
-// so every tile covers the same image area and moves about the same number of
-// bytes.  The padded input tile (all input channels, 128 bytes per pixel) is
-// double-buffered in LDS, and the waves are specialised:
+// One 8-wave workgroup per CU computes a 64-output-channel slice and walks a
+// static list of tiles.  A tile is a group of image rows of one block: R rows
+// of a high block or R/2 rows of a low block (R = 8 for blocks of 32, 4 for
+// blocks of 64), so every tile covers the same image area.  The padded input
+// tile (all input channels, 128 bytes per pixel) is triple-buffered in LDS
+// and the waves are specialised:
 //
-//   waves 0-7  (consumers): MFMA over tile j from one buffer, then the
-//              epilogue (bias, residual, ReLU, rounding) stored directly to
-//              global memory;
-//   waves 8-11 (producers): stage tile j+1 into the other buffer.
+//   waves 0-3  (consumers): wave c owns output channels co0 + 32 * (c & 1)
+//              + [0, 32) and half (c >> 1) of the tile; its 32 x 9 x C_in
+//              weights live in its registers for the whole launch;
+//   waves 4-7  (producers): finish staging tile i (wait for its copies,
+//              write its 2x2 averages), then issue the copies of tile i + 1,
+//              while the consumers compute tile i - 1.
 //
-// Staging issues every load of the tile before waiting once:
+// Staging:
 //   - pixels that are plain copies (interior, same-resolution halo,
 //     nearest-upsampled halo) go straight from global memory to LDS with
-//     global_load_lds_dwordx4 (gfx950);
+//     global_load_lds_dwordx4 (gfx950), issued one step before they are
+//     needed;
 //   - pixels that are 2x2 averages (a low tile read from the dense map, or a
-//     halo pixel across a resolution boundary) are loaded into registers
-//     with non-temporal loads, averaged and written to LDS;
+//     halo pixel across a resolution boundary) are loaded into registers,
+//     averaged a step later and written to LDS;
 //   - pixels outside the image are written as zeros.
-// One barrier per tile hands the buffer from the producers to the consumers.
-// The barrier carries no memory fence, so the consumers' epilogue stores stay
-// in flight while the next tile is computed.
+// One barrier per step hands the buffers over.  It carries no memory fence,
+// so the consumers' epilogue stores stay in flight while the next tile is
+// computed.
 //
 // MFMA v_mfma_f32_16x16x32_{f16,bf16}: weights are the A operand (16 output
-// channels), pixels the B operand (16 pixels).  Consumer wave w owns the
-// 16-pixel sub-tiles w, w + 8 (of up to 16) and all four 16-channel
-// sub-tiles; a lane's result is 4 consecutive output channels of one pixel.
+// channels), pixels the B operand (16 consecutive pixels of one tile row).
+// One B fragment of input row r serves output rows r, r - 1 and r - 2 (taps
+// ky = 0, 1, 2), so a wave reads each input row once per kx and K-step.
+// The 16 A rows of channel block j are channels kg * 8 + j * 4 + {0..3} of
+// the wave's 32 (kg = row / 4): a lane's results are 8 consecutive channels
+// of one pixel, and one store instruction writes 64 contiguous bytes of each
+// of 16 pixels.
 //
 // LDS rows (a weight row [tap][co] or a tile pixel) are 128 bytes = 8
-// sub-chunks of 16 bytes; sub-chunk q of row r lives at position q ^ (r & 7)
-// so that 8 consecutive rows read at one sub-chunk hit 8 distinct 16-byte
-// bank groups.
+// sub-chunks of 16 bytes.  Sub-chunk q of weight row r lives at position
+// q ^ (r & 7); sub-chunk q of the tile pixel in column v lives at position
+// q ^ ((v >> 1) & 7), so the 16 pixels of an MFMA operand read at one
+// sub-chunk hit all 64 banks once, and a pixel's position does not depend on
+// its row.
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -64,12 +73,12 @@ template <> struct MFR<bf16> {
 constexpr int RNT = 64;           // output channels per workgroup
 constexpr int RROW = 128;         // LDS bytes per row: 64 channels of 16 bits
 constexpr int RSUB = RROW / 16;   // 16-byte sub-chunks per row
-constexpr int RW_BYTES = 9 * RNT * RROW;
-constexpr int RMT = 256;          // most output pixels of one tile
-constexpr int NCW = 8;            // consumer waves
+constexpr int RW_BYTES = 9 * RNT * RROW;  // the weight slice of a workgroup, staged once
+constexpr int NCW = 4;            // consumer waves
 constexpr int NPW = 4;            // producer waves
 constexpr int RWG = 64 * (NCW + NPW);
 constexpr int PT = 64 * NPW;      // producer threads
+constexpr int NBUF = 3;           // tile buffers
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -85,8 +94,8 @@ __device__ __forceinline__ void dma16(const void* g, unsigned char* window) {
 __device__ __forceinline__ int res_div(int p, float inv_d) { return (int)(((float)p + 0.5f) * inv_d); }
 
 struct RTile {
-    int n, gy, gx, high, slot, e, pe, r0, rows, M, in_px;
-    float inv_e;
+    int n, gy, gx, high, slot, e, pe, r0, rows, in_px;
+    float inv_pe;
 };
 
 template <int SRC, int DST, bool ONE>
@@ -109,10 +118,9 @@ __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const 
     t.r0 = grp * rr;
     if (t.r0 >= t.e) return false;
     t.rows = min(rr, t.e - t.r0);
-    t.M = t.rows * t.e;
     t.pe = t.e + 2;
     t.in_px = (t.rows + 2) * t.pe;
-    t.inv_e = 1.0f / (float)t.e;
+    t.inv_pe = 1.0f / (float)t.pe;
     return true;
 }
 
@@ -213,61 +221,143 @@ __device__ __forceinline__ uint4 avg4_raw(uint4 a, uint4 b, uint4 c, uint4 d) {
     return vavg4<T, 8>(va, vb, vc, vd).raw;
 }
 
-// Average pass: the slots of a tile whose value is a 2x2 average.  For a
-// low tile read from the dense map that is every pixel; otherwise only halo
-// pixels can be averages.  Up to AV items per producer thread per batch.
-constexpr int AV = 4;
+// LDS slot (16-byte unit) of sub-chunk q of tile pixel (u, v): position
+// q ^ ((v >> 1) & 7) inside the pixel's 128 bytes.  The 16 consecutive pixels
+// of an MFMA operand then hit 16 distinct (parity of v, position) pairs, i.e.
+// all 64 banks once, whatever the row.
+__device__ __forceinline__ int tile_pos(int v, int q) { return q ^ ((v >> 1) & 7); }
+__device__ __forceinline__ int tile_slot(int u, int v, int pe, int q) { return (u * pe + v) * RSUB + tile_pos(v, q); }
+
+// How the interior (columns 1..e) of padded tile row u is filled: zeros,
+// a contiguous copy of e pixels, a nearest upsampling of e/2 pixels (each
+// used twice), or per-pixel items (2x2 averages) of the register path.
+enum RowKind { ROW_ZERO = 0, ROW_COPY = 1, ROW_NEAR = 2, ROW_ITEMS = 3 };
+struct RowSrc {
+    int kind, which, off;  // which: base 0 or 1; off: element offset of the row's first interior pixel
+};
+
+template <int SRC>
+__device__ __forceinline__ RowSrc row_src(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t, int u) {
+    RowSrc S{ROW_ITEMS, 0, 0};
+    const int C = a.C_in;
+    if constexpr (SRC == SRC_PADDED) {
+        S.kind = ROW_COPY;
+        S.which = t.high ? 0 : 1;
+        S.off = ((t.slot * t.pe + t.r0 + u) * t.pe + 1) * C;
+        return S;
+    }
+    const int r = t.r0 + u - 1;  // block-local row
+    const int dy = r < 0 ? 0 : (r >= t.e ? 2 : 1);
+    const int d = dy * 3 + 1;    // the block above, the block itself, or the block below
+    if constexpr (SRC == SRC_DENSE) {
+        if (!t.high) return S;   // every pixel of a low tile is a 2x2 average
+        const int Y = t.gy * g.bs + r;
+        if ((unsigned)Y >= (unsigned)g.H) {
+            S.kind = ROW_ZERO;
+            return S;
+        }
+        if (!((nb.high >> d) & 1)) return S;  // a low neighbour row: averages
+        S.kind = ROW_COPY;
+        S.off = (Y * g.W + t.gx * g.bs) * C;
+        return S;
+    } else {
+        if (!((nb.valid >> d) & 1)) {
+            S.kind = ROW_ZERO;
+            return S;
+        }
+        const int nhigh = (nb.high >> d) & 1;
+        const int ns = dy == 0 ? nb.slot[1] : (dy == 1 ? nb.slot[4] : nb.slot[7]);
+        if (ns >= (nhigh ? a.hi_cap : a.lo_cap)) {
+            S.kind = ROW_ZERO;
+            return S;
+        }
+        const int u2 = r - (dy - 1) * t.e;  // row inside that block
+        if (nhigh == t.high) {
+            S.kind = ROW_COPY;
+            S.which = nhigh ? 0 : 1;
+            S.off = (ns * t.e + u2) * t.e * C;
+        } else if (t.high) {                // low neighbour of a high block: nearest upsampling
+            const int lb = g.bs >> 1;
+            S.kind = ROW_NEAR;
+            S.which = 1;
+            S.off = (ns * lb + (u2 >> 1)) * lb * C;
+        }                                   // else a high neighbour of a low block: averages
+        return S;
+    }
+}
+
+// The register path of staging: every pixel of the two halo columns, and
+// every interior pixel of the rows filled by items (all rows of a low tile
+// read from the dense map; otherwise at most the top and the bottom row).
+// An item is one 16-byte sub-chunk: zero, one load, or four loads averaged.
+// Up to AV items per producer thread per batch; a batch's loads are issued
+// in one step and written to LDS in the next.
+constexpr int AV = 5;
 
 template <typename T, int SRC>
 struct ResAvg {
-    uint4 v[AV][4];  // raw loaded data (kept packed until the average is taken)
+    uint4 v[AV][4];  // raw loaded data (kept packed until the value is formed)
     int slot[AV];    // LDS slot, -1 = none
+    int kind[AV];    // 0 zero, 1 copy, 2 average
 
-    // item h -> tile pixel (u, v): every pixel, or the halo ring
-    __device__ __forceinline__ static bool item_pixel(const RTile& t, bool all, int h, int& u, int& v) {
-        if (all) {
-            u = res_div(h, 1.0f / (float)t.pe);
-            v = h - u * t.pe;
-            return true;
+    struct Plan {
+        bool all;     // every pixel of the tile
+        int top, bot; // 1 if row 0 / row rows+1 is filled by items
+        int n;        // items
+    };
+    __device__ __forceinline__ static Plan plan(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t) {
+        Plan P{false, 0, 0, 0};
+        if (SRC == SRC_DENSE && !t.high) {
+            P.all = true;
+            P.n = t.in_px * RSUB;
+            return P;
         }
-        const int side = t.rows + 2;
-        if (h < side) { u = h; v = 0; return true; }                  // left column
-        h -= side;
-        if (h < side) { u = h; v = t.pe - 1; return true; }           // right column
-        h -= side;
-        if (h < t.e) { u = 0; v = 1 + h; return t.r0 == 0; }          // top row
-        h -= t.e;
-        u = t.rows + 1;                                               // bottom row
-        v = 1 + h;
-        return t.r0 + t.rows == t.e;
+        P.top = row_src<SRC>(g, a, nb, t, 0).kind == ROW_ITEMS;
+        P.bot = row_src<SRC>(g, a, nb, t, t.rows + 1).kind == ROW_ITEMS;
+        P.n = (2 * (t.rows + 2) + t.e * (P.top + P.bot)) * RSUB;
+        return P;
     }
-    __device__ __forceinline__ static bool all_avg(const RTile& t) { return SRC == SRC_DENSE && !t.high; }
-    __device__ __forceinline__ static int n_items(const RTile& t) {
-        if constexpr (SRC == SRC_PADDED) return 0;
-        if constexpr (SRC == SRC_PACKED) {
-            if (t.high) return 0;
+    // item pixel h -> tile pixel (u, v)
+    __device__ __forceinline__ static void item_pixel(const RTile& t, const Plan& P, int h, int& u, int& v) {
+        if (P.all) {
+            u = res_div(h, t.inv_pe);
+            v = h - u * t.pe;
+            return;
         }
-        const int pix = all_avg(t) ? t.in_px : 2 * (t.rows + 2) + 2 * t.e;
-        return pix * RSUB;
+        const int ring = 2 * (t.rows + 2);
+        if (h < ring) {
+            u = h >> 1;
+            v = (h & 1) ? t.pe - 1 : 0;
+            return;
+        }
+        h -= ring;
+        const bool top = P.top && h < t.e;
+        if (!top && P.top) h -= t.e;
+        u = top ? 0 : t.rows + 1;
+        v = 1 + h;
+    }
+    __device__ __forceinline__ void clear() {
+#pragma unroll
+        for (int i = 0; i < AV; ++i) slot[i] = -1;
     }
     __device__ __forceinline__ void issue(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
-                                          const T* base0, const T* base1, int base, int ptid) {
-        const bool all = all_avg(t);
-        const int items = n_items(t);
+                                          const Plan& P, const T* base0, const T* base1, int base, int ptid) {
 #pragma unroll
         for (int i = 0; i < AV; ++i) {
             slot[i] = -1;
+            kind[i] = 0;
             const int it = base + i * PT + ptid;
-            int u, w;
-            if (it < items && item_pixel(t, all, it >> 3, u, w)) {
+            if (it < P.n) {
+                int u, w;
+                item_pixel(t, P, it >> 3, u, w);
                 const int q = it & 7;
+                slot[i] = tile_slot(u, w, t.pe, q);
                 if (q * 8 < a.C_in) {
                     const RLoc L = res_loc<SRC>(g, a, nb, t, u, w, q * 8);
+                    const T* p0 = (L.which ? base1 : base0) + L.off;
+                    kind[i] = L.mode;
+                    if (L.mode >= 1) v[i][0] = ld_nt16(p0);
                     if (L.mode == 2) {
-                        const T* p0 = (L.which ? base1 : base0) + L.off;
-                        const int p = u * t.pe + w;
-                        slot[i] = p * RSUB + (q ^ (p & 7));
-                        v[i][0] = ld_nt16(p0);
                         v[i][1] = ld_nt16(p0 + a.C_in);
                         v[i][2] = ld_nt16(p0 + L.row);
                         v[i][3] = ld_nt16(p0 + L.row + a.C_in);
@@ -279,113 +369,136 @@ struct ResAvg {
     __device__ __forceinline__ void commit(unsigned char* buf) const {
 #pragma unroll
         for (int i = 0; i < AV; ++i)
-            if (slot[i] >= 0)
-                *reinterpret_cast<uint4*>(buf + slot[i] * 16) = avg4_raw<T>(v[i][0], v[i][1], v[i][2], v[i][3]);
+            if (slot[i] >= 0) {
+                uint4 val = uint4{0u, 0u, 0u, 0u};
+                if (kind[i] == 1) val = v[i][0];
+                else if (kind[i] == 2) val = avg4_raw<T>(v[i][0], v[i][1], v[i][2], v[i][3]);
+                *reinterpret_cast<uint4*>(buf + slot[i] * 16) = val;
+            }
     }
 };
 
-// Stages tile t completely into `buf` (producer waves, ptid = 0..PT-1):
-// every copy by DMA, every zero slot, and the first batch of averages are
-// issued before a single wait; returns with every write to `buf` complete.
+// First half of staging tile t into `buf` (producer waves, ptid = 0..PT-1):
+// the interiors of copied rows by DMA, 8 pixels a window (a uniform source
+// address plus a per-lane constant), zero rows, and the loads of the first
+// batch of register items (held in av).  Nothing is waited for.
 template <typename T, int SRC>
-__device__ __forceinline__ void res_stage(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
-                                          unsigned char* buf, int ptid) {
+__device__ __forceinline__ void rw_issue(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
+                                         unsigned char* buf, int ptid, ResAvg<T, SRC>& av) {
     const T *b0, *b1;
     res_bases<T, SRC>(g, a, t, b0, b1);
-    const int lane = lane_id(), pwave = ptid >> 6;
-    const int nwin = (t.in_px * RSUB + 63) >> 6;  // 64-slot windows = 8 pixels each
+    const int lane = lane_id(), pwave = ptid >> 6, i = lane >> 3;
+    const int C = a.C_in;
+    const int wpr = t.e >> 3;  // windows per row interior
+    const int nwin = (t.rows + 2) * wpr;
     for (int w = pwave; w < nwin; w += NPW) {
-        const int pw = w * 8;                       // first pixel of the window (uniform)
-        const int u0 = pw / t.pe, v0 = pw - u0 * t.pe;
-        int u = u0, v = v0 + (lane >> 3);
-        if (v >= t.pe) {                            // a window spans at most two rows (pe >= 10)
-            v -= t.pe;
-            ++u;
+        const int u = w / wpr, k = w - u * wpr;
+        const RowSrc S = row_src<SRC>(g, a, nb, t, u);
+        if (S.kind == ROW_ITEMS) continue;
+        const int v0 = 1 + 8 * k;                           // the window's first tile column
+        const int q = (lane & 7) ^ (((v0 + i) >> 1) & 7);   // the sub-chunk this lane's slot holds
+        unsigned char* win = buf + (u * t.pe + v0) * RROW;
+        if (S.kind != ROW_ZERO && q * 8 < C) {
+            const int px = S.kind == ROW_COPY ? 8 * k + i : ((8 * k + i) >> 1);
+            dma16((S.which ? b1 : b0) + S.off + px * C + q * 8, win);
+        } else {
+            *reinterpret_cast<uint4*>(win + lane * 16) = uint4{0u, 0u, 0u, 0u};
         }
-        const int p = pw + (lane >> 3);
-        const int q = (lane & 7) ^ (lane >> 3);     // p & 7 == lane >> 3 inside a window
-        RLoc L{0, 0, 0, 0};
-        const bool in = p < t.in_px;
-        if (in && q * 8 < a.C_in) L = res_loc<SRC>(g, a, nb, t, u, v, q * 8);
-        if (in && L.mode == 1) dma16((L.which ? b1 : b0) + L.off, buf + w * 1024);
-        if (in && L.mode == 0) *reinterpret_cast<uint4*>(buf + w * 1024 + lane * 16) = uint4{0u, 0u, 0u, 0u};
     }
-    const int navg = ResAvg<T, SRC>::n_items(t);
-    for (int base = 0; base < navg; base += PT * AV) {
-        ResAvg<T, SRC> av;
-        av.issue(g, a, nb, t, b0, b1, base, ptid);
-        av.commit(buf);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // DMA (vmcnt) and LDS writes (lgkmcnt) done
+    const typename ResAvg<T, SRC>::Plan P = ResAvg<T, SRC>::plan(g, a, nb, t);
+    av.issue(g, a, nb, t, P, b0, b1, 0, ptid);
 }
 
-// MFMA over one tile and its epilogue, for a consumer wave cw owning NMS
-// 16-pixel sub-tiles (pixels (cw + NCW * ms) * 16 + l16) and NKS 32-channel
-// K-steps per tap.  Fully unrolled; the fragments of the next K-step are
-// read from LDS while the MFMAs of the current one run.
-template <typename T, int DST, int NMS, int NKS>
-__device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, const RTile& t, int cw,
-                                            const unsigned char* s_w, const unsigned char* buf,
-                                            const float (&bv)[4][4], int co0, int vec_out, bool relu) {
+// Second half: waits for the tile's copies and first-batch loads, writes the
+// averages (further batches are loaded and written here).  Returns with
+// every LDS write of the tile issued; the caller waits for lgkmcnt.
+template <typename T, int SRC>
+__device__ __forceinline__ void rw_complete(const Geo& g, const ConvArgs& a, const Neigh& nb, const RTile& t,
+                                            unsigned char* buf, int ptid, ResAvg<T, SRC>& av) {
+    __builtin_amdgcn_s_waitcnt(0);
+    av.commit(buf);
+    const typename ResAvg<T, SRC>::Plan P = ResAvg<T, SRC>::plan(g, a, nb, t);
+    if (P.n > PT * AV) {
+        const T *b0, *b1;
+        res_bases<T, SRC>(g, a, t, b0, b1);
+        for (int base = PT * AV; base < P.n; base += PT * AV) {
+            av.issue(g, a, nb, t, P, b0, b1, base, ptid);
+            av.commit(buf);
+        }
+    }
+}
+
+// MFMA over one unit of a consumer wave's part of a tile of extent E (the
+// 16-pixel column strip `strip`, M output rows from row0) and NKS 32-channel
+// K-steps per tap, then the epilogue: bias, optional residual, optional
+// ReLU, rounding, and the stores (2x2 nearest for a low block written to the
+// dense map).
+template <typename T, int DST, int E, int M, int NKS>
+__device__ __forceinline__ void rw_compute(const Geo& g, const ConvArgs& a, const RTile& t, int strip, int row0,
+                                           const unsigned char* buf, const typename MFR<T>::frag (&Wr)[9][NKS][2],
+                                           const float (&bv)[2][4], int cobase, int vec_out, bool relu) {
     typedef MFR<T> mf;
     typedef typename mf::frag frag;
+    constexpr int PE = E + 2, RB = PE * RROW;  // LDS bytes per padded tile row
     const int lane = lane_id(), l16 = lane & 15, kg = lane >> 4;
-    int pbase[NMS];
+
+    floatx4 acc[M][2];
 #pragma unroll
-    for (int ms = 0; ms < NMS; ++ms) {
-        const int m = min((cw + NCW * ms) * 16 + l16, t.M - 1);
-        const int mi = res_div(m, t.inv_e);
-        pbase[ms] = mi * t.pe + (m - mi * t.e);
+    for (int o = 0; o < M; ++o)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[o][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // The unit's B fragments in order (ks, kx, input row ir), each read from LDS
+    // PD fragments ahead of its MFMAs.
+    constexpr int NIR = M + 2, F = NKS * 3 * NIR;
+    int pb[3];  // per-lane byte offset of input row 0 for kx = 0, 1, 2 (without the K-step)
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+        const int col = strip * 16 + kx + l16;
+        pb[kx] = (row0 * PE + col) * RROW + (tile_pos(col, kg) << 4);
     }
-    // per-lane byte offsets of the weight fragments (row & 7 == l16 & 7 for every weight row used)
-    int wbase[NKS];
+    auto load = [&](int f) -> frag {
+        const int ks = f / (3 * NIR), kx = (f / NIR) % 3, ir = f % NIR;
+        // sub-chunk ks * 4 + kg sits at position tile_pos(col, kg) ^ (4 * ks): the K-step
+        // flips bit 2 of the position, i.e. XORs 64 into the byte offset
+        return *reinterpret_cast<const frag*>(buf + ((pb[kx] ^ (ks << 6)) + ir * RB));
+    };
+    // ring of PD + 1 fragments: fragment f + PD is read while the MFMAs of f run
+    constexpr int PD = M <= 2 ? 5 : 2;
+    frag P[PD + 1];
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) wbase[ks] = l16 * RROW + (((ks * 4 + kg) ^ (l16 & 7)) << 4);
-
-    floatx4 acc[NMS][4];
+    for (int f = 0; f < PD; ++f) P[f] = load(f);
+    __builtin_amdgcn_sched_group_barrier(0x100, PD, 0);  // schedule: the first PD reads
 #pragma unroll
-    for (int ms = 0; ms < NMS; ++ms)
+    for (int f = 0; f < F; ++f) {
+        if (f + PD < F) P[(f + PD) % (PD + 1)] = load(f + PD);
+        const int ks = f / (3 * NIR), kx = (f / NIR) % 3, ir = f % NIR;
+        int n = 0;
 #pragma unroll
-        for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    constexpr int S = 9 * NKS;  // K-steps (even: 18, or 9 with one odd step left)
-    frag wf[2][4], pf[2][NMS];
-    auto load = [&](int step, int b) {
-        const int tap = NKS == 2 ? (step >> 1) : step, ks = NKS == 2 ? (step & 1) : 0;
-        const int ky = tap >= 6 ? 2 : (tap >= 3 ? 1 : 0);
-        const int toff = ky * t.pe + (tap - 3 * ky);
-        const int q = ks * 4 + kg;
+        for (int ky = 0; ky < 3; ++ky) {
+            const int o = ir - ky;
+            if (o >= 0 && o < M) {
+                n += 2;
 #pragma unroll
-        for (int ns = 0; ns < 4; ++ns)
-            wf[b][ns] = *reinterpret_cast<const frag*>(s_w + wbase[ks] + (tap * RNT + ns * 16) * RROW);
-#pragma unroll
-        for (int ms = 0; ms < NMS; ++ms) {
-            const int r = pbase[ms] + toff;
-            pf[b][ms] = *reinterpret_cast<const frag*>(buf + r * RROW + ((q ^ (r & 7)) << 4));
+                for (int j = 0; j < 2; ++j) acc[o][j] = mf::mma(Wr[ky * 3 + kx][ks][j], P[f % (PD + 1)], acc[o][j]);
+            }
         }
-    };
-    auto mma = [&](int b) {
-#pragma unroll
-        for (int ms = 0; ms < NMS; ++ms)
-#pragma unroll
-            for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = mf::mma(wf[b][ns], pf[b][ms], acc[ms][ns]);
-    };
-    load(0, 0);
-#pragma unroll 1
-    for (int step = 0; step + 1 < S; step += 2) {
-        load(step + 1, 1);
-        mma(0);
-        if (step + 2 < S) load(step + 2, 0);
-        mma(1);
+        // then, per fragment: the read PD ahead, and this fragment's MFMAs
+        if (f + PD < F) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (n == 2) __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        else if (n == 4) __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        else __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
     }
-    if (S & 1) mma(0);
 
-    // -- epilogue: channels co0 + ns*16 + kg*4 + {0..3} of pixel (cw + NCW*ms)*16 + l16
+    // -- epilogue: channels cobase + kg*8 + {0..7} of pixel (row0 + o, strip*16 + l16)
     const int Co = a.C_out;
+    const int co = cobase + kg * 8;
+    if (co >= Co) return;
+    const bool full = vec_out && co + 8 <= Co;
     T* obase;  // the tile's block in its output stack, or the tile's image
     const T* rbase = nullptr;
     if constexpr (DST == DST_PACKED) {
-        const size_t blk = (size_t)t.slot * t.e * t.e * Co;
+        const size_t blk = (size_t)t.slot * E * E * Co;
         obase = (T*)(t.high ? a.out_hi : a.out_lo) + blk;
         const T* rb = (const T*)(t.high ? a.res_hi : a.res_lo);
         if (rb) rbase = rb + blk;
@@ -393,55 +506,47 @@ __device__ __forceinline__ void res_compute(const Geo& g, const ConvArgs& a, con
         obase = (T*)a.out_hi + (size_t)t.n * g.H * g.W * Co;
     }
 #pragma unroll
-    for (int ms = 0; ms < NMS; ++ms) {
-        const int m = (cw + NCW * ms) * 16 + l16;
-        if (m >= t.M) continue;
-        const int mi = res_div(m, t.inv_e);
-        const int i = t.r0 + mi, j = m - mi * t.e;
-        int off;  // element offset of channel 0 of this pixel (the first of 2x2 for a low block)
-        int down = 0;
+    for (int o = 0; o < M; ++o) {
+        const int i = t.r0 + row0 + o, jx = strip * 16 + l16;  // block-local output pixel
+        int off, down = 0;  // element offset of channel 0 of the pixel (the first of 2x2 for a low block)
         if constexpr (DST == DST_PACKED) {
-            off = (i * t.e + j) * Co;
+            off = (i * E + jx) * Co;
         } else {
-            const int Y = t.gy * g.bs + (t.high ? i : 2 * i), X = t.gx * g.bs + (t.high ? j : 2 * j);
+            const int Y = t.gy * g.bs + (t.high ? i : 2 * i), X = t.gx * g.bs + (t.high ? jx : 2 * jx);
             off = (Y * g.W + X) * Co;
             down = g.W * Co;
         }
+        float f[8];
 #pragma unroll
-        for (int ns = 0; ns < 4; ++ns) {
-            const int co = co0 + ns * 16 + kg * 4;
-            if (co >= Co) continue;
-            const bool full = vec_out && co + 4 <= Co;
-            float f[4];
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) f[r] = acc[ms][ns][r] + bv[ns][r];
-            if (rbase) {
+            for (int r = 0; r < 4; ++r) f[j * 4 + r] = acc[o][j][r] + bv[j][r];
+        if (rbase) {
+            if (full) {
+                const Vec<T, 8> rv = vload<T, 8>(rbase + off + co);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) f[e] += to_f32(rv.e[e]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (co + e < Co) f[e] += to_f32(rbase[off + co + e]);
+            }
+        }
+        Vec<T, 8> ov;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ov.e[e] = from_f32<T>(relu ? fmaxf(f[e], 0.0f) : f[e]);
+        const int reps = (DST == DST_DENSE && !t.high) ? 2 : 1;
+        for (int dy = 0; dy < reps; ++dy)
+            for (int dx = 0; dx < reps; ++dx) {
+                T* q = obase + off + dy * down + dx * Co + co;
                 if (full) {
-                    const Vec<T, 4> rv = vload<T, 4>(rbase + off + co);
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) f[r] += to_f32(rv.e[r]);
+                    st_nt16(q, ov.raw);
                 } else {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (co + r < Co) f[r] += to_f32(rbase[off + co + r]);
+                    for (int e = 0; e < 8; ++e)
+                        if (co + e < Co) q[e] = ov.e[e];
                 }
             }
-            Vec<T, 4> o;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) o.e[r] = from_f32<T>(relu ? fmaxf(f[r], 0.0f) : f[r]);
-            const int reps = (DST == DST_DENSE && !t.high) ? 2 : 1;
-            for (int dy = 0; dy < reps; ++dy)
-                for (int dx = 0; dx < reps; ++dx) {
-                    T* q = obase + off + dy * down + dx * Co + co;
-                    if (full) {
-                        st_nt8(q, o.raw);
-                    } else {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            if (co + r < Co) q[r] = o.e[r];
-                    }
-                }
-        }
     }
 }
 
@@ -457,20 +562,37 @@ __device__ __forceinline__ void res_barrier() {
 template <typename T, int SRC, int DST, bool ONE, int NKS>
 __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int R,
                                                      int G, int ntiles, int buf_bytes, int vec_out) {
+    typedef typename MFR<T>::frag frag;
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* s_w = smem;
-    unsigned char* s_buf0 = smem + RW_BYTES;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const bool producer = wave >= NCW;
     const int ptid = (int)threadIdx.x - 64 * NCW;
-    const int lane = lane_id(), kg = lane >> 4;
+    const int lane = lane_id(), l16 = lane & 15, kg = lane >> 4;
     const int co0 = blockIdx.y * RNT;
 
-    if (producer) {
-        // weights of this workgroup's output channels first (they do not depend on the
-        // mask): rows [tap][co], 64 channels each
+    WaveMaskT<ONE> wm;
+    wm.init(mask, (int)g.B);  // issues the mask read
+
+    // consumer c: output channels co0 + 32 * (c & 1) + [0, 32), half (c >> 1) of every tile
+    const int h = wave & 1, half = wave >> 1;
+    const int cobase = co0 + 32 * h;
+    float bv[2][4];
+    // The weight slice of this workgroup (rows [tap][co], 64 channels each) is
+    // copied to LDS by the consumers while the producers plan and issue tile 0;
+    // it sits over buffers 1 and 2 until the consumers hold it in registers.
+    unsigned char* s_w = smem + buf_bytes;
+    if (!producer) {
+        const T* __restrict__ bias = (const T*)a.bias;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = cobase + kg * 8 + j * 4 + r;
+                bv[j][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
+            }
         const T* __restrict__ wgt = (const T*)a.weight;
-        for (int w0 = (wave - NCW) * 64; w0 < 9 * RNT * RSUB; w0 += PT) {
+#pragma unroll
+        for (int w0 = wave * 64; w0 < 9 * RNT * RSUB; w0 += 64 * NCW) {
             const int s = w0 + lane;
             const int row = s >> 3, q = (s & 7) ^ (row & 7);
             const int tap = row / RNT, col = row - tap * RNT;
@@ -480,49 +602,113 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
         }
     }
 
-    WaveMaskT<ONE> wm;
-    wm.init(mask, (int)g.B);
-
-    const T* __restrict__ bias = (const T*)a.bias;
-    const bool relu = (a.flags & 1) != 0;
-    float bv[4][4];  // bias of channels co0 + ns*16 + kg*4 + r
-#pragma unroll
-    for (int ns = 0; ns < 4; ++ns)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int co = co0 + ns * 16 + kg * 4 + r;
-            bv[ns][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
+    // This workgroup's tiles are pos, pos + nwg, ...  Workgroups are spread
+    // over the XCDs round-robin; pos numbers them XCD by XCD, so the tiles of
+    // one block (which share halo rows) run on one XCD and share its L2.
+    const int nwg = (int)gridDim.x;
+    const int pos = (nwg & 7) ? (int)blockIdx.x : (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
+    int tile = pos;
+    auto next_tile = [&](RTile& t, Neigh& nb) -> bool {
+        while (tile < ntiles) {
+            const bool ok = res_tile<SRC, DST, ONE>(g, a, wm, R, G, tile, t, nb);
+            tile += nwg;
+            if (ok) return true;
         }
+        return false;
+    };
+    auto bufn = [&](int k) { return smem + (k == 0 ? 0 : (k == 1 ? buf_bytes : 2 * buf_bytes)); };
 
-    // Step i: the producers stage tile i of this workgroup's sequence into buffer i & 1
-    // while the consumers compute tile i - 1 from the other buffer.  Every wave walks
-    // the sequence identically, so all of them leave the loop together.
-    int tile = blockIdx.x;
-    RTile t;            // the tile the consumers compute in this step
-    bool have = false;  // ... if any
-    for (int it = 0;; ++it) {
+    // Step i: the consumers compute tile i (buffer i % 3) while the producers
+    // complete tile i + 1 (buffer (i + 1) % 3: wait for its copies, write its
+    // register items) and issue tile i + 2 (buffer (i + 2) % 3).
+    // Before the loop:
+    //   producers: issue tile 0 | (1) | complete tile 0 | (2) | issue tile 1
+    //   consumers: weights -> LDS | (1) | weights -> registers | (2)
+    // Both roles walk the same tile sequence and take two barriers before the
+    // loop and one per step, so they leave together.  The roles have separate
+    // loops so that the producers' in-flight items and the consumers' weights
+    // do not compete for registers.
+    RTile t0, t1;  // tiles i and i + 1
+    Neigh nb0, nb1;
+    bool h0 = next_tile(t0, nb0);
+    bool h1 = h0 ? next_tile(t1, nb1) : false;
+    if (producer) {
+        ResAvg<T, SRC> av;
+        av.clear();
+        if (h0) rw_issue<T, SRC>(g, a, nb0, t0, bufn(0), ptid, av);
+        res_barrier();                             // (1) the weights are in LDS
+        if (h0) rw_complete<T, SRC>(g, a, nb0, t0, bufn(0), ptid, av);
+        __builtin_amdgcn_s_waitcnt(0xC07F);        // lgkmcnt(0): tile 0's LDS writes are done
+        res_barrier();                             // (2) tile 0 is staged, the weights are in registers
+        if (h1) rw_issue<T, SRC>(g, a, nb1, t1, bufn(1), ptid, av);
+        int b = 0;  // i % 3
+        while (h0) {
+            RTile t2;
+            Neigh nb2;
+            const bool h2 = h1 ? next_tile(t2, nb2) : false;
+            const int b1 = b == NBUF - 1 ? 0 : b + 1, b2 = b1 == NBUF - 1 ? 0 : b1 + 1;
+            if (h1) rw_complete<T, SRC>(g, a, nb1, t1, bufn(b1), ptid, av);
+            if (h2) rw_issue<T, SRC>(g, a, nb2, t2, bufn(b2), ptid, av);
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this step's LDS writes are done
+            res_barrier();
+            h0 = h1;
+            t1 = t2;
+            nb1 = nb2;
+            h1 = h2;
+            b = b1;
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
+    }
+
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's weight copies (and bias, mask) have landed
+    res_barrier();                  // (1)
+    // A row m of channel block j is channel kg' * 8 + j * 4 + (m & 3) of the wave's 32 (kg' = m >> 2)
+    frag Wr[9][NKS][2];
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int row = tap * RNT + 32 * h + (l16 >> 2) * 8 + j * 4 + (l16 & 3);
+                Wr[tap][ks][j] = *reinterpret_cast<const frag*>(s_w + row * RROW + (((ks * 4 + kg) ^ (row & 7)) << 4));
+            }
+    const bool relu = (a.flags & 1) != 0;
+    // All counters: the weight reads, and (for the compiler's wait tracking) no LDS
+    // copy pending on this path, which keeps the waits for the MFMA operands partial.
+    __builtin_amdgcn_s_waitcnt(0);
+    res_barrier();  // (2)
+
+    int b = 0;
+    while (h0) {
         RTile t2;
         Neigh nb2;
-        bool have2 = false;
-        while (tile < ntiles && !(have2 = res_tile<SRC, DST, ONE>(g, a, wm, R, G, tile, t2, nb2))) tile += gridDim.x;
-        tile += gridDim.x;
-        if (!have && !have2) break;
-        unsigned char* sbuf = s_buf0 + (it & 1) * buf_bytes;
-        unsigned char* cbuf = s_buf0 + ((it & 1) ^ 1) * buf_bytes;
-        if (producer) {
-            // the staging wait also covers the weight copies of the first step
-            if (have2) res_stage<T, SRC>(g, a, nb2, t2, sbuf, ptid);
-            __builtin_amdgcn_s_waitcnt(0);
-        } else if (have) {
-            const int nst = (t.M + 15) >> 4;
-            const int nms = nst > wave ? min(2, (nst - wave + NCW - 1) / NCW) : 0;
-            if (nms == 2) res_compute<T, DST, 2, NKS>(g, a, t, wave, s_w, cbuf, bv, co0, vec_out, relu);
-            else if (nms == 1) res_compute<T, DST, 1, NKS>(g, a, t, wave, s_w, cbuf, bv, co0, vec_out, relu);
-            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this tile's LDS reads are done
+        const bool h2 = h1 ? next_tile(t2, nb2) : false;
+        const unsigned char* buf = bufn(b);
+        if (t0.high) {
+            if (t0.e == 32) {  // 8 rows x 2 strips: strip `half`, two rows at a time
+#pragma unroll 1
+                for (int r = 0; r < 8; r += 2)
+                    rw_compute<T, DST, 32, 2, NKS>(g, a, t0, half, r, buf, Wr, bv, cobase, vec_out, relu);
+            } else {           // 4 rows x 4 strips: strips 2 * half and 2 * half + 1, two rows at a time
+#pragma unroll 1
+                for (int u = 0; u < 4; ++u)
+                    rw_compute<T, DST, 64, 2, NKS>(g, a, t0, 2 * half + (u >> 1), 2 * (u & 1), buf, Wr, bv, cobase,
+                                                   vec_out, relu);
+            }
+        } else {
+            if (t0.e == 16) rw_compute<T, DST, 16, 2, NKS>(g, a, t0, 0, 2 * half, buf, Wr, bv, cobase, vec_out, relu);
+            else rw_compute<T, DST, 32, 2, NKS>(g, a, t0, half, 0, buf, Wr, bv, cobase, vec_out, relu);
         }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this tile's LDS reads are done
         res_barrier();
-        t = t2;
-        have = have2;
+        (void)nb2;
+        t0 = t1;
+        h0 = h1;
+        t1 = t2;
+        h1 = h2;
+        b = b == NBUF - 1 ? 0 : b + 1;
     }
 }
 
@@ -539,16 +725,25 @@ int cu_count() {
 
 inline bool aligned_to(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; }
 
+// Image rows per high tile (a low tile has half as many): 8 for blocks of
+// 32, 4 for blocks of 64, so that every tile has 256 output pixels and each
+// consumer half is whole 16-pixel strips of whole rows; 0 = not supported.
+int res_rows(int bs) { return bs == 32 ? 8 : (bs == 64 ? 4 : 0); }
+
+int res_buf_bytes(int bs, int R) {
+    const int lb = bs / 2;
+    const int px_h = (R + 2) * (bs + 2), px_l = (R / 2 + 2) * (lb + 2);
+    return (px_h > px_l ? px_h : px_l) * RROW;
+}
+
 template <typename T, int SRC, int DST, bool ONE, int NKS>
 hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, hipStream_t st) {
-    const int G = (g.bs + R - 1) / R;
+    const int G = g.bs / R;  // tiles per block, for both classes
     const long long ntiles = g.B * G;
-    const int lb = g.bs / 2;
-    const int px_h = (R + 2) * (g.bs + 2), px_l = (R / 2 + 2) * (lb + 2);
-    const int buf_bytes = (px_h > px_l ? px_h : px_l) * RROW;
-    const int smem = RW_BYTES + 2 * buf_bytes;
-    const int ob = 4 * (int)sizeof(T);
-    const int vec_out = (a.C_out % 4 == 0) && aligned_to(a.out_hi, ob) && aligned_to(a.out_lo, ob) &&
+    const int buf_bytes = res_buf_bytes(g.bs, R);
+    const int smem = NBUF * buf_bytes;
+    const int ob = 16;
+    const int vec_out = (a.C_out % 8 == 0) && aligned_to(a.out_hi, ob) && aligned_to(a.out_lo, ob) &&
                         aligned_to(a.res_hi, ob) && aligned_to(a.res_lo, ob);
     static int attr_bytes = 0;
     if (smem > attr_bytes) {
@@ -562,19 +757,6 @@ hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, 
     hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, G, (int)ntiles,
                        buf_bytes, vec_out);
     return hipGetLastError();
-}
-
-// Image rows per tile: the largest even R <= bs whose two tile buffers fit
-// beside the weights (a tile covers at most RMT output pixels).
-int res_rows(int bs) {
-    const int budget = (160 * 1024 - RW_BYTES) / 2 / RROW;  // pixels per buffer
-    int best = 0;
-    for (int R = 2; R <= bs; R += 2) {
-        const int lb = bs / 2;
-        const int px = (R + 2) * (bs + 2) > (R / 2 + 2) * (lb + 2) ? (R + 2) * (bs + 2) : (R / 2 + 2) * (lb + 2);
-        if (px <= budget && R * bs <= RMT) best = R;
-    }
-    return best;
 }
 
 template <typename T, bool ONE, int NKS>
@@ -596,14 +778,16 @@ hipError_t res_t(ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask, co
 
 bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
-    if (a.C_in % 8 || a.C_in > 64 || g.bs < 16 || g.bs > 64) return false;
+    if (a.C_in % 8 || a.C_in > 64 || res_rows(g.bs) == 0) return false;
     if (!aligned_to(a.in_hi, 16) || !aligned_to(a.in_lo, 16) || !aligned_to(a.weight, 16)) return false;
     // element offsets inside one image or one stack are 32-bit
     const long long img = (long long)g.H * g.W * (a.C_in > a.C_out ? a.C_in : a.C_out);
     const long long cap = (a.hi_cap > a.lo_cap ? a.hi_cap : a.lo_cap) + 1LL;
     const long long stk = cap * (g.bs + 2) * (g.bs + 2) * (a.C_in > a.C_out ? a.C_in : a.C_out);
     if (img >= (1LL << 31) || stk >= (1LL << 31)) return false;
-    return res_rows(g.bs) > 0;
+    // three tile buffers, the last two of which also hold the weights at start-up
+    const int bb = res_buf_bytes(g.bs, res_rows(g.bs));
+    return NBUF * bb <= 160 * 1024 && 2 * bb >= RW_BYTES;
 }
 
 hipError_t launch_conv_res(int dtype, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask, const ConvArgs& a,

@@ -31,6 +31,8 @@ CASES = [
     Case("bs256_bf16", "bf16", 1, 16, 24, 256, 512, 256, p_low=0.5, seed=6),
     Case("allhigh_f16", "f16", 1, 16, 16, 32, 64, 16, mask_kind="high", seed=7),
     Case("alllow_bf16", "bf16", 1, 16, 16, 32, 64, 16, mask_kind="low", seed=8),
+    Case("bs64_c64_bf16", "bf16", 1, 64, 64, 128, 192, 64, seed=14),
+    Case("blocks1056_f16", "f16", 1, 8, 8, 1024, 1056, 32, seed=12),  # more than 1024 blocks
 ]
 LAYOUTS = ["nchw", "nhwc"]
 TDT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
@@ -110,10 +112,14 @@ def test_convolutions_match_oracle(c, layout):
     torch.cuda.synchronize()
 
 
+EPI_CASES = [Case("epilogue_f16", "f16", 2, 40, 72, 32, 48, 16, seed=11),
+             Case("epilogue_bs32_f16", "f16", 2, 40, 72, 64, 96, 32, seed=13)]
+
+
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_block_conv_epilogue_relu_residual(layout):
+@pytest.mark.parametrize("c", EPI_CASES, ids=_ids(EPI_CASES))
+def test_block_conv_epilogue_relu_residual(c, layout):
     import paper_2011_12025_amd as sb
-    c = Case("epilogue_f16", "f16", 2, 40, 72, 32, 48, 16, seed=11)
     mask, x, w, b, ref = prepared(c)
     log(f"[epilogue] {c.name} {layout}")
     g = np.random.default_rng(99)
