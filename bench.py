@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP16_PEAK_TFLOPS = 2516.6      # MI355X dense fp16 MFMA
 MALL_BYTES = 256 << 20         # Infinity Cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_stage1.json")
-KERNEL_SOURCES = ["sb_conv.hip", "sb_pixel.h", "sb_common.h"]
+KERNEL_SOURCES = ["sb_conv_res.hip", "sb_common.h", "sb_pixel.h", "sb_kernels.h"]
 
 WL = dict(N=1, C=64, H=256, W=512, bs=32, dtype="f16", p_low=0.5, seed=0)
 
@@ -280,7 +280,7 @@ def main():
                      "speedup_vs_miopen": round(miopen_ms / bd_ms["layer"], 3),
                      "theoretical_flop_speedup": round(dense_flop / block_flop, 3)},
         "pad_GBps": breakdown["pad"]["GB/s"],
-        "roofline": {"bound": "hbm", "kernel": "k_conv<f16,NHWC,SRC_DENSE,DST_DENSE> (segblocks_layer)",
+        "roofline": {"bound": "hbm", "kernel": "k_conv_res<f16,SRC_DENSE,DST_DENSE> (segblocks_layer)",
                      "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": layer_bytes,
