@@ -201,6 +201,19 @@ struct WaveMaskT {
         pre = wave_excl5(c);
         tot = wave_sum5(c);
     }
+    // The same as init, with the first 1024 mask bytes already copied to LDS
+    // by stage_mask (bytes past B zero): many waves reading the one global
+    // line of a small mask at once wait for each other, one LDS copy per
+    // workgroup does not.
+    __device__ __forceinline__ void init_staged(const uint8_t* m, int nbytes, const uint8_t* s_mask) {
+        mask = m;
+        B = nbytes;
+        aligned = (reinterpret_cast<uintptr_t>(m) & 15) == 0;
+        first = nonzero_bytes16(*reinterpret_cast<const uint4*>(s_mask + 16 * lane_id()));
+        const int c = __popc(first);
+        pre = wave_excl5(c);
+        tot = wave_sum5(c);
+    }
     // valid-byte bits of this lane's chunk of a stride
     __device__ __forceinline__ uint32_t inside(int stride) const {
         const int b0 = stride + 16 * lane_id();
@@ -269,6 +282,28 @@ struct WaveMaskT {
 };
 typedef WaveMaskT<false> WaveMask;
 
+// One wave copies mask bytes [0, min(B, 1024)) to s_mask (1024 bytes, 16-byte
+// aligned LDS), zero past B; the workgroup then synchronises before any wave
+// calls WaveMaskT::init_staged.
+__device__ __forceinline__ void stage_mask(const uint8_t* __restrict__ m, int B, uint8_t* s_mask) {
+    const int b0 = 16 * lane_id();
+    uint4 v = uint4{0u, 0u, 0u, 0u};
+    if (b0 < B) {
+        if ((reinterpret_cast<uintptr_t>(m) & 15) == 0 && b0 + 16 <= B) {
+            v = *reinterpret_cast<const uint4*>(m + b0);
+        } else {
+            uint8_t bytes[16];
+#pragma unroll
+            for (int b = 0; b < 16; ++b) bytes[b] = (b0 + b < B) ? m[b0 + b] : (uint8_t)0;
+            v.x = bytes[0] | (bytes[1] << 8) | (bytes[2] << 16) | ((uint32_t)bytes[3] << 24);
+            v.y = bytes[4] | (bytes[5] << 8) | (bytes[6] << 16) | ((uint32_t)bytes[7] << 24);
+            v.z = bytes[8] | (bytes[9] << 8) | (bytes[10] << 16) | ((uint32_t)bytes[11] << 24);
+            v.w = bytes[12] | (bytes[13] << 8) | (bytes[14] << 16) | ((uint32_t)bytes[15] << 24);
+        }
+    }
+    *reinterpret_cast<uint4*>(s_mask + b0) = v;
+}
+
 // Class and slot of a block and of its 8 neighbours.  Neighbour index
 // d = (dy+1)*3 + (dx+1); d = 4 is the block itself.
 struct Neigh {
@@ -295,6 +330,65 @@ __device__ __forceinline__ Neigh wave_neighbourhood(const WaveMaskT<ONE>& wm, in
     }
 #pragma unroll
     for (int d = 0; d < 9; ++d) r.slot[d] = WITH_SLOTS ? wm.slot(t[d], (r.high >> d) & 1) : 0;
+    return r;
+}
+
+// Block plan of a mask of up to 1024 blocks as a table in LDS: bit (k & 15)
+// of hi[k >> 4] is block k's class, slot[k] its rank among the earlier blocks
+// of that class.  One wave builds it from the staged mask (stage_mask); the
+// lookups are then plain LDS reads instead of chains of cross-lane reads on
+// the CU's one scalar unit.
+struct PlanTable {
+    uint16_t hi[64];
+    uint16_t slot[1024];
+};
+
+__device__ __forceinline__ void build_plan_table(const uint8_t* s_mask, PlanTable* pt) {
+    const int l = lane_id();
+    const uint32_t bits = nonzero_bytes16(*reinterpret_cast<const uint4*>(s_mask + 16 * l));  // zero past B
+    const int pre = wave_excl5(__popc(bits));
+    pt->hi[l] = (uint16_t)bits;
+    uint32_t w[8];
+#pragma unroll
+    for (int b = 0; b < 16; b += 2) {
+        uint32_t two = 0;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int nb = pre + __popc(bits & ((1u << (b + i)) - 1u));  // high blocks before 16 l + b + i
+            const uint32_t sl = ((bits >> (b + i)) & 1u) ? (uint32_t)nb : (uint32_t)(16 * l + b + i - nb);
+            two |= sl << (16 * i);
+        }
+        w[b / 2] = two;
+    }
+    *reinterpret_cast<uint4*>(&pt->slot[16 * l]) = uint4{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<uint4*>(&pt->slot[16 * l + 8]) = uint4{w[4], w[5], w[6], w[7]};
+}
+
+// Class and slot of block k (wave-uniform k), from the table.
+__device__ __forceinline__ bool table_high(const PlanTable* pt, int k) {
+    return __builtin_amdgcn_readfirstlane((int)((pt->hi[k >> 4] >> (k & 15)) & 1u)) != 0;
+}
+__device__ __forceinline__ int table_slot(const PlanTable* pt, int k) {
+    return __builtin_amdgcn_readfirstlane((int)pt->slot[k]);
+}
+
+// Neighbourhood of block (n, gy, gx) from the table: lane d < 9 looks up
+// neighbour d, then the results are made wave-uniform.
+__device__ __forceinline__ Neigh table_neighbourhood(const PlanTable* pt, int GH, int GW, int n, int gy, int gx) {
+    const int l = lane_id();
+    int vd = 0, hb = 0, sl = 0;
+    if (l < 9) {
+        const int ny = gy + l / 3 - 1, nx = gx + l % 3 - 1;
+        vd = (ny >= 0 && ny < GH && nx >= 0 && nx < GW);
+        const int t = (n * GH + (vd ? ny : gy)) * GW + (vd ? nx : gx);
+        hb = (pt->hi[t >> 4] >> (t & 15)) & 1;
+        sl = pt->slot[t];
+    }
+    Neigh r;
+    r.valid = (uint32_t)__ballot(vd) & 0x1FFu;
+    r.high = (uint32_t)__ballot(hb) & 0x1FFu;
+#pragma unroll
+    for (int d = 0; d < 9; ++d) r.slot[d] = __builtin_amdgcn_readlane(sl, d);
     return r;
 }
 

@@ -286,6 +286,7 @@ hipError_t combine_t(int layout, const Geo& g, const void* hi, const void* lo, c
 
 hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask, void* hi,
                         int hi_cap, void* lo, int lo_cap, hipStream_t st) {
+    if (rows_fit(dtype, layout, g, {x, hi, lo})) return launch_split_rows(dtype, g, x, mask, hi, hi_cap, lo, lo_cap, st);
     switch (dtype) {
     case 0: return split_t<float>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, st);
     case 1: return split_t<f16>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, st);
@@ -295,6 +296,8 @@ hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, cons
 
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
                       void* hp, void* lp, int hi_cap, int lo_cap, hipStream_t st) {
+    if (rows_fit(dtype, layout, g, {hi, lo, hp, lp}))
+        return launch_pad_rows(dtype, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
     switch (dtype) {
     case 0: return pad_t<float>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
     case 1: return pad_t<f16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
@@ -304,6 +307,7 @@ hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const
 
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
                           int hi_cap, int lo_cap, void* y, hipStream_t st) {
+    if (rows_fit(dtype, layout, g, {hi, lo, y})) return launch_combine_rows(dtype, g, hi, lo, mask, hi_cap, lo_cap, y, st);
     switch (dtype) {
     case 0: return combine_t<float>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, st);
     case 1: return combine_t<f16>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, st);

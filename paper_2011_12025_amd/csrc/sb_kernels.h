@@ -1,6 +1,8 @@
 // Internal launcher interface between the C ABI (sb_api.hip) and the kernels.
 #pragma once
 
+#include <initializer_list>
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -36,6 +38,16 @@ hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, c
 // g.C is ignored by the convolution launcher (C_in / C_out are in ConvArgs).
 hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g,
                        const uint8_t* mask, const ConvArgs& a, hipStream_t st);
+
+// Row-job split / pad / combine for channels-last tensors of whole 16-byte
+// pixels with 16-byte aligned buffers; rows_fit tells whether they apply.
+bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const void*> ptrs);
+hipError_t launch_split_rows(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap,
+                             void* lo, int lo_cap, hipStream_t st);
+hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp,
+                           void* lp, int hi_cap, int lo_cap, hipStream_t st);
+hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
+                               int hi_cap, int lo_cap, void* y, hipStream_t st);
 
 // Persistent convolution with LDS-resident weights (channels-last fp16/bf16,
 // C_in <= 64, 16 <= bs <= 64); conv_res_fits tells whether it applies.
