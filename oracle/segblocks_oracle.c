@@ -237,6 +237,101 @@ void orc_conv3x3_valid(const float* P, long S, int Cin, int E, const float* w,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Strided block convolution (the encoder's convolutions on block stacks).  */
+/* ------------------------------------------------------------------------ */
+
+/* P[S][Cin][E+2][E+2] (padded blocks), w[Cout][Cin][K][K] with K = 1 or 3,
+ * stride st = 1 or 2 dividing E, bias[Cout] (or NULL)
+ * -> out[S][Cout][E/st][E/st] in fp64:
+ *    out[i][j] = bias[co] + sum_ci sum_ky sum_kx
+ *                w[co][ci][ky][kx] * P[ci][st*i + ky + o][st*j + kx + o],
+ *    o = 1 - K/2.
+ * A 3x3 kernel is centred on block pixel (st*i, st*j) with one pixel of
+ * padding (row 0 of a padded block is block row -1, so a stride-2 output
+ * only ever reads the top and left halo); a 1x1 kernel reads block pixel
+ * (st*i, st*j).  This is an ordinary strided convolution of the block with
+ * the halo BlockPad gives it.  Accumulated in fp64 in the order ci, ky, kx. */
+void orc_conv_block(const float* P, long S, int Cin, int E, const float* w, int K, int st,
+                    const float* bias, int Cout, double* out)
+{
+    const int pe = E + 2, Eo = E / st, o = 1 - K / 2;
+    for (long s = 0; s < S; ++s)
+    for (int co = 0; co < Cout; ++co)
+    for (int i = 0; i < Eo; ++i)
+    for (int j = 0; j < Eo; ++j) {
+        double acc = 0.0;
+        for (int ci = 0; ci < Cin; ++ci) {
+            const float* p = P + ((s * Cin + ci) * pe) * (long)pe;
+            const float* wk = w + ((long)co * Cin + ci) * K * K;
+            for (int ky = 0; ky < K; ++ky)
+                for (int kx = 0; kx < K; ++kx)
+                    acc += (double)wk[ky * K + kx] * (double)p[(st * i + ky + o) * pe + (st * j + kx + o)];
+        }
+        if (bias) acc += (double)bias[co];
+        out[((s * Cout + co) * Eo + i) * (long)Eo + j] = acc;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dense layers of the encoder around the block stages.                     */
+/* ------------------------------------------------------------------------ */
+
+/* x[N][Cin][H][W], w[Cout][Cin][K][K], zero padding `pad`, stride st,
+ * bias[Cout] (or NULL) -> out[N][Cout][Ho][Wo] in fp64 with
+ * Ho = (H + 2 pad - K) / st + 1 (likewise Wo); order ci, ky, kx. */
+void orc_conv_dense(const float* x, int N, int Cin, int H, int W, const float* w, int K, int st, int pad,
+                    const float* bias, int Cout, double* out)
+{
+    const int Ho = (H + 2 * pad - K) / st + 1, Wo = (W + 2 * pad - K) / st + 1;
+    for (int n = 0; n < N; ++n)
+    for (int co = 0; co < Cout; ++co)
+    for (int i = 0; i < Ho; ++i)
+    for (int j = 0; j < Wo; ++j) {
+        double acc = 0.0;
+        for (int ci = 0; ci < Cin; ++ci) {
+            const float* img = x + ((long)n * Cin + ci) * H * (long)W;
+            const float* wk = w + ((long)co * Cin + ci) * K * K;
+            for (int ky = 0; ky < K; ++ky) {
+                const int y = st * i + ky - pad;
+                if (y < 0 || y >= H) continue;
+                for (int kx = 0; kx < K; ++kx) {
+                    const int xx = st * j + kx - pad;
+                    if (xx < 0 || xx >= W) continue;
+                    acc += (double)wk[ky * K + kx] * (double)img[(long)y * W + xx];
+                }
+            }
+        }
+        if (bias) acc += (double)bias[co];
+        out[(((long)n * Cout + co) * Ho + i) * (long)Wo + j] = acc;
+    }
+}
+
+/* x[N][C][H][W] -> y[N][C][Ho][Wo]: maximum over the K x K window at stride
+ * st with `pad` pixels of padding that never win (they are not candidates). */
+void orc_maxpool(const float* x, int N, int C, int H, int W, int K, int st, int pad, float* y)
+{
+    const int Ho = (H + 2 * pad - K) / st + 1, Wo = (W + 2 * pad - K) / st + 1;
+    for (int n = 0; n < N; ++n)
+    for (int c = 0; c < C; ++c) {
+        const float* img = x + ((long)n * C + c) * H * (long)W;
+        for (int i = 0; i < Ho; ++i)
+        for (int j = 0; j < Wo; ++j) {
+            float m = -INFINITY;
+            for (int ky = 0; ky < K; ++ky) {
+                const int yy = st * i + ky - pad;
+                if (yy < 0 || yy >= H) continue;
+                for (int kx = 0; kx < K; ++kx) {
+                    const int xx = st * j + kx - pad;
+                    if (xx < 0 || xx >= W) continue;
+                    if (img[(long)yy * W + xx] > m) m = img[(long)yy * W + xx];
+                }
+            }
+            y[(((long)n * C + c) * Ho + i) * (long)Wo + j] = m;
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
 /* BlockCombine: nearest-upsample the low blocks and reassemble the map.     */
 /* ------------------------------------------------------------------------ */
 

@@ -107,3 +107,30 @@ def mask_correlated(seed: int, N: int, GH: int, GW: int, q_low: float, sigma: fl
         order = np.lexsort((np.arange(B), s[n].reshape(-1)))
         out[n, order[:nlow]] = 0
     return out.reshape(N, GH, GW)
+
+
+ENCODER_WIDTHS = (64, 128, 256, 512)
+ENCODER_STRIDES = (1, 2, 2, 2)
+
+
+def encoder_weights(seed: int, dtype: str, C_in: int = 3) -> dict:
+    """Random-init weights of the ResNet-18 encoder (folded batch norm = a
+    per-channel bias): stem 7x7 C_in->64, four stages of two basic blocks of
+    two 3x3 convolutions, a 1x1 shortcut where a block changes stride or
+    width.  Every tensor has its own tag (100 + its index), OIHW, N(0, 1/fan_in)."""
+    specs = [("stem", 64, C_in, 7)]
+    cin = 64
+    for si, (width, stride) in enumerate(zip(ENCODER_WIDTHS, ENCODER_STRIDES)):
+        for bi in range(2):
+            st = stride if bi == 0 else 1
+            p = f"s{si + 1}.b{bi}."
+            specs.append((p + "c1", width, cin, 3))
+            if st != 1 or cin != width:
+                specs.append((p + "sc", width, cin, 1))
+            specs.append((p + "c2", width, width, 3))
+            cin = width
+    out = {}
+    for i, (name, co, ci, k) in enumerate(specs):
+        out[name + ".w"] = conv_weight(seed, co, ci, k, dtype, tag=100 + 2 * i)
+        out[name + ".b"] = conv_bias(seed, co, k * k * ci, dtype, tag=101 + 2 * i)
+    return out
