@@ -144,6 +144,44 @@ int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H
                     const uint8_t* mask, int bs, const void* weight, const void* bias,
                     int C_out, void* y, hipStream_t stream);
 
+/* The encoder's block convolutions (paper: Method -- the network keeps its
+ * blocks through the downsampling stages, so blocks shrink with the map):
+ * K x K convolution, K in {1, 3}, at stride S in {1, 2}, of every block of
+ * the packed stacks, BlockPad fused for K = 3 (one pixel of halo; a stride-2
+ * output only reads the top and left halo), with the epilogue of
+ * segblocks_block_conv3x3 (bias, residual, SB_FLAG_RELU, one rounding):
+ *   out[s,co,i,j] = bias[co] + sum_{ci,ky,kx} w[co,ci,ky,kx]
+ *                   * padded[s,ci, S*i + ky + 1 - K/2, S*j + kx + 1 - K/2]
+ * hi [nh,C_in,bs,bs], lo [nl,C_in,bs/2,bs/2]
+ *   -> hi_out [nh,C_out,bs/S,bs/S], lo_out [nl,C_out,bs/(2S),bs/(2S)];
+ * residual_hi / residual_lo (or NULL) have the outputs' shapes.  H, W, bs
+ * describe the INPUT map.  weight: OHWI memory [C_out][K][K][C_in].
+ * Channels-last (SB_NHWC) fp16 / bf16 with C_in % 8 == 0 only (else
+ * SB_EINVAL); bs / 2 must be divisible by S. */
+int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout,
+                            int N, int C_in, int H, int W, const uint8_t* mask, int bs,
+                            const void* weight, const void* bias, int C_out,
+                            int ksize, int stride, int flags,
+                            const void* residual_hi, const void* residual_lo,
+                            void* hi_out, void* lo_out, int hi_cap, int lo_cap,
+                            hipStream_t stream);
+
+/* Dense convolution around the block stages (the encoder's 7x7/2 stem):
+ * x [N,C_in,H,W] -> y [N,C_out,Ho,Wo], Ho = (H + 2 pad - K) / stride + 1,
+ *   y = bias + sum w * x (zero padding), then max(0, .) if SB_FLAG_RELU.
+ * weight OHWI memory [C_out][K][K][C_in], bias [C_out] or NULL.
+ * Channels-last fp16 / bf16; the workgroup's LDS (weights padded to a
+ * multiple of 32 K values plus one input patch) must fit in 160 KiB. */
+int segblocks_conv2d(const void* x, int dtype, int layout, int N, int C_in, int H, int W,
+                     const void* weight, const void* bias, int C_out, int ksize, int stride,
+                     int pad, int flags, void* y, hipStream_t stream);
+
+/* Max-pooling (the encoder's 3x3/2 pool after the stem): y = max over the
+ * K x K window at `stride`, padding positions never win.  Channels-last,
+ * any dtype; pad < ksize. */
+int segblocks_maxpool(const void* x, int dtype, int layout, int N, int C, int H, int W,
+                      int ksize, int stride, int pad, void* y, hipStream_t stream);
+
 /* Description of the last failure on the calling thread ("" if none).  The
  * string stays valid until the next call on the same thread. */
 const char* segblocks_last_error(void);

@@ -66,10 +66,10 @@ def _stream(t: torch.Tensor):
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
 
-def _weight(weight: torch.Tensor, layout: int) -> torch.Tensor:
+def _weight(weight: torch.Tensor, layout: int, k: int = 3) -> torch.Tensor:
     """The weight in the call's memory format (OHWI memory for channels_last)."""
-    if weight.dim() != 4 or tuple(weight.shape[2:]) != (3, 3):
-        raise ValueError("weight must be [C_out, C_in, 3, 3]")
+    if weight.dim() != 4 or tuple(weight.shape[2:]) != (k, k):
+        raise ValueError(f"weight must be [C_out, C_in, {k}, {k}]")
     return weight.contiguous(memory_format=_fmt(layout))
 
 
@@ -188,4 +188,60 @@ def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bi
     y = _empty((N, C_out, H, W), x, layout) if out is None else out
     _b.call("segblocks_layer", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(mask), bs, _ptr(weight), _ptr(bias),
             C_out, _ptr(y), _stream(x))
+    return y
+
+
+def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
+                  weight: torch.Tensor, bias=None, stride: int = 1, relu: bool = False, residual=None, out=None):
+    """K x K block convolution (K = weight.shape[2], 1 or 3) at `stride` (1 or
+    2) of channels-last packed stacks, BlockPad fused, epilogue
+    act(conv + bias + residual); outputs have block sides bs/stride and
+    bs/(2 stride).  H, W, bs describe the input map."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = _b.SB_NHWC
+    _check_layout(layout, hi, lo)
+    k = weight.shape[2]
+    C_in, C_out, N = ref.shape[1], weight.shape[0], mask.shape[0]
+    weight = _weight(weight, layout, k)
+    bias = None if bias is None else bias.contiguous()
+    bo, lo_e = bs // stride, bs // 2 // stride
+    if out is None:
+        ho = _empty((hi.shape[0], C_out, bo, bo), ref, layout)
+        lo_o = _empty((lo.shape[0], C_out, lo_e, lo_e), ref, layout)
+    else:
+        ho, lo_o = out
+    rh, rl = (None, None) if residual is None else residual
+    _b.call("segblocks_block_conv_ex", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
+            _ptr(weight), _ptr(bias), C_out, k, stride, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl),
+            _ptr(ho), _ptr(lo_o), hi.shape[0], lo.shape[0], _stream(ref))
+    return ho, lo_o
+
+
+def conv2d(x: torch.Tensor, weight: torch.Tensor, bias=None, stride: int = 1, padding: int = 0,
+           relu: bool = False, out=None):
+    """Dense K x K convolution of a channels-last map with zero padding (the
+    encoder's stem), bias and optional ReLU."""
+    layout = _b.SB_NHWC
+    _check_layout(layout, x)
+    N, C_in, H, W = x.shape
+    k = weight.shape[2]
+    weight = _weight(weight, layout, k)
+    bias = None if bias is None else bias.contiguous()
+    C_out = weight.shape[0]
+    Ho, Wo = (H + 2 * padding - k) // stride + 1, (W + 2 * padding - k) // stride + 1
+    y = _empty((N, C_out, Ho, Wo), x, layout) if out is None else out
+    _b.call("segblocks_conv2d", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(weight), _ptr(bias), C_out, k,
+            stride, padding, _b.SB_FLAG_RELU if relu else 0, _ptr(y), _stream(x))
+    return y
+
+
+def maxpool(x: torch.Tensor, k: int = 3, stride: int = 2, padding: int = 1, out=None):
+    """k x k max-pooling of a channels-last map at `stride` with `padding`."""
+    layout = _b.SB_NHWC
+    _check_layout(layout, x)
+    N, C, H, W = x.shape
+    Ho, Wo = (H + 2 * padding - k) // stride + 1, (W + 2 * padding - k) // stride + 1
+    y = _empty((N, C, Ho, Wo), x, layout) if out is None else out
+    _b.call("segblocks_maxpool", _ptr(x), _dt(x), layout, N, C, H, W, k, stride, padding, _ptr(y), _stream(x))
     return y

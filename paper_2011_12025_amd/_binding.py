@@ -20,7 +20,8 @@ SB_NCHW, SB_NHWC = 0, 1
 SB_FLAG_RELU = 1
 
 EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_conv3x3", "segblocks_combine",
-           "segblocks_block_conv3x3", "segblocks_layer", "segblocks_last_error"]
+           "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
+           "segblocks_maxpool", "segblocks_last_error"]
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -33,6 +34,10 @@ _SIGS = {
     "segblocks_block_conv3x3": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I,
                                 _P],
     "segblocks_layer": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P],
+    "segblocks_block_conv_ex": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P,
+                                _I, _I, _P],
+    "segblocks_conv2d": [_P, _I, _I, _I, _I, _I, _I, _P, _P, _I, _I, _I, _I, _I, _P, _P],
+    "segblocks_maxpool": [_P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P],
 }
 
 _lib = None

@@ -242,4 +242,82 @@ int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H
     return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, mask, a, stream));
 }
 
+int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
+                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int ksize,
+                            int stride, int flags, const void* residual_hi, const void* residual_lo, void* hi_out,
+                            void* lo_out, int hi_cap, int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_block_conv_ex";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if (ksize != 1 && ksize != 3) return fail(SB_EINVAL, fn, "ksize must be 1 or 3 (got %d)", ksize);
+    if (stride != 1 && stride != 2) return fail(SB_EINVAL, fn, "stride must be 1 or 2 (got %d)", stride);
+    if ((bs / 2) % stride) return fail(SB_ESHAPE, fn, "stride %d does not divide the low block side %d", stride, bs / 2);
+    if (layout != SB_NHWC || dtype == SB_F32 || C_in % 8)
+        return fail(SB_EINVAL, fn, "supported: channels-last fp16 / bf16 with C_in %% 8 == 0");
+    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
+        return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2, bo = bs / stride, lo_e = lb / stride;
+    const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
+    const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
+    const Range rho{hi_out, hi_cap * (long long)C_out * bo * bo * es};
+    const Range rlo{lo_out, lo_cap * (long long)C_out * lo_e * lo_e * es};
+    const Range rrh{residual_hi, hi_cap * (long long)C_out * bo * bo * es};
+    const Range rrl{residual_lo, lo_cap * (long long)C_out * lo_e * lo_e * es};
+    if (any_overlap({rho, rlo}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    return hip_status(fn, sb::launch_bconv(dtype, g, mask, a, ksize, stride, stream));
+}
+
+int segblocks_conv2d(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const void* weight,
+                     const void* bias, int C_out, int ksize, int stride, int pad, int flags, void* y,
+                     hipStream_t stream) {
+    const char* fn = "segblocks_conv2d";
+    if (layout != SB_NHWC || (dtype != SB_F16 && dtype != SB_BF16))
+        return fail(SB_EINVAL, fn, "supported: channels-last fp16 / bf16");
+    if (N <= 0 || C_in <= 0 || H <= 0 || W <= 0 || C_out <= 0)
+        return fail(SB_EINVAL, fn, "N, C_in, H, W, C_out must be positive");
+    if (ksize < 1 || stride < 1 || pad < 0 || pad >= ksize)
+        return fail(SB_EINVAL, fn, "need ksize >= 1, stride >= 1, 0 <= pad < ksize (got %d, %d, %d)", ksize, stride, pad);
+    if (!x || !weight || !y) return fail(SB_EINVAL, fn, "x, weight or y is NULL");
+    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if (H + 2 * pad < ksize || W + 2 * pad < ksize) return fail(SB_ESHAPE, fn, "kernel larger than the padded map");
+    if (sb::conv2d_lds_bytes(dtype, C_in, ksize, stride) > 160 * 1024)
+        return fail(SB_ESHAPE, fn, "ksize %d, stride %d, C_in %d need more than 160 KiB of LDS", ksize, stride, C_in);
+    const long long Ho = (H + 2 * pad - ksize) / stride + 1, Wo = (W + 2 * pad - ksize) / stride + 1;
+    const long long es = esize(dtype);
+    if ((long long)N * H * W * C_in > (1LL << 40) || (long long)N * Ho * Wo * C_out > (1LL << 40))
+        return fail(SB_ESHAPE, fn, "problem too large");
+    const Range rx{x, (long long)N * C_in * H * W * es}, ry{y, (long long)N * C_out * Ho * Wo * es};
+    const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
+    if (any_overlap({ry}, {rx, rw, rb})) return fail(SB_EINVAL, fn, "y overlaps an input");
+    return hip_status(fn, sb::launch_conv2d(dtype, x, N, C_in, H, W, weight, bias, C_out, ksize, stride, pad, flags, y,
+                                            stream));
+}
+
+int segblocks_maxpool(const void* x, int dtype, int layout, int N, int C, int H, int W, int ksize, int stride, int pad,
+                      void* y, hipStream_t stream) {
+    const char* fn = "segblocks_maxpool";
+    if (dtype != SB_F32 && dtype != SB_F16 && dtype != SB_BF16) return fail(SB_EINVAL, fn, "bad dtype %d", dtype);
+    if (layout != SB_NHWC) return fail(SB_EINVAL, fn, "supported: channels-last");
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0) return fail(SB_EINVAL, fn, "N, C, H, W must be positive");
+    if (ksize < 1 || stride < 1 || pad < 0 || pad >= ksize)
+        return fail(SB_EINVAL, fn, "need ksize >= 1, stride >= 1, 0 <= pad < ksize (got %d, %d, %d)", ksize, stride, pad);
+    if (!x || !y) return fail(SB_EINVAL, fn, "x or y is NULL");
+    if (H + 2 * pad < ksize || W + 2 * pad < ksize) return fail(SB_ESHAPE, fn, "window larger than the padded map");
+    const long long Ho = (H + 2 * pad - ksize) / stride + 1, Wo = (W + 2 * pad - ksize) / stride + 1;
+    if ((long long)N * H * W * C > (1LL << 40)) return fail(SB_ESHAPE, fn, "problem too large");
+    const long long es = esize(dtype);
+    const Range rx{x, (long long)N * C * H * W * es}, ry{y, (long long)N * C * Ho * Wo * es};
+    if (any_overlap({ry}, {rx})) return fail(SB_EINVAL, fn, "y overlaps x");
+    return hip_status(fn, sb::launch_maxpool(dtype, x, N, C, H, W, ksize, stride, pad, y, stream));
+}
+
 }  // extern "C"

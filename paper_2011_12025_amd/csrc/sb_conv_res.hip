@@ -591,7 +591,6 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
                 bv[j][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
             }
         const T* __restrict__ wgt = (const T*)a.weight;
-#pragma unroll
         for (int w0 = wave * 64; w0 < 9 * RNT * RSUB; w0 += 64 * NCW) {
             const int s = w0 + lane;
             const int row = s >> 3, q = (s & 7) ^ (row & 7);

@@ -49,6 +49,17 @@ hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* 
 hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
                                int hi_cap, int lo_cap, void* y, hipStream_t st);
 
+// Encoder kernels (channels-last fp16/bf16): block convolution K x K
+// (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
+// max-pooling (any dtype).  conv2d_lds_bytes: LDS of one dense-conv workgroup.
+hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
+                        hipStream_t st);
+int conv2d_lds_bytes(int dtype, int C_in, int K, int S);
+hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W, const void* w, const void* bias,
+                         int C_out, int K, int S, int P, int flags, void* y, hipStream_t st);
+hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, int K, int S, int P, void* y,
+                          hipStream_t st);
+
 // Persistent convolution with LDS-resident weights (channels-last fp16/bf16,
 // C_in <= 64, 16 <= bs <= 64); conv_res_fits tells whether it applies.
 bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
