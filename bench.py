@@ -48,6 +48,10 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--breakdown-iters", type=int, default=100)
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle sample length (0 = skip)")
+    p.add_argument("--workload", default="layer", choices=["layer", "sweep", "encoder", "encoder-batched"],
+                   help="layer: the headline single layer (one JSON line); sweep: the four ResNet-18 stage shapes "
+                        "over low-res fractions; encoder: the N=1 ResNet-18 encoder; encoder-batched: N=4 encoders "
+                        "over mask quantiles, image block sizes and fp16/bf16 (one JSON line per point)")
     p.add_argument("--profile-run", action="store_true",
                    help="short run for rocprofv3 counters: a 256 MiB copy of known size, then the layer")
     return p.parse_args()
@@ -67,6 +71,9 @@ def main():
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the block-conv path "
               "would shard over images or block rows, see the design notes", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload != "layer":
+        return bench_suite(args)
 
     import numpy as np
     import torch
@@ -291,6 +298,237 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))
+
+
+# ---------------------------------------------------------------------------
+# configuration sweeps: the four ResNet-18 stage shapes, the encoder
+# ---------------------------------------------------------------------------
+
+SWEEP_LAYERS = [(64, 256, 512, 32), (128, 128, 256, 16), (256, 64, 128, 8), (512, 32, 64, 4)]
+SWEEP_FRACTIONS = [0.0, 0.25, 0.5, 0.75, 1.0]
+
+
+def _gpu_ms(torch, launch, iters, warm=3):
+    """Average time of `iters` back-to-back calls of launch(i), events on the
+    current stream around the batch; the GPU is held by a sleep first so
+    that the host has queued the batch before the clock starts."""
+    for i in range(warm):
+        launch(i)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(iters):
+        launch(i)
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
+def _cold_ms(torch, launch, iters, flush):
+    """Median of single calls, each after writing a 1 GiB buffer (which
+    evicts L2 and the Infinity Cache) outside the timed events."""
+    ts = []
+    for i in range(iters):
+        flush.zero_()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        launch(i)
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ts.sort()
+    return ts[len(ts) // 2]
+
+
+def _emit(d):
+    print(json.dumps(d), flush=True)
+
+
+def bench_sweep(args, torch, np, sb, B, inputs):
+    """Four 3x3 block-conv layers shaped like ResNet-18's stages of a
+    1024x2048 image, sharing one 8x16 block grid, exact-fraction masks
+    (nested over f): the fused layer (dense in, dense out) and the fused-pad
+    conv (packed in, packed out), against MIOpen's dense conv."""
+    import torch.nn.functional as F
+    lib, dev, cl = B.lib(), torch.device("cuda:0"), torch.channels_last
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    it = args.breakdown_iters
+    for li, (C, H, W, bs) in enumerate(SWEEP_LAYERS):
+        lb, es = bs // 2, 2
+        x0 = inputs.feature_map(0, 1, C, H, W, "f16")
+        w = inputs.conv_weight(0, C, C, 3, "f16").to(dev).contiguous(memory_format=cl)
+        b = inputs.conv_bias(0, C, 9 * C, "f16").to(dev)
+        map_bytes = C * H * W * es
+        R = max(2, -(-2 * MALL_BYTES // (2 * map_bytes)))
+        xs = [x0.to(dev).contiguous(memory_format=cl) for _ in range(R)]
+        ys = [torch.empty_like(xs[0]) for _ in range(R)]
+        dense_flop = 2.0 * 9 * C * C * H * W
+        miopen_ms = _gpu_ms(torch, lambda i: F.conv2d(xs[i % R], w, b, padding=1), it)
+        t_f0 = None
+        for f in SWEEP_FRACTIONS:
+            mask_np = inputs.mask_exact_fraction(0, 1, H // bs, W // bs, f)
+            nh = int(mask_np.sum()); nl = mask_np.size - nh
+            mask = torch.from_numpy(mask_np).to(dev)
+            his = [torch.empty((nh, C, bs, bs), dtype=torch.float16, device=dev, memory_format=cl) for _ in range(R)]
+            los = [torch.empty((nl, C, lb, lb), dtype=torch.float16, device=dev, memory_format=cl) for _ in range(R)]
+            hos = [torch.empty_like(t) for t in his]
+            loos = [torch.empty_like(t) for t in los]
+            for r in range(R):
+                sb.split(xs[r], mask, bs, counts=(nh, nl), out=(his[r], los[r]))
+
+            def layer(i):
+                rc = lib.segblocks_layer(P(xs[i % R]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs, P(w), P(b), C,
+                                         P(ys[i % R]), stream)
+                if rc:
+                    raise RuntimeError(lib.segblocks_last_error().decode())
+
+            def bconv(i):
+                r = i % R
+                rc = lib.segblocks_block_conv3x3(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
+                                                 P(w), P(b), C, 0, None, None, P(hos[r]), P(loos[r]), nh, nl, stream)
+                if rc:
+                    raise RuntimeError(lib.segblocks_last_error().decode())
+
+            def bconv_ex(i):
+                r = i % R
+                rc = lib.segblocks_block_conv_ex(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
+                                                 P(w), P(b), C, 3, 1, 0, None, None, P(hos[r]), P(loos[r]), nh, nl,
+                                                 stream)
+                if rc:
+                    raise RuntimeError(lib.segblocks_last_error().decode())
+
+            t_layer = _gpu_ms(torch, layer, it)
+            t_bconv = _gpu_ms(torch, bconv, it)
+            t_ex = _gpu_ms(torch, bconv_ex, it)
+            if t_f0 is None:
+                t_f0 = t_layer
+            block_flop = 2.0 * 9 * C * C * (nh * bs * bs + nl * lb * lb)
+            _emit({"workload": "sweep", "layer": li + 1, "C": C, "H": H, "W": W, "bs": bs, "low_fraction": f,
+                   "n_high": nh, "n_low": nl, "layer_us": round(t_layer * 1e3, 2),
+                   "block_conv_us": round(t_bconv * 1e3, 2), "block_conv_ex_us": round(t_ex * 1e3, 2),
+                   "miopen_conv2d_us": round(miopen_ms * 1e3, 2),
+                   "layer_effective_TFLOPs": round(dense_flop / (t_layer * 1e-3) / 1e12, 1),
+                   "layer_TFLOPs": round(block_flop / (t_layer * 1e-3) / 1e12, 1),
+                   "block_conv_TFLOPs": round(block_flop / (t_bconv * 1e-3) / 1e12, 1),
+                   "block_conv_mfma_frac": round(block_flop / (t_bconv * 1e-3) / 1e12 / FP16_PEAK_TFLOPS, 4),
+                   "speedup_vs_miopen": round(miopen_ms / t_layer, 3),
+                   "speedup_vs_ours_all_high": round(t_f0 / t_layer, 3),
+                   "theoretical_flop_speedup": round(dense_flop / block_flop, 3)})
+            del his, los, hos, loos
+        del xs, ys
+        torch.cuda.empty_cache()
+
+
+def _encoder_flop(N, H, W, mask_np, image_block):
+    """(dense, block) FLOPs of the ResNet-18 encoder at an HxW input: the
+    stem is dense in both; every stage convolution is counted on the pixels
+    it computes (a low block computes a quarter of its pixels)."""
+    from paper_2011_12025_amd.encoder import STRIDES, WIDTHS
+    nh = int(mask_np.sum()); nl = mask_np.size - nh
+    Hs, Ws = H // 2, W // 2
+    stem = 2.0 * 49 * 3 * 64 * N * Hs * Ws
+    dense, block = stem, stem
+    Hm, Wm, bs, cin = H // 4, W // 4, image_block // 4, 64
+    for width, stride in zip(WIDTHS, STRIDES):
+        for bi in range(2):
+            st = stride if bi == 0 else 1
+            bo = bs // st
+            dpx, bpx = N * (Hm // st) * (Wm // st), nh * bo * bo + nl * (bo // 2) ** 2
+            convs = [(9, cin, width), (9, width, width)]
+            if st != 1 or cin != width:
+                convs.append((1, cin, width))
+            for kk, ci, co in convs:
+                dense += 2.0 * kk * ci * co * dpx
+                block += 2.0 * kk * ci * co * bpx
+            Hm, Wm, bs, cin = Hm // st, Wm // st, bo, width
+    return dense, block
+
+
+def _dense_encoder(F, x, Wt):
+    """The ordinary ResNet-18 encoder through torch (MIOpen), the dense comparator."""
+    from paper_2011_12025_amd.encoder import STRIDES, WIDTHS
+    h = F.relu(F.conv2d(x, Wt["stem.w"], Wt["stem.b"], stride=2, padding=3))
+    h = F.max_pool2d(h, 3, 2, 1)
+    for si, (width, stride) in enumerate(zip(WIDTHS, STRIDES)):
+        for bi in range(2):
+            st = stride if bi == 0 else 1
+            p = f"s{si + 1}.b{bi}."
+            h1 = F.relu(F.conv2d(h, Wt[p + "c1.w"], Wt[p + "c1.b"], stride=st, padding=1))
+            sc = F.conv2d(h, Wt[p + "sc.w"], Wt[p + "sc.b"], stride=st) if p + "sc.w" in Wt else h
+            h = F.relu(F.conv2d(h1, Wt[p + "c2.w"], Wt[p + "c2.b"], padding=1) + sc)
+    return h
+
+
+def bench_encoder(args, torch, np, sb, B, inputs, batched):
+    """ResNet-18 encoder forward at 1024x2048: the block encoder replayed as
+    one HIP graph (warm: back to back; cold: after evicting the caches), our
+    all-high encoder, and the dense encoder through MIOpen."""
+    import torch.nn.functional as F
+    from paper_2011_12025_amd.encoder import BlockEncoder
+    dev, cl = torch.device("cuda:0"), torch.channels_last
+    H, W = 1024, 2048
+    it = max(10, args.breakdown_iters // 5)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    if batched:
+        N, dtypes, blocks, qs, kind = 4, ["f16", "bf16"], [64, 128, 256], [0.25, 0.5, 0.75], "correlated"
+    else:
+        N, dtypes, blocks, qs, kind = 1, ["f16"], [128], [0.5], "bernoulli"
+    TD = {"f16": torch.float16, "bf16": torch.bfloat16}
+    for dt in dtypes:
+        x = inputs.feature_map(0, N, 3, H, W, dt).to(dev).contiguous(memory_format=cl)
+        Wt = inputs.encoder_weights(0, dt)
+        Wd = {k: (v.to(dev).contiguous(memory_format=cl) if v.dim() == 4 else v.to(dev)) for k, v in Wt.items()}
+        dense_ms = _gpu_ms(torch, lambda i: _dense_encoder(F, x, Wd), it)
+        dense_cold = _cold_ms(torch, lambda i: _dense_encoder(F, x, Wd), it, flush)
+        for blk in blocks:
+            GH, GW = H // blk, W // blk
+            enc = BlockEncoder(Wt, blk)
+            ones = torch.ones((N, GH, GW), dtype=torch.uint8, device=dev)
+            g1, _ = enc.capture(x, ones, (N * GH * GW, 0))
+            allhigh_ms = _gpu_ms(torch, lambda i: g1.replay(), it)
+            del g1
+            for q in qs:
+                if kind == "correlated":
+                    mask_np = inputs.mask_correlated(0, N, GH, GW, q)
+                else:
+                    mask_np = inputs.mask_bernoulli(0, N, GH, GW, q)
+                nh = int(mask_np.sum()); nl = mask_np.size - nh
+                mask = torch.from_numpy(mask_np).to(dev)
+                g, y = enc.capture(x, mask, (nh, nl))
+                warm = _gpu_ms(torch, lambda i: g.replay(), it)
+                cold = _cold_ms(torch, lambda i: g.replay(), it, flush)
+                dense_flop, block_flop = _encoder_flop(N, H, W, mask_np, blk)
+                _emit({"workload": "encoder-batched" if batched else "encoder", "dtype": dt, "N": N,
+                       "image": f"{H}x{W}x3", "image_block": blk, "mask": kind, "low_fraction": q,
+                       "n_high": nh, "n_low": nl, "ms_warm": round(warm, 4), "ms_cold": round(cold, 4),
+                       "images_per_s": round(N / (warm * 1e-3), 1),
+                       "effective_TFLOPs": round(dense_flop / (warm * 1e-3) / 1e12, 1),
+                       "block_TFLOPs": round(block_flop / (warm * 1e-3) / 1e12, 1),
+                       "dense_GFLOP": round(dense_flop / 1e9, 2), "block_GFLOP": round(block_flop / 1e9, 2),
+                       "ours_all_high_ms": round(allhigh_ms, 4), "miopen_dense_ms": round(dense_ms, 4),
+                       "miopen_dense_cold_ms": round(dense_cold, 4),
+                       "speedup_vs_miopen": round(dense_ms / warm, 3),
+                       "speedup_vs_ours_all_high": round(allhigh_ms / warm, 3),
+                       "theoretical_flop_speedup": round(dense_flop / block_flop, 3)})
+                del g, y
+            del enc
+            torch.cuda.empty_cache()
+
+
+def bench_suite(args):
+    import numpy as np
+    import torch
+
+    import paper_2011_12025_amd as sb
+    import paper_2011_12025_amd._binding as B
+    from paper_2011_12025_amd import inputs
+    torch.cuda.set_device(0)
+    if args.workload == "sweep":
+        bench_sweep(args, torch, np, sb, B, inputs)
+    else:
+        bench_encoder(args, torch, np, sb, B, inputs, batched=args.workload == "encoder-batched")
 
 
 if __name__ == "__main__":

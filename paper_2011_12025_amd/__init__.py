@@ -88,18 +88,22 @@ def count(mask: torch.Tensor):
     return nh.value, nl.value
 
 
-def split(x: torch.Tensor, mask: torch.Tensor, bs: int, counts=None, layout=None):
+def split(x: torch.Tensor, mask: torch.Tensor, bs: int, counts=None, layout=None, out=None):
     """BlockSample: returns (hi [nh,C,bs,bs], lo [nl,C,bs/2,bs/2]).
 
-    ``counts`` = (n_high, n_low) sizes the stacks; without it they are counted
-    (one host synchronisation)."""
+    ``counts`` = (n_high, n_low) sizes the stacks; without it (and without
+    ``out``) they are counted (one host synchronisation)."""
     mask = _mask(mask)
     layout = layout_of(x) if layout is None else layout
     _check_layout(layout, x)
     N, C, H, W = x.shape
-    nh, nl = counts if counts is not None else count(mask)
-    hi = _empty((nh, C, bs, bs), x, layout)
-    lo = _empty((nl, C, bs // 2, bs // 2), x, layout)
+    if out is not None:
+        hi, lo = out
+        nh, nl = hi.shape[0], lo.shape[0]
+    else:
+        nh, nl = counts if counts is not None else count(mask)
+        hi = _empty((nh, C, bs, bs), x, layout)
+        lo = _empty((nl, C, bs // 2, bs // 2), x, layout)
     _b.call("segblocks_split", _ptr(x), _dt(x), layout, N, C, H, W, _ptr(mask), bs, _ptr(hi), nh, _ptr(lo), nl,
             _stream(x))
     return hi, lo

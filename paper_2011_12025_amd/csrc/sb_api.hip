@@ -273,6 +273,7 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
     if (any_overlap({rho, rlo}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
         return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
     sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    if (sb::igemm_fits(dtype, layout, g, a)) return hip_status(fn, sb::launch_igemm(dtype, g, mask, a, ksize, stride, stream));
     return hip_status(fn, sb::launch_bconv(dtype, g, mask, a, ksize, stride, stream));
 }
 

@@ -482,6 +482,8 @@ hipError_t conv_t(int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint
 hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
                        const ConvArgs& a, hipStream_t st) {
     if (conv_res_fits(dtype, layout, g, a)) return launch_conv_res(dtype, src, dst, g, mask, a, st);
+    if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits(dtype, layout, g, a))
+        return launch_igemm(dtype, g, mask, a, 3, 1, st);
     switch (dtype) {
     case 0: return conv_t<float>(layout, src, dst, g, mask, a, st);
     case 1: return conv_t<f16>(layout, src, dst, g, mask, a, st);

@@ -1,0 +1,670 @@
+// Block convolutions of packed channels-last stacks as one implicit GEMM over
+// the pixels of many blocks (the deeper layers of the encoder, where blocks
+// shrink to a few pixels and the channel counts grow).
+//
+// GEMM view: rows = output pixels of one class's stack, in stack order (slot,
+// row, column), so a workgroup tile spans as many blocks as it takes; columns
+// = output channels; K = taps x input channels, walked in steps of one tap
+// and 64 channels (128 bytes of every pixel and of every weight row).
+//
+// BlockPad is fused into the pixel gather.  At start-up a workgroup builds
+// the block plan in LDS (for every block the number of high blocks before
+// it, by a workgroup-wide scan of the mask) and then, for each of its tile
+// pixels and taps, a source descriptor: a pixel of the high or the low stack
+// (own block, same-resolution neighbour, or the low neighbour's pixel
+// nearest-upsampled), the 2x2 cell of a high neighbour to average, or zero
+// (outside the image, or a neighbour past its stack's capacity).  Stride-2
+// and 1x1 convolutions only change which padded pixel a tap reads.
+//
+// Pipeline (three LDS stages): weights and pixels of step s+2 go global ->
+// LDS by DMA (global_load_lds, 16 bytes per lane) while the MFMAs of step s
+// run, so every wave issues the same number of DMAs per step and waits for
+// step s+1 with a constant count.  A pixel that is a 2x2 average gets its
+// top-left source by that DMA; its three other sources are copied into a side
+// buffer of LDS (issued one step ahead, before the next step's DMAs, so the
+// same wait covers them), then averaged in fp32 in the library's fixed order
+// over the top-left value.  Rows of 128
+// bytes carry an XOR swizzle of their 16-byte chunks so that the 16 rows
+// read by one MFMA operand hit distinct banks.
+//
+// Split K: when the tiles alone do not fill the chip, the K steps of a tile
+// are divided among grid.z workgroups that write fp32 partial tiles to a
+// workspace owned by the library; a second kernel sums them in split order
+// (deterministic) and runs the epilogue.
+//
+// MFMA: v_mfma_f32_16x16x32_{f16,bf16}, weights as A (16 output channels),
+// pixels as B (16 pixels).  Eight waves (two per SIMD, so that one wave's
+// address work overlaps the other's MFMAs) in a WM x (8 / WM) grid, each
+// 16 x MS pixel and 16 x NS channel fragments.  The weight rows of each 32-channel group
+// are permuted in LDS so that a lane ends with 8 consecutive output channels
+// of one pixel and stores them as one 16-byte write.
+#include <mutex>
+
+#include "sb_common.h"
+#include "sb_kernels.h"
+
+namespace sb {
+
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+template <typename T> struct GMF;
+template <> struct GMF<f16> {
+    typedef halfx8 frag;
+    static __device__ __forceinline__ floatx4 mma(frag a, frag b, floatx4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+};
+template <> struct GMF<bf16> {
+    typedef bf16x8 frag;
+    static __device__ __forceinline__ floatx4 mma(frag a, frag b, floatx4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+constexpr int GROWB = 128;     // LDS bytes per row: 64 channels of one pixel / one weight row
+constexpr int GKC = 64;        // channels per K step
+constexpr int GWAVES = 8;      // waves per workgroup
+constexpr int GWG = 64 * GWAVES;
+constexpr int GNST = 3;        // LDS stages
+constexpr int GMAXB = 8192;    // blocks whose plan fits the LDS table
+constexpr int GMAXC = 4096;    // input channels the zero row covers
+
+// A row of zeros that pixels outside the image (and 2x2-average pixels before
+// their average is written) are copied from; device globals start zeroed and
+// this one is never written.
+__device__ __align__(16) uint4 g_zero_row[GMAXC * 2 / 16];
+
+// source descriptor: kind in bits 30..31, pixel index (in its stack) below
+constexpr uint32_t GK_HI = 0u, GK_LO = 1u, GK_AVG = 2u, GK_ZERO = 3u;
+__device__ __forceinline__ uint32_t gdesc(uint32_t kind, int pix) { return (kind << 30) | (uint32_t)pix; }
+
+// byte offset of 16-byte chunk q of LDS row r (XOR swizzle, see above)
+__device__ __forceinline__ int gsw(int r, int q) { return r * GROWB + ((q ^ ((r >> 1) & 7)) << 4); }
+
+// output channel held by LDS weight row r of a tile (within its 32-row group:
+// row 16h + l, l = 4 kg + i, holds channel 8 kg + 4 h + i)
+__device__ __forceinline__ int gperm(int r) {
+    const int l = r & 15;
+    return (r & ~31) + (l >> 2) * 8 + ((r >> 4) & 1) * 4 + (l & 3);
+}
+
+// s_waitcnt operand that waits until at most n vector-memory operations are
+// outstanding (lgkm and export counts left alone)
+constexpr unsigned gvm_wait(int n) { return 0x0F70u | (unsigned)(n & 0xF) | ((unsigned)(n >> 4) << 14); }
+
+// Workgroup barrier without the memory fences of __syncthreads (which would
+// wait for the DMAs of the step after next): LDS writes are waited for here,
+// DMAs by the explicit count before it.
+__device__ __forceinline__ void gbarrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// 16-byte LDS read and write that complete before returning.  Written as
+// inline assembly so that the compiler, which cannot tell the step that just
+// landed from the DMAs still in flight, does not wait for all of them first.
+typedef unsigned int gu32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 glds_read16(const void* p) {
+    gu32x4 r;
+    const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)p;
+    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(a) : "memory");
+    return uint4{r.x, r.y, r.z, r.w};
+}
+__device__ __forceinline__ void glds_write16(void* p, uint4 v) {
+    const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)p;
+    const gu32x4 w = {v.x, v.y, v.z, v.w};
+    asm volatile("ds_write_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" ::"v"(a), "v"(w) : "memory");
+}
+
+__device__ __forceinline__ void gdma16(const void* g, unsigned char* window) {
+    __builtin_amdgcn_global_load_lds(g, (lds_ptr)window, 16, 0, 0);
+}
+
+// ((a + b) + (c + d)) * 0.25 per element of four 16-byte vectors of T
+template <typename T>
+__device__ __forceinline__ uint4 gavg(uint4 a, uint4 b, uint4 c, uint4 d) {
+    Vec<T, 8> va, vb, vc, vd, r;
+    va.raw = a; vb.raw = b; vc.raw = c; vd.raw = d;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r.e[i] = avg4(va.e[i], vb.e[i], vc.e[i], vd.e[i]);
+    return r.raw;
+}
+
+// Smallest block k whose class-c count through k exceeds s (the block of
+// slot s of class c); hb[k] = high blocks before block k.
+__device__ __forceinline__ int gblock_of(const uint16_t* hb, int B, int c, int s) {
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        const int cnt = c ? (int)hb[mid + 1] : (mid + 1 - (int)hb[mid + 1]);
+        if (cnt > s) hi = mid;
+        else lo = mid + 1;
+    }
+    return lo;
+}
+
+// DMA of one step's weight rows: wrow[j] points at this lane's chunk of its
+// weight row, off selects the tap and the 64 channels.
+template <typename T, int AR>
+__device__ __forceinline__ void gissue_a(const T* const (&wrow)[AR], unsigned char* st, int off, int wave) {
+#pragma unroll
+    for (int j = 0; j < AR; ++j) gdma16(wrow[j] + off, st + (wave * AR + j) * 1024);
+}
+
+// DMA of one step's pixel rows (zeros for pixels outside the image; the
+// top-left source of a 2x2-average pixel).
+template <typename T, int BR>
+__device__ __forceinline__ void gissue_b(const uint32_t* s_desc, const int (&prow)[BR], const int (&pq)[BR], int KT,
+                                         int tap, int c, const T* __restrict__ in_hi, const T* __restrict__ in_lo,
+                                         const T* zrow, int C_in, unsigned char* st, int wave) {
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        const uint32_t d = s_desc[prow[j] * KT + tap];
+        const uint32_t kind = d >> 30;
+        const T* base = kind == GK_LO ? in_lo : (kind == GK_ZERO ? zrow : in_hi);
+        const size_t pix = kind != GK_ZERO ? (size_t)(d & 0x3FFFFFFFu) : 0;
+        gdma16(base + pix * C_in + c + pq[j], st + (wave * BR + j) * 1024);
+    }
+}
+
+// N DMAs of zeros into a stage that no step reads (keeps the count per step constant)
+template <typename T, int N>
+__device__ __forceinline__ void gissue_pad(const T* zrow, unsigned char* st, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) gdma16(zrow + (lane & 7) * 8, st + (wave * N + j) * 1024);
+}
+
+// The three other sources (right, below, below-right) of this lane's
+// 2x2-average pixels of one step, copied into the side buffer: window
+// (wave * BR + j) * 3 + t, this lane's slot at lane * 16.
+template <typename T, int BR>
+__device__ __forceinline__ void gissue_side(const uint32_t* s_desc, const int (&prow)[BR], const int (&pq)[BR], int KT,
+                                            int tap, int c, const T* __restrict__ in_hi, int C_in, int bs,
+                                            unsigned char* side, int wave) {
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        const uint32_t d = s_desc[prow[j] * KT + tap];
+        if ((d >> 30) == GK_AVG) {
+            const T* p0 = in_hi + (size_t)(d & 0x3FFFFFFFu) * C_in + c + pq[j];
+            unsigned char* w = side + (wave * BR + j) * 3 * 1024;
+            gdma16(p0 + C_in, w);
+            gdma16(p0 + (size_t)bs * C_in, w + 1024);
+            gdma16(p0 + (size_t)(bs + 1) * C_in, w + 2048);
+        }
+    }
+}
+
+// Replaces the top-left value of every 2x2-average pixel of a landed step
+// (st: the step's pixel tile) by the average of its four sources.
+template <typename T, int BR>
+__device__ __forceinline__ void gcommit_side(const uint32_t* s_desc, const int (&prow)[BR], int KT, int tap,
+                                             unsigned char* st, const unsigned char* side, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        const uint32_t d = s_desc[prow[j] * KT + tap];
+        if ((d >> 30) == GK_AVG) {
+            unsigned char* slot = st + (wave * BR + j) * 1024 + lane * 16;
+            const unsigned char* w = side + (wave * BR + j) * 3 * 1024 + lane * 16;
+            const uint4 va = glds_read16(slot), vb = glds_read16(w), vc = glds_read16(w + 1024),
+                        vd = glds_read16(w + 2048);
+            glds_write16(slot, gavg<T>(va, vb, vc, vd));
+        }
+    }
+}
+
+struct GParams {
+    int tiles_h;    // M tiles of the high class (the low class's follow)
+    int eo_h, eo_l; // output extents
+    int cpt;        // K steps per tap (C_in / 64)
+    int splits;     // workgroups sharing the K steps of a tile (grid.z)
+    float* part;    // fp32 partial tiles [tile][n tile][split][TM * TN] when splits > 1
+    int* rows;      // valid output rows of each M tile, written when splits > 1
+};
+
+// Bias, residual, ReLU and the store of a finished tile: lane holds channels
+// co0 + wn*NS*16 + jj*32 + kg*8 + 0..7 of pixel row m0 + wm*MS*16 + ms*16 + l16.
+template <typename T, int WM, int MS, int NS>
+__device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const ConvArgs& a, int high, int m0,
+                                          int rows_valid, int co0) {
+    const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
+    const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
+    const int C_out = a.C_out;
+    const T* __restrict__ bias = (const T*)a.bias;
+    const T* __restrict__ res = (const T*)(high ? a.res_hi : a.res_lo);
+    T* __restrict__ out = (T*)(high ? a.out_hi : a.out_lo);
+    const bool relu = (a.flags & 1) != 0;
+#pragma unroll
+    for (int jj = 0; jj < NS / 2; ++jj) {
+        const int co = co0 + wn * NS * 16 + jj * 32 + kg * 8;
+        if (co >= C_out) continue;
+        float bv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) bv[i] = bias ? to_f32(bias[co + i]) : 0.0f;
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms) {
+            const int m = m0 + wm * MS * 16 + ms * 16 + l16;
+            if (m >= rows_valid) continue;
+            float f[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f[i] = acc[ms][2 * jj][i] + bv[i];
+                f[4 + i] = acc[ms][2 * jj + 1][i] + bv[4 + i];
+            }
+            const size_t off = (size_t)m * C_out + co;
+            if (res) {
+                Vec<T, 8> rv;
+                rv.raw = *reinterpret_cast<const uint4*>(res + off);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
+            }
+            Vec<T, 8> o;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
+            *reinterpret_cast<uint4*>(out + off) = o.raw;
+        }
+    }
+}
+
+// fp32 partial tile of one split: fragment (ms, ns) of a wave is 64 lanes x 16 bytes, contiguous
+template <int TILE, int MS, int NS>
+__device__ __forceinline__ size_t gpart_off(int tile_lin, int split, int splits, int wave, int ms, int ns, int lane) {
+    return ((size_t)tile_lin * splits + split) * TILE + ((size_t)((wave * MS + ms) * NS + ns) * 64 + lane) * 4;
+}
+
+template <typename T, int KS, int ST, int WM, int MS, int NS>
+__global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, GParams gp) {
+    typedef GMF<T> mf;
+    typedef typename mf::frag frag;
+    constexpr int KT = KS * KS;
+    constexpr int WN = GWAVES / WM;
+    constexpr int TM = WM * MS * 16, TN = WN * NS * 16;
+    constexpr int A_BYTES = TN * GROWB, B_BYTES = TM * GROWB, STAGE = A_BYTES + B_BYTES;
+    constexpr int BR = TM / (8 * GWAVES);   // pixel rows of 8 per wave per step (one DMA each)
+    constexpr int AR = TN / (8 * GWAVES);   // weight rows of 8 per wave per step
+    static_assert(BR >= 1 && AR >= 1 && NS % 2 == 0, "tile shape");
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* s_stage = smem;
+    uint32_t* s_desc = reinterpret_cast<uint32_t*>(smem + GNST * STAGE);
+    int* s_pk = reinterpret_cast<int*>(smem + GNST * STAGE + TM * KT * 4);
+    int* s_pij = s_pk + TM;
+    unsigned char* s_side = smem + GNST * STAGE + TM * KT * 4 + 2 * TM * 4;
+    uint16_t* s_hb = reinterpret_cast<uint16_t*>(s_side + GWAVES * BR * 3 * 1024);
+    __shared__ int s_wsum[GWAVES];
+
+    const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int B = (int)g.B;
+
+    // ---- block plan: s_hb[k] = high blocks before k (k = 0..B)
+    {
+        const int per = (B + GWG - 1) / GWG;
+        const int k0 = tid * per;
+        int c = 0;
+        for (int i = 0; i < per; ++i) {
+            const int k = k0 + i;
+            if (k < B) c += mask[k] != 0;
+        }
+        int x = c;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int y = __shfl_up(x, d, 64);
+            if (lane >= d) x += y;
+        }
+        if (lane == 63) s_wsum[wave] = x;
+        __syncthreads();
+        int run = x - c;
+        for (int w = 0; w < wave; ++w) run += s_wsum[w];
+        for (int i = 0; i < per; ++i) {
+            const int k = k0 + i;
+            if (k < B) {
+                s_hb[k] = (uint16_t)run;
+                run += mask[k] != 0;
+            }
+        }
+        if (tid == GWG - 1) s_hb[B] = (uint16_t)run;
+        __syncthreads();
+    }
+    const int n_high = s_hb[B];
+    const int high = (int)blockIdx.x < gp.tiles_h;
+    const int mt = high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h;
+    const int eo = high ? gp.eo_h : gp.eo_l;
+    const int eo2 = eo * eo;
+    const int count = min(high ? n_high : B - n_high, high ? a.hi_cap : a.lo_cap);
+    const int rows_valid = count * eo2;
+    const int m0 = mt * TM;
+    if (gp.splits > 1 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0) gp.rows[blockIdx.x] = rows_valid;
+    if (m0 >= rows_valid) return;  // uniform over the workgroup
+    const int co0 = (int)blockIdx.y * TN;
+    const int bs = g.bs, lb = bs >> 1;
+    const int e_in = high ? bs : lb;
+    const int C_in = a.C_in, C_out = a.C_out;
+    const int cpt = gp.cpt;
+    const int nsteps = KT * cpt;
+    const int z = (int)blockIdx.z;
+    const int s_first = z * nsteps / gp.splits;
+    const int n = (z + 1) * nsteps / gp.splits - s_first;  // steps of this workgroup (>= 1)
+
+    // this lane's DMA rows and chunks: LDS slot (lane & 7) of row r holds global chunk (lane & 7) ^ ((r >> 1) & 7)
+    const T* wrow[AR];
+#pragma unroll
+    for (int j = 0; j < AR; ++j) {
+        const int r = (wave * AR + j) * 8 + (lane >> 3);
+        const int co = min(co0 + gperm(r), C_out - 1);
+        wrow[j] = (const T*)a.weight + (size_t)co * KT * C_in + (((lane & 7) ^ ((r >> 1) & 7)) * 8);
+    }
+    int prow[BR], pq[BR];
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        prow[j] = (wave * BR + j) * 8 + (lane >> 3);
+        pq[j] = ((lane & 7) ^ ((prow[j] >> 1) & 7)) * 8;
+    }
+    const T* __restrict__ in_hi = (const T*)a.in_hi;
+    const T* __restrict__ in_lo = (const T*)a.in_lo;
+    const T* zrow = reinterpret_cast<const T*>(g_zero_row);
+
+    // the first step's weights are in flight while the descriptors are built
+    int tap0 = s_first / cpt, c0 = s_first - (s_first / cpt) * cpt;
+    gissue_a<T, AR>(wrow, s_stage, tap0 * C_in + c0 * GKC, wave);
+
+    // ---- source descriptors: first the block and position of each tile pixel,
+    // then (pixel, tap) pairs over the whole workgroup
+    if (tid < TM) {
+        const int m = m0 + tid;
+        int k = -1, ij = 0;
+        if (m < rows_valid) {
+            const int slot = m / eo2;
+            const int rem = m - slot * eo2;
+            const int i = rem / eo;
+            ij = (i << 16) | (rem - i * eo);
+            k = gblock_of(s_hb, B, high, slot);
+        }
+        s_pk[tid] = k;
+        s_pij[tid] = ij;
+    }
+    __syncthreads();
+    const int per_img = g.GH * g.GW;
+    for (int idx = tid; idx < TM * KT; idx += GWG) {
+        const int p = idx / KT, t = idx - (idx / KT) * KT;
+        const int k = s_pk[p];
+        uint32_t ds = gdesc(GK_ZERO, 0);
+        if (k >= 0) {
+            const int i = s_pij[p] >> 16, j = s_pij[p] & 0xFFFF;
+            const int kbefore = s_hb[k];
+            const int slot = high ? kbefore : k - kbefore;
+            const int ky = t / KS, kx = t - (t / KS) * KS;
+            const int uu = ST * i + ky - KS / 2, vv = ST * j + kx - KS / 2;
+            const int dy = uu < 0 ? -1 : (uu >= e_in ? 1 : 0);
+            const int dx = vv < 0 ? -1 : (vv >= e_in ? 1 : 0);
+            if (dy == 0 && dx == 0) {
+                ds = gdesc(high ? GK_HI : GK_LO, (slot * e_in + uu) * e_in + vv);
+            } else {
+                const int nn = k / per_img;
+                const int r = k - nn * per_img;
+                const int gy = r / g.GW, gx = r - (r / g.GW) * g.GW;
+                const int ny = gy + dy, nx = gx + dx;
+                if (ny >= 0 && ny < g.GH && nx >= 0 && nx < g.GW) {
+                    const int k2 = (nn * g.GH + ny) * g.GW + nx;
+                    const int before = s_hb[k2];
+                    const int h2 = (int)s_hb[k2 + 1] - before;
+                    const int s2 = h2 ? before : k2 - before;
+                    const int u2 = uu - dy * e_in, v2 = vv - dx * e_in;
+                    if (s2 < (h2 ? a.hi_cap : a.lo_cap)) {
+                        if (h2 == high) ds = gdesc(high ? GK_HI : GK_LO, (s2 * e_in + u2) * e_in + v2);
+                        else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
+                        else ds = gdesc(GK_AVG, (s2 * bs + 2 * u2) * bs + 2 * v2);
+                    }
+                }
+            }
+        }
+        s_desc[idx] = ds;
+    }
+    __syncthreads();
+
+    // ---- prologue: step 0 (2x2 averages, pixels), step 1 (weights, pixels)
+    int tap1 = tap0, c1 = c0 + 1;
+    if (c1 == cpt) { c1 = 0; ++tap1; }
+    gissue_side<T, BR>(s_desc, prow, pq, KT, tap0, c0 * GKC, in_hi, C_in, bs, s_side, wave);
+    gissue_b<T, BR>(s_desc, prow, pq, KT, tap0, c0 * GKC, in_hi, in_lo, zrow, C_in, s_stage + A_BYTES, wave);
+    if (n > 1) {
+        gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
+        gissue_b<T, BR>(s_desc, prow, pq, KT, tap1, c1 * GKC, in_hi, in_lo, zrow, C_in, s_stage + STAGE + A_BYTES,
+                        wave);
+    } else {
+        gissue_pad<T, AR + BR>(zrow, s_stage + STAGE, wave, lane);
+    }
+    __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
+    gcommit_side<T, BR>(s_desc, prow, KT, tap0, s_stage + A_BYTES, s_side, wave, lane);
+    gbarrier();
+
+    floatx4 acc[MS][NS];
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns) acc[ms][ns] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    const int wm = wave % WM, wn = wave / WM;
+    const int l16 = lane & 15, kg = lane >> 4;
+    // (tap, chunk) of step s + 1 and s + 2
+    int ta = tap1, ca = c1;
+    int tb = tap1, cb = c1 + 1;
+    if (cb == cpt) { cb = 0; ++tb; }
+    int b_cur = 0;
+
+    for (int s = 0; s < n; ++s) {
+        unsigned char* cur = s_stage + b_cur * STAGE;
+        const int b1 = b_cur == GNST - 1 ? 0 : b_cur + 1;
+        const int b2 = b1 == GNST - 1 ? 0 : b1 + 1;
+        if (s + 1 < n) gissue_side<T, BR>(s_desc, prow, pq, KT, ta, ca * GKC, in_hi, C_in, bs, s_side, wave);
+        if (s + 2 < n) {
+            gissue_a<T, AR>(wrow, s_stage + b2 * STAGE, tb * C_in + cb * GKC, wave);
+            gissue_b<T, BR>(s_desc, prow, pq, KT, tb, cb * GKC, in_hi, in_lo, zrow, C_in,
+                            s_stage + b2 * STAGE + A_BYTES, wave);
+        } else {
+            gissue_pad<T, AR + BR>(zrow, s_stage + b2 * STAGE, wave, lane);
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            frag af[NS], bf[MS];
+#pragma unroll
+            for (int ns = 0; ns < NS; ++ns)
+                af[ns] = *reinterpret_cast<const frag*>(cur + gsw(wn * NS * 16 + ns * 16 + l16, ks * 4 + kg));
+#pragma unroll
+            for (int ms = 0; ms < MS; ++ms)
+                bf[ms] = *reinterpret_cast<const frag*>(cur + A_BYTES + gsw(wm * MS * 16 + ms * 16 + l16, ks * 4 + kg));
+#pragma unroll
+            for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+                for (int ns = 0; ns < NS; ++ns) acc[ms][ns] = mf::mma(af[ns], bf[ms], acc[ms][ns]);
+        }
+        // step s + 1 has landed once only step s + 2's DMAs can be outstanding
+        __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
+        if (s + 1 < n) gcommit_side<T, BR>(s_desc, prow, KT, ta, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
+        gbarrier();
+        b_cur = b1;
+        ta = tb; ca = cb;
+        if (++cb == cpt) { cb = 0; ++tb; }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the padding DMAs
+
+    if (gp.splits == 1) {
+        gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0);
+    } else {
+        const int tile_lin = (int)blockIdx.x * (int)gridDim.y + (int)blockIdx.y;
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+            for (int ns = 0; ns < NS; ++ns)
+                *reinterpret_cast<floatx4*>(gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, ns,
+                                                                                lane)) = acc[ms][ns];
+    }
+}
+
+// Sums the split partial tiles in split order and runs the epilogue.
+template <typename T, int WM, int MS, int NS>
+__global__ __launch_bounds__(GWG) void k_igemm_reduce(ConvArgs a, GParams gp) {
+    constexpr int WN = GWAVES / WM;
+    constexpr int TM = WM * MS * 16, TN = WN * NS * 16;
+    const int rows_valid = gp.rows[blockIdx.x];
+    const int high = (int)blockIdx.x < gp.tiles_h;
+    const int m0 = (high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h) * TM;
+    if (m0 >= rows_valid) return;
+    const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
+    const int tile_lin = (int)blockIdx.x * (int)gridDim.y + (int)blockIdx.y;
+    floatx4 acc[MS][NS];
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns)
+            acc[ms][ns] = *reinterpret_cast<const floatx4*>(
+                gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, ns, lane));
+    for (int z = 1; z < gp.splits; ++z) {
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+            for (int ns = 0; ns < NS; ++ns)
+                acc[ms][ns] += *reinterpret_cast<const floatx4*>(
+                    gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, ns, lane));
+    }
+    gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, (int)blockIdx.y * TN);
+}
+
+// One workspace per device for the split partials, grown on demand (never
+// while the stream is being captured into a graph).  A buffer that is
+// outgrown is not freed, since a graph captured earlier may still use it:
+// every buffer lives until the process ends (at most twice the largest
+// request in total).  Calls that run concurrently on one device share the
+// workspace and must be ordered by the caller.
+struct GPool {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+GPool g_pool[64];
+std::mutex g_pool_mu;
+
+hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    GPool& P = g_pool[dev];
+    if (P.bytes < bytes) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(st, &cs);
+        if (e != hipSuccess) return e;
+        if (cs != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
+        size_t nb = 16u << 20;
+        while (nb < bytes) nb <<= 1;
+        void* p = nullptr;
+        e = hipMalloc(&p, nb);
+        if (e != hipSuccess) return e;
+        P.p = p;
+        P.bytes = nb;
+    }
+    *out = P.p;
+    return hipSuccess;
+}
+
+int g_cus = 0;
+
+inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <int TM, int TN, int KT>
+constexpr int igemm_smem_fixed() {
+    return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4 + GWAVES * (TM / (8 * GWAVES)) * 3 * 1024;
+}
+
+template <typename T, int KS, int ST, int WM, int MS, int NS>
+hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
+    constexpr int TM = WM * MS * 16, TN = (GWAVES / WM) * NS * 16;
+    const int eo_h = g.bs / ST, eo_l = (g.bs / 2) / ST;
+    GParams gp;
+    gp.eo_h = eo_h;
+    gp.eo_l = eo_l;
+    gp.cpt = a.C_in / GKC;
+    gp.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + TM - 1) / TM);
+    const int tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + TM - 1) / TM);
+    const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
+    static int attr = 0;
+    if (smem > attr) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_igemm<T, KS, ST, WM, MS, NS>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+        attr = smem;
+    }
+    const int tiles = gp.tiles_h + tiles_l;
+    if (tiles == 0) return hipSuccess;
+    const int tiles_n = (a.C_out + TN - 1) / TN;
+    // split K while the workgroups do not cover the compute units once and
+    // every split keeps at least four K steps
+    if (g_cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&g_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || g_cus <= 0)
+            g_cus = 256;
+    }
+    const int nsteps = KS * KS * gp.cpt;
+    int S = 1;
+    while (S < 16 && (long long)tiles * tiles_n * S < g_cus && nsteps / (2 * S) >= 4) S *= 2;
+    gp.splits = S;
+    gp.part = nullptr;
+    gp.rows = nullptr;
+    if (S > 1) {
+        const size_t part_bytes = (size_t)tiles * tiles_n * S * TM * TN * 4;
+        void* ws = nullptr;
+        hipError_t e = gworkspace(part_bytes + (size_t)tiles * 4, st, &ws);
+        if (e != hipSuccess) return e;
+        gp.part = (float*)ws;
+        gp.rows = (int*)((char*)ws + part_bytes);
+    }
+    const dim3 grid((unsigned)tiles, (unsigned)tiles_n, (unsigned)S);
+    hipLaunchKernelGGL((k_igemm<T, KS, ST, WM, MS, NS>), grid, dim3(GWG), smem, st, g, mask, a, gp);
+    if (S > 1) {
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_igemm_reduce<T, WM, MS, NS>), dim3((unsigned)tiles, (unsigned)tiles_n), dim3(GWG), 0, st,
+                           a, gp);
+    }
+    return hipGetLastError();
+}
+
+template <typename T, int KS, int ST>
+hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
+    if (a.C_out <= 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, st);
+    return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, st);
+}
+
+template <typename T>
+hipError_t igemm_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ks, int stride, hipStream_t st) {
+    if (ks == 3) return stride == 1 ? igemm_tile<T, 3, 1>(g, mask, a, st) : igemm_tile<T, 3, 2>(g, mask, a, st);
+    return stride == 1 ? igemm_tile<T, 1, 1>(g, mask, a, st) : igemm_tile<T, 1, 2>(g, mask, a, st);
+}
+
+}  // namespace
+
+bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
+    if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
+    if (a.C_in % GKC || a.C_in > GMAXC || a.C_out % 8 || g.B > GMAXB) return false;
+    if (!galigned(a.in_hi) || !galigned(a.in_lo) || !galigned(a.weight) || !galigned(a.out_hi) ||
+        !galigned(a.out_lo) || !galigned(a.res_hi) || !galigned(a.res_lo))
+        return false;
+    // pixel indices of the stacks fit the 30 bits of a descriptor
+    const long long lb = g.bs / 2;
+    if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * lb * lb >= (1LL << 30)) return false;
+    const int smem = igemm_smem_fixed<128, 128, 9>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
+    return smem + GWAVES * 4 <= 160 * 1024;
+}
+
+hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
+                        hipStream_t st) {
+    if (dtype == 1) return igemm_t<f16>(g, mask, a, ksize, stride, st);
+    return igemm_t<bf16>(g, mask, a, ksize, stride, st);
+}
+
+}  // namespace sb

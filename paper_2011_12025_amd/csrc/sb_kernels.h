@@ -52,6 +52,11 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
 // Encoder kernels (channels-last fp16/bf16): block convolution K x K
 // (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
 // max-pooling (any dtype).  conv2d_lds_bytes: LDS of one dense-conv workgroup.
+// multi-block implicit GEMM on packed channels-last stacks (fp16 / bf16,
+// C_in % 64 == 0, C_out % 8 == 0, at most 8192 blocks), BlockPad fused
+bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
+hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
+                        hipStream_t st);
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         hipStream_t st);
 int conv2d_lds_bytes(int dtype, int C_in, int K, int S);

@@ -63,3 +63,19 @@ class BlockEncoder:
         if counts is None:
             counts = count(mask)
         return self.stages(self.stem(x), mask, counts)
+
+    def capture(self, x: torch.Tensor, mask: torch.Tensor, counts):
+        """Records one forward into a HIP graph, so that a replay costs one
+        host call instead of one per kernel.  x and mask stay the graph's
+        inputs (write new values into them before a replay; the block counts
+        are fixed at capture).  Returns (graph, output tensor)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self(x, mask, counts)          # first launches set kernel attributes outside the capture
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            y = self(x, mask, counts)
+        return g, y

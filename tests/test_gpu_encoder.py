@@ -61,6 +61,15 @@ BCASES = [
     BCase("k3s2_res_nobias_f16", "f16", 1, 64, 64, 32, 32, 8, 3, 2, residual=True, relu=True, bias=False, seed=67),
     BCase("k3s2_blocks1120_f16", "f16", 1, 16, 16, 128, 140, 4, 3, 2, seed=68),   # more than 1024 blocks
     BCase("k1s1_f16", "f16", 1, 24, 24, 16, 16, 8, 1, 1, seed=69),
+    # multi-block implicit GEMM (C_in % 64 == 0): tiles spanning many blocks
+    BCase("ig_k3s1_c128_bs4_res_f16", "f16", 1, 128, 128, 32, 48, 4, 3, 1, relu=True, residual=True, seed=75),
+    BCase("ig_k3s2_c256_co512_bf16", "bf16", 1, 256, 512, 32, 64, 8, 3, 2, relu=True, seed=76),
+    BCase("ig_k3s1_c64_co64_bs16_f16", "f16", 2, 64, 64, 64, 64, 16, 3, 1, seed=77),
+    BCase("ig_k1s2_c128_co256_f16", "f16", 1, 128, 256, 32, 32, 8, 1, 2, seed=78),
+    BCase("ig_k3s1_bs2_bf16", "bf16", 1, 64, 64, 16, 32, 2, 3, 1, p_low=0.6, seed=79),
+    BCase("ig_blocks1200_f16", "f16", 1, 64, 64, 120, 160, 4, 3, 1, seed=80),
+    BCase("ig_alllow_k3s2_f16", "f16", 1, 64, 128, 32, 32, 8, 3, 2, mask_kind="low", seed=81),
+    BCase("ig_allhigh_k3s1_bf16", "bf16", 1, 128, 64, 16, 32, 8, 3, 1, mask_kind="high", seed=82),
 ]
 
 
@@ -193,3 +202,31 @@ def test_encoder(dtype, mask_kind, seed):
     log(f"[encoder] max-norm relative error {rel:.3e}")
     assert rel <= NORM_TOL[dtype]
     assert sb is not None
+
+
+def test_encoder_graph_replays_match_eager():
+    """The encoder captured as one HIP graph: every replay, with eager work of
+    the program between replays and new data written into the static input,
+    equals the eager forward bit for bit (the kernels are deterministic)."""
+    from paper_2011_12025_amd.encoder import BlockEncoder
+    log("[encoder graph] f16 3x128x256 block 64")
+    N, H, W, blk = 1, 128, 256, 64
+    Wt = inputs.encoder_weights(93, "f16")
+    mask_np = inputs.mask_bernoulli(93, N, H // blk, W // blk, 0.5)
+    nh = int(mask_np.sum())
+    counts = (nh, mask_np.size - nh)
+    mask = torch.from_numpy(mask_np).cuda()
+    xa = _cl(inputs.feature_map(93, N, 3, H, W, "f16"))
+    xb = _cl(inputs.feature_map(94, N, 3, H, W, "f16"))
+    enc = BlockEncoder(Wt, blk)
+    ya, yb = enc(xa, mask, counts).clone(), enc(xb, mask, counts).clone()
+    x = xa.clone(memory_format=torch.channels_last)
+    g, y = enc.capture(x, mask, counts)
+    for r, (src, ref) in enumerate([(xa, ya), (xb, yb), (xa, ya), (xb, yb)]):
+        enc(xb if r % 2 == 0 else xa, mask, counts)       # eager work between replays
+        torch.cuda.synchronize()
+        x.copy_(src)
+        y.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), f"replay {r} differs from the eager forward"
