@@ -14,8 +14,14 @@
 //               4 x 64 output tile and the weights (K*K*C_in padded to a
 //               multiple of 32) are staged in LDS; each lane gathers its 8
 //               K values through a table of patch offsets.
+//   k_stem    : the same for at most 4 input channels and K <= 8 (the stem):
+//               K is ordered (ky, kx padded to 8, channel padded to 4), so the
+//               8 K values of an MFMA operand lane are two adjacent input
+//               pixels of the LDS tile (16 bytes) instead of a gather; the
+//               weight rows are permuted so that a lane stores 8 consecutive
+//               output channels (16 bytes) of a pixel.
 //   k_maxpool : dense K x K max-pooling at a stride with padding that never
-//               wins.
+//               wins; k_maxpool_v does 16 bytes of channels per thread.
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -324,6 +330,154 @@ hipError_t bconv_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksi
     return stride == 1 ? run_bconv<T, 1, 1>(g, mask, a, st) : run_bconv<T, 1, 2>(g, mask, a, st);
 }
 
+// ---------------------------------------------------------------------------
+// stem: dense convolution of a map with at most 4 channels
+// ---------------------------------------------------------------------------
+constexpr int ST_TH = 16, ST_TW = 64;  // output tile: 16 rows (four per wave) x 64 columns x 64 channels
+
+// output channel of LDS weight row r (within a 32-row group, row 16h + 4kg + i
+// holds channel 8kg + 4h + i), so that a lane's two fragments of a group
+// hold 8 consecutive channels
+__device__ __forceinline__ int stem_perm(int r) {
+    const int l = r & 15;
+    return (r & ~31) + (l >> 2) * 8 + ((r >> 4) & 1) * 4 + (l & 3);
+}
+
+template <typename T>
+__global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, int H, int W,
+                                             const T* __restrict__ w, const T* __restrict__ bias, int C_out, int K,
+                                             int S, int P, int flags, T* __restrict__ y, int Ho, int Wo, int TY,
+                                             int TX) {
+    typedef EMF<T> mf;
+    typedef typename mf::frag frag;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int WROW = K * 32 + 8;                          // elements per LDS weight row (padded: no bank conflicts)
+    const int IH = S * (ST_TH - 1) + K, IW = S * (ST_TW - 1) + 8;
+    T* s_w = reinterpret_cast<T*>(smem);                  // [64][WROW]: (ky, kx8, ci4)
+    T* s_in = s_w + 64 * WROW;                            // [IH][IW][4]
+
+    const int tile = (int)blockIdx.x;
+    const int n = tile / (TY * TX), tr = tile - n * TY * TX, ty = tr / TX, tx = tr - ty * TX;
+    const int oy0 = ty * ST_TH, ox0 = tx * ST_TW, co0 = blockIdx.y * 64;
+    const int Y0 = oy0 * S - P, X0 = ox0 * S - P;
+    const int tid = threadIdx.x;
+
+    for (int i = tid; i < 64 * K * 32; i += WG) {
+        const int r = i / (K * 32), rem = i - r * (K * 32);
+        const int ky = rem >> 5, kx = (rem & 31) >> 2, ci = rem & 3;
+        const int co = co0 + stem_perm(r);
+        T v = from_f32<T>(0.0f);
+        if (co < C_out && kx < K && ci < C_in) v = w[(((size_t)co * K + ky) * K + kx) * C_in + ci];
+        s_w[r * WROW + rem] = v;
+    }
+    const T* __restrict__ img = x + (size_t)n * H * W * C_in;
+    for (int i = tid; i < IH * IW; i += WG) {
+        const int r = i / IW, c = i - r * IW;
+        const int yy = Y0 + r, xx = X0 + c;
+        Vec<T, 4> v = vzero<T, 4>();
+        if (yy >= 0 && yy < H && xx >= 0 && xx < W) {
+            const T* p = img + ((size_t)yy * W + xx) * C_in;
+#pragma unroll
+            for (int ci = 0; ci < 4; ++ci)
+                if (ci < C_in) v.e[ci] = p[ci];
+        }
+        *reinterpret_cast<uint2*>(s_in + (size_t)i * 4) = v.raw;
+    }
+    __syncthreads();
+
+    const int wave = tid >> 6, lane = tid & 63, l16 = lane & 15, kg = lane >> 4;
+    const bool relu = (flags & 1) != 0;
+    float bv[2][8];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int co = co0 + jj * 32 + kg * 8 + i;
+            bv[jj][i] = (bias && co < C_out) ? to_f32(bias[co]) : 0.0f;
+        }
+    for (int rr = 0; rr < ST_TH / 4; ++rr) {
+        const int ol = wave * (ST_TH / 4) + rr;  // output row within the tile
+        floatx4 acc[4][4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int ns = 0; ns < 4; ++ns) acc[t][ns] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int ky = 0; ky < K; ++ky) {
+            frag wf[4], bf[4];
+#pragma unroll
+            for (int ns = 0; ns < 4; ++ns)
+                wf[ns] = *reinterpret_cast<const frag*>(s_w + (ns * 16 + l16) * WROW + ky * 32 + kg * 8);
+            const T* row = s_in + (size_t)((S * ol + ky) * IW) * 4;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const T* p = row + (size_t)(S * (t * 16 + l16) + 2 * kg) * 4;
+                const uint2 lo = *reinterpret_cast<const uint2*>(p), hi = *reinterpret_cast<const uint2*>(p + 4);
+                bf[t] = as_frag<T>(uint4{lo.x, lo.y, hi.x, hi.y});
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int ns = 0; ns < 4; ++ns) acc[t][ns] = mf::mma(wf[ns], bf[t], acc[t][ns]);
+        }
+        const int oy = oy0 + ol;
+        if (oy >= Ho) continue;
+        T* yrow = y + ((size_t)n * Ho + oy) * Wo * C_out;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int ox = ox0 + t * 16 + l16;
+            if (ox >= Wo) continue;
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+                const int co = co0 + jj * 32 + kg * 8;
+                if (co >= C_out) continue;
+                Vec<T, 8> o;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float f0 = acc[t][2 * jj][i] + bv[jj][i], f1 = acc[t][2 * jj + 1][i] + bv[jj][4 + i];
+                    o.e[i] = from_f32<T>(relu ? fmaxf(f0, 0.0f) : f0);
+                    o.e[4 + i] = from_f32<T>(relu ? fmaxf(f1, 0.0f) : f1);
+                }
+                *reinterpret_cast<uint4*>(yrow + (size_t)ox * C_out + co) = o.raw;
+            }
+        }
+    }
+}
+
+// Max-pooling, 16 bytes of channels per thread (C a multiple of 16 / sizeof(T)).
+template <typename T>
+__global__ __launch_bounds__(WG) void k_maxpool_v(const T* __restrict__ x, int N, int C, int H, int W, int K, int S,
+                                                  int P, T* __restrict__ y, int Ho, int Wo) {
+    constexpr int V = 16 / (int)sizeof(T);
+    const int CV = C / V;
+    const long long total = (long long)N * Ho * Wo * CV;
+    const long long i = (long long)blockIdx.x * WG + threadIdx.x;
+    if (i >= total) return;
+    const int cv = (int)(i % CV);
+    const long long pix = i / CV;
+    const int ox = (int)(pix % Wo), oy = (int)((pix / Wo) % Ho), n = (int)(pix / ((long long)Wo * Ho));
+    float m[V];
+    Vec<T, V> best = vzero<T, V>();
+#pragma unroll
+    for (int e = 0; e < V; ++e) m[e] = -INFINITY;
+    for (int ky = 0; ky < K; ++ky) {
+        const int yy = oy * S + ky - P;
+        if (yy < 0 || yy >= H) continue;
+        for (int kx = 0; kx < K; ++kx) {
+            const int xx = ox * S + kx - P;
+            if (xx < 0 || xx >= W) continue;
+            Vec<T, V> v;
+            v.raw = *reinterpret_cast<const uint4*>(x + (((size_t)n * H + yy) * W + xx) * C + cv * V);
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+                if (to_f32(v.e[e]) > m[e]) {
+                    m[e] = to_f32(v.e[e]);
+                    best.e[e] = v.e[e];
+                }
+        }
+    }
+    *reinterpret_cast<uint4*>(y + pix * C + cv * V) = best.raw;
+}
+
 }  // namespace
 
 int conv2d_lds_bytes(int dtype, int C_in, int K, int S) {
@@ -339,9 +493,39 @@ hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const Conv
     return bconv_t<bf16>(g, mask, a, ksize, stride, st);
 }
 
+namespace {
+template <typename T>
+hipError_t stem_t(const void* x, int N, int C_in, int H, int W, const void* w, const void* bias, int C_out, int K,
+                  int S, int P, int flags, void* y, int Ho, int Wo, hipStream_t st) {
+    const int TY = (Ho + ST_TH - 1) / ST_TH, TX = (Wo + ST_TW - 1) / ST_TW;
+    const int smem = stem_lds_bytes(K, S);
+    static int set = 0;
+    if (smem > set) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_stem<T>, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+        set = smem;
+    }
+    const dim3 grid((unsigned)(N * TY * TX), (unsigned)((C_out + 63) / 64));
+    hipLaunchKernelGGL(k_stem<T>, grid, dim3(WG), smem, st, (const T*)x, C_in, H, W, (const T*)w, (const T*)bias,
+                       C_out, K, S, P, flags, (T*)y, Ho, Wo, TY, TX);
+    return hipGetLastError();
+}
+}  // namespace
+
+int stem_lds_bytes(int K, int S) {
+    const int IH = S * (ST_TH - 1) + K, IW = S * (ST_TW - 1) + 8;
+    return (64 * (K * 32 + 8) + IH * IW * 4) * 2;
+}
+
 hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W, const void* w, const void* bias,
                          int C_out, int K, int S, int P, int flags, void* y, hipStream_t st) {
     const int Ho = (H + 2 * P - K) / S + 1, Wo = (W + 2 * P - K) / S + 1;
+    // the stem path: few input channels, 16-byte channel groups of the output
+    if (C_in <= 4 && K <= 8 && C_out % 8 == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0 &&
+        stem_lds_bytes(K, S) <= 160 * 1024) {
+        if (dtype == 1) return stem_t<f16>(x, N, C_in, H, W, w, bias, C_out, K, S, P, flags, y, Ho, Wo, st);
+        return stem_t<bf16>(x, N, C_in, H, W, w, bias, C_out, K, S, P, flags, y, Ho, Wo, st);
+    }
     const int TY = (Ho + DC_TH - 1) / DC_TH, TX = (Wo + DC_TW - 1) / DC_TW;
     const int KP = (K * K * C_in + 31) / 32 * 32;
     const int smem = conv2d_lds_bytes(dtype, C_in, K, S);
@@ -374,6 +558,15 @@ hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, 
     const long long total = (long long)N * Ho * Wo * C;
     const unsigned grid = (unsigned)((total + WG - 1) / WG);
     if (total == 0) return hipSuccess;
+    const int es = dtype == 0 ? 4 : 2;
+    if ((C * es) % 16 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {
+        const long long tv = total * es / 16;
+        const unsigned gv = (unsigned)((tv + WG - 1) / WG);
+        if (dtype == 0) hipLaunchKernelGGL(k_maxpool_v<float>, dim3(gv), dim3(WG), 0, st, (const float*)x, N, C, H, W, K, S, P, (float*)y, Ho, Wo);
+        else if (dtype == 1) hipLaunchKernelGGL(k_maxpool_v<f16>, dim3(gv), dim3(WG), 0, st, (const f16*)x, N, C, H, W, K, S, P, (f16*)y, Ho, Wo);
+        else hipLaunchKernelGGL(k_maxpool_v<bf16>, dim3(gv), dim3(WG), 0, st, (const bf16*)x, N, C, H, W, K, S, P, (bf16*)y, Ho, Wo);
+        return hipGetLastError();
+    }
     if (dtype == 0) hipLaunchKernelGGL(k_maxpool<float>, dim3(grid), dim3(WG), 0, st, (const float*)x, N, C, H, W, K, S, P, (float*)y, Ho, Wo);
     else if (dtype == 1) hipLaunchKernelGGL(k_maxpool<f16>, dim3(grid), dim3(WG), 0, st, (const f16*)x, N, C, H, W, K, S, P, (f16*)y, Ho, Wo);
     else hipLaunchKernelGGL(k_maxpool<bf16>, dim3(grid), dim3(WG), 0, st, (const bf16*)x, N, C, H, W, K, S, P, (bf16*)y, Ho, Wo);

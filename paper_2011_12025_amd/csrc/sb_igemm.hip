@@ -505,33 +505,64 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     }
 }
 
-// Sums the split partial tiles in split order and runs the epilogue.
+// Sums the split partial tiles in split order and runs the epilogue.  One
+// thread per (tile, wave, ms, ns pair, lane) of the multiply kernel, so the
+// whole grid shares the work; a thread holds 8 consecutive output channels
+// of one pixel, exactly as the multiply kernel's lane does.
 template <typename T, int WM, int MS, int NS>
-__global__ __launch_bounds__(GWG) void k_igemm_reduce(ConvArgs a, GParams gp) {
+__global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, int tiles, int tiles_n) {
     constexpr int WN = GWAVES / WM;
     constexpr int TM = WM * MS * 16, TN = WN * NS * 16;
-    const int rows_valid = gp.rows[blockIdx.x];
-    const int high = (int)blockIdx.x < gp.tiles_h;
-    const int m0 = (high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h) * TM;
-    if (m0 >= rows_valid) return;
-    const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
-    const int tile_lin = (int)blockIdx.x * (int)gridDim.y + (int)blockIdx.y;
-    floatx4 acc[MS][NS];
-#pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-        for (int ns = 0; ns < NS; ++ns)
-            acc[ms][ns] = *reinterpret_cast<const floatx4*>(
-                gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, ns, lane));
+    constexpr int PER_TILE = GWAVES * MS * (NS / 2) * 64;
+    const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (gid >= (long long)tiles * tiles_n * PER_TILE) return;
+    const int tile_lin = (int)(gid / PER_TILE);
+    int r = (int)(gid - (long long)tile_lin * PER_TILE);
+    const int lane = r & 63;
+    r >>= 6;
+    const int jj = r % (NS / 2);
+    r /= (NS / 2);
+    const int ms = r % MS;
+    const int wave = r / MS;
+    const int tx = tile_lin / tiles_n, ty = tile_lin - tx * tiles_n;
+    const int rows_valid = gp.rows[tx];
+    const int high = tx < gp.tiles_h;
+    const int m0 = (high ? tx : tx - gp.tiles_h) * TM;
+    const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
+    const int m = m0 + wm * MS * 16 + ms * 16 + l16;
+    const int co = ty * TN + wn * NS * 16 + jj * 32 + kg * 8;
+    if (m >= rows_valid || co >= a.C_out) return;
+    floatx4 lo = *reinterpret_cast<const floatx4*>(
+        gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj, lane));
+    floatx4 hi = *reinterpret_cast<const floatx4*>(
+        gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj + 1, lane));
     for (int z = 1; z < gp.splits; ++z) {
-#pragma unroll
-        for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-            for (int ns = 0; ns < NS; ++ns)
-                acc[ms][ns] += *reinterpret_cast<const floatx4*>(
-                    gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, ns, lane));
+        lo += *reinterpret_cast<const floatx4*>(
+            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj, lane));
+        hi += *reinterpret_cast<const floatx4*>(
+            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj + 1, lane));
     }
-    gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, (int)blockIdx.y * TN);
+    const T* __restrict__ bias = (const T*)a.bias;
+    const T* __restrict__ res = (const T*)(high ? a.res_hi : a.res_lo);
+    T* __restrict__ out = (T*)(high ? a.out_hi : a.out_lo);
+    const bool relu = (a.flags & 1) != 0;
+    float f[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[i] = lo[i] + (bias ? to_f32(bias[co + i]) : 0.0f);
+        f[4 + i] = hi[i] + (bias ? to_f32(bias[co + 4 + i]) : 0.0f);
+    }
+    const size_t off = (size_t)m * a.C_out + co;
+    if (res) {
+        Vec<T, 8> rv;
+        rv.raw = *reinterpret_cast<const uint4*>(res + off);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
+    }
+    Vec<T, 8> o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
+    *reinterpret_cast<uint4*>(out + off) = o.raw;
 }
 
 // One workspace per device for the split partials, grown on demand (never
@@ -628,8 +659,9 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     if (S > 1) {
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((k_igemm_reduce<T, WM, MS, NS>), dim3((unsigned)tiles, (unsigned)tiles_n), dim3(GWG), 0, st,
-                           a, gp);
+        const long long threads = (long long)tiles * tiles_n * GWAVES * MS * (NS / 2) * 64;
+        hipLaunchKernelGGL((k_igemm_reduce<T, WM, MS, NS>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, a,
+                           gp, tiles, tiles_n);
     }
     return hipGetLastError();
 }

@@ -60,6 +60,7 @@ hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const Conv
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         hipStream_t st);
 int conv2d_lds_bytes(int dtype, int C_in, int K, int S);
+int stem_lds_bytes(int K, int S);
 hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W, const void* w, const void* bias,
                          int C_out, int K, int S, int P, int flags, void* y, hipStream_t st);
 hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, int K, int S, int P, void* y,
