@@ -13,7 +13,16 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Pointers are DEVICE pointers unless stated otherwise.  The caller owns
- *    every buffer; the library allocates no device memory.
+ *    every input and output buffer.  One exception to "no library memory":
+ *    channels-last fp16/bf16 block convolutions with C_in % 64 == 0
+ *    (segblocks_block_conv3x3 beyond C_in = 64, segblocks_block_conv_ex)
+ *    may split their reduction over several workgroups and then keep fp32
+ *    partial tiles in a per-device workspace that the library allocates on
+ *    first need and keeps until the process ends.  It is grown only outside
+ *    stream capture: a call that needs more than the workspace holds while
+ *    its stream is being captured into a graph fails with SB_EHIP
+ *    (run the same call once before capturing).  Calls that overlap on one
+ *    device share the workspace and must be ordered by the caller.
  *  - Logical dimensions are always N, C, H, W.  `layout` selects the memory
  *    format of every 4-d tensor of the call (input, stacks, output and the
  *    convolution weight):
