@@ -312,6 +312,24 @@ struct Neigh {
     int slot[9];     // slot of neighbour d in its class's stack
 };
 
+// Slot of neighbour d (run-time d) as a choice between register values.  Each
+// slot is read with a constant index and passed through an empty asm, so the
+// optimiser cannot turn the choice back into one load at a computed offset:
+// such a load keeps the Neigh in memory, and the compiler then places it in
+// LDS indexed by the flat thread id, whose computation reads the work-group
+// size from the dispatch packet in host memory (microseconds per wave at
+// kernel start).
+__device__ __forceinline__ int neigh_slot(const Neigh& nb, int d) {
+    int r = 0;
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+        int v = nb.slot[i];
+        asm("" : "+v"(v));
+        r = d == i ? v : r;
+    }
+    return r;
+}
+
 // Neighbourhood of block (n, gy, gx): classes and, when WITH_SLOTS, slots.
 // Wave-uniform; all 64 lanes of the wave must call it.
 template <bool WITH_SLOTS, bool ONE>

@@ -171,10 +171,7 @@ __device__ __forceinline__ RLoc res_loc(const Geo& g, const ConvArgs& a, const N
     } else {
         if (!((nb.valid >> d) & 1)) return L;
         const int nhigh = (nb.high >> d) & 1;
-        int ns = nb.slot[0];  // nb.slot[d] with constant indices, so nb stays in registers
-#pragma unroll
-        for (int i = 1; i < 9; ++i)
-            if (d == i) ns = nb.slot[i];
+        const int ns = neigh_slot(nb, d);
         if (ns >= (nhigh ? a.hi_cap : a.lo_cap)) return L;
         const int u2 = r - (dy - 1) * t.e, v2 = j - (dx - 1) * t.e;
         const int bs = g.bs, lb = bs >> 1;
@@ -266,7 +263,7 @@ __device__ __forceinline__ RowSrc row_src(const Geo& g, const ConvArgs& a, const
             return S;
         }
         const int nhigh = (nb.high >> d) & 1;
-        const int ns = dy == 0 ? nb.slot[1] : (dy == 1 ? nb.slot[4] : nb.slot[7]);
+        const int ns = neigh_slot(nb, dy * 3 + 1);
         if (ns >= (nhigh ? a.hi_cap : a.lo_cap)) {
             S.kind = ROW_ZERO;
             return S;

@@ -63,10 +63,7 @@ __device__ __forceinline__ Src<T> packed_src(const T* __restrict__ hi, const T* 
     const int d = (dy + 1) * 3 + (dx + 1);
     if (!((nb.valid >> d) & 1)) return src_zero<T>();
     const int nhigh = (nb.high >> d) & 1;
-    int ns = nb.slot[0];  // nb.slot[d] with constant indices, so nb stays in registers
-#pragma unroll
-    for (int i = 1; i < 9; ++i)
-        if (d == i) ns = nb.slot[i];
+    const int ns = neigh_slot(nb, d);
     if (ns >= (nhigh ? hi_cap : lo_cap)) return src_zero<T>();
     const int u2 = uu - dy * e, v2 = vv - dx * e;
     if (nhigh == own_high) return src_copy<T>(stack_at<T, L>(nhigh ? hi : lo, ns, C, e, u2, v2, c));

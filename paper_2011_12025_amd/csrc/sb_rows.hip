@@ -282,7 +282,7 @@ __global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const
         const int r = u - 1;
         const int dy = r < 0 ? 0 : (r >= e ? 2 : 1), dn = dy * 3 + 1;
         const int nhigh = (nb.high >> dn) & 1;
-        const int ns = dy == 0 ? nb.slot[1] : (dy == 1 ? nb.slot[4] : nb.slot[7]);
+        const int ns = neigh_slot(nb, dn);
         const bool zero_row = !((nb.valid >> dn) & 1) || ns >= (nhigh ? hi_cap : lo_cap);
         const int u2 = r - (dy - 1) * e, lb = bs >> 1;
         int kind = 0;            // 0 zero, 1 copy (pixel w - 1), 2 nearest (pixel (w - 1) / 2), 3 average (cell at 2(w - 1))
