@@ -237,19 +237,75 @@ __global__ __launch_bounds__(WG) void k_combine_rows(const T* __restrict__ hi, c
 
 // ---------------------------------------------------------------------------
 // pad: hi, lo -> hp, lp
+//
+// A job is one padded row, done in one pass of loads then stores (a second
+// pass would wait for the first pass's stores: one counter covers loads and
+// stores).  Jobs [0, B (lb + 2)) are rows 0 .. lb + 1 of every block (all of
+// a low padded block); the rest are rows lb + 2 .. bs + 1 of the high slots,
+// whose blocks come from an inverse of the plan (LDS table) or a wave-level
+// search, so no job is empty.
 // ---------------------------------------------------------------------------
-constexpr int PADM = 5;  // vectors per lane and pass over a padded row
+constexpr int PADM = 5;   // vectors per lane and pass (up to four loads each)
+
+// Where the interior (columns 1..e) of padded row u of the block comes from:
+// one row of one block (uniform) -- this block's row, or the row next to it in
+// the block above or below -- copied at equal resolution (kind 1),
+// nearest-upsampled from a low neighbour (2), 2x2-averaged from a high
+// neighbour (3), or zero outside the image or past a stack's capacity (0).
+// Only the two halo columns need the per-pixel rule (packed_src).
+template <typename T>
+__device__ __forceinline__ const T* pad_row_source(const T* __restrict__ hi, const T* __restrict__ lo, int C, int bs,
+                                                   const Neigh& nb, bool high, int hi_cap, int lo_cap, int u,
+                                                   int& kind) {
+    const int lb = bs >> 1, e = high ? bs : lb;
+    const int r = u - 1;
+    const int dy = r < 0 ? 0 : (r >= e ? 2 : 1), dn = dy * 3 + 1;
+    const int nhigh = (nb.high >> dn) & 1;
+    const int ns = neigh_slot(nb, dn);
+    kind = 0;
+    if (!((nb.valid >> dn) & 1) || ns >= (nhigh ? hi_cap : lo_cap)) return nullptr;
+    const int u2 = r - (dy - 1) * e;
+    if (nhigh == (int)high) {
+        kind = 1;
+        return (nhigh ? hi : lo) + ((size_t)(ns * e + u2) * e) * C;
+    }
+    if (high) {
+        kind = 2;
+        return lo + ((size_t)(ns * lb + (u2 >> 1)) * lb) * C;
+    }
+    kind = 3;
+    return hi + ((size_t)(ns * bs + 2 * u2) * bs) * C;
+}
 
 template <typename T, bool ONE>
-__global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const T* __restrict__ lo, int C,
+__global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, const T* __restrict__ lo, int C,
                                                  const uint8_t* __restrict__ mask, int bs, int B, int GH, int GW,
                                                  int per_wave, T* __restrict__ hp, T* __restrict__ lp, int hi_cap,
                                                  int lo_cap) {
     constexpr int V = 16 / (int)sizeof(T);
     const int lane = lane_id();
-    const int CV = C / V, ph = bs + 2;
-    const int njobs = B * ph;
-    ROWS_PLAN_PREAMBLE();
+    const int CV = C / V, lb = bs >> 1, ph = lb + 2, ex = bs - lb;
+    const int jobs_a = B * ph;
+    const int njobs = jobs_a + hi_cap * ex;
+    __shared__ __align__(16) uint8_t s_mask[1024];
+    __shared__ __align__(16) PlanTable s_pt;
+    __shared__ uint16_t s_inv[1024];  // block of each high slot (one table)
+    __shared__ int s_nh;
+    if (wave_id() == 0) {
+        stage_mask(mask, B, s_mask);
+        if (ONE) {
+            build_plan_table(s_mask, &s_pt);
+            const int c = __popc(nonzero_bytes16(*reinterpret_cast<const uint4*>(s_mask + 16 * lane)));
+            const int tot = wave_sum5(c);
+            if (lane == 0) s_nh = tot;
+        }
+    }
+    __syncthreads();
+    if (ONE) {
+        for (int k = (int)threadIdx.x; k < B; k += WG)
+            if ((s_pt.hi[k >> 4] >> (k & 15)) & 1) s_inv[s_pt.slot[k]] = (uint16_t)k;
+        __syncthreads();
+    }
     int job = ((int)blockIdx.x * RW_WAVES + wave_id()) * per_wave;
     const int end = min(njobs, job + per_wave);
     if (job >= end) return;
@@ -260,7 +316,22 @@ __global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const
     bool high = false;
     int s = 0;
     for (; job < end; ++job) {
-        const int k = job / ph, u = job - k * ph;
+        int k, u;
+        if (job < jobs_a) {
+            k = job / ph;
+            u = job - k * ph;
+        } else {
+            const int j = job - jobs_a;
+            const int hs = j / ex;
+            u = ph + (j - hs * ex);
+            if (ONE) {
+                if (hs >= s_nh) continue;
+                k = s_inv[hs];
+            } else {
+                k = wm.wm.find_nth(hs, true);
+                if (k < 0) continue;
+            }
+        }
         if (k != kcur) {
             int n, gy, gx;
             coords(k, GH, GW, n, gy, gx);
@@ -269,36 +340,11 @@ __global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const
             s = nb.slot[4];
             kcur = k;
         }
-        const int e = high ? bs : (bs >> 1), pe = e + 2;
-        if (u >= pe || s >= (high ? hi_cap : lo_cap)) continue;
-        const int nv = pe * CV;
+        if (s >= (high ? hi_cap : lo_cap)) continue;
+        const int e = high ? bs : lb, pe = e + 2, nv = pe * CV;
+        int kind;
+        const T* row = pad_row_source<T>(hi, lo, C, bs, nb, high, hi_cap, lo_cap, u, kind);
         T* d = (high ? hp : lp) + ((size_t)(s * pe + u) * pe) * C;
-        // The interior (columns 1..e) of padded row u comes from one row of one
-        // block (uniform): this block's row, or the row next to it in the block
-        // above or below; copied at equal resolution, nearest-upsampled from a
-        // low neighbour, 2x2-averaged from a high neighbour, zero outside the
-        // image or past a stack's capacity.  Only the two halo columns need the
-        // per-pixel rule (packed_src).
-        const int r = u - 1;
-        const int dy = r < 0 ? 0 : (r >= e ? 2 : 1), dn = dy * 3 + 1;
-        const int nhigh = (nb.high >> dn) & 1;
-        const int ns = neigh_slot(nb, dn);
-        const bool zero_row = !((nb.valid >> dn) & 1) || ns >= (nhigh ? hi_cap : lo_cap);
-        const int u2 = r - (dy - 1) * e, lb = bs >> 1;
-        int kind = 0;            // 0 zero, 1 copy (pixel w - 1), 2 nearest (pixel (w - 1) / 2), 3 average (cell at 2(w - 1))
-        const T* row = nullptr;  // channel 0 of the source row's first pixel
-        if (!zero_row) {
-            if (nhigh == high) {
-                kind = 1;
-                row = (nhigh ? hi : lo) + ((size_t)(ns * e + u2) * e) * C;
-            } else if (high) {
-                kind = 2;
-                row = lo + ((size_t)(ns * lb + (u2 >> 1)) * lb) * C;
-            } else {
-                kind = 3;
-                row = hi + ((size_t)(ns * bs + 2 * u2) * bs) * C;
-            }
-        }
         for (int ib = 0; ib < nv; ib += 64 * PADM) {
             uint4 v[PADM][4];
             int mode[PADM];
@@ -310,13 +356,13 @@ __global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const
                     const int w = i / CV, c = (i - w * CV) * V;
                     const T* src = nullptr;
                     bool avg = false;
-                    int d1 = C, d2 = bs * C;
+                    int d1c = C, d2c = bs * C;
                     if (w == 0 || w == pe - 1) {
-                        const Src<T> sp = packed_src<T, NHWC>(hi, lo, C, bs, nb, hi_cap, lo_cap, r, w - 1, c);
+                        const Src<T> sp = packed_src<T, NHWC>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, w - 1, c);
                         src = sp.p;
                         avg = sp.avg;
-                        d1 = sp.d1;
-                        d2 = sp.d2;
+                        d1c = sp.d1;
+                        d2c = sp.d2;
                     } else if (kind == 1) {
                         src = row + (w - 1) * C + c;
                     } else if (kind == 2) {
@@ -331,9 +377,9 @@ __global__ __launch_bounds__(WG) void k_pad_rows(const T* __restrict__ hi, const
                         mode[m] = avg ? 2 : 1;
                         v[m][0] = ld_nt16(src);
                         if (avg) {
-                            v[m][1] = ld_nt16(src + d1);
-                            v[m][2] = ld_nt16(src + d2);
-                            v[m][3] = ld_nt16(src + d2 + d1);
+                            v[m][1] = ld_nt16(src + d1c);
+                            v[m][2] = ld_nt16(src + d2c);
+                            v[m][3] = ld_nt16(src + d2c + d1c);
                         }
                     }
                 }
@@ -386,7 +432,7 @@ hipError_t combine_rows(const Geo& g, const void* hi, const void* lo, const uint
 template <typename T, bool ONE>
 hipError_t pad_rows(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
                     int hi_cap, int lo_cap, hipStream_t st) {
-    const long long jobs = g.B * (g.bs + 2);
+    const long long jobs = g.B * (g.bs / 2 + 2) + (long long)hi_cap * (g.bs - g.bs / 2);
     const int grid = rows_grid(jobs);
     const long long waves = (long long)grid * RW_WAVES;
     const int per_wave = (int)((jobs + waves - 1) / waves);
