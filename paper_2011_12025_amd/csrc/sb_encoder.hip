@@ -362,26 +362,56 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
     const int Y0 = oy0 * S - P, X0 = ox0 * S - P;
     const int tid = threadIdx.x;
 
-    for (int i = tid; i < 64 * K * 32; i += WG) {
-        const int r = i / (K * 32), rem = i - r * (K * 32);
-        const int ky = rem >> 5, kx = (rem & 31) >> 2, ci = rem & 3;
-        const int co = co0 + stem_perm(r);
-        T v = from_f32<T>(0.0f);
-        if (co < C_out && kx < K && ci < C_in) v = w[(((size_t)co * K + ky) * K + kx) * C_in + ci];
-        s_w[r * WROW + rem] = v;
+    // Staging in batches: every thread issues SB loads before it writes any of
+    // them to LDS, so the loads of a batch are in flight together.
+    constexpr int SB = 8;
+    const int nw = 64 * K * 32;
+    for (int base = tid; base < nw; base += WG * SB) {
+        T v[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * WG;
+            v[u] = from_f32<T>(0.0f);
+            if (i < nw) {
+                const int r = i / (K * 32), rem = i - r * (K * 32);
+                const int ky = rem >> 5, kx = (rem & 31) >> 2, ci = rem & 3;
+                const int co = co0 + stem_perm(r);
+                if (co < C_out && kx < K && ci < C_in) v[u] = w[(((size_t)co * K + ky) * K + kx) * C_in + ci];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * WG;
+            if (i < nw) {
+                const int r = i / (K * 32), rem = i - r * (K * 32);
+                s_w[r * WROW + rem] = v[u];
+            }
+        }
     }
     const T* __restrict__ img = x + (size_t)n * H * W * C_in;
-    for (int i = tid; i < IH * IW; i += WG) {
-        const int r = i / IW, c = i - r * IW;
-        const int yy = Y0 + r, xx = X0 + c;
-        Vec<T, 4> v = vzero<T, 4>();
-        if (yy >= 0 && yy < H && xx >= 0 && xx < W) {
-            const T* p = img + ((size_t)yy * W + xx) * C_in;
+    const int np = IH * IW;
+    for (int base = tid; base < np; base += WG * SB) {
+        Vec<T, 4> v[SB];
 #pragma unroll
-            for (int ci = 0; ci < 4; ++ci)
-                if (ci < C_in) v.e[ci] = p[ci];
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * WG;
+            v[u] = vzero<T, 4>();
+            if (i < np) {
+                const int r = i / IW, c = i - r * IW;
+                const int yy = Y0 + r, xx = X0 + c;
+                if (yy >= 0 && yy < H && xx >= 0 && xx < W) {
+                    const T* p = img + ((size_t)yy * W + xx) * C_in;
+#pragma unroll
+                    for (int ci = 0; ci < 4; ++ci)
+                        if (ci < C_in) v[u].e[ci] = p[ci];
+                }
+            }
         }
-        *reinterpret_cast<uint2*>(s_in + (size_t)i * 4) = v.raw;
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * WG;
+            if (i < np) *reinterpret_cast<uint2*>(s_in + (size_t)i * 4) = v[u].raw;
+        }
     }
     __syncthreads();
 
