@@ -603,6 +603,7 @@ hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) {
 }
 
 int g_cus = 0;
+constexpr int GSPLIT_COST = 6;  // the partial-sum pass, in K steps (about 1 us each)
 
 inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -632,8 +633,10 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     const int tiles = gp.tiles_h + tiles_l;
     if (tiles == 0) return hipSuccess;
     const int tiles_n = (a.C_out + TN - 1) / TN;
-    // split K while the workgroups do not cover the compute units once and
-    // every split keeps at least four K steps
+    // Split K: one workgroup per CU at a time (LDS), each taking about the
+    // same time per K step, so a launch costs about rounds x steps per split;
+    // a split costs the partial-sum pass on top.  Take the cheapest split that
+    // keeps at least four steps per workgroup.
     if (g_cus == 0) {
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -642,7 +645,18 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     }
     const int nsteps = KS * KS * gp.cpt;
     int S = 1;
-    while (S < 16 && (long long)tiles * tiles_n * S < g_cus && nsteps / (2 * S) >= 4) S *= 2;
+    {
+        const long long wgs = (long long)tiles * tiles_n;
+        long long best = 0;
+        for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
+            const long long rounds = (wgs * c + g_cus - 1) / g_cus;
+            const long long cost = rounds * ((nsteps + c - 1) / c) + (c > 1 ? GSPLIT_COST : 0);
+            if (c == 1 || cost < best) {
+                best = cost;
+                S = c;
+            }
+        }
+    }
     gp.splits = S;
     gp.part = nullptr;
     gp.rows = nullptr;
