@@ -88,6 +88,16 @@ __device__ __forceinline__ void dma16(const void* g, unsigned char* window) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr)window, 16, 0, 0);
 }
 
+// 16 zero bytes to LDS.  Written in assembly so that the compiler does not
+// wait for the wave's pending LDS copies first (it cannot tell that they
+// fill other bytes); the LDS-counter wait before the next barrier covers it.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void lds_zero16(unsigned char* p) {
+    const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)p;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(z) : "memory");
+}
+
 // q = p / d for 0 <= p < 4096 and 1 <= d <= 128: (p + 0.5) / d in fp32 is at
 // least 0.5 / d away from an integer and its rounding error is below 2^-11,
 // so truncation gives the exact quotient.
@@ -399,7 +409,7 @@ __device__ __forceinline__ void rw_issue(const Geo& g, const ConvArgs& a, const 
             const int px = S.kind == ROW_COPY ? 8 * k + i : ((8 * k + i) >> 1);
             dma16((S.which ? b1 : b0) + S.off + px * C + q * 8, win);
         } else {
-            *reinterpret_cast<uint4*>(win + lane * 16) = uint4{0u, 0u, 0u, 0u};
+            lds_zero16(win + lane * 16);
         }
     }
     const typename ResAvg<T, SRC>::Plan P = ResAvg<T, SRC>::plan(g, a, nb, t);
@@ -567,26 +577,18 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     const int lane = lane_id(), l16 = lane & 15, kg = lane >> 4;
     const int co0 = blockIdx.y * RNT;
 
-    WaveMaskT<ONE> wm;
-    wm.init(mask, (int)g.B);  // issues the mask read
-
     // consumer c: output channels co0 + 32 * (c & 1) + [0, 32), half (c >> 1) of every tile
     const int h = wave & 1, half = wave >> 1;
     const int cobase = co0 + 32 * h;
-    float bv[2][4];
+    const int cb = cobase + kg * 8;  // the first of this lane's 8 output channels
+    const T* __restrict__ bias = (const T*)a.bias;
+    Vec<T, 8> braw;                  // their bias, converted once the weights are in registers
     // The weight slice of this workgroup (rows [tap][co], 64 channels each) is
     // copied to LDS by the consumers while the producers plan and issue tile 0;
     // it sits over buffers 1 and 2 until the consumers hold it in registers.
+    // The consumers issue these copies before they read the mask.
     unsigned char* s_w = smem + buf_bytes;
     if (!producer) {
-        const T* __restrict__ bias = (const T*)a.bias;
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int co = cobase + kg * 8 + j * 4 + r;
-                bv[j][r] = (bias && co < a.C_out) ? to_f32(bias[co]) : 0.0f;
-            }
         const T* __restrict__ wgt = (const T*)a.weight;
         for (int w0 = wave * 64; w0 < 9 * RNT * RSUB; w0 += 64 * NCW) {
             const int s = w0 + lane;
@@ -594,9 +596,19 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
             const int tap = row / RNT, col = row - tap * RNT;
             const int co = co0 + col, ci = q * 8;
             if (co < a.C_out && ci < a.C_in) dma16(wgt + ((size_t)co * 9 + tap) * a.C_in + ci, s_w + w0 * 16);
-            else *reinterpret_cast<uint4*>(s_w + s * 16) = uint4{0u, 0u, 0u, 0u};
+            else lds_zero16(s_w + s * 16);
+        }
+        if (bias) {
+            if (cb + 8 <= a.C_out && (reinterpret_cast<uintptr_t>(bias) & 15) == 0) {
+                braw = vload<T, 8>(bias + cb);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) braw.e[e] = bias[min(cb + e, a.C_out - 1)];
+            }
         }
     }
+    WaveMaskT<ONE> wm;
+    wm.init(mask, (int)g.B);
 
     // This workgroup's tiles are pos, pos + nwg, ...  Workgroups are spread
     // over the XCDs round-robin; pos numbers them XCD by XCD, so the tiles of
@@ -671,6 +683,11 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
                 Wr[tap][ks][j] = *reinterpret_cast<const frag*>(s_w + row * RROW + (((ks * 4 + kg) ^ (row & 7)) << 4));
             }
     const bool relu = (a.flags & 1) != 0;
+    float bv[2][4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bv[j][r] = (bias && cb + j * 4 + r < a.C_out) ? to_f32(braw.e[j * 4 + r]) : 0.0f;
     // All counters: the weight reads, and (for the compiler's wait tracking) no LDS
     // copy pending on this path, which keeps the waits for the MFMA operands partial.
     __builtin_amdgcn_s_waitcnt(0);
