@@ -39,6 +39,7 @@
 // are permuted in LDS so that a lane ends with 8 consecutive output channels
 // of one pixel and stores them as one 16-byte write.
 #include <mutex>
+#include <type_traits>
 
 #include "sb_common.h"
 #include "sb_kernels.h"
@@ -226,6 +227,7 @@ struct GParams {
     int splits;     // workgroups sharing the K steps of a tile (grid.z)
     float* part;    // fp32 partial tiles [tile][n tile][split][TM * TN] when splits > 1
     int* rows;      // valid output rows of each M tile, written when splits > 1
+    const void* lo_pad;  // the low stack with its 1-pixel halo [lo_cap][lb+2][lb+2][C_in], or nullptr
 };
 
 // Bias, residual, ReLU and the store of a finished tile: lane holds channels
@@ -365,7 +367,9 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         pq[j] = ((lane & 7) ^ ((prow[j] >> 1) & 7)) * 8;
     }
     const T* __restrict__ in_hi = (const T*)a.in_hi;
-    const T* __restrict__ in_lo = (const T*)a.in_lo;
+    // a low tile reads the padded low stack when there is one (uniform)
+    const bool lpad = !high && gp.lo_pad != nullptr;
+    const T* __restrict__ in_lo = lpad ? (const T*)gp.lo_pad : (const T*)a.in_lo;
     const T* zrow = reinterpret_cast<const T*>(g_zero_row);
 
     // the first step's weights are in flight while the descriptors are built
@@ -401,7 +405,9 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
             const int uu = ST * i + ky - KS / 2, vv = ST * j + kx - KS / 2;
             const int dy = uu < 0 ? -1 : (uu >= e_in ? 1 : 0);
             const int dx = vv < 0 ? -1 : (vv >= e_in ? 1 : 0);
-            if (dy == 0 && dx == 0) {
+            if (lpad) {  // a low tile over the padded low stack: every source is a copy
+                ds = gdesc(GK_LO, (slot * (lb + 2) + uu + 1) * (lb + 2) + vv + 1);
+            } else if (dy == 0 && dx == 0) {
                 ds = gdesc(high ? GK_HI : GK_LO, (slot * e_in + uu) * e_in + vv);
             } else {
                 const int nn = k / per_img;
@@ -660,13 +666,34 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     gp.splits = S;
     gp.part = nullptr;
     gp.rows = nullptr;
-    if (S > 1) {
-        const size_t part_bytes = (size_t)tiles * tiles_n * S * TM * TN * 4;
+    gp.lo_pad = nullptr;
+    // A low block's halo pixels across a resolution boundary are 2x2 averages
+    // of the high neighbour: four loads per element in the K loop, which make
+    // the low tiles the last to finish.  A 3 x 3 convolution with both classes
+    // can pad the low stack once instead (BlockPad of the low blocks), so that
+    // every low-tile source is a plain copy.  Measured, the extra pass pays at
+    // 128 input channels (about 5 us less at 25-75 % low blocks) and costs 1-4 us
+    // at 64, 256 and 512, so it is taken there only.
+    const bool pad_low = KS == 3 && tiles_l > 0 && a.hi_cap > 0 && a.C_in > 64 && a.C_in <= 128;
+    const size_t part_bytes = S > 1 ? ((size_t)tiles * tiles_n * S * TM * TN * 4 + (size_t)tiles * 4 + 255) / 256 * 256 : 0;
+    const size_t pad_bytes = pad_low ? (size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * sizeof(T) : 0;
+    if (part_bytes + pad_bytes > 0) {
         void* ws = nullptr;
-        hipError_t e = gworkspace(part_bytes + (size_t)tiles * 4, st, &ws);
+        hipError_t e = gworkspace(part_bytes + pad_bytes, st, &ws);
         if (e != hipSuccess) return e;
-        gp.part = (float*)ws;
-        gp.rows = (int*)((char*)ws + part_bytes);
+        if (S > 1) {
+            gp.part = (float*)ws;
+            gp.rows = (int*)((char*)ws + (size_t)tiles * tiles_n * S * TM * TN * 4);
+        }
+        if (pad_low) {
+            void* lp = (char*)ws + part_bytes;
+            Geo pg = g;
+            pg.C = a.C_in;
+            e = launch_pad_rows(std::is_same<T, f16>::value ? 1 : 2, pg, a.in_hi, a.in_lo, mask,
+                                nullptr, lp, a.hi_cap, a.lo_cap, st);
+            if (e != hipSuccess) return e;
+            gp.lo_pad = lp;
+        }
     }
     const dim3 grid((unsigned)tiles, (unsigned)tiles_n, (unsigned)S);
     hipLaunchKernelGGL((k_igemm<T, KS, ST, WM, MS, NS>), grid, dim3(GWG), smem, st, g, mask, a, gp);
@@ -702,7 +729,8 @@ bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
         return false;
     // pixel indices of the stacks fit the 30 bits of a descriptor
     const long long lb = g.bs / 2;
-    if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * lb * lb >= (1LL << 30)) return false;
+    if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * (lb + 2) * (lb + 2) >= (1LL << 30))
+        return false;
     const int smem = igemm_smem_fixed<128, 128, 9>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
     return smem + GWAVES * 4 <= 160 * 1024;
 }

@@ -41,6 +41,7 @@ hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Ge
 
 // Row-job split / pad / combine for channels-last tensors of whole 16-byte
 // pixels with 16-byte aligned buffers; rows_fit tells whether they apply.
+// launch_pad_rows with hp == nullptr pads the low blocks only (into lp).
 bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const void*> ptrs);
 hipError_t launch_split_rows(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap,
                              void* lo, int lo_cap, hipStream_t st);

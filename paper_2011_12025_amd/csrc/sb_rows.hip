@@ -286,7 +286,7 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
     const int lane = lane_id();
     const int CV = C / V, lb = bs >> 1, ph = lb + 2, ex = bs - lb;
     const int jobs_a = B * ph;
-    const int njobs = jobs_a + hi_cap * ex;
+    const int njobs = jobs_a + (hp ? hi_cap * ex : 0);  // no high output: the low blocks only
     __shared__ __align__(16) uint8_t s_mask[1024];
     __shared__ __align__(16) PlanTable s_pt;
     __shared__ uint16_t s_inv[1024];  // block of each high slot (one table)
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
             s = nb.slot[4];
             kcur = k;
         }
-        if (s >= (high ? hi_cap : lo_cap)) continue;
+        if (s >= (high ? hi_cap : lo_cap) || (high && !hp)) continue;
         const int e = high ? bs : lb, pe = e + 2, nv = pe * CV;
         int kind;
         const T* row = pad_row_source<T>(hi, lo, C, bs, nb, high, hi_cap, lo_cap, u, kind);
@@ -432,7 +432,7 @@ hipError_t combine_rows(const Geo& g, const void* hi, const void* lo, const uint
 template <typename T, bool ONE>
 hipError_t pad_rows(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
                     int hi_cap, int lo_cap, hipStream_t st) {
-    const long long jobs = g.B * (g.bs / 2 + 2) + (long long)hi_cap * (g.bs - g.bs / 2);
+    const long long jobs = g.B * (g.bs / 2 + 2) + (hp ? (long long)hi_cap * (g.bs - g.bs / 2) : 0LL);
     const int grid = rows_grid(jobs);
     const long long waves = (long long)grid * RW_WAVES;
     const int per_wave = (int)((jobs + waves - 1) / waves);
