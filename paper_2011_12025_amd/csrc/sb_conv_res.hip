@@ -11,7 +11,8 @@
 //
 //   waves 0-3  (consumers): wave c owns output channels co0 + 32 * (c & 1)
 //              + [0, 32) and half (c >> 1) of the tile; its 32 x 9 x C_in
-//              weights live in its registers for the whole launch;
+//              weights are loaded into its registers at start-up and stay
+//              there for the whole launch;
 //   waves 4-7  (producers): finish staging tile i (wait for its copies,
 //              write its 2x2 averages), then issue the copies of tile i + 1,
 //              while the consumers compute tile i - 1.
@@ -38,12 +39,12 @@
 // of one pixel, and one store instruction writes 64 contiguous bytes of each
 // of 16 pixels.
 //
-// LDS rows (a weight row [tap][co] or a tile pixel) are 128 bytes = 8
-// sub-chunks of 16 bytes.  Sub-chunk q of weight row r lives at position
-// q ^ (r & 7); sub-chunk q of the tile pixel in column v lives at position
-// q ^ ((v >> 1) & 7), so the 16 pixels of an MFMA operand read at one
-// sub-chunk hit all 64 banks once, and a pixel's position does not depend on
-// its row.
+// A tile pixel in LDS is 128 bytes = 8 sub-chunks of 16 bytes; sub-chunk q of
+// the pixel in column v lives at position q ^ ((v >> 1) & 7), so the 16
+// pixels of an MFMA operand read at one sub-chunk hit all 64 banks once, and
+// a pixel's position does not depend on its row.  The weights never pass
+// through LDS: each consumer lane loads its A fragments (16 bytes each)
+// directly.
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -73,7 +74,6 @@ template <> struct MFR<bf16> {
 constexpr int RNT = 64;           // output channels per workgroup
 constexpr int RROW = 128;         // LDS bytes per row: 64 channels of 16 bits
 constexpr int RSUB = RROW / 16;   // 16-byte sub-chunks per row
-constexpr int RW_BYTES = 9 * RNT * RROW;  // the weight slice of a workgroup, staged once
 constexpr int NCW = 4;            // consumer waves
 constexpr int NPW = 4;            // producer waves
 constexpr int RWG = 64 * (NCW + NPW);
@@ -583,21 +583,26 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     const int cb = cobase + kg * 8;  // the first of this lane's 8 output channels
     const T* __restrict__ bias = (const T*)a.bias;
     Vec<T, 8> braw;                  // their bias, converted once the weights are in registers
-    // The weight slice of this workgroup (rows [tap][co], 64 channels each) is
-    // copied to LDS by the consumers while the producers plan and issue tile 0;
-    // it sits over buffers 1 and 2 until the consumers hold it in registers.
-    // The consumers issue these copies before they read the mask.
-    unsigned char* s_w = smem + buf_bytes;
+    // A consumer loads its 32 x 9 x C_in weights straight into registers while
+    // the producers plan and issue tile 0 (16 bytes per lane and fragment; the
+    // LDS copy engine stays free for the tile).  Row m of channel block j of a
+    // fragment is channel kg' * 8 + j * 4 + (m & 3) of the wave's 32 (kg' = m >> 2).
+    frag Wr[9][NKS][2];
     if (!producer) {
         const T* __restrict__ wgt = (const T*)a.weight;
-        for (int w0 = wave * 64; w0 < 9 * RNT * RSUB; w0 += 64 * NCW) {
-            const int s = w0 + lane;
-            const int row = s >> 3, q = (s & 7) ^ (row & 7);
-            const int tap = row / RNT, col = row - tap * RNT;
-            const int co = co0 + col, ci = q * 8;
-            if (co < a.C_out && ci < a.C_in) dma16(wgt + ((size_t)co * 9 + tap) * a.C_in + ci, s_w + w0 * 16);
-            else lds_zero16(s_w + s * 16);
-        }
+        const int co = cobase + (l16 >> 2) * 8 + (l16 & 3);
+#pragma unroll
+        for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int c = co + j * 4, ci = (ks * 4 + kg) * 8;
+                    if (c < a.C_out && ci < a.C_in)
+                        Wr[tap][ks][j] = *reinterpret_cast<const frag*>(wgt + ((size_t)c * 9 + tap) * a.C_in + ci);
+                    else
+                        Wr[tap][ks][j] = frag{};
+                }
         if (bias) {
             if (cb + 8 <= a.C_out && (reinterpret_cast<uintptr_t>(bias) & 15) == 0) {
                 braw = vload<T, 8>(bias + cb);
@@ -630,9 +635,9 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     // complete tile i + 1 (buffer (i + 1) % 3: wait for its copies, write its
     // register items) and issue tile i + 2 (buffer (i + 2) % 3).
     // Before the loop:
-    //   producers: issue tile 0 | (1) | complete tile 0 | (2) | issue tile 1
-    //   consumers: weights -> LDS | (1) | weights -> registers | (2)
-    // Both roles walk the same tile sequence and take two barriers before the
+    //   producers: issue tile 0, complete tile 0 | (0) | issue tile 1
+    //   consumers: weights -> registers           | (0)
+    // Both roles walk the same tile sequence and take one barrier before the
     // loop and one per step, so they leave together.  The roles have separate
     // loops so that the producers' in-flight items and the consumers' weights
     // do not compete for registers.
@@ -644,10 +649,9 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
         ResAvg<T, SRC> av;
         av.clear();
         if (h0) rw_issue<T, SRC>(g, a, nb0, t0, bufn(0), ptid, av);
-        res_barrier();                             // (1) the weights are in LDS
         if (h0) rw_complete<T, SRC>(g, a, nb0, t0, bufn(0), ptid, av);
         __builtin_amdgcn_s_waitcnt(0xC07F);        // lgkmcnt(0): tile 0's LDS writes are done
-        res_barrier();                             // (2) tile 0 is staged, the weights are in registers
+        res_barrier();                             // (0) tile 0 is staged, the weights are in registers
         if (h1) rw_issue<T, SRC>(g, a, nb1, t1, bufn(1), ptid, av);
         int b = 0;  // i % 3
         while (h0) {
@@ -669,29 +673,16 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
         return;
     }
 
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's weight copies (and bias, mask) have landed
-    res_barrier();                  // (1)
-    // A row m of channel block j is channel kg' * 8 + j * 4 + (m & 3) of the wave's 32 (kg' = m >> 2)
-    frag Wr[9][NKS][2];
-#pragma unroll
-    for (int tap = 0; tap < 9; ++tap)
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int row = tap * RNT + 32 * h + (l16 >> 2) * 8 + j * 4 + (l16 & 3);
-                Wr[tap][ks][j] = *reinterpret_cast<const frag*>(s_w + row * RROW + (((ks * 4 + kg) ^ (row & 7)) << 4));
-            }
     const bool relu = (a.flags & 1) != 0;
     float bv[2][4];
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) bv[j][r] = (bias && cb + j * 4 + r < a.C_out) ? to_f32(braw.e[j * 4 + r]) : 0.0f;
-    // All counters: the weight reads, and (for the compiler's wait tracking) no LDS
-    // copy pending on this path, which keeps the waits for the MFMA operands partial.
+    // All counters: the weight loads, and (for the compiler's wait tracking) nothing
+    // pending on this path, which keeps the waits for the MFMA operands partial.
     __builtin_amdgcn_s_waitcnt(0);
-    res_barrier();  // (2)
+    res_barrier();  // (0)
 
     int b = 0;
     while (h0) {
@@ -798,9 +789,9 @@ bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     const long long cap = (a.hi_cap > a.lo_cap ? a.hi_cap : a.lo_cap) + 1LL;
     const long long stk = cap * (g.bs + 2) * (g.bs + 2) * (a.C_in > a.C_out ? a.C_in : a.C_out);
     if (img >= (1LL << 31) || stk >= (1LL << 31)) return false;
-    // three tile buffers, the last two of which also hold the weights at start-up
+    // three tile buffers
     const int bb = res_buf_bytes(g.bs, res_rows(g.bs));
-    return NBUF * bb <= 160 * 1024 && 2 * bb >= RW_BYTES;
+    return NBUF * bb <= 160 * 1024;
 }
 
 hipError_t launch_conv_res(int dtype, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask, const ConvArgs& a,
