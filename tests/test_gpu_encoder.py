@@ -70,6 +70,9 @@ BCASES = [
     BCase("ig_blocks1200_f16", "f16", 1, 64, 64, 120, 160, 4, 3, 1, seed=80),
     BCase("ig_alllow_k3s2_f16", "f16", 1, 64, 128, 32, 32, 8, 3, 2, mask_kind="low", seed=81),
     BCase("ig_allhigh_k3s1_bf16", "bf16", 1, 128, 64, 16, 32, 8, 3, 1, mask_kind="high", seed=82),
+    # 128 input channels with both classes: the low stack is padded once before the GEMM
+    BCase("ig_lowpad_k3s2_c128_bf16", "bf16", 2, 128, 128, 32, 64, 8, 3, 2, relu=True, seed=83),
+    BCase("ig_lowpad_k3s1_c128_bs16_f16", "f16", 2, 128, 64, 64, 96, 16, 3, 1, p_low=0.75, residual=True, seed=84),
 ]
 
 
