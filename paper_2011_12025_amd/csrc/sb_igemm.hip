@@ -162,17 +162,26 @@ __device__ __forceinline__ void gissue_a(const T* const (&wrow)[AR], unsigned ch
 // DMA of one step's pixel rows (zeros for pixels outside the image; the
 // top-left source of a 2x2-average pixel).
 template <typename T, int BR>
-__device__ __forceinline__ void gissue_b(const uint32_t* s_desc, const int (&prow)[BR], const int (&pq)[BR], int KT,
-                                         int tap, int c, const T* __restrict__ in_hi, const T* __restrict__ in_lo,
-                                         const T* zrow, int C_in, unsigned char* st, int wave) {
+__device__ __forceinline__ void gissue_b(const uint32_t (&dsc)[BR], const int (&pq)[BR], int c,
+                                         const T* __restrict__ in_hi, const T* __restrict__ in_lo, const T* zrow,
+                                         int C_in, unsigned char* st, int wave) {
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
-        const uint32_t d = s_desc[prow[j] * KT + tap];
+        const uint32_t d = dsc[j];
         const uint32_t kind = d >> 30;
         const T* base = kind == GK_LO ? in_lo : (kind == GK_ZERO ? zrow : in_hi);
         const size_t pix = kind != GK_ZERO ? (size_t)(d & 0x3FFFFFFFu) : 0;
         gdma16(base + pix * C_in + c + pq[j], st + (wave * BR + j) * 1024);
     }
+}
+
+// This lane's pixel-row descriptors of one tap, held in registers for the
+// steps of that tap.
+template <int BR>
+__device__ __forceinline__ void gload_desc(const uint32_t* s_desc, const int (&prow)[BR], int KT, int tap,
+                                           uint32_t (&dsc)[BR]) {
+#pragma unroll
+    for (int j = 0; j < BR; ++j) dsc[j] = s_desc[prow[j] * KT + tap];
 }
 
 // N DMAs of zeros into a stage that no step reads (keeps the count per step constant)
@@ -186,12 +195,12 @@ __device__ __forceinline__ void gissue_pad(const T* zrow, unsigned char* st, int
 // 2x2-average pixels of one step, copied into the side buffer: window
 // (wave * BR + j) * 3 + t, this lane's slot at lane * 16.
 template <typename T, int BR>
-__device__ __forceinline__ void gissue_side(const uint32_t* s_desc, const int (&prow)[BR], const int (&pq)[BR], int KT,
-                                            int tap, int c, const T* __restrict__ in_hi, int C_in, int bs,
-                                            unsigned char* side, int wave) {
+__device__ __forceinline__ void gissue_side(const uint32_t (&dsc)[BR], const int (&pq)[BR], int c,
+                                            const T* __restrict__ in_hi, int C_in, int bs, unsigned char* side,
+                                            int wave) {
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
-        const uint32_t d = s_desc[prow[j] * KT + tap];
+        const uint32_t d = dsc[j];
         if ((d >> 30) == GK_AVG) {
             const T* p0 = in_hi + (size_t)(d & 0x3FFFFFFFu) * C_in + c + pq[j];
             unsigned char* w = side + (wave * BR + j) * 3 * 1024;
@@ -205,11 +214,11 @@ __device__ __forceinline__ void gissue_side(const uint32_t* s_desc, const int (&
 // Replaces the top-left value of every 2x2-average pixel of a landed step
 // (st: the step's pixel tile) by the average of its four sources.
 template <typename T, int BR>
-__device__ __forceinline__ void gcommit_side(const uint32_t* s_desc, const int (&prow)[BR], int KT, int tap,
-                                             unsigned char* st, const unsigned char* side, int wave, int lane) {
+__device__ __forceinline__ void gcommit_side(const uint32_t (&dsc)[BR], unsigned char* st, const unsigned char* side,
+                                             int wave, int lane) {
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
-        const uint32_t d = s_desc[prow[j] * KT + tap];
+        const uint32_t d = dsc[j];
         if ((d >> 30) == GK_AVG) {
             unsigned char* slot = st + (wave * BR + j) * 1024 + lane * 16;
             const unsigned char* w = side + (wave * BR + j) * 3 * 1024 + lane * 16;
@@ -435,17 +444,19 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     // ---- prologue: step 0 (2x2 averages, pixels), step 1 (weights, pixels)
     int tap1 = tap0, c1 = c0 + 1;
     if (c1 == cpt) { c1 = 0; ++tap1; }
-    gissue_side<T, BR>(s_desc, prow, pq, KT, tap0, c0 * GKC, in_hi, C_in, bs, s_side, wave);
-    gissue_b<T, BR>(s_desc, prow, pq, KT, tap0, c0 * GKC, in_hi, in_lo, zrow, C_in, s_stage + A_BYTES, wave);
+    uint32_t d0[BR], dA[BR], dB[BR];  // descriptors of steps 0 / s + 1 / s + 2
+    gload_desc<BR>(s_desc, prow, KT, tap0, d0);
+    gload_desc<BR>(s_desc, prow, KT, tap1 < KT ? tap1 : tap0, dA);
+    gissue_side<T, BR>(d0, pq, c0 * GKC, in_hi, C_in, bs, s_side, wave);
+    gissue_b<T, BR>(d0, pq, c0 * GKC, in_hi, in_lo, zrow, C_in, s_stage + A_BYTES, wave);
     if (n > 1) {
         gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
-        gissue_b<T, BR>(s_desc, prow, pq, KT, tap1, c1 * GKC, in_hi, in_lo, zrow, C_in, s_stage + STAGE + A_BYTES,
-                        wave);
+        gissue_b<T, BR>(dA, pq, c1 * GKC, in_hi, in_lo, zrow, C_in, s_stage + STAGE + A_BYTES, wave);
     } else {
         gissue_pad<T, AR + BR>(zrow, s_stage + STAGE, wave, lane);
     }
     __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-    gcommit_side<T, BR>(s_desc, prow, KT, tap0, s_stage + A_BYTES, s_side, wave, lane);
+    gcommit_side<T, BR>(d0, s_stage + A_BYTES, s_side, wave, lane);
     gbarrier();
 
     floatx4 acc[MS][NS];
@@ -460,17 +471,17 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     int ta = tap1, ca = c1;
     int tb = tap1, cb = c1 + 1;
     if (cb == cpt) { cb = 0; ++tb; }
+    gload_desc<BR>(s_desc, prow, KT, tb < KT ? tb : tap0, dB);
     int b_cur = 0;
 
     for (int s = 0; s < n; ++s) {
         unsigned char* cur = s_stage + b_cur * STAGE;
         const int b1 = b_cur == GNST - 1 ? 0 : b_cur + 1;
         const int b2 = b1 == GNST - 1 ? 0 : b1 + 1;
-        if (s + 1 < n) gissue_side<T, BR>(s_desc, prow, pq, KT, ta, ca * GKC, in_hi, C_in, bs, s_side, wave);
+        if (s + 1 < n) gissue_side<T, BR>(dA, pq, ca * GKC, in_hi, C_in, bs, s_side, wave);
         if (s + 2 < n) {
             gissue_a<T, AR>(wrow, s_stage + b2 * STAGE, tb * C_in + cb * GKC, wave);
-            gissue_b<T, BR>(s_desc, prow, pq, KT, tb, cb * GKC, in_hi, in_lo, zrow, C_in,
-                            s_stage + b2 * STAGE + A_BYTES, wave);
+            gissue_b<T, BR>(dB, pq, cb * GKC, in_hi, in_lo, zrow, C_in, s_stage + b2 * STAGE + A_BYTES, wave);
         } else {
             gissue_pad<T, AR + BR>(zrow, s_stage + b2 * STAGE, wave, lane);
         }
@@ -490,11 +501,17 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         }
         // step s + 1 has landed once only step s + 2's DMAs can be outstanding
         __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-        if (s + 1 < n) gcommit_side<T, BR>(s_desc, prow, KT, ta, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
+        if (s + 1 < n) gcommit_side<T, BR>(dA, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
         gbarrier();
         b_cur = b1;
         ta = tb; ca = cb;
-        if (++cb == cpt) { cb = 0; ++tb; }
+#pragma unroll
+        for (int j = 0; j < BR; ++j) dA[j] = dB[j];
+        if (++cb == cpt) {  // a new tap: its descriptors (read a step before they are used)
+            cb = 0;
+            ++tb;
+            if (tb < KT) gload_desc<BR>(s_desc, prow, KT, tb, dB);
+        }
     }
     __builtin_amdgcn_s_waitcnt(0);  // the padding DMAs
 
