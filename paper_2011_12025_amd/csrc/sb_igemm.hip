@@ -626,7 +626,11 @@ hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) {
 }
 
 int g_cus = 0;
-constexpr int GSPLIT_COST = 6;  // the partial-sum pass, in K steps (about 1 us each)
+// Launch cost model, in K steps (about 1 us each): a workgroup's start-up
+// (mask plan, descriptors, first stages), and the partial-sum pass, which
+// reads every split's partial tiles.
+constexpr int GSTART_COST = 5;
+constexpr int GSPLIT_COST = 5;  // plus one per split
 
 inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -657,9 +661,10 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     if (tiles == 0) return hipSuccess;
     const int tiles_n = (a.C_out + TN - 1) / TN;
     // Split K: one workgroup per CU at a time (LDS), each taking about the
-    // same time per K step, so a launch costs about rounds x steps per split;
-    // a split costs the partial-sum pass on top.  Take the cheapest split that
-    // keeps at least four steps per workgroup.
+    // same time per K step, so a launch costs about rounds x (steps per split
+    // + start-up); a split costs the partial-sum pass on top, which grows with
+    // the number of splits.  Take the cheapest split that keeps at least four
+    // steps per workgroup.
     if (g_cus == 0) {
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -673,7 +678,7 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
         long long best = 0;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
             const long long rounds = (wgs * c + g_cus - 1) / g_cus;
-            const long long cost = rounds * ((nsteps + c - 1) / c) + (c > 1 ? GSPLIT_COST : 0);
+            const long long cost = rounds * ((nsteps + c - 1) / c + GSTART_COST) + (c > 1 ? GSPLIT_COST + c : 0);
             if (c == 1 || cost < best) {
                 best = cost;
                 S = c;
