@@ -630,7 +630,7 @@ int g_cus = 0;
 // (mask plan, descriptors, first stages), and the partial-sum pass, which
 // reads every split's partial tiles.
 constexpr int GSTART_COST = 5;
-constexpr int GSPLIT_COST = 5;  // plus one per split
+constexpr int GSPLIT_COST = 10;  // plus one per split
 
 inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
