@@ -17,12 +17,15 @@
  *    channels-last fp16/bf16 block convolutions with C_in % 64 == 0
  *    (segblocks_block_conv3x3 beyond C_in = 64, segblocks_block_conv_ex)
  *    may split their reduction over several workgroups and then keep fp32
- *    partial tiles in a per-device workspace that the library allocates on
- *    first need and keeps until the process ends.  It is grown only outside
- *    stream capture: a call that needs more than the workspace holds while
- *    its stream is being captured into a graph fails with SB_EHIP
- *    (run the same call once before capturing).  Calls that overlap on one
- *    device share the workspace and must be ordered by the caller.
+ *    partial tiles (and, at 128 input channels, the padded low stack) in a
+ *    per-device workspace that the library allocates on first need and
+ *    keeps until the process ends; segblocks_layer with more than 256 input
+ *    channels (channels-last fp16/bf16) keeps its packed stacks in a second
+ *    one.  They are grown only outside stream capture: a call that needs
+ *    more than a workspace holds while its stream is being captured into a
+ *    graph fails with SB_EHIP (run the same call once before capturing).
+ *    Calls that overlap on one device share the workspaces and must be
+ *    ordered by the caller.
  *  - Logical dimensions are always N, C, H, W.  `layout` selects the memory
  *    format of every 4-d tensor of the call (input, stacks, output and the
  *    convolution weight):

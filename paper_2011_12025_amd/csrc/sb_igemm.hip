@@ -588,26 +588,29 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
     *reinterpret_cast<uint4*>(out + off) = o.raw;
 }
 
-// One workspace per device for the split partials, grown on demand (never
-// while the stream is being captured into a graph).  A buffer that is
-// outgrown is not freed, since a graph captured earlier may still use it:
-// every buffer lives until the process ends (at most twice the largest
-// request in total).  Calls that run concurrently on one device share the
-// workspace and must be ordered by the caller.
+}  // namespace
+
+// Workspaces per device (pool 0: the GEMM's split partials and padded low
+// stack; pool 1: the packed stacks of a fused layer routed through the GEMM),
+// grown on demand (never while the stream is being captured into a graph).
+// A buffer that is outgrown is not freed, since a graph captured earlier may
+// still use it: every buffer lives until the process ends (at most twice the
+// largest request in total).  Calls that run concurrently on one device
+// share the workspaces and must be ordered by the caller.
 struct GPool {
     void* p = nullptr;
     size_t bytes = 0;
 };
-GPool g_pool[64];
-std::mutex g_pool_mu;
+static GPool g_pool[2][64];
+static std::mutex g_pool_mu;
 
-hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) {
+hipError_t lib_workspace(int pool, size_t bytes, hipStream_t st, void** out) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (dev < 0 || dev >= 64 || pool < 0 || pool > 1) return hipErrorInvalidValue;
     std::lock_guard<std::mutex> lk(g_pool_mu);
-    GPool& P = g_pool[dev];
+    GPool& P = g_pool[pool][dev];
     if (P.bytes < bytes) {
         hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
         e = hipStreamIsCapturing(st, &cs);
@@ -624,6 +627,10 @@ hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) {
     *out = P.p;
     return hipSuccess;
 }
+
+namespace {
+
+hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) { return lib_workspace(0, bytes, st, out); }
 
 int g_cus = 0;
 // Launch cost model, in K steps (about 1 us each): a workgroup's start-up

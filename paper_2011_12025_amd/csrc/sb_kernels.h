@@ -56,6 +56,9 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
 // multi-block implicit GEMM on packed channels-last stacks (fp16 / bf16,
 // C_in % 64 == 0, C_out % 8 == 0, at most 8192 blocks), BlockPad fused
 bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
+// Library-owned device memory: pool 0 belongs to the GEMM (split partials,
+// padded low stack), pool 1 to a fused layer routed through the GEMM.
+hipError_t lib_workspace(int pool, size_t bytes, hipStream_t st, void** out);
 hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         hipStream_t st);
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,

@@ -179,3 +179,24 @@ def test_full_size_layer_stage1_config():
     assert_bitexact(lp, ref["lp"], "full-size pad lo")
     ho, lo_o = sb.conv3x3(hp, lp, md, c.bs, c.H, c.W, w.cuda(), b.cuda())
     assert torch.equal(sb.combine(ho, lo_o, md, c.bs, c.H, c.W), y)
+
+
+# Fused layers with more than 256 input channels run as split, the implicit
+# GEMM's block convolution and combine over library workspace stacks.
+DEEP_CASES = [Case("deep512_f16", "f16", 1, 512, 64, 32, 64, 8, seed=21),
+              Case("deep384_bf16", "bf16", 2, 384, 128, 16, 32, 4, p_low=0.6, seed=22),
+              Case("deep512_allhigh_f16", "f16", 1, 512, 32, 16, 32, 4, mask_kind="high", seed=23)]
+
+
+@pytest.mark.parametrize("c", DEEP_CASES, ids=_ids(DEEP_CASES))
+def test_deep_layer_matches_oracle(c):
+    import paper_2011_12025_amd as sb
+    mask, x, w, b, ref = prepared(c)
+    log(f"[deep layer] {c.name} N={c.N} C={c.C}->{c.Co} {c.H}x{c.W} bs={c.bs}")
+    md = torch.from_numpy(mask).cuda()
+    y = sb.layer(to_dev(x, "nhwc"), md, c.bs, w.cuda(), None if b is None else b.cuda())
+    assert_conv_close(y, y64_from_stacks(c, mask, ref["ho64"], ref["lo64"]), c.dtype, 9 * c.C, "layer")
+    # a second call reuses the workspace
+    y2 = sb.layer(to_dev(x, "nhwc"), md, c.bs, w.cuda(), None if b is None else b.cuda())
+    assert torch.equal(y, y2)
+    torch.cuda.synchronize()
