@@ -19,9 +19,9 @@
  *    may split their reduction over several workgroups and then keep fp32
  *    partial tiles (and, at 128 input channels, the padded low stack) in a
  *    per-device workspace that the library allocates on first need and
- *    keeps until the process ends; segblocks_layer with more than 256 input
- *    channels (channels-last fp16/bf16) keeps its packed stacks in a second
- *    one.  They are grown only outside stream capture: a call that needs
+ *    keeps until the process ends; segblocks_layer with 128 or more than
+ *    256 input channels (channels-last fp16/bf16, C_in % 64 == 0) keeps its
+ *    packed stacks in a second one.  They are grown only outside stream capture: a call that needs
  *    more than a workspace holds while its stream is being captured into a
  *    graph fails with SB_EHIP (run the same call once before capturing).
  *    Calls that overlap on one device share the workspaces and must be

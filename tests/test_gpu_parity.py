@@ -181,9 +181,11 @@ def test_full_size_layer_stage1_config():
     assert torch.equal(sb.combine(ho, lo_o, md, c.bs, c.H, c.W), y)
 
 
-# Fused layers with more than 256 input channels run as split, the implicit
-# GEMM's block convolution and combine over library workspace stacks.
+# Fused layers with 128 or more than 256 input channels run as split, the
+# implicit GEMM's block convolution and combine over library workspace stacks.
 DEEP_CASES = [Case("deep512_f16", "f16", 1, 512, 64, 32, 64, 8, seed=21),
+              Case("c128_layer_f16", "f16", 2, 128, 128, 32, 64, 8, seed=24),
+              Case("c128_layer_alllow_bf16", "bf16", 1, 128, 64, 32, 32, 16, mask_kind="low", seed=25),
               Case("deep384_bf16", "bf16", 2, 384, 128, 16, 32, 4, p_low=0.6, seed=22),
               Case("deep512_allhigh_f16", "f16", 1, 512, 32, 16, 32, 4, mask_kind="high", seed=23)]
 
