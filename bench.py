@@ -44,8 +44,10 @@ WL = dict(N=1, C=64, H=256, W=512, bs=32, dtype="f16", p_low=0.5, seed=0)
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=20)
+    # 1000 warm-up layers (about 20 ms of GPU work) bring the clocks to their
+    # steady state; after 20 the timed steps still ran 10-15 % slower
+    p.add_argument("--steps", type=int, default=1000)
+    p.add_argument("--warmup", type=int, default=1000)
     p.add_argument("--breakdown-iters", type=int, default=100)
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle sample length (0 = skip)")
     p.add_argument("--workload", default="layer", choices=["layer", "sweep", "encoder", "encoder-batched"],
