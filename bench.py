@@ -48,7 +48,7 @@ def parse():
     # steady state; after 20 the timed steps still ran 10-15 % slower
     p.add_argument("--steps", type=int, default=1000)
     p.add_argument("--warmup", type=int, default=1000)
-    p.add_argument("--breakdown-iters", type=int, default=100)
+    p.add_argument("--breakdown-iters", type=int, default=400)
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle sample length (0 = skip)")
     p.add_argument("--workload", default="layer", choices=["layer", "sweep", "encoder", "encoder-batched"],
                    help="layer: the headline single layer (one JSON line); sweep: the four ResNet-18 stage shapes "
@@ -194,7 +194,9 @@ def main():
         for i in range(5):
             launch(name, i)
         torch.cuda.synchronize()
-        torch.cuda._sleep(20_000_000)          # lets the host queue the whole batch first
+        torch.cuda._sleep(60_000_000)          # lets the host queue the whole batch first
+        for i in range(iters):                 # untimed: the clocks settle again after the sleep
+            launch(name, i)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for i in range(iters):
@@ -313,11 +315,14 @@ SWEEP_FRACTIONS = [0.0, 0.25, 0.5, 0.75, 1.0]
 def _gpu_ms(torch, launch, iters, warm=3):
     """Average time of `iters` back-to-back calls of launch(i), events on the
     current stream around the batch; the GPU is held by a sleep first so
-    that the host has queued the batch before the clock starts."""
+    that the host has queued the batch before the clock starts, and `iters`
+    untimed calls after the sleep let the clocks settle again."""
     for i in range(warm):
         launch(i)
     torch.cuda.synchronize()
-    torch.cuda._sleep(20_000_000)
+    torch.cuda._sleep(60_000_000)
+    for i in range(iters):
+        launch(i)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(iters):
