@@ -510,7 +510,7 @@ hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Ge
     // Measured on the stage shapes of a 1024x2048 image (8x16 blocks): at 128
     // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us;
     // at 256 the general kernel is faster (40-44 against 46-69 us) and stays.
-    if (src == SRC_DENSE && dst == DST_DENSE && (a.C_in <= 128 || a.C_in > 256) && layout == NHWC &&
+    if (src == SRC_DENSE && dst == DST_DENSE && ((a.C_in > 64 && a.C_in <= 128) || a.C_in > 256) && layout == NHWC &&
         (dtype == 1 || dtype == 2)) {
         const ConvArgs p{a.in_hi, a.in_hi, a.weight, a.bias, nullptr, nullptr, a.out_hi, a.out_hi,
                          a.C_in, a.C_out, a.flags, (int)g.B, (int)g.B};
