@@ -362,43 +362,59 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
     const int Y0 = oy0 * S - P, X0 = ox0 * S - P;
     const int tid = threadIdx.x;
 
-    // Staging in batches: every thread issues SB loads before it writes any of
-    // them to LDS, so the loads of a batch are in flight together.
-    constexpr int SB = 8;
-    const int nw = 64 * K * 32;
-    for (int base = tid; base < nw; base += WG * SB) {
-        T v[SB];
+    // Staging in batches: every thread issues a batch of loads before it
+    // writes any of them to LDS, so the loads of a batch are in flight
+    // together.  The batches cover the whole weight slice (7 x 7 taps: one
+    // batch) and the whole input tile (one batch): each further batch is one
+    // more memory round trip at kernel start, about 3 us each.
+    // Element i of a staged array is (row, column) = (i / width, i % width);
+    // a thread's elements are WG apart, so both advance by constants (no
+    // division per element).
+    constexpr int SBW = 56, SBI = 20;
+    const int KW = K * 32, nw = 64 * KW;
+    const int dwq = WG / KW, dwr = WG - dwq * KW;
+    for (int base = tid; base < nw; base += WG * SBW) {
+        T v[SBW];
+        int r = base / KW, rem = base - r * KW;
 #pragma unroll
-        for (int u = 0; u < SB; ++u) {
+        for (int u = 0; u < SBW; ++u) {
             const int i = base + u * WG;
             v[u] = from_f32<T>(0.0f);
             if (i < nw) {
-                const int r = i / (K * 32), rem = i - r * (K * 32);
                 const int ky = rem >> 5, kx = (rem & 31) >> 2, ci = rem & 3;
                 const int co = co0 + stem_perm(r);
                 if (co < C_out && kx < K && ci < C_in) v[u] = w[(((size_t)co * K + ky) * K + kx) * C_in + ci];
             }
+            r += dwq;
+            rem += dwr;
+            if (rem >= KW) { rem -= KW; ++r; }
         }
+        r = base / KW;
+        rem = base - r * KW;
 #pragma unroll
-        for (int u = 0; u < SB; ++u) {
+        for (int u = 0; u < SBW; ++u) {
             const int i = base + u * WG;
-            if (i < nw) {
-                const int r = i / (K * 32), rem = i - r * (K * 32);
-                s_w[r * WROW + rem] = v[u];
-            }
+            if (i < nw) s_w[r * WROW + rem] = v[u];
+            r += dwq;
+            rem += dwr;
+            if (rem >= KW) { rem -= KW; ++r; }
         }
     }
     const T* __restrict__ img = x + (size_t)n * H * W * C_in;
     const int np = IH * IW;
-    for (int base = tid; base < np; base += WG * SB) {
-        Vec<T, 4> v[SB];
+    const int diq = WG / IW, dir = WG - diq * IW;
+    for (int base = tid; base < np; base += WG * SBI) {
+        Vec<T, 4> v[SBI];
+        int r = base / IW, c = base - r * IW;
 #pragma unroll
-        for (int u = 0; u < SB; ++u) {
+        for (int u = 0; u < SBI; ++u) {
             const int i = base + u * WG;
             v[u] = vzero<T, 4>();
+            const int yy = Y0 + r, xx = X0 + c;
+            r += diq;
+            c += dir;
+            if (c >= IW) { c -= IW; ++r; }
             if (i < np) {
-                const int r = i / IW, c = i - r * IW;
-                const int yy = Y0 + r, xx = X0 + c;
                 if (yy >= 0 && yy < H && xx >= 0 && xx < W) {
                     const T* p = img + ((size_t)yy * W + xx) * C_in;
 #pragma unroll
@@ -408,7 +424,7 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
             }
         }
 #pragma unroll
-        for (int u = 0; u < SB; ++u) {
+        for (int u = 0; u < SBI; ++u) {
             const int i = base + u * WG;
             if (i < np) *reinterpret_cast<uint2*>(s_in + (size_t)i * 4) = v[u].raw;
         }
