@@ -333,7 +333,8 @@ hipError_t bconv_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksi
 // ---------------------------------------------------------------------------
 // stem: dense convolution of a map with at most 4 channels
 // ---------------------------------------------------------------------------
-constexpr int ST_TH = 16, ST_TW = 64;  // output tile: 16 rows (four per wave) x 64 columns x 64 channels
+constexpr int ST_WG = 512, ST_WAVES = ST_WG / 64;  // eight waves, one workgroup per CU
+constexpr int ST_TH = 32, ST_TW = 64;  // output tile: 32 rows (four per wave) x 64 columns x 64 channels
 
 // output channel of LDS weight row r (within a 32-row group, row 16h + 4kg + i
 // holds channel 8kg + 4h + i), so that a lane's two fragments of a group
@@ -344,7 +345,7 @@ __device__ __forceinline__ int stem_perm(int r) {
 }
 
 template <typename T>
-__global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, int H, int W,
+__global__ __launch_bounds__(ST_WG) void k_stem(const T* __restrict__ x, int C_in, int H, int W,
                                              const T* __restrict__ w, const T* __restrict__ bias, int C_out, int K,
                                              int S, int P, int flags, T* __restrict__ y, int Ho, int Wo, int TY,
                                              int TX) {
@@ -368,17 +369,17 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
     // batch) and the whole input tile (one batch): each further batch is one
     // more memory round trip at kernel start, about 3 us each.
     // Element i of a staged array is (row, column) = (i / width, i % width);
-    // a thread's elements are WG apart, so both advance by constants (no
+    // a thread's elements are ST_WG apart, so both advance by constants (no
     // division per element).
-    constexpr int SBW = 56, SBI = 20;
+    constexpr int SBW = 28, SBI = 20;
     const int KW = K * 32, nw = 64 * KW;
-    const int dwq = WG / KW, dwr = WG - dwq * KW;
-    for (int base = tid; base < nw; base += WG * SBW) {
+    const int dwq = ST_WG / KW, dwr = ST_WG - dwq * KW;
+    for (int base = tid; base < nw; base += ST_WG * SBW) {
         T v[SBW];
         int r = base / KW, rem = base - r * KW;
 #pragma unroll
         for (int u = 0; u < SBW; ++u) {
-            const int i = base + u * WG;
+            const int i = base + u * ST_WG;
             v[u] = from_f32<T>(0.0f);
             if (i < nw) {
                 const int ky = rem >> 5, kx = (rem & 31) >> 2, ci = rem & 3;
@@ -393,7 +394,7 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
         rem = base - r * KW;
 #pragma unroll
         for (int u = 0; u < SBW; ++u) {
-            const int i = base + u * WG;
+            const int i = base + u * ST_WG;
             if (i < nw) s_w[r * WROW + rem] = v[u];
             r += dwq;
             rem += dwr;
@@ -402,13 +403,13 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
     }
     const T* __restrict__ img = x + (size_t)n * H * W * C_in;
     const int np = IH * IW;
-    const int diq = WG / IW, dir = WG - diq * IW;
-    for (int base = tid; base < np; base += WG * SBI) {
+    const int diq = ST_WG / IW, dir = ST_WG - diq * IW;
+    for (int base = tid; base < np; base += ST_WG * SBI) {
         Vec<T, 4> v[SBI];
         int r = base / IW, c = base - r * IW;
 #pragma unroll
         for (int u = 0; u < SBI; ++u) {
-            const int i = base + u * WG;
+            const int i = base + u * ST_WG;
             v[u] = vzero<T, 4>();
             const int yy = Y0 + r, xx = X0 + c;
             r += diq;
@@ -425,7 +426,7 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
         }
 #pragma unroll
         for (int u = 0; u < SBI; ++u) {
-            const int i = base + u * WG;
+            const int i = base + u * ST_WG;
             if (i < np) *reinterpret_cast<uint2*>(s_in + (size_t)i * 4) = v[u].raw;
         }
     }
@@ -441,8 +442,8 @@ __global__ __launch_bounds__(WG) void k_stem(const T* __restrict__ x, int C_in, 
             const int co = co0 + jj * 32 + kg * 8 + i;
             bv[jj][i] = (bias && co < C_out) ? to_f32(bias[co]) : 0.0f;
         }
-    for (int rr = 0; rr < ST_TH / 4; ++rr) {
-        const int ol = wave * (ST_TH / 4) + rr;  // output row within the tile
+    for (int rr = 0; rr < ST_TH / ST_WAVES; ++rr) {
+        const int ol = wave * (ST_TH / ST_WAVES) + rr;  // output row within the tile
         floatx4 acc[4][4];
 #pragma unroll
         for (int t = 0; t < 4; ++t)
@@ -552,7 +553,7 @@ hipError_t stem_t(const void* x, int N, int C_in, int H, int W, const void* w, c
         set = smem;
     }
     const dim3 grid((unsigned)(N * TY * TX), (unsigned)((C_out + 63) / 64));
-    hipLaunchKernelGGL(k_stem<T>, grid, dim3(WG), smem, st, (const T*)x, C_in, H, W, (const T*)w, (const T*)bias,
+    hipLaunchKernelGGL(k_stem<T>, grid, dim3(ST_WG), smem, st, (const T*)x, C_in, H, W, (const T*)w, (const T*)bias,
                        C_out, K, S, P, flags, (T*)y, Ho, Wo, TY, TX);
     return hipGetLastError();
 }
