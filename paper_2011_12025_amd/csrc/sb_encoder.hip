@@ -333,8 +333,8 @@ hipError_t bconv_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksi
 // ---------------------------------------------------------------------------
 // stem: dense convolution of a map with at most 4 channels
 // ---------------------------------------------------------------------------
-constexpr int ST_WG = 512, ST_WAVES = ST_WG / 64;  // eight waves, one workgroup per CU
-constexpr int ST_TH = 32, ST_TW = 64;  // output tile: 32 rows (four per wave) x 64 columns x 64 channels
+constexpr int ST_WG = 1024, ST_WAVES = ST_WG / 64;  // sixteen waves, one workgroup per CU
+constexpr int ST_TH = 32, ST_TW = 64;  // output tile: 32 rows (two per wave) x 64 columns x 64 channels
 
 // output channel of LDS weight row r (within a 32-row group, row 16h + 4kg + i
 // holds channel 8kg + 4h + i), so that a lane's two fragments of a group
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(ST_WG) void k_stem(const T* __restrict__ x, int C_i
     // Element i of a staged array is (row, column) = (i / width, i % width);
     // a thread's elements are ST_WG apart, so both advance by constants (no
     // division per element).
-    constexpr int SBW = 28, SBI = 20;
+    constexpr int SBW = 14, SBI = 10;
     const int KW = K * 32, nw = 64 * KW;
     const int dwq = ST_WG / KW, dwr = ST_WG - dwq * KW;
     for (int base = tid; base < nw; base += ST_WG * SBW) {
