@@ -132,9 +132,9 @@ def main():
 
     def args_for(name, s):
         if name == "layer":
-            return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, wp, bp, C, P(s["y"]), stream)
+            return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, wp, bp, C, P(s["y"]), None, 0, stream)
         if name == "layer_allhigh":
-            return (P(s["x"]), DT, LAY, N, C, H, W, on, bs, wp, bp, C, P(s["yc"]), stream)
+            return (P(s["x"]), DT, LAY, N, C, H, W, on, bs, wp, bp, C, P(s["yc"]), None, 0, stream)
         if name == "split":
             return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, P(s["hi"]), nh, P(s["lo"]), nl, stream)
         if name == "pad":
@@ -146,7 +146,7 @@ def main():
             return (P(s["ho"]), P(s["lo_o"]), DT, LAY, N, C, H, W, mk, bs, nh, nl, P(s["yc"]), stream)
         if name == "block_conv3x3":
             return (P(s["hi"]), P(s["lo"]), DT, LAY, N, C, H, W, mk, bs, wp, bp, C, 0, None, None, P(s["ho"]),
-                    P(s["lo_o"]), nh, nl, stream)
+                    P(s["lo_o"]), nh, nl, None, 0, stream)
         raise KeyError(name)
 
     FN = dict(layer=lib.segblocks_layer, layer_allhigh=lib.segblocks_layer, split=lib.segblocks_split,
@@ -364,6 +364,19 @@ def bench_sweep(args, torch, np, sb, B, inputs):
     it = args.breakdown_iters
     for li, (C, H, W, bs) in enumerate(SWEEP_LAYERS):
         lb, es = bs // 2, 2
+        # one workspace per call site, sized for the largest need over the fractions
+        B_ = (H // bs) * (W // bs)
+        ws_layer = sb.layer_workspace_size(torch.float16, B.SB_NHWC, 1, C, H, W, bs, C)
+        ws_bc = max(sb.block_conv3x3_workspace_size(torch.float16, B.SB_NHWC, 1, C, H, W, bs, C, h, B_ - h)
+                    for h in range(B_ + 1))
+        ws_ex = max(sb.block_conv_ex_workspace_size(torch.float16, 1, C, H, W, bs, C, 3, 1, h, B_ - h)
+                    for h in range(B_ + 1))
+        wsl, wsb, wse = [None if n == 0 else torch.empty(n + 256, dtype=torch.uint8, device=dev)
+                         for n in (ws_layer, ws_bc, ws_ex)]
+
+        def wsp(t):
+            return (None, 0) if t is None else (ctypes.c_void_p(t.data_ptr() + (-t.data_ptr()) % 256),
+                                                t.numel() - (-t.data_ptr()) % 256)
         x0 = inputs.feature_map(0, 1, C, H, W, "f16")
         w = inputs.conv_weight(0, C, C, 3, "f16").to(dev).contiguous(memory_format=cl)
         b = inputs.conv_bias(0, C, 9 * C, "f16").to(dev)
@@ -387,14 +400,15 @@ def bench_sweep(args, torch, np, sb, B, inputs):
 
             def layer(i):
                 rc = lib.segblocks_layer(P(xs[i % R]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs, P(w), P(b), C,
-                                         P(ys[i % R]), stream)
+                                         P(ys[i % R]), *wsp(wsl), stream)
                 if rc:
                     raise RuntimeError(lib.segblocks_last_error().decode())
 
             def bconv(i):
                 r = i % R
                 rc = lib.segblocks_block_conv3x3(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
-                                                 P(w), P(b), C, 0, None, None, P(hos[r]), P(loos[r]), nh, nl, stream)
+                                                 P(w), P(b), C, 0, None, None, P(hos[r]), P(loos[r]), nh, nl,
+                                                 *wsp(wsb), stream)
                 if rc:
                     raise RuntimeError(lib.segblocks_last_error().decode())
 
@@ -402,7 +416,7 @@ def bench_sweep(args, torch, np, sb, B, inputs):
                 r = i % R
                 rc = lib.segblocks_block_conv_ex(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
                                                  P(w), P(b), C, 3, 1, 0, None, None, P(hos[r]), P(loos[r]), nh, nl,
-                                                 stream)
+                                                 *wsp(wse), stream)
                 if rc:
                     raise RuntimeError(lib.segblocks_last_error().decode())
 

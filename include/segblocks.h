@@ -13,19 +13,21 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Pointers are DEVICE pointers unless stated otherwise.  The caller owns
- *    every input and output buffer.  One exception to "no library memory":
- *    channels-last fp16/bf16 block convolutions with C_in % 64 == 0
- *    (segblocks_block_conv3x3 beyond C_in = 64, segblocks_block_conv_ex)
- *    may split their reduction over several workgroups and then keep fp32
- *    partial tiles (and, at 128 input channels, the padded low stack) in a
- *    per-device workspace that the library allocates on first need and
- *    keeps until the process ends; segblocks_layer with 128 or more than
- *    256 input channels (channels-last fp16/bf16, C_in % 64 == 0) keeps its
- *    packed stacks in a second one.  They are grown only outside stream capture: a call that needs
- *    more than a workspace holds while its stream is being captured into a
- *    graph fails with SB_EHIP (run the same call once before capturing).
- *    Calls that overlap on one device share the workspaces and must be
- *    ordered by the caller.
+ *    every buffer; the library allocates no device memory.  Three calls may
+ *    need scratch memory beyond their inputs and outputs (fp32 partial tiles
+ *    of a reduction split over several workgroups, a padded copy of the low
+ *    stack, the packed stacks of a fused layer with many channels):
+ *    segblocks_block_conv3x3, segblocks_block_conv_ex and segblocks_layer
+ *    take it as a `workspace` pointer with its size `ws_bytes`.  The size a
+ *    call needs depends only on its shapes, capacities and device, and is
+ *    given by segblocks_block_conv3x3_workspace_size,
+ *    segblocks_block_conv_ex_workspace_size and
+ *    segblocks_layer_workspace_size (0 = none needed; NULL is then fine).  A
+ *    workspace must be 256-byte aligned and must not overlap any argument;
+ *    a smaller one (or NULL when one is needed) fails with SB_ENOMEM before
+ *    anything is launched.  The workspace holds no state between calls, but
+ *    it is in use until the call's kernels finish on `stream`: calls that
+ *    may overlap need workspaces of their own.
  *  - Logical dimensions are always N, C, H, W.  `layout` selects the memory
  *    format of every 4-d tensor of the call (input, stacks, output and the
  *    convolution weight):
@@ -51,7 +53,9 @@
  *  - bs must be even and >= 2, and divide H and W.  Low blocks have extent
  *    lb = bs/2.
  *  - Every call except segblocks_count is asynchronous on `stream` and
- *    performs no host synchronisation.  Arguments are validated on the host
+ *    performs no host synchronisation.  Calls may come from several host
+ *    threads at once (the library's launch-setup state is per device and
+ *    guarded).  Arguments are validated on the host
  *    before anything is launched; on failure nothing is launched, the call
  *    returns a negative sb_status and segblocks_last_error() describes it.
  *    Device faults surface at the caller's next synchronisation.
@@ -68,6 +72,7 @@
 #ifndef SEGBLOCKS_H
 #define SEGBLOCKS_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -81,7 +86,8 @@ typedef enum {
     SB_OK = 0,
     SB_EINVAL = -1, /* null pointer, bad enum, non-positive size, aliasing   */
     SB_ESHAPE = -2, /* bs odd or < 2, bs does not divide H or W, too large   */
-    SB_EHIP = -3    /* a HIP runtime call failed (message from the runtime)  */
+    SB_EHIP = -3,   /* a HIP runtime call failed (message from the runtime)  */
+    SB_ENOMEM = -4  /* the workspace argument is NULL or smaller than needed */
 } sb_status;
 
 /* Flags of segblocks_block_conv3x3. */
@@ -144,17 +150,22 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
                             const void* weight, const void* bias, int C_out, int flags,
                             const void* residual_hi, const void* residual_lo,
                             void* hi_out, void* lo_out, int hi_cap, int lo_cap,
-                            hipStream_t stream);
+                            void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* One complete block-conv layer, fused into a single kernel:
+/* One complete block-conv layer:
  *   y = combine(conv3x3(pad(split(x))))
  * x [N,C_in,H,W] -> y [N,C_out,H,W]; weight/bias as in segblocks_conv3x3.
- * Intermediate values are rounded to `dtype` exactly where the four-call
- * chain stores them, so the result equals that chain's up to the order of
- * the fp32 accumulation. */
+ * Channels-last fp16/bf16 with C_in <= 64 and blocks of 32 or 64 run as one
+ * kernel (the packed stacks never reach memory); channels-last fp16/bf16
+ * with C_in % 64 == 0 and 64 < C_in <= 128 or C_in > 256 run as three
+ * (split, the block convolution of segblocks_block_conv3x3, combine) over
+ * packed stacks in the workspace; everything else runs as one general
+ * kernel.  Intermediate values are rounded to `dtype` exactly where the
+ * four-call chain stores them, so the result equals that chain's up to the
+ * order of the fp32 accumulation. */
 int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W,
                     const uint8_t* mask, int bs, const void* weight, const void* bias,
-                    int C_out, void* y, hipStream_t stream);
+                    int C_out, void* y, void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* The encoder's block convolutions (paper: Method -- the network keeps its
  * blocks through the downsampling stages, so blocks shrink with the map):
@@ -176,7 +187,21 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
                             int ksize, int stride, int flags,
                             const void* residual_hi, const void* residual_lo,
                             void* hi_out, void* lo_out, int hi_cap, int lo_cap,
-                            hipStream_t stream);
+                            void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace sizes (bytes, HOST out-parameter) of segblocks_block_conv3x3,
+ * segblocks_block_conv_ex and segblocks_layer for the given shapes and
+ * stack capacities on the current device; the arguments mean what they mean
+ * in those calls and are validated the same way.  The size assumes 16-byte
+ * aligned buffers (a call with less aligned buffers takes a route that needs
+ * no more).  Pure host functions: nothing is launched. */
+int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
+                                           int bs, int C_out, int hi_cap, int lo_cap, size_t* bytes);
+int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
+                                           int bs, int C_out, int ksize, int stride,
+                                           int hi_cap, int lo_cap, size_t* bytes);
+int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
+                                   int C_out, size_t* bytes);
 
 /* Dense convolution around the block stages (the encoder's 7x7/2 stem):
  * x [N,C_in,H,W] -> y [N,C_out,Ho,Wo], Ho = (H + 2 pad - K) / stride + 1,

@@ -40,7 +40,7 @@ def build(force: bool = False) -> str:
     """Compile the oracle's C source into ``_liboracle.so`` (gcc, no fast-math)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math",
+        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
                                "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
@@ -53,6 +53,8 @@ def _L():
     global _lib
     if _lib is None:
         lib = ctypes.CDLL(build())
+        lib.orc_set_threads.argtypes = [ctypes.c_int]
+        lib.orc_get_threads.restype = ctypes.c_int
         lib.orc_round.restype = ctypes.c_double
         lib.orc_round.argtypes = [ctypes.c_double, ctypes.c_int]
         lib.orc_round_array.argtypes = [_dp, _fp, ctypes.c_long, ctypes.c_int]
@@ -70,6 +72,15 @@ def _L():
         lib.orc_maxpool.argtypes = [_fp] + [ctypes.c_int] * 7 + [_fp]
         _lib = lib
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """Host threads the convolutions use (n <= 0: all that OpenMP offers)."""
+    _L().orc_set_threads(int(n))
+
+
+def threads() -> int:
+    return int(_L().orc_get_threads())
 
 
 def _f32(a):

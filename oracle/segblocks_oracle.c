@@ -23,9 +23,14 @@
  *     (stable compaction); the paper leaves the order open.
  *
  * Build: gcc -O2 -ffp-contract=off (no fast-math) so that the fp32
- * arithmetic below is performed exactly as written.
+ * arithmetic below is performed exactly as written; -fopenmp lets the
+ * convolutions hand whole output planes (one block or image and one output
+ * channel each) to separate host threads.  Each output value is still
+ * accumulated by one thread in the fixed order stated at each function, so
+ * the result does not depend on the thread count.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -33,6 +38,17 @@
 #define ORC_F32 0
 #define ORC_F16 1
 #define ORC_BF16 2
+
+/* Host threads used by the convolutions (n <= 0: OpenMP's default). */
+void orc_set_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+}
+
+int orc_get_threads(void)
+{
+    return omp_get_max_threads();
+}
 
 /* ------------------------------------------------------------------------ */
 /* Rounding to the storage type, from the IEEE-754 definition.               */
@@ -219,6 +235,7 @@ void orc_conv3x3_valid(const float* P, long S, int Cin, int E, const float* w,
                        const float* bias, int Cout, double* out)
 {
     const int pe = E + 2;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
     for (long s = 0; s < S; ++s)
     for (int co = 0; co < Cout; ++co)
     for (int i = 0; i < E; ++i)
@@ -255,6 +272,7 @@ void orc_conv_block(const float* P, long S, int Cin, int E, const float* w, int 
                     const float* bias, int Cout, double* out)
 {
     const int pe = E + 2, Eo = E / st, o = 1 - K / 2;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
     for (long s = 0; s < S; ++s)
     for (int co = 0; co < Cout; ++co)
     for (int i = 0; i < Eo; ++i)
@@ -283,6 +301,7 @@ void orc_conv_dense(const float* x, int N, int Cin, int H, int W, const float* w
                     const float* bias, int Cout, double* out)
 {
     const int Ho = (H + 2 * pad - K) / st + 1, Wo = (W + 2 * pad - K) / st + 1;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
     for (int n = 0; n < N; ++n)
     for (int co = 0; co < Cout; ++co)
     for (int i = 0; i < Ho; ++i)

@@ -18,7 +18,9 @@ import torch
 
 from . import _binding as _b
 
-__all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "layer", "layout_of"]
+__all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "block_conv_ex", "layer", "conv2d",
+           "maxpool", "layout_of", "block_conv3x3_workspace_size", "block_conv_ex_workspace_size",
+           "layer_workspace_size"]
 
 _DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
 
@@ -77,6 +79,48 @@ def _mask(mask: torch.Tensor) -> torch.Tensor:
     if mask.dtype != torch.uint8 or mask.dim() != 3 or not mask.is_contiguous():
         raise ValueError("mask must be a contiguous uint8 tensor [N, GH, GW]")
     return mask
+
+
+def _query(fn: str, *args) -> int:
+    n = ctypes.c_size_t(0)
+    _b.call(fn, *args, ctypes.byref(n))
+    return int(n.value)
+
+
+def block_conv3x3_workspace_size(dtype: torch.dtype, layout: int, N: int, C_in: int, H: int, W: int, bs: int,
+                                 C_out: int, hi_cap: int, lo_cap: int) -> int:
+    """Bytes of workspace that block_conv3x3 needs for these shapes (0 = none)."""
+    return _query("segblocks_block_conv3x3_workspace_size", _DT[dtype], layout, N, C_in, H, W, bs, C_out, hi_cap,
+                  lo_cap)
+
+
+def block_conv_ex_workspace_size(dtype: torch.dtype, N: int, C_in: int, H: int, W: int, bs: int, C_out: int,
+                                 k: int, stride: int, hi_cap: int, lo_cap: int) -> int:
+    """Bytes of workspace that block_conv_ex needs for these shapes (0 = none)."""
+    return _query("segblocks_block_conv_ex_workspace_size", _DT[dtype], _b.SB_NHWC, N, C_in, H, W, bs, C_out, k,
+                  stride, hi_cap, lo_cap)
+
+
+def layer_workspace_size(dtype: torch.dtype, layout: int, N: int, C_in: int, H: int, W: int, bs: int,
+                         C_out: int) -> int:
+    """Bytes of workspace that layer needs for these shapes (0 = none)."""
+    return _query("segblocks_layer_workspace_size", _DT[dtype], layout, N, C_in, H, W, bs, C_out)
+
+
+def _ws(nbytes: int, device, workspace):
+    """(pointer, size) of the workspace of a call: the caller's uint8 tensor, or
+    a new one from torch's allocator.  The pointer is 256-byte aligned."""
+    if nbytes == 0:
+        return None, 0, None
+    if workspace is None:
+        workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    p = workspace.data_ptr()
+    off = (-p) % 256
+    if workspace.numel() - off < nbytes:
+        raise ValueError(f"workspace too small: need {nbytes} bytes (256-byte aligned)")
+    return ctypes.c_void_p(p + off), workspace.numel() - off, workspace
 
 
 def count(mask: torch.Tensor):
@@ -158,9 +202,12 @@ def combine(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: 
 
 
 def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
-                  weight: torch.Tensor, bias=None, relu: bool = False, residual=None, layout=None, out=None):
+                  weight: torch.Tensor, bias=None, relu: bool = False, residual=None, layout=None, out=None,
+                  workspace=None):
     """3x3 block convolution with BlockPad fused into the tile load (packed in,
-    packed out); optional epilogue act(conv + bias + residual)."""
+    packed out); optional epilogue act(conv + bias + residual).  ``workspace``:
+    a uint8 tensor of at least block_conv3x3_workspace_size() + 256 bytes, or
+    None (one is taken from torch's allocator when the call needs one)."""
     mask = _mask(mask)
     ref = hi if hi.shape[0] else lo
     layout = layout_of(ref) if layout is None else layout
@@ -174,14 +221,19 @@ def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
     else:
         ho, lo_o = out
     rh, rl = (None, None) if residual is None else residual
+    need = block_conv3x3_workspace_size(ref.dtype, layout, N, C_in, H, W, bs, C_out, hi.shape[0], lo.shape[0])
+    wp, wn, _keep = _ws(need, ref.device, workspace)
     _b.call("segblocks_block_conv3x3", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
             _ptr(weight), _ptr(bias), C_out, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl), _ptr(ho),
-            _ptr(lo_o), hi.shape[0], lo.shape[0], _stream(ref))
+            _ptr(lo_o), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
     return ho, lo_o
 
 
-def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bias=None, layout=None, out=None):
-    """One fused block-conv layer: combine(conv3x3(pad(split(x)))) in one kernel."""
+def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bias=None, layout=None, out=None,
+          workspace=None):
+    """One block-conv layer: combine(conv3x3(pad(split(x)))), fused (see
+    segblocks_layer for the routes).  ``workspace`` as in block_conv3x3, sized
+    by layer_workspace_size()."""
     mask = _mask(mask)
     layout = layout_of(x) if layout is None else layout
     _check_layout(layout, x)
@@ -190,17 +242,21 @@ def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bi
     weight = _weight(weight, layout)
     bias = None if bias is None else bias.contiguous()
     y = _empty((N, C_out, H, W), x, layout) if out is None else out
+    need = layer_workspace_size(x.dtype, layout, N, C_in, H, W, bs, C_out)
+    wp, wn, _keep = _ws(need, x.device, workspace)
     _b.call("segblocks_layer", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(mask), bs, _ptr(weight), _ptr(bias),
-            C_out, _ptr(y), _stream(x))
+            C_out, _ptr(y), wp, wn, _stream(x))
     return y
 
 
 def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
-                  weight: torch.Tensor, bias=None, stride: int = 1, relu: bool = False, residual=None, out=None):
+                  weight: torch.Tensor, bias=None, stride: int = 1, relu: bool = False, residual=None, out=None,
+                  workspace=None):
     """K x K block convolution (K = weight.shape[2], 1 or 3) at `stride` (1 or
     2) of channels-last packed stacks, BlockPad fused, epilogue
     act(conv + bias + residual); outputs have block sides bs/stride and
-    bs/(2 stride).  H, W, bs describe the input map."""
+    bs/(2 stride).  H, W, bs describe the input map.  ``workspace`` as in
+    block_conv3x3, sized by block_conv_ex_workspace_size()."""
     mask = _mask(mask)
     ref = hi if hi.shape[0] else lo
     layout = _b.SB_NHWC
@@ -216,9 +272,11 @@ def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
     else:
         ho, lo_o = out
     rh, rl = (None, None) if residual is None else residual
+    need = block_conv_ex_workspace_size(ref.dtype, N, C_in, H, W, bs, C_out, k, stride, hi.shape[0], lo.shape[0])
+    wp, wn, _keep = _ws(need, ref.device, workspace)
     _b.call("segblocks_block_conv_ex", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
             _ptr(weight), _ptr(bias), C_out, k, stride, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl),
-            _ptr(ho), _ptr(lo_o), hi.shape[0], lo.shape[0], _stream(ref))
+            _ptr(ho), _ptr(lo_o), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
     return ho, lo_o
 
 

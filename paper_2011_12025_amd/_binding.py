@@ -21,10 +21,15 @@ SB_FLAG_RELU = 1
 
 EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_conv3x3", "segblocks_combine",
            "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
-           "segblocks_maxpool", "segblocks_last_error"]
+           "segblocks_maxpool", "segblocks_block_conv3x3_workspace_size", "segblocks_block_conv_ex_workspace_size",
+           "segblocks_layer_workspace_size", "segblocks_last_error"]
+
+SB_OK, SB_EINVAL, SB_ESHAPE, SB_EHIP, SB_ENOMEM = 0, -1, -2, -3, -4
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
+_Z = ctypes.c_size_t
+_ZP = ctypes.POINTER(ctypes.c_size_t)
 _SIGS = {
     "segblocks_count": [_P, _I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), _P],
     "segblocks_split": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _I, _P],
@@ -32,10 +37,13 @@ _SIGS = {
     "segblocks_conv3x3": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P, _I, _I, _P],
     "segblocks_combine": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P],
     "segblocks_block_conv3x3": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I,
-                                _P],
-    "segblocks_layer": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P],
+                                _P, _Z, _P],
+    "segblocks_layer": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P, _Z, _P],
     "segblocks_block_conv_ex": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P,
-                                _I, _I, _P],
+                                _I, _I, _P, _Z, _P],
+    "segblocks_block_conv3x3_workspace_size": [_I] * 10 + [_ZP],
+    "segblocks_block_conv_ex_workspace_size": [_I] * 12 + [_ZP],
+    "segblocks_layer_workspace_size": [_I] * 8 + [_ZP],
     "segblocks_conv2d": [_P, _I, _I, _I, _I, _I, _I, _P, _P, _I, _I, _I, _I, _I, _P, _P],
     "segblocks_maxpool": [_P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P],
 }

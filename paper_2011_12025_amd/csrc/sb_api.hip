@@ -1,7 +1,9 @@
 // C ABI of libsegblocks.so (declared in include/segblocks.h): host-side
-// argument validation, then one kernel launch on the caller's stream.
-// Nothing here allocates device memory and nothing touches the GPU before
-// every argument has been checked.
+// argument validation, then the kernel launches on the caller's stream.
+// The library allocates no device memory: scratch space of the convolutions
+// comes from the caller's workspace argument, whose size the *_workspace_size
+// queries give; nothing touches the GPU before every argument, the workspace
+// included, has been checked.
 #include <stdarg.h>
 #include <stdio.h>
 
@@ -81,6 +83,15 @@ int check_conv_shape(const char* fn, int C_in, int C_out, int bs, const void* we
     if (C_in <= 0 || C_out <= 0) return fail(SB_EINVAL, fn, "C_in and C_out must be positive");
     if (!weight) return fail(SB_EINVAL, fn, "weight is NULL");
     if (bs > 256) return fail(SB_ESHAPE, fn, "convolution supports block sizes up to 256 (got %d)", bs);
+    return SB_OK;
+}
+
+// A workspace of at least `need` bytes, 256-byte aligned (none needed: anything goes).
+int check_ws(const char* fn, size_t need, const void* ws, size_t ws_bytes) {
+    if (need == 0) return SB_OK;
+    if (!ws || ws_bytes < need)
+        return fail(SB_ENOMEM, fn, "needs a workspace of %zu bytes (got %zu at %p)", need, ws ? ws_bytes : (size_t)0, ws);
+    if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(SB_EINVAL, fn, "workspace must be 256-byte aligned");
     return SB_OK;
 }
 
@@ -176,7 +187,9 @@ int segblocks_conv3x3(const void* hi_pad, const void* lo_pad, int dtype, int lay
     if (any_overlap({rho, rlo}, {rhp, rlp, rw, rb, Range{mask, g.B}}))
         return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
     sb::ConvArgs a{hi_pad, lo_pad, weight, bias, nullptr, nullptr, hi_out, lo_out, C_in, C_out, 0, hi_cap, lo_cap};
-    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PADDED, sb::DST_PACKED, g, mask, a, stream));
+    // padded stacks never take a route with scratch memory
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PADDED, sb::DST_PACKED, g, mask, a, sb::Ws{nullptr, 0},
+                                          stream));
 }
 
 int segblocks_combine(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
@@ -199,7 +212,7 @@ int segblocks_combine(const void* hi, const void* lo, int dtype, int layout, int
 int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
                             const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int flags,
                             const void* residual_hi, const void* residual_lo, void* hi_out, void* lo_out,
-                            int hi_cap, int lo_cap, hipStream_t stream) {
+                            int hi_cap, int lo_cap, void* workspace, size_t ws_bytes, hipStream_t stream) {
     const char* fn = "segblocks_block_conv3x3";
     sb::Geo g;
     int s;
@@ -212,6 +225,9 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
         (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
         (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
         return s;
+    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    const size_t need = sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a);
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype), lb = bs / 2;
     const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
     const Range rw{weight, (long long)C_out * C_in * 9 * es}, rb{bias, bias ? C_out * es : 0};
@@ -220,42 +236,60 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
     // the residual may be read at exactly the output location it feeds (in-place add is not allowed either)
     const Range rrh{residual_hi, hi_cap * (long long)C_out * bs * bs * es};
     const Range rrl{residual_lo, lo_cap * (long long)C_out * lb * lb * es};
-    if (any_overlap({rho, rlo}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
-        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
-    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
-    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, mask, a, stream));
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({rho, rlo, rws}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, mask, a,
+                                          sb::Ws{workspace, ws_bytes}, stream));
 }
 
 int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const uint8_t* mask,
-                    int bs, const void* weight, const void* bias, int C_out, void* y, hipStream_t stream) {
+                    int bs, const void* weight, const void* bias, int C_out, void* y, void* workspace,
+                    size_t ws_bytes, hipStream_t stream) {
     const char* fn = "segblocks_layer";
     sb::Geo g;
     int s;
     if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
     if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
     if (!x || !y) return fail(SB_EINVAL, fn, "x or y is NULL");
+    sb::ConvArgs a{x, nullptr, weight, bias, nullptr, nullptr, y, nullptr, C_in, C_out, 0, 0, 0};
+    const size_t need = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype);
     const Range rx{x, (long long)N * C_in * H * W * es}, ry{y, (long long)N * C_out * H * W * es};
     const Range rw{weight, (long long)C_out * C_in * 9 * es}, rb{bias, bias ? C_out * es : 0};
-    if (any_overlap({ry}, {rx, rw, rb, Range{mask, g.B}})) return fail(SB_EINVAL, fn, "y overlaps an input");
-    sb::ConvArgs a{x, nullptr, weight, bias, nullptr, nullptr, y, nullptr, C_in, C_out, 0, 0, 0};
-    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, mask, a, stream));
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({ry, rws}, {rx, rw, rb, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "y or the workspace overlaps an input, or each other");
+    return hip_status(fn, sb::launch_conv(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, mask, a,
+                                          sb::Ws{workspace, ws_bytes}, stream));
 }
 
-int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
-                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int ksize,
-                            int stride, int flags, const void* residual_hi, const void* residual_lo, void* hi_out,
-                            void* lo_out, int hi_cap, int lo_cap, hipStream_t stream) {
-    const char* fn = "segblocks_block_conv_ex";
-    sb::Geo g;
-    int s;
-    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
-    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+namespace {
+
+// Validation shared by segblocks_block_conv_ex and its workspace query (no pointers).
+int check_conv_ex_shape(const char* fn, int dtype, int layout, int C_in, int bs, int ksize, int stride) {
     if (ksize != 1 && ksize != 3) return fail(SB_EINVAL, fn, "ksize must be 1 or 3 (got %d)", ksize);
     if (stride != 1 && stride != 2) return fail(SB_EINVAL, fn, "stride must be 1 or 2 (got %d)", stride);
     if ((bs / 2) % stride) return fail(SB_ESHAPE, fn, "stride %d does not divide the low block side %d", stride, bs / 2);
     if (layout != SB_NHWC || dtype == SB_F32 || C_in % 8)
         return fail(SB_EINVAL, fn, "supported: channels-last fp16 / bf16 with C_in %% 8 == 0");
+    return SB_OK;
+}
+
+}  // namespace
+
+int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
+                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int ksize,
+                            int stride, int flags, const void* residual_hi, const void* residual_lo, void* hi_out,
+                            void* lo_out, int hi_cap, int lo_cap, void* workspace, size_t ws_bytes,
+                            hipStream_t stream) {
+    const char* fn = "segblocks_block_conv_ex";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if ((s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride))) return s;
     if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
     if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
         return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
@@ -263,6 +297,9 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
         (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
         (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
         return s;
+    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    const size_t need = sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0;
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype), lb = bs / 2, bo = bs / stride, lo_e = lb / stride;
     const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
     const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
@@ -270,11 +307,69 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
     const Range rlo{lo_out, lo_cap * (long long)C_out * lo_e * lo_e * es};
     const Range rrh{residual_hi, hi_cap * (long long)C_out * bo * bo * es};
     const Range rrl{residual_lo, lo_cap * (long long)C_out * lo_e * lo_e * es};
-    if (any_overlap({rho, rlo}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
-        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
-    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
-    if (sb::igemm_fits(dtype, layout, g, a)) return hip_status(fn, sb::launch_igemm(dtype, g, mask, a, ksize, stride, stream));
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({rho, rlo, rws}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    if (sb::igemm_fits(dtype, layout, g, a))
+        return hip_status(fn, sb::launch_igemm(dtype, g, mask, a, ksize, stride, sb::Ws{workspace, ws_bytes}, stream));
     return hip_status(fn, sb::launch_bconv(dtype, g, mask, a, ksize, stride, stream));
+}
+
+namespace {
+
+// Geometry of a workspace query: the checks of check_geo without a mask.
+int check_query(const char* fn, int dtype, int layout, int N, int C_in, int H, int W, int bs, int C_out,
+                size_t* bytes, sb::Geo& g) {
+    static const uint8_t any = 0;
+    if (!bytes) return fail(SB_EINVAL, fn, "bytes is NULL");
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, &any, bs, g))) return s;
+    if (C_out <= 0) return fail(SB_EINVAL, fn, "C_out must be positive");
+    if (bs > 256) return fail(SB_ESHAPE, fn, "convolution supports block sizes up to 256 (got %d)", bs);
+    return SB_OK;
+}
+
+}  // namespace
+
+int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs, int C_out,
+                                           int hi_cap, int lo_cap, size_t* bytes) {
+    const char* fn = "segblocks_block_conv3x3_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
+        return s;
+    sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, hi_cap,
+                   lo_cap};
+    *bytes = sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a);
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs, int C_out,
+                                           int ksize, int stride, int hi_cap, int lo_cap, size_t* bytes) {
+    const char* fn = "segblocks_block_conv_ex_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) ||
+        (s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride)) || (s = check_caps(fn, hi_cap, lo_cap)))
+        return s;
+    sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, hi_cap,
+                   lo_cap};
+    *bytes = sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0;
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs, int C_out,
+                                   size_t* bytes) {
+    const char* fn = "segblocks_layer_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g))) return s;
+    sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, 0, 0};
+    *bytes = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
+    g_err.clear();
+    return SB_OK;
 }
 
 int segblocks_conv2d(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const void* weight,

@@ -442,14 +442,8 @@ hipError_t run_conv(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStr
     const int ob = 4 * (int)sizeof(T);  // one epilogue vector: 4 channels
     const int vec_out = (a.C_out % 4 == 0) && aligned(a.out_hi, ob) && aligned(a.out_lo, ob) &&
                         aligned(a.res_hi, ob) && aligned(a.res_lo, ob);
-    // raise the kernel's dynamic-LDS limit to what this launch needs (kept per instantiation)
-    static int attr_bytes = 0;
-    if (smem > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_conv<T, L, SRC, DST, VEC>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-        if (e != hipSuccess) return e;
-        attr_bytes = smem;
-    }
+    hipError_t e = ensure_dyn_lds((const void*)k_conv<T, L, SRC, DST, VEC>, smem);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(g.B * G), (unsigned)((a.C_out + NT - 1) / NT));
     hipLaunchKernelGGL((k_conv<T, L, SRC, DST, VEC>), grid, dim3(WG), smem, st, g, mask, a, Rh, Rl, G, w_off,
                        vec_out);
@@ -479,49 +473,86 @@ hipError_t conv_t(int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint
 
 }  // namespace
 
-// A fused layer (dense map in and out) with many channels as split, the
+// A fused layer (dense map in and out) with many channels runs as split, the
 // GEMM's block convolution (BlockPad fused) and combine over packed stacks
-// in library workspace, with room for every block in either class (the
+// in the caller's workspace, with room for every block in either class (the
 // counts are only known on the device).  The values equal the one-kernel
 // layer's up to the order of the fp32 accumulation.
-hipError_t layer_via_packed(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
-    const size_t es = 2, cap = (size_t)g.B, lb = (size_t)g.bs / 2;
-    const size_t hi_in = cap * g.bs * g.bs * a.C_in * es, lo_in = cap * lb * lb * a.C_in * es;
-    const size_t hi_out = cap * g.bs * g.bs * a.C_out * es, lo_out = cap * lb * lb * a.C_out * es;
-    void* ws = nullptr;
-    hipError_t e = lib_workspace(1, hi_in + lo_in + hi_out + lo_out, st, &ws);
-    if (e != hipSuccess) return e;
-    char* base = (char*)ws;
-    void *hi = base, *lo = base + hi_in, *ho = base + hi_in + lo_in, *lo_o = base + hi_in + lo_in + hi_out;
-    Geo gi = g, go = g;
-    gi.C = a.C_in;
-    go.C = a.C_out;
-    if ((e = launch_split_rows(dtype, gi, a.in_hi, mask, hi, (int)cap, lo, (int)cap, st)) != hipSuccess) return e;
-    const ConvArgs p{hi, lo, a.weight, a.bias, nullptr, nullptr, ho, lo_o, a.C_in, a.C_out, a.flags, (int)cap, (int)cap};
-    if ((e = launch_igemm(dtype, g, mask, p, 3, 1, st)) != hipSuccess) return e;
-    return launch_combine_rows(dtype, go, ho, lo_o, mask, (int)cap, (int)cap, a.out_hi, st);
-}
+namespace {
 
-hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
-                       const ConvArgs& a, hipStream_t st) {
-    if (conv_res_fits(dtype, layout, g, a)) return launch_conv_res(dtype, src, dst, g, mask, a, st);
-    if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits(dtype, layout, g, a))
-        return launch_igemm(dtype, g, mask, a, 3, 1, st);
+inline size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+
+bool layer_packed_route(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     // Measured on the stage shapes of a 1024x2048 image (8x16 blocks): at 128
     // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us;
     // at 256 the general kernel is faster (40-44 against 46-69 us) and stays.
-    if (src == SRC_DENSE && dst == DST_DENSE && ((a.C_in > 64 && a.C_in <= 128) || a.C_in > 256) && layout == NHWC &&
-        (dtype == 1 || dtype == 2)) {
-        const ConvArgs p{a.in_hi, a.in_hi, a.weight, a.bias, nullptr, nullptr, a.out_hi, a.out_hi,
-                         a.C_in, a.C_out, a.flags, (int)g.B, (int)g.B};
-        Geo gi = g;
-        gi.C = a.C_in;
-        Geo go = g;
-        go.C = a.C_out;
-        if (igemm_fits(dtype, layout, g, p) && rows_fit(dtype, layout, gi, {a.in_hi}) &&
-            rows_fit(dtype, layout, go, {a.out_hi}))
-            return layer_via_packed(dtype, g, mask, a, st);
-    }
+    if (!((a.C_in > 64 && a.C_in <= 128) || a.C_in > 256) || layout != NHWC || (dtype != 1 && dtype != 2))
+        return false;
+    Geo gi = g, go = g;
+    gi.C = a.C_in;
+    go.C = a.C_out;
+    ConvArgs p = a;
+    p.hi_cap = p.lo_cap = (int)g.B;
+    return igemm_fits_shape(dtype, layout, g, p) && rows_fit(dtype, layout, gi, {}) && rows_fit(dtype, layout, go, {});
+}
+
+// the packed stacks of the route: [hi in][lo in][hi out][lo out][GEMM workspace]
+struct PackedLayout {
+    size_t hi_in, lo_in, hi_out, lo_out, gemm, total;
+};
+
+PackedLayout packed_layout(const Geo& g, const ConvArgs& a) {
+    const size_t es = 2, cap = (size_t)g.B, lb = (size_t)g.bs / 2;
+    PackedLayout L;
+    L.hi_in = round256(cap * g.bs * g.bs * a.C_in * es);
+    L.lo_in = round256(cap * lb * lb * a.C_in * es);
+    L.hi_out = round256(cap * g.bs * g.bs * a.C_out * es);
+    L.lo_out = round256(cap * lb * lb * a.C_out * es);
+    ConvArgs p = a;
+    p.hi_cap = p.lo_cap = (int)cap;
+    L.gemm = igemm_ws_bytes(g, p, 3, 1);
+    L.total = L.hi_in + L.lo_in + L.hi_out + L.lo_out + L.gemm;
+    return L;
+}
+
+hipError_t layer_via_packed(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
+    const PackedLayout L = packed_layout(g, a);
+    if (ws.bytes < L.total || !ws.p) return hipErrorInvalidValue;
+    const int cap = (int)g.B;
+    char* base = (char*)ws.p;
+    void *hi = base, *lo = base + L.hi_in, *ho = base + L.hi_in + L.lo_in;
+    void* lo_o = base + L.hi_in + L.lo_in + L.hi_out;
+    const Ws gws{base + L.hi_in + L.lo_in + L.hi_out + L.lo_out, L.gemm};
+    Geo gi = g, go = g;
+    gi.C = a.C_in;
+    go.C = a.C_out;
+    hipError_t e = launch_split_rows(dtype, gi, a.in_hi, mask, hi, cap, lo, cap, st);
+    if (e != hipSuccess) return e;
+    const ConvArgs p{hi, lo, a.weight, a.bias, nullptr, nullptr, ho, lo_o, a.C_in, a.C_out, a.flags, cap, cap};
+    if ((e = launch_igemm(dtype, g, mask, p, 3, 1, gws, st)) != hipSuccess) return e;
+    return launch_combine_rows(dtype, go, ho, lo_o, mask, cap, cap, a.out_hi, st);
+}
+
+}  // namespace
+
+size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const ConvArgs& a) {
+    if (conv_res_fits_shape(dtype, layout, g, a)) return 0;
+    if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits_shape(dtype, layout, g, a))
+        return igemm_ws_bytes(g, a, 3, 1);
+    if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a))
+        return packed_layout(g, a).total;
+    return 0;
+}
+
+hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
+                       const ConvArgs& a, Ws ws, hipStream_t st) {
+    if (conv_res_fits(dtype, layout, g, a)) return launch_conv_res(dtype, src, dst, g, mask, a, st);
+    if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits(dtype, layout, g, a))
+        return launch_igemm(dtype, g, mask, a, 3, 1, ws, st);
+    if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a) &&
+        reinterpret_cast<uintptr_t>(a.in_hi) % 16 == 0 && reinterpret_cast<uintptr_t>(a.out_hi) % 16 == 0 &&
+        reinterpret_cast<uintptr_t>(a.weight) % 16 == 0)
+        return layer_via_packed(dtype, g, mask, a, ws, st);
     switch (dtype) {
     case 0: return conv_t<float>(layout, src, dst, g, mask, a, st);
     case 1: return conv_t<f16>(layout, src, dst, g, mask, a, st);

@@ -716,17 +716,6 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     }
 }
 
-int cu_count() {
-    static int n = 0;
-    if (n == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            n = 256;
-    }
-    return n;
-}
-
 inline bool aligned_to(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; }
 
 // Image rows per high tile (a low tile has half as many): 8 for blocks of
@@ -749,14 +738,10 @@ hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, 
     const int ob = 16;
     const int vec_out = (a.C_out % 8 == 0) && aligned_to(a.out_hi, ob) && aligned_to(a.out_lo, ob) &&
                         aligned_to(a.res_hi, ob) && aligned_to(a.res_lo, ob);
-    static int attr_bytes = 0;
-    if (smem > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_conv_res<T, SRC, DST, ONE, NKS>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-        if (e != hipSuccess) return e;
-        attr_bytes = smem;
-    }
-    const int nwg = (int)(ntiles < cu_count() ? ntiles : cu_count());
+    hipError_t e = ensure_dyn_lds((const void*)k_conv_res<T, SRC, DST, ONE, NKS>, smem);
+    if (e != hipSuccess) return e;
+    const int cus = device_cus();
+    const int nwg = (int)(ntiles < cus ? ntiles : cus);
     const dim3 grid((unsigned)nwg, (unsigned)((a.C_out + RNT - 1) / RNT));
     hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, G, (int)ntiles,
                        buf_bytes, vec_out);
@@ -781,9 +766,13 @@ hipError_t res_t(ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask, co
 }  // namespace
 
 bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
+    if (!aligned_to(a.in_hi, 16) || !aligned_to(a.in_lo, 16) || !aligned_to(a.weight, 16)) return false;
+    return conv_res_fits_shape(dtype, layout, g, a);
+}
+
+bool conv_res_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
     if (a.C_in % 8 || a.C_in > 64 || res_rows(g.bs) == 0) return false;
-    if (!aligned_to(a.in_hi, 16) || !aligned_to(a.in_lo, 16) || !aligned_to(a.weight, 16)) return false;
     // element offsets inside one image or one stack are 32-bit
     const long long img = (long long)g.H * g.W * (a.C_in > a.C_out ? a.C_in : a.C_out);
     const long long cap = (a.hi_cap > a.lo_cap ? a.hi_cap : a.lo_cap) + 1LL;

@@ -546,12 +546,8 @@ hipError_t stem_t(const void* x, int N, int C_in, int H, int W, const void* w, c
                   int S, int P, int flags, void* y, int Ho, int Wo, hipStream_t st) {
     const int TY = (Ho + ST_TH - 1) / ST_TH, TX = (Wo + ST_TW - 1) / ST_TW;
     const int smem = stem_lds_bytes(K, S);
-    static int set = 0;
-    if (smem > set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_stem<T>, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-        if (e != hipSuccess) return e;
-        set = smem;
-    }
+    hipError_t e = ensure_dyn_lds((const void*)k_stem<T>, smem);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(N * TY * TX), (unsigned)((C_out + 63) / 64));
     hipLaunchKernelGGL(k_stem<T>, grid, dim3(ST_WG), smem, st, (const T*)x, C_in, H, W, (const T*)w, (const T*)bias,
                        C_out, K, S, P, flags, (T*)y, Ho, Wo, TY, TX);
@@ -578,21 +574,13 @@ hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W
     const int smem = conv2d_lds_bytes(dtype, C_in, K, S);
     const dim3 grid((unsigned)(N * TY * TX), (unsigned)((C_out + 63) / 64));
     if (dtype == 1) {
-        static int set = 0;
-        if (smem > set) {
-            hipError_t e = hipFuncSetAttribute((const void*)k_conv2d<f16>, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-            if (e != hipSuccess) return e;
-            set = smem;
-        }
+        hipError_t e = ensure_dyn_lds((const void*)k_conv2d<f16>, smem);
+        if (e != hipSuccess) return e;
         hipLaunchKernelGGL(k_conv2d<f16>, grid, dim3(WG), smem, st, (const f16*)x, C_in, H, W, (const f16*)w,
                            (const f16*)bias, C_out, K, S, P, flags, (f16*)y, Ho, Wo, TY, TX, KP);
     } else {
-        static int set = 0;
-        if (smem > set) {
-            hipError_t e = hipFuncSetAttribute((const void*)k_conv2d<bf16>, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-            if (e != hipSuccess) return e;
-            set = smem;
-        }
+        hipError_t e = ensure_dyn_lds((const void*)k_conv2d<bf16>, smem);
+        if (e != hipSuccess) return e;
         hipLaunchKernelGGL(k_conv2d<bf16>, grid, dim3(WG), smem, st, (const bf16*)x, C_in, H, W, (const bf16*)w,
                            (const bf16*)bias, C_out, K, S, P, flags, (bf16*)y, Ho, Wo, TY, TX, KP);
     }

@@ -38,7 +38,6 @@
 // 16 x MS pixel and 16 x NS channel fragments.  The weight rows of each 32-channel group
 // are permuted in LDS so that a lane ends with 8 consecutive output channels
 // of one pixel and stores them as one 16-byte write.
-#include <mutex>
 #include <type_traits>
 
 #include "sb_common.h"
@@ -590,49 +589,8 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
 
 }  // namespace
 
-// Workspaces per device (pool 0: the GEMM's split partials and padded low
-// stack; pool 1: the packed stacks of a fused layer routed through the GEMM),
-// grown on demand (never while the stream is being captured into a graph).
-// A buffer that is outgrown is not freed, since a graph captured earlier may
-// still use it: every buffer lives until the process ends (at most twice the
-// largest request in total).  Calls that run concurrently on one device
-// share the workspaces and must be ordered by the caller.
-struct GPool {
-    void* p = nullptr;
-    size_t bytes = 0;
-};
-static GPool g_pool[2][64];
-static std::mutex g_pool_mu;
-
-hipError_t lib_workspace(int pool, size_t bytes, hipStream_t st, void** out) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64 || pool < 0 || pool > 1) return hipErrorInvalidValue;
-    std::lock_guard<std::mutex> lk(g_pool_mu);
-    GPool& P = g_pool[pool][dev];
-    if (P.bytes < bytes) {
-        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-        e = hipStreamIsCapturing(st, &cs);
-        if (e != hipSuccess) return e;
-        if (cs != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
-        size_t nb = 16u << 20;
-        while (nb < bytes) nb <<= 1;
-        void* p = nullptr;
-        e = hipMalloc(&p, nb);
-        if (e != hipSuccess) return e;
-        P.p = p;
-        P.bytes = nb;
-    }
-    *out = P.p;
-    return hipSuccess;
-}
-
 namespace {
 
-hipError_t gworkspace(size_t bytes, hipStream_t st, void** out) { return lib_workspace(0, bytes, st, out); }
-
-int g_cus = 0;
 // Launch cost model, in K steps (about 1 us each): a workgroup's start-up
 // (mask plan, descriptors, first stages), and the partial-sum pass, which
 // reads every split's partial tiles.
@@ -640,51 +598,44 @@ constexpr int GSTART_COST = 5;
 constexpr int GSPLIT_COST = 10;  // plus one per split
 
 inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+inline size_t ground256(size_t b) { return (b + 255) / 256 * 256; }
 
 template <int TM, int TN, int KT>
 constexpr int igemm_smem_fixed() {
     return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4 + GWAVES * (TM / (8 * GWAVES)) * 3 * 1024;
 }
 
-template <typename T, int KS, int ST, int WM, int MS, int NS>
-hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
-    constexpr int TM = WM * MS * 16, TN = (GWAVES / WM) * NS * 16;
-    const int eo_h = g.bs / ST, eo_l = (g.bs / 2) / ST;
-    GParams gp;
-    gp.eo_h = eo_h;
-    gp.eo_l = eo_l;
-    gp.cpt = a.C_in / GKC;
-    gp.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + TM - 1) / TM);
-    const int tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + TM - 1) / TM);
-    const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
-    static int attr = 0;
-    if (smem > attr) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_igemm<T, KS, ST, WM, MS, NS>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-        if (e != hipSuccess) return e;
-        attr = smem;
-    }
-    const int tiles = gp.tiles_h + tiles_l;
-    if (tiles == 0) return hipSuccess;
-    const int tiles_n = (a.C_out + TN - 1) / TN;
+// Everything about a launch that the host decides from the shapes alone:
+// tile counts (from the stack capacities), the K split, the padded low stack,
+// and the caller's workspace that they take.
+struct IgPlan {
+    int TM, TN, tiles_h, tiles_l, tiles_n, splits;
+    bool pad_low;
+    size_t part_bytes, pad_bytes;
+};
+
+IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
+    IgPlan p;
+    p.TM = 128;
+    p.TN = a.C_out <= 64 ? 64 : 128;
+    const int eo_h = g.bs / stride, eo_l = (g.bs / 2) / stride;
+    p.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + p.TM - 1) / p.TM);
+    p.tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + p.TM - 1) / p.TM);
+    p.tiles_n = (a.C_out + p.TN - 1) / p.TN;
+    const int tiles = p.tiles_h + p.tiles_l;
     // Split K: one workgroup per CU at a time (LDS), each taking about the
     // same time per K step, so a launch costs about rounds x (steps per split
     // + start-up); a split costs the partial-sum pass on top, which grows with
     // the number of splits.  Take the cheapest split that keeps at least four
     // steps per workgroup.
-    if (g_cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&g_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || g_cus <= 0)
-            g_cus = 256;
-    }
-    const int nsteps = KS * KS * gp.cpt;
+    const int cus = device_cus();
+    const int nsteps = ks * ks * (a.C_in / GKC);
     int S = 1;
     {
-        const long long wgs = (long long)tiles * tiles_n;
+        const long long wgs = (long long)tiles * p.tiles_n;
         long long best = 0;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
-            const long long rounds = (wgs * c + g_cus - 1) / g_cus;
+            const long long rounds = (wgs * c + cus - 1) / cus;
             const long long cost = rounds * ((nsteps + c - 1) / c + GSTART_COST) + (c > 1 ? GSPLIT_COST + c : 0);
             if (c == 1 || cost < best) {
                 best = cost;
@@ -692,10 +643,7 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
             }
         }
     }
-    gp.splits = S;
-    gp.part = nullptr;
-    gp.rows = nullptr;
-    gp.lo_pad = nullptr;
+    p.splits = tiles > 0 ? S : 1;
     // A low block's halo pixels across a resolution boundary are 2x2 averages
     // of the high neighbour: four loads per element in the K loop, which make
     // the low tiles the last to finish.  A 3 x 3 convolution with both classes
@@ -703,31 +651,53 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
     // every low-tile source is a plain copy.  Measured, the extra pass pays at
     // 128 input channels (about 5 us less at 25-75 % low blocks) and costs 1-4 us
     // at 64, 256 and 512, so it is taken there only.
-    const bool pad_low = KS == 3 && tiles_l > 0 && a.hi_cap > 0 && a.C_in > 64 && a.C_in <= 128;
-    const size_t part_bytes = S > 1 ? ((size_t)tiles * tiles_n * S * TM * TN * 4 + (size_t)tiles * 4 + 255) / 256 * 256 : 0;
-    const size_t pad_bytes = pad_low ? (size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * sizeof(T) : 0;
-    if (part_bytes + pad_bytes > 0) {
-        void* ws = nullptr;
-        hipError_t e = gworkspace(part_bytes + pad_bytes, st, &ws);
+    p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && a.C_in > 64 && a.C_in <= 128;
+    p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 4)
+                                : 0;
+    p.pad_bytes = p.pad_low ? ground256((size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * 2) : 0;
+    return p;
+}
+
+template <typename T, int KS, int ST, int WM, int MS, int NS>
+hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
+    constexpr int TM = WM * MS * 16, TN = (GWAVES / WM) * NS * 16;
+    const IgPlan pl = igemm_plan(g, a, KS, ST);
+    if (pl.TM != TM || pl.TN != TN) return hipErrorInvalidValue;
+    const int tiles = pl.tiles_h + pl.tiles_l;
+    if (tiles == 0) return hipSuccess;
+    if (ws.bytes < pl.part_bytes + pl.pad_bytes || (pl.part_bytes + pl.pad_bytes > 0 && !ws.p))
+        return hipErrorInvalidValue;  // the entry points check the workspace before anything is launched
+    GParams gp;
+    gp.eo_h = g.bs / ST;
+    gp.eo_l = (g.bs / 2) / ST;
+    gp.cpt = a.C_in / GKC;
+    gp.tiles_h = pl.tiles_h;
+    const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
+    hipError_t e = ensure_dyn_lds((const void*)k_igemm<T, KS, ST, WM, MS, NS>, smem);
+    if (e != hipSuccess) return e;
+    const int tiles_n = pl.tiles_n;
+    const int S = pl.splits;
+    gp.splits = S;
+    gp.part = nullptr;
+    gp.rows = nullptr;
+    gp.lo_pad = nullptr;
+    if (S > 1) {
+        gp.part = (float*)ws.p;
+        gp.rows = (int*)((char*)ws.p + (size_t)tiles * tiles_n * S * TM * TN * 4);
+    }
+    if (pl.pad_low) {
+        void* lp = (char*)ws.p + pl.part_bytes;
+        Geo pg = g;
+        pg.C = a.C_in;
+        e = launch_pad_rows(std::is_same<T, f16>::value ? 1 : 2, pg, a.in_hi, a.in_lo, mask, nullptr, lp, a.hi_cap,
+                            a.lo_cap, st);
         if (e != hipSuccess) return e;
-        if (S > 1) {
-            gp.part = (float*)ws;
-            gp.rows = (int*)((char*)ws + (size_t)tiles * tiles_n * S * TM * TN * 4);
-        }
-        if (pad_low) {
-            void* lp = (char*)ws + part_bytes;
-            Geo pg = g;
-            pg.C = a.C_in;
-            e = launch_pad_rows(std::is_same<T, f16>::value ? 1 : 2, pg, a.in_hi, a.in_lo, mask,
-                                nullptr, lp, a.hi_cap, a.lo_cap, st);
-            if (e != hipSuccess) return e;
-            gp.lo_pad = lp;
-        }
+        gp.lo_pad = lp;
     }
     const dim3 grid((unsigned)tiles, (unsigned)tiles_n, (unsigned)S);
     hipLaunchKernelGGL((k_igemm<T, KS, ST, WM, MS, NS>), grid, dim3(GWG), smem, st, g, mask, a, gp);
     if (S > 1) {
-        hipError_t e = hipGetLastError();
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
         const long long threads = (long long)tiles * tiles_n * GWAVES * MS * (NS / 2) * 64;
         hipLaunchKernelGGL((k_igemm_reduce<T, WM, MS, NS>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, a,
@@ -737,25 +707,24 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipSt
 }
 
 template <typename T, int KS, int ST>
-hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, hipStream_t st) {
-    if (a.C_out <= 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, st);
-    return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, st);
+hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
+    if (a.C_out <= 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st);
+    return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, ws, st);
 }
 
 template <typename T>
-hipError_t igemm_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ks, int stride, hipStream_t st) {
-    if (ks == 3) return stride == 1 ? igemm_tile<T, 3, 1>(g, mask, a, st) : igemm_tile<T, 3, 2>(g, mask, a, st);
-    return stride == 1 ? igemm_tile<T, 1, 1>(g, mask, a, st) : igemm_tile<T, 1, 2>(g, mask, a, st);
+hipError_t igemm_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ks, int stride, Ws ws,
+                   hipStream_t st) {
+    if (ks == 3)
+        return stride == 1 ? igemm_tile<T, 3, 1>(g, mask, a, ws, st) : igemm_tile<T, 3, 2>(g, mask, a, ws, st);
+    return stride == 1 ? igemm_tile<T, 1, 1>(g, mask, a, ws, st) : igemm_tile<T, 1, 2>(g, mask, a, ws, st);
 }
 
 }  // namespace
 
-bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
+bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
     if (a.C_in % GKC || a.C_in > GMAXC || a.C_out % 8 || g.B > GMAXB) return false;
-    if (!galigned(a.in_hi) || !galigned(a.in_lo) || !galigned(a.weight) || !galigned(a.out_hi) ||
-        !galigned(a.out_lo) || !galigned(a.res_hi) || !galigned(a.res_lo))
-        return false;
     // pixel indices of the stacks fit the 30 bits of a descriptor
     const long long lb = g.bs / 2;
     if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * (lb + 2) * (lb + 2) >= (1LL << 30))
@@ -764,10 +733,22 @@ bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     return smem + GWAVES * 4 <= 160 * 1024;
 }
 
-hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
+bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
+    if (!galigned(a.in_hi) || !galigned(a.in_lo) || !galigned(a.weight) || !galigned(a.out_hi) ||
+        !galigned(a.out_lo) || !galigned(a.res_hi) || !galigned(a.res_lo))
+        return false;
+    return igemm_fits_shape(dtype, layout, g, a);
+}
+
+size_t igemm_ws_bytes(const Geo& g, const ConvArgs& a, int ksize, int stride) {
+    const IgPlan p = igemm_plan(g, a, ksize, stride);
+    return p.part_bytes + p.pad_bytes;
+}
+
+hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride, Ws ws,
                         hipStream_t st) {
-    if (dtype == 1) return igemm_t<f16>(g, mask, a, ksize, stride, st);
-    return igemm_t<bf16>(g, mask, a, ksize, stride, st);
+    if (dtype == 1) return igemm_t<f16>(g, mask, a, ksize, stride, ws, st);
+    return igemm_t<bf16>(g, mask, a, ksize, stride, ws, st);
 }
 
 }  // namespace sb

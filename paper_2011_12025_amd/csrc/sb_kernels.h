@@ -8,6 +8,11 @@
 
 namespace sb {
 
+// Launch-setup state kept per device (sb_host.hip): the number of compute
+// units, and the dynamic-LDS limit of a kernel raised to at least `bytes`.
+int device_cus();
+hipError_t ensure_dyn_lds(const void* kernel, int bytes);
+
 // Geometry of one call: logical N, C, H, W; block size; block grid.
 struct Geo {
     int N, C, H, W, bs, GH, GW;
@@ -35,9 +40,20 @@ hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const
                       const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, hipStream_t st);
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
                           const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st);
+// Device memory that a launch needs beyond its inputs and outputs, supplied
+// by the caller (at least the bytes that the matching *_ws_bytes function
+// returns for the same shapes, 256-byte aligned).
+struct Ws {
+    void* p;
+    size_t bytes;
+};
+
 // g.C is ignored by the convolution launcher (C_in / C_out are in ConvArgs).
 hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g,
-                       const uint8_t* mask, const ConvArgs& a, hipStream_t st);
+                       const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st);
+// Workspace of launch_conv for these shapes and capacities, assuming every
+// buffer is 16-byte aligned (a call with less aligned buffers needs no more).
+size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const ConvArgs& a);
 
 // Row-job split / pad / combine for channels-last tensors of whole 16-byte
 // pixels with 16-byte aligned buffers; rows_fit tells whether they apply.
@@ -54,13 +70,13 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
 // (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
 // max-pooling (any dtype).  conv2d_lds_bytes: LDS of one dense-conv workgroup.
 // multi-block implicit GEMM on packed channels-last stacks (fp16 / bf16,
-// C_in % 64 == 0, C_out % 8 == 0, at most 8192 blocks), BlockPad fused
+// C_in % 64 == 0, C_out % 8 == 0, at most 8192 blocks), BlockPad fused;
+// igemm_fits_shape leaves out the pointer alignment that igemm_fits checks.
+bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a);
 bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
-// Library-owned device memory: pool 0 belongs to the GEMM (split partials,
-// padded low stack), pool 1 to a fused layer routed through the GEMM.
-hipError_t lib_workspace(int pool, size_t bytes, hipStream_t st, void** out);
+size_t igemm_ws_bytes(const Geo& g, const ConvArgs& a, int ksize, int stride);
 hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
-                        hipStream_t st);
+                        Ws ws, hipStream_t st);
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         hipStream_t st);
 int conv2d_lds_bytes(int dtype, int C_in, int K, int S);
@@ -71,7 +87,9 @@ hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, 
                           hipStream_t st);
 
 // Persistent convolution with LDS-resident weights (channels-last fp16/bf16,
-// C_in <= 64, 16 <= bs <= 64); conv_res_fits tells whether it applies.
+// C_in <= 64, blocks of 32 or 64); conv_res_fits tells whether it applies,
+// conv_res_fits_shape the same without the pointer alignment.
+bool conv_res_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a);
 bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
 hipError_t launch_conv_res(int dtype, ConvSrc src, ConvDst dst, const Geo& g, const uint8_t* mask,
                            const ConvArgs& a, hipStream_t st);

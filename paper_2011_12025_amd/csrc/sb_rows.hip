@@ -399,14 +399,7 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
 }
 
 int rows_grid(long long waves) {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-            cus = 256;
-    }
-    const long long cap = (long long)cus * 8;  // workgroups: up to 32 waves per CU
+    const long long cap = (long long)device_cus() * 8;  // workgroups: up to 32 waves per CU
     const long long wgs = (waves + RW_WAVES - 1) / RW_WAVES;
     return (int)(wgs < cap ? wgs : cap);
 }

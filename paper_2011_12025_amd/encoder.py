@@ -12,7 +12,9 @@ from __future__ import annotations
 
 import torch
 
-from . import block_conv3x3, block_conv_ex, combine, conv2d, count, maxpool, split
+from . import (block_conv3x3, block_conv3x3_workspace_size, block_conv_ex, block_conv_ex_workspace_size, combine,
+               conv2d, count, maxpool, split)
+from ._binding import SB_NHWC
 
 WIDTHS = (64, 128, 256, 512)
 STRIDES = (1, 2, 2, 2)
@@ -34,26 +36,50 @@ class BlockEncoder:
         h = conv2d(x, self.w["stem.w"], self.w["stem.b"], stride=2, padding=3, relu=True)
         return maxpool(h, 3, 2, 1)
 
+    def workspace_bytes(self, N: int, H: int, W: int, dtype: torch.dtype, counts) -> int:
+        """Largest workspace any stage convolution needs for an N x 64 x H x W
+        stage-1 map with block counts (n_high, n_low); the convolutions run
+        one after the other on one stream, so they share one buffer."""
+        nh, nl = counts
+        bs, need = self.image_block // 4, 0
+        cin = WIDTHS[0]
+        for si, (width, stride) in enumerate(zip(WIDTHS, STRIDES)):
+            for bi in range(2):
+                st = stride if bi == 0 else 1
+                if st == 1:
+                    need = max(need, block_conv3x3_workspace_size(dtype, SB_NHWC, N, cin, H, W, bs, width, nh, nl))
+                else:
+                    need = max(need, block_conv_ex_workspace_size(dtype, N, cin, H, W, bs, width, 3, st, nh, nl))
+                if st != 1 or cin != width:
+                    need = max(need, block_conv_ex_workspace_size(dtype, N, cin, H, W, bs, width, 1, st, nh, nl))
+                bs, H, W = bs // st, H // st, W // st
+                need = max(need, block_conv3x3_workspace_size(dtype, SB_NHWC, N, width, H, W, bs, width, nh, nl))
+                cin = width
+        return need
+
     def stages(self, h: torch.Tensor, mask: torch.Tensor, counts=None) -> torch.Tensor:
         N, C, H, W = h.shape
         bs = self.image_block // 4
         hi, lo = split(h, mask, bs, counts=counts)
+        nbytes = self.workspace_bytes(N, H, W, h.dtype, (hi.shape[0], lo.shape[0]))
+        ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=h.device) if nbytes else None
         for si, (width, stride) in enumerate(zip(WIDTHS, STRIDES)):
             for bi in range(2):
                 st = stride if bi == 0 else 1
                 p = f"s{si + 1}.b{bi}."
                 w1, b1 = self.w[p + "c1.w"], self.w[p + "c1.b"]
                 if st == 1:
-                    h1 = block_conv3x3(hi, lo, mask, bs, H, W, w1, b1, relu=True)
+                    h1 = block_conv3x3(hi, lo, mask, bs, H, W, w1, b1, relu=True, workspace=ws)
                 else:
-                    h1 = block_conv_ex(hi, lo, mask, bs, H, W, w1, b1, stride=st, relu=True)
+                    h1 = block_conv_ex(hi, lo, mask, bs, H, W, w1, b1, stride=st, relu=True, workspace=ws)
                 if p + "sc.w" in self.w:
-                    sc = block_conv_ex(hi, lo, mask, bs, H, W, self.w[p + "sc.w"], self.w[p + "sc.b"], stride=st)
+                    sc = block_conv_ex(hi, lo, mask, bs, H, W, self.w[p + "sc.w"], self.w[p + "sc.b"], stride=st,
+                                       workspace=ws)
                 else:
                     sc = (hi, lo)
                 bs, H, W = bs // st, H // st, W // st
                 hi, lo = block_conv3x3(h1[0], h1[1], mask, bs, H, W, self.w[p + "c2.w"], self.w[p + "c2.b"],
-                                       relu=True, residual=sc)
+                                       relu=True, residual=sc, workspace=ws)
         return combine(hi, lo, mask, bs, H, W)
 
     def __call__(self, x: torch.Tensor, mask: torch.Tensor, counts=None) -> torch.Tensor:
@@ -68,13 +94,9 @@ class BlockEncoder:
         """Records one forward into a HIP graph, so that a replay costs one
         host call instead of one per kernel.  x and mask stay the graph's
         inputs (write new values into them before a replay; the block counts
-        are fixed at capture).  Returns (graph, output tensor)."""
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            self(x, mask, counts)          # first launches set kernel attributes outside the capture
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
+        are fixed at capture).  Nothing needs to run before the capture: the
+        library allocates nothing, and the workspace and every intermediate
+        come from torch's graph memory pool.  Returns (graph, output tensor)."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             y = self(x, mask, counts)

@@ -85,15 +85,17 @@ def test_conv_and_layer_validation(lib):
                               ctypes.c_void_p(0x78000000), 1, 0, None)
     assert r == -2 and "256" in lib.segblocks_last_error().decode()
     # missing weight
-    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, NULL, NULL, 8, ctypes.c_void_p(0x50000000), None)
+    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, NULL, NULL, 8, ctypes.c_void_p(0x50000000), NULL, 0,
+                            None)
     assert r == -1 and "weight" in lib.segblocks_last_error().decode()
     # output aliasing the input
-    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, ctypes.c_void_p(0x60000000), NULL, 8, FAKE, None)
+    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, ctypes.c_void_p(0x60000000), NULL, 8, FAKE, NULL, 0,
+                            None)
     assert r == -1 and "overlap" in lib.segblocks_last_error().decode()
     # unknown flag on the fused-pad convolution
     r = lib.segblocks_block_conv3x3(FAKE, FAKE2, 1, 1, 1, 8, 32, 32, ctypes.c_void_p(0x30000000), 16,
                                     ctypes.c_void_p(0x60000000), NULL, 8, 4, NULL, NULL,
-                                    ctypes.c_void_p(0x70000000), ctypes.c_void_p(0x78000000), 1, 3, None)
+                                    ctypes.c_void_p(0x70000000), ctypes.c_void_p(0x78000000), 1, 3, NULL, 0, None)
     assert r == -1 and "flags" in lib.segblocks_last_error().decode()
 
 
@@ -106,3 +108,61 @@ def test_pad_combine_count_validation(lib):
     nh, nl = ctypes.c_int(), ctypes.c_int()
     r = lib.segblocks_count(NULL, 1, 2, 2, ctypes.byref(nh), ctypes.byref(nl), None)
     assert r == -1
+
+
+def _ws_query(lib, fn, *args):
+    n = ctypes.c_size_t(12345)
+    r = getattr(lib, fn)(*args, ctypes.byref(n))
+    return r, n.value
+
+
+def test_workspace_size_queries(lib):
+    """The sizes depend on the route the shapes take: none for the resident
+    convolution (64 channels, blocks of 32), split-K partials for the deep
+    stages, the packed stacks for a fused layer with 512 channels."""
+    r, n = _ws_query(lib, "segblocks_block_conv3x3_workspace_size", 1, 1, 1, 64, 256, 512, 32, 64, 128, 128)
+    assert r == 0 and n == 0
+    r, n = _ws_query(lib, "segblocks_block_conv_ex_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 1, 128, 128)
+    assert r == 0 and n > 0 and n % 256 == 0
+    r, n = _ws_query(lib, "segblocks_layer_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512)
+    # at least the packed input and output stacks of both classes
+    assert r == 0 and n >= 2 * 128 * (16 + 4) * 512 * 2
+    r, n = _ws_query(lib, "segblocks_layer_workspace_size", 0, 0, 1, 16, 64, 64, 16, 16)
+    assert r == 0 and n == 0        # fp32 NCHW: the general kernel, no scratch
+    # bad arguments are rejected like the calls themselves
+    r, _ = _ws_query(lib, "segblocks_block_conv_ex_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 5, 1, 128, 128)
+    assert r == -1 and "ksize" in lib.segblocks_last_error().decode()
+    r, _ = _ws_query(lib, "segblocks_layer_workspace_size", 1, 1, 1, 64, 30, 64, 4, 64)
+    assert r == -2
+    r = lib.segblocks_layer_workspace_size(1, 1, 1, 64, 32, 64, 4, 64, None)
+    assert r == -1 and "bytes is NULL" in lib.segblocks_last_error().decode()
+
+
+def test_calls_reject_missing_or_small_workspace(lib):
+    """SB_ENOMEM before anything is launched when the workspace is NULL or
+    smaller than the query's size; SB_EINVAL when it is misaligned or
+    overlaps an argument (fake device addresses: nothing is dereferenced)."""
+    _, need = _ws_query(lib, "segblocks_block_conv_ex_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 1, 128, 128)
+    P = ctypes.c_void_p
+    base = 0x100000000
+    args = [P(base), P(base + 0x1000000), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL,
+            512, 3, 1, 0, NULL, NULL, P(base + 0x4000000), P(base + 0x5000000), 128, 128]
+    ws = base + 0x10000000
+    assert lib.segblocks_block_conv_ex(*args, NULL, 0, None) == b.SB_ENOMEM
+    assert "workspace" in lib.segblocks_last_error().decode()
+    assert lib.segblocks_block_conv_ex(*args, P(ws), need - 1, None) == b.SB_ENOMEM
+    assert lib.segblocks_block_conv_ex(*args, P(ws + 16), need, None) == b.SB_EINVAL
+    assert "aligned" in lib.segblocks_last_error().decode()
+    assert lib.segblocks_block_conv_ex(*args, P(base + 0x4000000), need, None) == b.SB_EINVAL   # = hi_out
+    assert "overlap" in lib.segblocks_last_error().decode()
+    # the fused layer with 512 channels takes its packed stacks from the workspace
+    _, lneed = _ws_query(lib, "segblocks_layer_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512)
+    largs = [P(base), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL, 512,
+             P(base + 0x4000000)]
+    assert lib.segblocks_layer(*largs, P(ws), lneed // 2, None) == b.SB_ENOMEM
+    # block_conv3x3 at a deep-stage shape
+    _, bneed = _ws_query(lib, "segblocks_block_conv3x3_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 128, 128)
+    assert bneed > 0
+    bargs = [P(base), P(base + 0x1000000), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL,
+             512, 0, NULL, NULL, P(base + 0x4000000), P(base + 0x5000000), 128, 128]
+    assert lib.segblocks_block_conv3x3(*bargs, NULL, 0, None) == b.SB_ENOMEM

@@ -208,12 +208,14 @@ def test_encoder(dtype, mask_kind, seed):
 
 
 def test_encoder_graph_replays_match_eager():
-    """The encoder captured as one HIP graph: every replay, with eager work of
-    the program between replays and new data written into the static input,
-    equals the eager forward bit for bit (the kernels are deterministic)."""
+    """The encoder captured as one HIP graph before any eager call: every
+    replay, with eager work of the program between replays and new data
+    written into the static input, equals the eager forward bit for bit (the
+    kernels are deterministic).  Blocks of 64 image pixels at 512 x 512 give
+    the deep stages split-K partials in the workspace."""
     from paper_2011_12025_amd.encoder import BlockEncoder
-    log("[encoder graph] f16 3x128x256 block 64")
-    N, H, W, blk = 1, 128, 256, 64
+    log("[encoder graph] f16 3x512x512 block 64")
+    N, H, W, blk = 1, 512, 512, 64
     Wt = inputs.encoder_weights(93, "f16")
     mask_np = inputs.mask_bernoulli(93, N, H // blk, W // blk, 0.5)
     nh = int(mask_np.sum())
@@ -222,9 +224,12 @@ def test_encoder_graph_replays_match_eager():
     xa = _cl(inputs.feature_map(93, N, 3, H, W, "f16"))
     xb = _cl(inputs.feature_map(94, N, 3, H, W, "f16"))
     enc = BlockEncoder(Wt, blk)
-    ya, yb = enc(xa, mask, counts).clone(), enc(xb, mask, counts).clone()
     x = xa.clone(memory_format=torch.channels_last)
-    g, y = enc.capture(x, mask, counts)
+    g, y = enc.capture(x, mask, counts)       # no call before the capture: nothing is allocated by the library
+    ws = enc.workspace_bytes(N, H // 4, W // 4, torch.float16, counts)
+    log(f"[encoder graph] captured; workspace {ws} bytes")
+    assert ws > 0
+    ya, yb = enc(xa, mask, counts).clone(), enc(xb, mask, counts).clone()
     for r, (src, ref) in enumerate([(xa, ya), (xb, yb), (xa, ya), (xb, yb)]):
         enc(xb if r % 2 == 0 else xa, mask, counts)       # eager work between replays
         torch.cuda.synchronize()
