@@ -189,6 +189,27 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
                             void* hi_out, void* lo_out, int hi_cap, int lo_cap,
                             void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* segblocks_block_conv_ex for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments, results and kernels, without the
+ * workspace.  Scratch space comes from a fixed buffer of
+ * SB_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs on
+ * until the process ends; a call that would need more (see
+ * segblocks_block_conv_ex_workspace_size) fails with SB_ENOMEM before
+ * anything is launched.  The call allocates nothing.  Every call on one
+ * device shares that device's buffer: calls that may overlap on one device
+ * (different streams, or host threads) race and must be ordered by the
+ * caller.  The buffer keeps the last call's contents; each call writes every
+ * scratch byte it reads, so nothing has to be cleared. */
+#define SB_NOALLOC_SCRATCH_BYTES (16u << 20)
+int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, int layout,
+                                    int N, int C_in, int H, int W, const uint8_t* mask, int bs,
+                                    const void* weight, const void* bias, int C_out,
+                                    int ksize, int stride, int flags,
+                                    const void* residual_hi, const void* residual_lo,
+                                    void* hi_out, void* lo_out, int hi_cap, int lo_cap,
+                                    hipStream_t stream);
+
 /* Workspace sizes (bytes, HOST out-parameter) of segblocks_block_conv3x3,
  * segblocks_block_conv_ex and segblocks_layer for the given shapes and
  * stack capacities on the current device; the arguments mean what they mean

@@ -7,6 +7,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -279,12 +280,41 @@ int check_conv_ex_shape(const char* fn, int dtype, int layout, int C_in, int bs,
 
 }  // namespace
 
-int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
-                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int ksize,
-                            int stride, int flags, const void* residual_hi, const void* residual_lo, void* hi_out,
-                            void* lo_out, int hi_cap, int lo_cap, void* workspace, size_t ws_bytes,
-                            hipStream_t stream) {
-    const char* fn = "segblocks_block_conv_ex";
+namespace {
+
+// The fixed scratch buffer of segblocks_block_conv_ex_noalloc: one copy per
+// device, at the device address that hipGetSymbolAddress gives on that
+// device (the array's name is a host-side stand-in and is never passed to a
+// kernel).  Looked up once per device, under a lock.
+constexpr size_t SCRATCH_BYTES = (size_t)SB_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch_dev[64];
+
+int scratch_address(const char* fn, void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(fn, e);
+    if (dev < 0 || dev >= 64) return fail(SB_EHIP, fn, "device %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(fn, e);
+        if (!p) return fail(SB_EHIP, fn, "no device address for the scratch buffer");
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return SB_OK;
+}
+
+// segblocks_block_conv_ex with the workspace either given by the caller or,
+// with fixed_scratch, the library's scratch buffer of this device.
+int block_conv_ex_impl(const char* fn, bool fixed_scratch, const void* hi, const void* lo, int dtype, int layout,
+                       int N, int C_in, int H, int W, const uint8_t* mask, int bs, const void* weight,
+                       const void* bias, int C_out, int ksize, int stride, int flags, const void* residual_hi,
+                       const void* residual_lo, void* hi_out, void* lo_out, int hi_cap, int lo_cap, void* workspace,
+                       size_t ws_bytes, hipStream_t stream) {
     sb::Geo g;
     int s;
     if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
@@ -299,7 +329,15 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
         return s;
     sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
     const size_t need = sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0;
-    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
+    if (fixed_scratch) {
+        if (need > SCRATCH_BYTES)
+            return fail(SB_ENOMEM, fn, "needs %zu bytes of scratch, more than the fixed %zu bytes", need,
+                        SCRATCH_BYTES);
+        workspace = nullptr;
+        ws_bytes = 0;
+    } else if ((s = check_ws(fn, need, workspace, ws_bytes))) {
+        return s;
+    }
     const long long es = esize(dtype), lb = bs / 2, bo = bs / stride, lo_e = lb / stride;
     const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
     const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
@@ -310,9 +348,37 @@ int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layou
     const Range rws{workspace, (long long)need};
     if (any_overlap({rho, rlo, rws}, {rh, rl, rw, rb, rrh, rrl, Range{mask, g.B}}))
         return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    if (fixed_scratch && need > 0) {
+        // every byte of scratch that a launch reads, it has written first (split
+        // partials, their row counts, the padded low stack): nothing to clear
+        if ((s = scratch_address(fn, &workspace))) return s;
+        ws_bytes = SCRATCH_BYTES;
+    }
     if (sb::igemm_fits(dtype, layout, g, a))
         return hip_status(fn, sb::launch_igemm(dtype, g, mask, a, ksize, stride, sb::Ws{workspace, ws_bytes}, stream));
     return hip_status(fn, sb::launch_bconv(dtype, g, mask, a, ksize, stride, stream));
+}
+
+}  // namespace
+
+int segblocks_block_conv_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H, int W,
+                            const uint8_t* mask, int bs, const void* weight, const void* bias, int C_out, int ksize,
+                            int stride, int flags, const void* residual_hi, const void* residual_lo, void* hi_out,
+                            void* lo_out, int hi_cap, int lo_cap, void* workspace, size_t ws_bytes,
+                            hipStream_t stream) {
+    return block_conv_ex_impl("segblocks_block_conv_ex", false, hi, lo, dtype, layout, N, C_in, H, W, mask, bs, weight,
+                              bias, C_out, ksize, stride, flags, residual_hi, residual_lo, hi_out, lo_out, hi_cap,
+                              lo_cap, workspace, ws_bytes, stream);
+}
+
+int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, int layout, int N, int C_in, int H,
+                                    int W, const uint8_t* mask, int bs, const void* weight, const void* bias,
+                                    int C_out, int ksize, int stride, int flags, const void* residual_hi,
+                                    const void* residual_lo, void* hi_out, void* lo_out, int hi_cap, int lo_cap,
+                                    hipStream_t stream) {
+    return block_conv_ex_impl("segblocks_block_conv_ex_noalloc", true, hi, lo, dtype, layout, N, C_in, H, W, mask, bs,
+                              weight, bias, C_out, ksize, stride, flags, residual_hi, residual_lo, hi_out, lo_out,
+                              hi_cap, lo_cap, nullptr, 0, stream);
 }
 
 namespace {
