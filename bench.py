@@ -55,7 +55,13 @@ def parse():
                         "over low-res fractions; encoder: the N=1 ResNet-18 encoder; encoder-batched: N=4 encoders "
                         "over mask quantiles, image block sizes and fp16/bf16 (one JSON line per point)")
     p.add_argument("--profile-run", action="store_true",
-                   help="short run for rocprofv3 counters: a 256 MiB copy of known size, then the layer")
+                   help="short run for rocprofv3 counters: a 256 MiB copy of known size, then 10 launches of "
+                        "--profile-op")
+    p.add_argument("--profile-op", default="layer",
+                   help="what --profile-run launches: layer, split, pad, combine, conv3x3, block_conv3x3 (the "
+                        "headline workload), or bconv:<stage>:<low fraction> / layer:<stage>:<low fraction> (the "
+                        "packed block convolution / fused layer at ResNet-18 stage 1-4 of a 1024x2048 image, "
+                        "exact-fraction mask)")
     return p.parse_args()
 
 
@@ -74,6 +80,8 @@ def main():
               "would shard over images or block rows, see the design notes", file=sys.stderr)
         sys.exit(2)
 
+    if args.profile_run and ":" in args.profile_op:
+        return profile_stage(args)
     if args.workload != "layer":
         return bench_suite(args)
 
@@ -166,9 +174,9 @@ def main():
         for _ in range(3):
             bcp.copy_(a)
         for i in range(10):
-            launch("layer", i)
+            launch(args.profile_op, i)
         torch.cuda.synchronize()
-        print(json.dumps({"profile_run": True, "copy_bytes": a.numel(), "layer_launches": 10}))
+        print(json.dumps({"profile_run": True, "copy_bytes": a.numel(), "op": args.profile_op, "launches": 10}))
         return
 
     # ---------------- warmup + the timed steps (the contract's region)
@@ -536,6 +544,40 @@ def bench_encoder(args, torch, np, sb, B, inputs, batched):
                 del g, y
             del enc
             torch.cuda.empty_cache()
+
+
+def profile_stage(args):
+    """--profile-run for one stage shape: a 256 MiB copy of known size, then
+    10 launches of the packed block convolution or the fused layer."""
+    import torch
+
+    import paper_2011_12025_amd as sb
+    import paper_2011_12025_amd._binding as B
+    from paper_2011_12025_amd import inputs
+    kind, stage, f = args.profile_op.split(":")
+    C, H, W, bs = SWEEP_LAYERS[int(stage) - 1]
+    f = float(f)
+    dev, cl = torch.device("cuda:0"), torch.channels_last
+    torch.cuda.set_device(dev)
+    mask_np = inputs.mask_exact_fraction(0, 1, H // bs, W // bs, f)
+    nh = int(mask_np.sum()); nl = mask_np.size - nh
+    mask = torch.from_numpy(mask_np).to(dev)
+    x = inputs.feature_map(0, 1, C, H, W, "f16").to(dev).contiguous(memory_format=cl)
+    w = inputs.conv_weight(0, C, C, 3, "f16").to(dev).contiguous(memory_format=cl)
+    b = inputs.conv_bias(0, C, 9 * C, "f16").to(dev)
+    hi, lo = sb.split(x, mask, bs, counts=(nh, nl))
+    a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    bcp = torch.empty_like(a)
+    for _ in range(3):
+        bcp.copy_(a)
+    for _ in range(10):
+        if kind == "bconv":
+            sb.block_conv3x3(hi, lo, mask, bs, H, W, w, b)
+        else:
+            sb.layer(x, mask, bs, w, b)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_run": True, "copy_bytes": a.numel(), "op": args.profile_op, "launches": 10,
+                      "n_high": nh, "n_low": nl}))
 
 
 def bench_suite(args):

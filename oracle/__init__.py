@@ -63,6 +63,7 @@ def _L():
         lib.orc_plan.argtypes = [_u8p, ctypes.c_long, _i32p, _i32p, _i32p, _i32p]
         lib.orc_split.argtypes = [_fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp, _fp]
         lib.orc_pad.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp, _fp]
+        lib.orc_pad_ex.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p] + [ctypes.c_int] * 3 + [_fp, _fp]
         lib.orc_conv3x3_valid.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, _fp, _fp,
                                           ctypes.c_int, _dp]
         lib.orc_combine.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, _fp]
@@ -150,8 +151,15 @@ def split(x, mask, bs: int, dtype: str):
     return hi, lo
 
 
-def pad(hi, lo, mask, bs: int, H: int, W: int, dtype: str):
-    """BlockPad: (hi, lo) -> (hi_pad[nh,C,bs+2,bs+2], lo_pad[nl,C,bs/2+2,bs/2+2])."""
+SAMPLING = {"avg": 0, "strided": 1, "zero": 2}
+
+
+def pad(hi, lo, mask, bs: int, H: int, W: int, dtype: str, sampling: str = "avg"):
+    """BlockPad: (hi, lo) -> (hi_pad[nh,C,bs+2,bs+2], lo_pad[nl,C,bs/2+2,bs/2+2]).
+
+    sampling: how a low block's halo samples a high neighbour, "avg" (2x2
+    average, the paper's choice) or "strided" (top-left pixel of the cell);
+    "zero" pads every block with zeros instead (no BlockPad)."""
     hi, lo = _f32(hi), _f32(lo)
     mask = np.ascontiguousarray(mask, dtype=np.uint8)
     N = mask.shape[0]
@@ -160,8 +168,8 @@ def pad(hi, lo, mask, bs: int, H: int, W: int, dtype: str):
     nh, nl = hi.shape[0], lo.shape[0]
     hp = np.zeros((nh, C, bs + 2, bs + 2), np.float32)
     lp = np.zeros((nl, C, bs // 2 + 2, bs // 2 + 2), np.float32)
-    _L().orc_pad(_ptr(hi, _fp), _ptr(lo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
-                 _ptr(hp, _fp), _ptr(lp, _fp))
+    _L().orc_pad_ex(_ptr(hi, _fp), _ptr(lo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
+                    SAMPLING[sampling], _ptr(hp, _fp), _ptr(lp, _fp))
     return hp, lp
 
 
@@ -202,13 +210,13 @@ def combine(hi, lo, mask, bs: int, H: int, W: int):
     return y
 
 
-def layer(x, mask, bs: int, w, b, dtype: str):
+def layer(x, mask, bs: int, w, b, dtype: str, sampling: str = "avg"):
     """One block-conv layer: combine(conv3x3(pad(split(x)))), rounding to the
     storage type wherever a stage stores its result."""
     x = _f32(x)
     N, C, H, W = x.shape
     hi, lo = split(x, mask, bs, dtype)
-    hp, lp = pad(hi, lo, mask, bs, H, W, dtype)
+    hp, lp = pad(hi, lo, mask, bs, H, W, dtype, sampling)
     ho, lo_o = conv3x3(hp, lp, w, b, dtype)
     return combine(ho, lo_o, mask, bs, H, W)
 
@@ -248,12 +256,12 @@ def _epilogue(acc, dtype: str, relu: bool, residual=None):
 
 
 def block_conv_ex(hi, lo, mask, bs: int, H: int, W: int, w, b, stride: int, dtype: str, relu: bool = False,
-                  residual=None):
+                  residual=None, sampling: str = "avg"):
     """Block convolution of both stacks (K = w.shape[2]) at `stride`, BlockPad
     halo for 3x3, with the epilogue of the encoder's convolutions: bias,
     optional residual (a (hi, lo) pair of the output's shape), optional ReLU,
     one rounding.  Output stacks have extents bs/stride and bs/(2 stride)."""
-    hp, lp = pad(hi, lo, mask, bs, H, W, dtype)
+    hp, lp = pad(hi, lo, mask, bs, H, W, dtype, sampling)
     rh, rl = (None, None) if residual is None else residual
     return (_epilogue(conv_block(hp, w, stride, b), dtype, relu, rh),
             _epilogue(conv_block(lp, w, stride, b), dtype, relu, rl))

@@ -164,9 +164,19 @@ void orc_split(const float* x, int N, int C, int H, int W, const uint8_t* mask,
  *   outside the image                 -> 0
  *   neighbour at the same resolution  -> copy
  *   high block, low neighbour         -> nearest-upsampled neighbour value
- *   low block, high neighbour         -> 2x2 average of the neighbour       */
-void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
-             const uint8_t* mask, int bs, int dtype, float* hp, float* lp)
+ *   low block, high neighbour         -> depends on `sampling` (the two
+ *       options the BlockPad section weighs, and the zero padding its
+ *       ablation compares them with):
+ *       ORC_PAD_AVG     2x2 average of the neighbour's cell (average sampling)
+ *       ORC_PAD_STRIDED the cell's top-left pixel (strided subsampling)
+ *   ORC_PAD_ZERO: every halo pixel is 0 (each block zero-padded on its own,
+ *       the padding BlockPad replaces).                                     */
+#define ORC_PAD_AVG 0
+#define ORC_PAD_STRIDED 1
+#define ORC_PAD_ZERO 2
+
+void orc_pad_ex(const float* hi, const float* lo, int N, int C, int H, int W,
+                const uint8_t* mask, int bs, int dtype, int sampling, float* hp, float* lp)
 {
     const int GH = H / bs, GW = W / bs, lb = bs / 2;
     const long B = (long)N * GH * GW;
@@ -193,6 +203,8 @@ void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
             float val;
             if (dy == 0 && dx == 0) {
                 val = own[((long)c * e + u) * e + v];
+            } else if (sampling == ORC_PAD_ZERO) {
+                val = 0.0f;
             } else {
                 const int ny = gy + dy, nx = gx + dx;
                 if (ny < 0 || ny >= GH || nx < 0 || nx >= GW) {
@@ -207,11 +219,14 @@ void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
                         val = lo[(((long)slot[nk] * C + c) * lb + u2) * lb + v2];
                     } else if (high) { /* low neighbour: nearest upsampling */
                         val = lo[(((long)slot[nk] * C + c) * lb + (u2 >> 1)) * lb + (v2 >> 1)];
-                    } else {           /* high neighbour: average sampling */
+                    } else {           /* high neighbour: average or strided sampling */
                         const float* q = hi + ((long)slot[nk] * C + c) * bs * bs;
                         const int r = 2 * u2, s = 2 * v2;
-                        val = orc_avg4(q[r * bs + s], q[r * bs + s + 1],
-                                       q[(r + 1) * bs + s], q[(r + 1) * bs + s + 1], dtype);
+                        if (sampling == ORC_PAD_STRIDED)
+                            val = q[r * bs + s];
+                        else
+                            val = orc_avg4(q[r * bs + s], q[r * bs + s + 1],
+                                           q[(r + 1) * bs + s], q[(r + 1) * bs + s + 1], dtype);
                     }
                 }
             }
@@ -219,6 +234,13 @@ void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
         }
     }
     free(slot);
+}
+
+/* BlockPad with average sampling, the module as the paper uses it. */
+void orc_pad(const float* hi, const float* lo, int N, int C, int H, int W,
+             const uint8_t* mask, int bs, int dtype, float* hp, float* lp)
+{
+    orc_pad_ex(hi, lo, N, C, H, W, mask, bs, dtype, ORC_PAD_AVG, hp, lp);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -12,6 +12,13 @@ They follow from the definitions in the paper's "Block modules" section:
   a nearest-upsampled value is the value itself, a padded high block is a
   window of zeropad1(Z) and a padded low block a window of zeropad1(pool(Z)).
 * A layer is therefore M*conv_pad1(Z) + (1-M)*up2(conv_pad1(pool(Z))).
+* With strided subsampling in place of the 2x2 average, a low block's halo
+  from a high neighbour is the top-left pixel of the cell, which is the
+  phase-(0,0) subsampled map S = Z[::2, ::2] there (and the low blocks' own
+  values elsewhere): a padded low block is a window of zeropad1(S), and a
+  layer is M*conv_pad1(Z) + (1-M)*up2(conv_pad1(S)).
+* With zero padding instead of BlockPad every block is convolved on its
+  own: high blocks conv_pad1(block), low blocks up2(conv_pad1(pool(block))).
 """
 from __future__ import annotations
 
@@ -66,6 +73,27 @@ def pad_closed_form(Z: np.ndarray, mask: np.ndarray, bs: int, dtype: str):
     return hw[m], lw[~m]          # boolean indexing keeps row-major (n, gy, gx) order
 
 
+def pad_closed_form_strided(Z: np.ndarray, mask: np.ndarray, bs: int):
+    """Padded stacks under strided sampling: windows of zeropad1(Z) for the
+    high blocks and of zeropad1(Z[::2, ::2]) for the low blocks."""
+    m = np.asarray(mask) != 0
+    zp = np.pad(Z, ((0, 0), (0, 0), (1, 1), (1, 1)))
+    sp = np.pad(Z[..., ::2, ::2], ((0, 0), (0, 0), (1, 1), (1, 1)))
+    return windows(zp, bs)[m], windows(sp, bs // 2)[~m]
+
+
+def blocks_of(z: np.ndarray, e: int) -> np.ndarray:
+    """[N, C, GH*e, GW*e] -> [N, GH, GW, C, e, e] (the blocks, without halo)."""
+    N, C, H, W = z.shape
+    return np.ascontiguousarray(z.reshape(N, C, H // e, e, W // e, e).transpose(0, 2, 4, 1, 3, 5))
+
+
+def unblock(t: np.ndarray) -> np.ndarray:
+    """Inverse of blocks_of."""
+    N, GH, GW, C, e, _ = t.shape
+    return np.ascontiguousarray(t.transpose(0, 3, 1, 4, 2, 5).reshape(N, C, GH * e, GW * e))
+
+
 def conv_pad1_f64(z: np.ndarray, w: np.ndarray, b) -> np.ndarray:
     """Ordinary zero-padded 3x3 convolution in float64 (torch library op)."""
     zt = torch.from_numpy(np.asarray(z, np.float64))
@@ -82,3 +110,24 @@ def layer_closed_form(x: np.ndarray, mask: np.ndarray, bs: int, w, b, dtype: str
     hi_part = conv_pad1_f64(Z, w, b)
     lo_part = up2(conv_pad1_f64(pool_f32(Z, dtype), w, b))
     return M * hi_part + (1 - M) * lo_part
+
+
+def layer_closed_form_strided(x: np.ndarray, mask: np.ndarray, bs: int, w, b, dtype: str) -> np.ndarray:
+    """float64 closed form of a layer whose BlockPad samples strided."""
+    M = pixel_mask(mask, bs)
+    Z = M * x + (1 - M) * up2(pool_f32(x, dtype))
+    return M * conv_pad1_f64(Z, w, b) + (1 - M) * up2(conv_pad1_f64(Z[..., ::2, ::2], w, b))
+
+
+def layer_closed_form_zero(x: np.ndarray, mask: np.ndarray, bs: int, w, b, dtype: str) -> np.ndarray:
+    """float64 closed form of a layer that zero-pads every block: each block
+    (pooled for a low block) convolved on its own with zero padding."""
+    M = pixel_mask(mask, bs)
+    N, C, H, W = x.shape
+    GH, GW = H // bs, W // bs
+    hb = blocks_of(x, bs).reshape(N * GH * GW, C, bs, bs)
+    lb = blocks_of(pool_f32(x, dtype), bs // 2).reshape(N * GH * GW, C, bs // 2, bs // 2)
+    Co = w.shape[0]
+    yh = unblock(conv_pad1_f64(hb, w, b).reshape(N, GH, GW, Co, bs, bs))
+    yl = unblock(conv_pad1_f64(lb, w, b).reshape(N, GH, GW, Co, bs // 2, bs // 2))
+    return M * yh + (1 - M) * up2(yl)

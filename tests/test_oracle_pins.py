@@ -14,6 +14,7 @@ import torch
 import torch.nn.functional as F
 
 import oracle
+from oracle_closed_forms import (layer_closed_form_strided, layer_closed_form_zero, pad_closed_form_strided)
 from oracle_closed_forms import (conv_pad1_f64, layer_closed_form, pad_closed_form, pixel_mask,
                                  pool_f32, to_type, up2)
 from paper_2011_12025_amd import inputs
@@ -246,6 +247,60 @@ def test_pad_closed_form_random_masks(dtype, bs):
         np.testing.assert_array_equal(lp, rlp)
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("bs", [2, 4, 6, 8])
+def test_pad_strided_closed_form_random_masks(dtype, bs):
+    """Strided sampling: high blocks are padded exactly as with average
+    sampling, low blocks are windows of the zero-padded phase-(0,0)
+    subsampled combined map, bit for bit."""
+    N, C, GH, GW = 2, 3, 3, 5
+    H, W = GH * bs, GW * bs
+    x = _x(45, N, C, H, W, dtype)
+    for p in [0.0, 0.3, 0.7, 1.0]:
+        mask = inputs.mask_bernoulli(46, N, GH, GW, p)
+        hi, lo = oracle.split(x, mask, bs, dtype)
+        hp, lp = oracle.pad(hi, lo, mask, bs, H, W, dtype, "strided")
+        Z = oracle.combine(hi, lo, mask, bs, H, W)
+        rhp, rlp = pad_closed_form_strided(Z, mask, bs)
+        np.testing.assert_array_equal(hp, rhp)
+        np.testing.assert_array_equal(lp, rlp)
+        ahp, alp = oracle.pad(hi, lo, mask, bs, H, W, dtype)
+        np.testing.assert_array_equal(hp, ahp)      # only low blocks' halos can differ
+        if 0.0 < p < 1.0 and dtype == "f32":
+            assert not np.array_equal(lp, alp)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_pad_zero_pads_each_block_alone(dtype):
+    """Zero padding: every block's halo is zero, whatever its neighbours."""
+    N, C, GH, GW, bs = 2, 3, 3, 4, 6
+    x = _x(47, N, C, GH * bs, GW * bs, dtype)
+    mask = inputs.mask_bernoulli(48, N, GH, GW, 0.5)
+    hi, lo = oracle.split(x, mask, bs, dtype)
+    hp, lp = oracle.pad(hi, lo, mask, bs, GH * bs, GW * bs, dtype, "zero")
+    np.testing.assert_array_equal(hp, np.pad(hi, ((0, 0), (0, 0), (1, 1), (1, 1))))
+    np.testing.assert_array_equal(lp, np.pad(lo, ((0, 0), (0, 0), (1, 1), (1, 1))))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("sampling", ["strided", "zero"])
+def test_layer_pad_variants_closed_form(dtype, sampling):
+    """Layers with the two BlockPad alternatives against their float64 closed
+    forms (strided: the subsampled map; zero: every block convolved alone)."""
+    N, C, Co, bs, GH, GW = 2, 5, 4, 6, 3, 4
+    x = _x(49, N, C, GH * bs, GW * bs, dtype)
+    w, b = _w(50, Co, C, dtype), _b(51, Co, C, dtype)
+    cf = layer_closed_form_strided if sampling == "strided" else layer_closed_form_zero
+    for p in [0.0, 0.25, 0.5, 0.75, 1.0]:
+        mask = inputs.mask_bernoulli(52, N, GH, GW, p)
+        y = oracle.layer(x, mask, bs, w, b, dtype, sampling)
+        ref = cf(x, mask, bs, w, b, dtype)
+        tol = {"f32": 2e-6, "f16": 1e-3, "bf16": 8e-3}[dtype]
+        assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
+        if sampling == "strided" and p == 0.0:      # all high: nothing is sampled, same as BlockPad
+            np.testing.assert_array_equal(y, oracle.layer(x, mask, bs, w, b, dtype))
+
+
 def test_conv3x3_valid_matches_library():
     g = np.random.default_rng(8)
     P = g.standard_normal((3, 5, 7, 7)).astype(np.float32)
@@ -341,6 +396,11 @@ def test_bruteforce_all_masks_4x4_grid():
     hp, lp = oracle.pad(hi, lo, mask, 4, 16, 16, "f32")
     Z = oracle.combine(hi, lo, mask, 4, 16, 16)
     rhp, rlp = pad_closed_form(Z, mask, 4, "f32")
+    np.testing.assert_array_equal(hp, rhp)
+    np.testing.assert_array_equal(lp, rlp)
+    del hp, lp, rhp, rlp
+    hp, lp = oracle.pad(hi, lo, mask, 4, 16, 16, "f32", "strided")
+    rhp, rlp = pad_closed_form_strided(Z, mask, 4)
     np.testing.assert_array_equal(hp, rhp)
     np.testing.assert_array_equal(lp, rlp)
     del hp, lp, rhp, rlp, Z
