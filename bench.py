@@ -140,9 +140,9 @@ def main():
 
     def args_for(name, s):
         if name == "layer":
-            return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, wp, bp, C, P(s["y"]), None, 0, stream)
+            return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, wp, bp, C, 0, P(s["y"]), None, 0, stream)
         if name == "layer_allhigh":
-            return (P(s["x"]), DT, LAY, N, C, H, W, on, bs, wp, bp, C, P(s["yc"]), None, 0, stream)
+            return (P(s["x"]), DT, LAY, N, C, H, W, on, bs, wp, bp, C, 0, P(s["yc"]), None, 0, stream)
         if name == "split":
             return (P(s["x"]), DT, LAY, N, C, H, W, mk, bs, P(s["hi"]), nh, P(s["lo"]), nl, stream)
         if name == "pad":
@@ -408,7 +408,7 @@ def bench_sweep(args, torch, np, sb, B, inputs):
 
             def layer(i):
                 rc = lib.segblocks_layer(P(xs[i % R]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs, P(w), P(b), C,
-                                         P(ys[i % R]), *wsp(wsl), stream)
+                                         0, P(ys[i % R]), *wsp(wsl), stream)
                 if rc:
                     raise RuntimeError(lib.segblocks_last_error().decode())
 

@@ -90,8 +90,20 @@ typedef enum {
     SB_ENOMEM = -4  /* the workspace argument is NULL or smaller than needed */
 } sb_status;
 
-/* Flags of segblocks_block_conv3x3. */
+/* Flags of the convolutions (segblocks_block_conv3x3, segblocks_block_conv_ex,
+ * segblocks_layer). */
 #define SB_FLAG_RELU 1 /* max(0, .) after bias (and residual) */
+/* BlockPad alternatives (paper: Method > Block modules > BlockPad weighs
+ * strided subsampling against average sampling for a low block's halo taken
+ * from a high neighbour; Experiments > Ablation studies, sampling pattern,
+ * also compares plain zero padding).  At most one of the two: */
+#define SB_FLAG_PAD_STRIDED 2 /* the high neighbour's cell gives its top-left pixel */
+#define SB_FLAG_PAD_ZERO 4    /* every block is zero-padded on its own (no BlockPad) */
+
+/* Sampling of segblocks_pad_ex (the same three choices). */
+#define SB_PAD_AVG 0
+#define SB_PAD_STRIDED 1
+#define SB_PAD_ZERO 2
 
 /* Number of high (mask != 0) and low blocks of a mask.  BLOCKING: copies the
  * mask to the host on `stream` and waits for it.  n_high / n_low are HOST
@@ -116,6 +128,18 @@ int segblocks_split(const void* x, int dtype, int layout, int N, int C, int H, i
 int segblocks_pad(const void* hi, const void* lo, int dtype, int layout,
                   int N, int C, int H, int W, const uint8_t* mask, int bs,
                   void* hi_pad, void* lo_pad, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* segblocks_pad with a choice of how a low block's halo samples a high
+ * neighbour (paper: Method > Block modules > BlockPad, the two options it
+ * weighs; Experiments > Ablation studies, sampling pattern):
+ *   SB_PAD_AVG      the 2x2 average of the neighbour's cell (= segblocks_pad)
+ *   SB_PAD_STRIDED  the cell's top-left pixel (strided subsampling)
+ *   SB_PAD_ZERO     no BlockPad: every halo pixel of every block is 0
+ * Any other value is SB_EINVAL.  Bit-exact like segblocks_pad. */
+int segblocks_pad_ex(const void* hi, const void* lo, int dtype, int layout,
+                     int N, int C, int H, int W, const uint8_t* mask, int bs,
+                     void* hi_pad, void* lo_pad, int hi_cap, int lo_cap, int sampling,
+                     hipStream_t stream);
 
 /* Block convolution on padded stacks (paper: Method -- the same filters are
  * applied to the high- and the low-resolution blocks).  3x3, stride 1,
@@ -143,7 +167,9 @@ int segblocks_combine(const void* hi, const void* lo, int dtype, int layout,
  * segblocks_conv3x3(segblocks_pad(hi, lo)) followed by the optional epilogue
  *   out = act(conv + bias + residual)
  * with residual_hi / residual_lo stacks shaped like the outputs (or both
- * NULL) and act = ReLU when flags & SB_FLAG_RELU.  hi/hi_out/residual_hi hold
+ * NULL) and act = ReLU when flags & SB_FLAG_RELU.  SB_FLAG_PAD_STRIDED or
+ * SB_FLAG_PAD_ZERO replace the fused BlockPad by its alternatives (as
+ * segblocks_pad_ex with SB_PAD_STRIDED / SB_PAD_ZERO).  hi/hi_out/residual_hi hold
  * hi_cap blocks, lo/lo_out/residual_lo lo_cap blocks. */
 int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layout,
                             int N, int C_in, int H, int W, const uint8_t* mask, int bs,
@@ -162,10 +188,12 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
  * packed stacks in the workspace; everything else runs as one general
  * kernel.  Intermediate values are rounded to `dtype` exactly where the
  * four-call chain stores them, so the result equals that chain's up to the
- * order of the fp32 accumulation. */
+ * order of the fp32 accumulation.  flags: SB_FLAG_RELU (after the bias) and
+ * the BlockPad alternatives, as for segblocks_block_conv3x3. */
 int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W,
                     const uint8_t* mask, int bs, const void* weight, const void* bias,
-                    int C_out, void* y, void* workspace, size_t ws_bytes, hipStream_t stream);
+                    int C_out, int flags, void* y, void* workspace, size_t ws_bytes,
+                    hipStream_t stream);
 
 /* The encoder's block convolutions (paper: Method -- the network keeps its
  * blocks through the downsampling stages, so blocks shrink with the map):
@@ -213,8 +241,9 @@ int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, i
 /* Workspace sizes (bytes, HOST out-parameter) of segblocks_block_conv3x3,
  * segblocks_block_conv_ex and segblocks_layer for the given shapes and
  * stack capacities on the current device; the arguments mean what they mean
- * in those calls and are validated the same way.  The size assumes 16-byte
- * aligned buffers (a call with less aligned buffers takes a route that needs
+ * in those calls and are validated the same way.  The size is the one of
+ * flags without the BlockPad alternatives, which need no more.  It assumes
+ * 16-byte aligned buffers (a call with less aligned buffers takes a route that needs
  * no more).  Pure host functions: nothing is launched. */
 int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
                                            int bs, int C_out, int hi_cap, int lo_cap, size_t* bytes);

@@ -75,6 +75,19 @@ def _weight(weight: torch.Tensor, layout: int, k: int = 3) -> torch.Tensor:
     return weight.contiguous(memory_format=_fmt(layout))
 
 
+_SAMPLING = {"avg": 0, "strided": 1, "zero": 2}
+
+
+def _flags(relu: bool, sampling: str) -> int:
+    """Convolution flags: ReLU and the BlockPad alternative ("avg" = BlockPad
+    with average sampling, "strided" = strided subsampling, "zero" = plain
+    zero padding of every block)."""
+    if sampling not in _SAMPLING:
+        raise ValueError(f"sampling must be one of {sorted(_SAMPLING)}")
+    return (_b.SB_FLAG_RELU if relu else 0) | {0: 0, 1: _b.SB_FLAG_PAD_STRIDED, 2: _b.SB_FLAG_PAD_ZERO}[
+        _SAMPLING[sampling]]
+
+
 def _mask(mask: torch.Tensor) -> torch.Tensor:
     if mask.dtype != torch.uint8 or mask.dim() != 3 or not mask.is_contiguous():
         raise ValueError("mask must be a contiguous uint8 tensor [N, GH, GW]")
@@ -153,8 +166,10 @@ def split(x: torch.Tensor, mask: torch.Tensor, bs: int, counts=None, layout=None
     return hi, lo
 
 
-def pad(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None):
-    """BlockPad: returns (hi_pad [nh,C,bs+2,bs+2], lo_pad [nl,C,bs/2+2,bs/2+2])."""
+def pad(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None,
+        sampling: str = "avg"):
+    """BlockPad: returns (hi_pad [nh,C,bs+2,bs+2], lo_pad [nl,C,bs/2+2,bs/2+2]).
+    sampling: "avg" (BlockPad's average sampling), "strided" or "zero"."""
     mask = _mask(mask)
     ref = hi if hi.shape[0] else lo
     layout = layout_of(ref) if layout is None else layout
@@ -163,8 +178,10 @@ def pad(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int,
     N = mask.shape[0]
     hp = _empty((hi.shape[0], C, bs + 2, bs + 2), ref, layout)
     lp = _empty((lo.shape[0], C, bs // 2 + 2, bs // 2 + 2), ref, layout)
-    _b.call("segblocks_pad", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, _ptr(hp), _ptr(lp),
-            hi.shape[0], lo.shape[0], _stream(ref))
+    if sampling not in _SAMPLING:
+        raise ValueError(f"sampling must be one of {sorted(_SAMPLING)}")
+    _b.call("segblocks_pad_ex", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, _ptr(hp),
+            _ptr(lp), hi.shape[0], lo.shape[0], _SAMPLING[sampling], _stream(ref))
     return hp, lp
 
 
@@ -203,7 +220,7 @@ def combine(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: 
 
 def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
                   weight: torch.Tensor, bias=None, relu: bool = False, residual=None, layout=None, out=None,
-                  workspace=None):
+                  workspace=None, sampling: str = "avg"):
     """3x3 block convolution with BlockPad fused into the tile load (packed in,
     packed out); optional epilogue act(conv + bias + residual).  ``workspace``:
     a uint8 tensor of at least block_conv3x3_workspace_size() + 256 bytes, or
@@ -224,13 +241,13 @@ def block_conv3x3(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
     need = block_conv3x3_workspace_size(ref.dtype, layout, N, C_in, H, W, bs, C_out, hi.shape[0], lo.shape[0])
     wp, wn, _keep = _ws(need, ref.device, workspace)
     _b.call("segblocks_block_conv3x3", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
-            _ptr(weight), _ptr(bias), C_out, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl), _ptr(ho),
+            _ptr(weight), _ptr(bias), C_out, _flags(relu, sampling), _ptr(rh), _ptr(rl), _ptr(ho),
             _ptr(lo_o), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
     return ho, lo_o
 
 
 def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bias=None, layout=None, out=None,
-          workspace=None):
+          workspace=None, relu: bool = False, sampling: str = "avg"):
     """One block-conv layer: combine(conv3x3(pad(split(x)))), fused (see
     segblocks_layer for the routes).  ``workspace`` as in block_conv3x3, sized
     by layer_workspace_size()."""
@@ -245,13 +262,13 @@ def layer(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, bi
     need = layer_workspace_size(x.dtype, layout, N, C_in, H, W, bs, C_out)
     wp, wn, _keep = _ws(need, x.device, workspace)
     _b.call("segblocks_layer", _ptr(x), _dt(x), layout, N, C_in, H, W, _ptr(mask), bs, _ptr(weight), _ptr(bias),
-            C_out, _ptr(y), wp, wn, _stream(x))
+            C_out, _flags(relu, sampling), _ptr(y), wp, wn, _stream(x))
     return y
 
 
 def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
                   weight: torch.Tensor, bias=None, stride: int = 1, relu: bool = False, residual=None, out=None,
-                  workspace=None):
+                  workspace=None, sampling: str = "avg"):
     """K x K block convolution (K = weight.shape[2], 1 or 3) at `stride` (1 or
     2) of channels-last packed stacks, BlockPad fused, epilogue
     act(conv + bias + residual); outputs have block sides bs/stride and
@@ -275,7 +292,7 @@ def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
     need = block_conv_ex_workspace_size(ref.dtype, N, C_in, H, W, bs, C_out, k, stride, hi.shape[0], lo.shape[0])
     wp, wn, _keep = _ws(need, ref.device, workspace)
     _b.call("segblocks_block_conv_ex", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
-            _ptr(weight), _ptr(bias), C_out, k, stride, _b.SB_FLAG_RELU if relu else 0, _ptr(rh), _ptr(rl),
+            _ptr(weight), _ptr(bias), C_out, k, stride, _flags(relu, sampling), _ptr(rh), _ptr(rl),
             _ptr(ho), _ptr(lo_o), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
     return ho, lo_o
 

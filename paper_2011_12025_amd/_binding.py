@@ -17,9 +17,10 @@ LIB_PATH = os.path.join(_HERE, "libsegblocks.so")
 
 SB_F32, SB_F16, SB_BF16 = 0, 1, 2
 SB_NCHW, SB_NHWC = 0, 1
-SB_FLAG_RELU = 1
+SB_FLAG_RELU, SB_FLAG_PAD_STRIDED, SB_FLAG_PAD_ZERO = 1, 2, 4
+SB_PAD_AVG, SB_PAD_STRIDED, SB_PAD_ZERO = 0, 1, 2
 
-EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_conv3x3", "segblocks_combine",
+EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_pad_ex", "segblocks_conv3x3", "segblocks_combine",
            "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
            "segblocks_maxpool", "segblocks_block_conv3x3_workspace_size", "segblocks_block_conv_ex_workspace_size",
            "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_last_error"]
@@ -34,11 +35,12 @@ _SIGS = {
     "segblocks_count": [_P, _I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), _P],
     "segblocks_split": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _I, _P],
     "segblocks_pad": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _P],
+    "segblocks_pad_ex": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _P],
     "segblocks_conv3x3": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P, _I, _I, _P],
     "segblocks_combine": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P],
     "segblocks_block_conv3x3": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I,
                                 _P, _Z, _P],
-    "segblocks_layer": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _P, _P, _Z, _P],
+    "segblocks_layer": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _P, _P, _Z, _P],
     "segblocks_block_conv_ex": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P,
                                 _I, _I, _P, _Z, _P],
     "segblocks_block_conv_ex_noalloc": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P,

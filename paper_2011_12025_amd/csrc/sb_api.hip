@@ -147,13 +147,16 @@ int segblocks_split(const void* x, int dtype, int layout, int N, int C, int H, i
     return hip_status(fn, sb::launch_split(dtype, layout, g, x, mask, hi, hi_cap, lo, lo_cap, stream));
 }
 
-int segblocks_pad(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
-                  const uint8_t* mask, int bs, void* hi_pad, void* lo_pad, int hi_cap, int lo_cap,
-                  hipStream_t stream) {
-    const char* fn = "segblocks_pad";
+namespace {
+
+int pad_impl(const char* fn, const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+             const uint8_t* mask, int bs, void* hi_pad, void* lo_pad, int hi_cap, int lo_cap, int sampling,
+             hipStream_t stream) {
     sb::Geo g;
     int s;
     if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (sampling != SB_PAD_AVG && sampling != SB_PAD_STRIDED && sampling != SB_PAD_ZERO)
+        return fail(SB_EINVAL, fn, "bad sampling %d", sampling);
     if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
         (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
         (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)))
@@ -164,7 +167,33 @@ int segblocks_pad(const void* hi, const void* lo, int dtype, int layout, int N, 
     const Range rlp{lo_pad, lo_cap * (long long)C * (lb + 2) * (lb + 2) * es};
     if (any_overlap({rhp, rlp}, {rh, rl, Range{mask, g.B}}))
         return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
-    return hip_status(fn, sb::launch_pad(dtype, layout, g, hi, lo, mask, hi_pad, lo_pad, hi_cap, lo_cap, stream));
+    return hip_status(fn, sb::launch_pad(dtype, layout, g, hi, lo, mask, hi_pad, lo_pad, hi_cap, lo_cap, sampling,
+                                         stream));
+}
+
+// Flags of the convolutions: ReLU and at most one BlockPad alternative.
+int check_conv_flags(const char* fn, int flags) {
+    if (flags & ~(SB_FLAG_RELU | SB_FLAG_PAD_STRIDED | SB_FLAG_PAD_ZERO))
+        return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((flags & SB_FLAG_PAD_STRIDED) && (flags & SB_FLAG_PAD_ZERO))
+        return fail(SB_EINVAL, fn, "SB_FLAG_PAD_STRIDED and SB_FLAG_PAD_ZERO exclude each other");
+    return SB_OK;
+}
+
+}  // namespace
+
+int segblocks_pad(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+                  const uint8_t* mask, int bs, void* hi_pad, void* lo_pad, int hi_cap, int lo_cap,
+                  hipStream_t stream) {
+    return pad_impl("segblocks_pad", hi, lo, dtype, layout, N, C, H, W, mask, bs, hi_pad, lo_pad, hi_cap, lo_cap,
+                    SB_PAD_AVG, stream);
+}
+
+int segblocks_pad_ex(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+                     const uint8_t* mask, int bs, void* hi_pad, void* lo_pad, int hi_cap, int lo_cap, int sampling,
+                     hipStream_t stream) {
+    return pad_impl("segblocks_pad_ex", hi, lo, dtype, layout, N, C, H, W, mask, bs, hi_pad, lo_pad, hi_cap, lo_cap,
+                    sampling, stream);
 }
 
 int segblocks_conv3x3(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C_in, int H, int W,
@@ -219,7 +248,7 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
     int s;
     if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
     if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
-    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((s = check_conv_flags(fn, flags))) return s;
     if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
         return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
     if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
@@ -245,15 +274,16 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
 }
 
 int segblocks_layer(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const uint8_t* mask,
-                    int bs, const void* weight, const void* bias, int C_out, void* y, void* workspace,
+                    int bs, const void* weight, const void* bias, int C_out, int flags, void* y, void* workspace,
                     size_t ws_bytes, hipStream_t stream) {
     const char* fn = "segblocks_layer";
     sb::Geo g;
     int s;
     if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
     if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if ((s = check_conv_flags(fn, flags))) return s;
     if (!x || !y) return fail(SB_EINVAL, fn, "x or y is NULL");
-    sb::ConvArgs a{x, nullptr, weight, bias, nullptr, nullptr, y, nullptr, C_in, C_out, 0, 0, 0};
+    sb::ConvArgs a{x, nullptr, weight, bias, nullptr, nullptr, y, nullptr, C_in, C_out, flags, 0, 0};
     const size_t need = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
     if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype);
@@ -320,7 +350,7 @@ int block_conv_ex_impl(const char* fn, bool fixed_scratch, const void* hi, const
     if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
     if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
     if ((s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride))) return s;
-    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((s = check_conv_flags(fn, flags))) return s;
     if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
         return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
     if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||

@@ -101,9 +101,10 @@ __device__ __forceinline__ Src<T> tile_src(const Geo& g, const ConvArgs& a, cons
         return src_copy<T>(stack_at<T, L>((const T*)(t.high ? a.in_hi : a.in_lo), t.slot, a.C_in, t.pe, u, pv, c));
     } else if constexpr (SRC == SRC_PACKED) {
         return packed_src<T, L>((const T*)a.in_hi, (const T*)a.in_lo, a.C_in, g.bs, nb, a.hi_cap, a.lo_cap, u - 1,
-                                pv - 1, c);
+                                pv - 1, c, pad_mode(a.flags));
     } else {
-        return dense_src<T, L>((const T*)a.in_hi, t.n, a.C_in, g.H, g.W, g.bs, t.gy, t.gx, nb, u - 1, pv - 1, c);
+        return dense_src<T, L>((const T*)a.in_hi, t.n, a.C_in, g.H, g.W, g.bs, t.gy, t.gx, nb, u - 1, pv - 1, c,
+                               pad_mode(a.flags));
     }
 }
 
@@ -536,9 +537,11 @@ hipError_t layer_via_packed(int dtype, const Geo& g, const uint8_t* mask, const 
 }  // namespace
 
 size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const ConvArgs& a) {
-    if (conv_res_fits_shape(dtype, layout, g, a)) return 0;
+    // packed stacks: the GEMM's need also where the resident kernel takes the call
+    // with average sampling, since the BlockPad alternatives go to the GEMM
     if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits_shape(dtype, layout, g, a))
         return igemm_ws_bytes(g, a, 3, 1);
+    if (conv_res_fits_shape(dtype, layout, g, a)) return 0;
     if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a))
         return packed_layout(g, a).total;
     return 0;

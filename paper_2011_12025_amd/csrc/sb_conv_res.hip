@@ -772,6 +772,8 @@ bool conv_res_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
 
 bool conv_res_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
+    // BlockPad with average sampling only: the alternatives go to the other kernels
+    if ((a.flags >> 1) & 3) return false;
     if (a.C_in % 8 || a.C_in > 64 || res_rows(g.bs) == 0) return false;
     // element offsets inside one image or one stack are 32-bit
     const long long img = (long long)g.H * g.W * (a.C_in > a.C_out ? a.C_in : a.C_out);

@@ -141,7 +141,7 @@ __global__ __launch_bounds__(WG) void k_bconv(Geo g, const uint8_t* __restrict__
 #pragma unroll
         for (int t = 0; t < 2; ++t)
             src[t] = pv[t] ? packed_src<T, NHWC>(hi, lo, C, g.bs, nb, a.hi_cap, a.lo_cap, ST * oy[t] + ky - KS / 2,
-                                                 ST * ox[t] + kx - KS / 2, 0)
+                                                 ST * ox[t] + kx - KS / 2, 0, pad_mode(a.flags))
                            : src_zero<T>();
         for (int ks = 0; ks < nks; ++ks) {
             const int c = ks * 32 + kg * 8;

@@ -132,7 +132,7 @@ __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, in
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* __restrict__ lo, int C, int H, int W,
                                             const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
-                                            T* __restrict__ hp, T* __restrict__ lp, int hi_cap, int lo_cap) {
+                                            T* __restrict__ hp, T* __restrict__ lp, int hi_cap, int lo_cap, int pm) {
     bool high;
     int slot, piece;
     slot_piece((int)blockIdx.x, hi_cap, Gh, Gl, high, slot, piece);
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* _
     item_coords<L, V>(it, pe, C, u, v, c);
     T* dst = (high ? hp : lp) + (size_t)slot * C * pe * pe + (size_t)it * V;
     if constexpr (L == NHWC || V == 1) {
-        const Src<T> s = packed_src<T, L>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, v - 1, c);
+        const Src<T> s = packed_src<T, L>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, v - 1, c, pm);
         SrcBatch<T, V, 1> b;
         b.issue(0, s);
         vstore<T, V>(dst, b.value(0));
@@ -224,13 +224,13 @@ hipError_t run_split(const Geo& g, const void* x, const uint8_t* mask, void* hi,
 
 template <typename T, int L, int V>
 hipError_t run_pad(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                   int hi_cap, int lo_cap, hipStream_t st) {
+                   int hi_cap, int lo_cap, int pm, hipStream_t st) {
     const int ph = g.bs + 2, pl = g.bs / 2 + 2;
     const int Gh = pieces((long long)ph * ph * g.C / V), Gl = pieces((long long)pl * pl * g.C / V);
     const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((k_pad<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)hi, (const T*)lo, g.C,
-                       g.H, g.W, mask, g.bs, (int)g.B, Gh, Gl, (T*)hp, (T*)lp, hi_cap, lo_cap);
+                       g.H, g.W, mask, g.bs, (int)g.B, Gh, Gl, (T*)hp, (T*)lp, hi_cap, lo_cap, pm);
     return hipGetLastError();
 }
 
@@ -259,14 +259,14 @@ hipError_t split_t(int layout, const Geo& g, const void* x, const uint8_t* mask,
 
 template <typename T>
 hipError_t pad_t(int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                 int hi_cap, int lo_cap, hipStream_t st) {
+                 int hi_cap, int lo_cap, int pm, hipStream_t st) {
     constexpr int VM = 16 / (int)sizeof(T);
     const bool al = aligned16(hi) && aligned16(lo) && aligned16(hp) && aligned16(lp);
     if (layout == NHWC) {
-        if (al && g.C % VM == 0) return run_pad<T, NHWC, VM>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
-        return run_pad<T, NHWC, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+        if (al && g.C % VM == 0) return run_pad<T, NHWC, VM>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+        return run_pad<T, NHWC, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     }
-    return run_pad<T, NCHW, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+    return run_pad<T, NCHW, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
 }
 
 template <typename T>
@@ -295,13 +295,13 @@ hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, cons
 }
 
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
-                      void* hp, void* lp, int hi_cap, int lo_cap, hipStream_t st) {
+                      void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st) {
     if (rows_fit(dtype, layout, g, {hi, lo, hp, lp}))
-        return launch_pad_rows(dtype, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+        return launch_pad_rows(dtype, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     switch (dtype) {
-    case 0: return pad_t<float>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
-    case 1: return pad_t<f16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
-    default: return pad_t<bf16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+    case 0: return pad_t<float>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    case 1: return pad_t<f16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    default: return pad_t<bf16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     }
 }
 

@@ -42,6 +42,7 @@
 
 #include "sb_common.h"
 #include "sb_kernels.h"
+#include "sb_pixel.h"
 
 namespace sb {
 
@@ -158,20 +159,36 @@ __device__ __forceinline__ void gissue_a(const T* const (&wrow)[AR], unsigned ch
     for (int j = 0; j < AR; ++j) gdma16(wrow[j] + off, st + (wave * AR + j) * 1024);
 }
 
-// DMA of one step's pixel rows (zeros for pixels outside the image; the
-// top-left source of a 2x2-average pixel).
+// This lane's pixel-row sources of one tap, decoded once per tap: a pointer
+// to chunk pq of the source row (the top-left pixel of a 2x2-average cell,
+// the zero row for pixels outside the image) and a bit per row that is a
+// 2x2 average.  A step then only adds its channel offset.
 template <typename T, int BR>
-__device__ __forceinline__ void gissue_b(const uint32_t (&dsc)[BR], const int (&pq)[BR], int c,
-                                         const T* __restrict__ in_hi, const T* __restrict__ in_lo, const T* zrow,
-                                         int C_in, unsigned char* st, int wave) {
+struct GRows {
+    const T* p[BR];
+    uint32_t avg;
+};
+
+template <typename T, int BR>
+__device__ __forceinline__ void gdecode(const uint32_t (&dsc)[BR], const int (&pq)[BR], const T* __restrict__ in_hi,
+                                        const T* __restrict__ in_lo, const T* zrow, int C_in, GRows<T, BR>& r) {
+    r.avg = 0;
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
         const uint32_t d = dsc[j];
         const uint32_t kind = d >> 30;
         const T* base = kind == GK_LO ? in_lo : (kind == GK_ZERO ? zrow : in_hi);
         const size_t pix = kind != GK_ZERO ? (size_t)(d & 0x3FFFFFFFu) : 0;
-        gdma16(base + pix * C_in + c + pq[j], st + (wave * BR + j) * 1024);
+        r.p[j] = base + pix * C_in + pq[j];
+        r.avg |= (kind == GK_AVG ? 1u : 0u) << j;
     }
+}
+
+// DMA of one step's pixel rows: channel offset c of every row.
+template <typename T, int BR>
+__device__ __forceinline__ void gissue_b(const GRows<T, BR>& r, int c, unsigned char* st, int wave) {
+#pragma unroll
+    for (int j = 0; j < BR; ++j) gdma16(r.p[j] + c, st + (wave * BR + j) * 1024);
 }
 
 // This lane's pixel-row descriptors of one tap, held in registers for the
@@ -194,14 +211,12 @@ __device__ __forceinline__ void gissue_pad(const T* zrow, unsigned char* st, int
 // 2x2-average pixels of one step, copied into the side buffer: window
 // (wave * BR + j) * 3 + t, this lane's slot at lane * 16.
 template <typename T, int BR>
-__device__ __forceinline__ void gissue_side(const uint32_t (&dsc)[BR], const int (&pq)[BR], int c,
-                                            const T* __restrict__ in_hi, int C_in, int bs, unsigned char* side,
+__device__ __forceinline__ void gissue_side(const GRows<T, BR>& r, int c, int C_in, int bs, unsigned char* side,
                                             int wave) {
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
-        const uint32_t d = dsc[j];
-        if ((d >> 30) == GK_AVG) {
-            const T* p0 = in_hi + (size_t)(d & 0x3FFFFFFFu) * C_in + c + pq[j];
+        if ((r.avg >> j) & 1u) {
+            const T* p0 = r.p[j] + c;
             unsigned char* w = side + (wave * BR + j) * 3 * 1024;
             gdma16(p0 + C_in, w);
             gdma16(p0 + (size_t)bs * C_in, w + 1024);
@@ -213,12 +228,11 @@ __device__ __forceinline__ void gissue_side(const uint32_t (&dsc)[BR], const int
 // Replaces the top-left value of every 2x2-average pixel of a landed step
 // (st: the step's pixel tile) by the average of its four sources.
 template <typename T, int BR>
-__device__ __forceinline__ void gcommit_side(const uint32_t (&dsc)[BR], unsigned char* st, const unsigned char* side,
-                                             int wave, int lane) {
+__device__ __forceinline__ void gcommit_side(uint32_t avg, unsigned char* st, const unsigned char* side, int wave,
+                                             int lane) {
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
-        const uint32_t d = dsc[j];
-        if ((d >> 30) == GK_AVG) {
+        if ((avg >> j) & 1u) {
             unsigned char* slot = st + (wave * BR + j) * 1024 + lane * 16;
             const unsigned char* w = side + (wave * BR + j) * 3 * 1024 + lane * 16;
             const uint4 va = glds_read16(slot), vb = glds_read16(w), vc = glds_read16(w + 1024),
@@ -308,7 +322,8 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     uint16_t* s_hb = reinterpret_cast<uint16_t*>(s_side + GWAVES * BR * 3 * 1024);
     __shared__ int s_wsum[GWAVES];
 
-    const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = (int)threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS windows are scalar addresses
     const int B = (int)g.B;
 
     // ---- block plan: s_hb[k] = high blocks before k (k = 0..B)
@@ -401,6 +416,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     }
     __syncthreads();
     const int per_img = g.GH * g.GW;
+    const int pm = pad_mode(a.flags);
     for (int idx = tid; idx < TM * KT; idx += GWG) {
         const int p = idx / KT, t = idx - (idx / KT) * KT;
         const int k = s_pk[p];
@@ -417,7 +433,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                 ds = gdesc(GK_LO, (slot * (lb + 2) + uu + 1) * (lb + 2) + vv + 1);
             } else if (dy == 0 && dx == 0) {
                 ds = gdesc(high ? GK_HI : GK_LO, (slot * e_in + uu) * e_in + vv);
-            } else {
+            } else if (pm != PM_ZERO) {  // zero padding leaves the halo at zero
                 const int nn = k / per_img;
                 const int r = k - nn * per_img;
                 const int gy = r / g.GW, gx = r - (r / g.GW) * g.GW;
@@ -431,7 +447,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                     if (s2 < (h2 ? a.hi_cap : a.lo_cap)) {
                         if (h2 == high) ds = gdesc(high ? GK_HI : GK_LO, (s2 * e_in + u2) * e_in + v2);
                         else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
-                        else ds = gdesc(GK_AVG, (s2 * bs + 2 * u2) * bs + 2 * v2);
+                        else ds = gdesc(pm == PM_STRIDED ? GK_HI : GK_AVG, (s2 * bs + 2 * u2) * bs + 2 * v2);
                     }
                 }
             }
@@ -443,19 +459,22 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     // ---- prologue: step 0 (2x2 averages, pixels), step 1 (weights, pixels)
     int tap1 = tap0, c1 = c0 + 1;
     if (c1 == cpt) { c1 = 0; ++tap1; }
-    uint32_t d0[BR], dA[BR], dB[BR];  // descriptors of steps 0 / s + 1 / s + 2
-    gload_desc<BR>(s_desc, prow, KT, tap0, d0);
-    gload_desc<BR>(s_desc, prow, KT, tap1 < KT ? tap1 : tap0, dA);
-    gissue_side<T, BR>(d0, pq, c0 * GKC, in_hi, C_in, bs, s_side, wave);
-    gissue_b<T, BR>(d0, pq, c0 * GKC, in_hi, in_lo, zrow, C_in, s_stage + A_BYTES, wave);
+    uint32_t dsc[BR];
+    GRows<T, BR> r0, rA, rB;  // pixel-row sources of steps 0 / s + 1 / s + 2
+    gload_desc<BR>(s_desc, prow, KT, tap0, dsc);
+    gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, r0);
+    gload_desc<BR>(s_desc, prow, KT, tap1 < KT ? tap1 : tap0, dsc);
+    gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, rA);
+    gissue_side<T, BR>(r0, c0 * GKC, C_in, bs, s_side, wave);
+    gissue_b<T, BR>(r0, c0 * GKC, s_stage + A_BYTES, wave);
     if (n > 1) {
         gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
-        gissue_b<T, BR>(dA, pq, c1 * GKC, in_hi, in_lo, zrow, C_in, s_stage + STAGE + A_BYTES, wave);
+        gissue_b<T, BR>(rA, c1 * GKC, s_stage + STAGE + A_BYTES, wave);
     } else {
         gissue_pad<T, AR + BR>(zrow, s_stage + STAGE, wave, lane);
     }
     __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-    gcommit_side<T, BR>(d0, s_stage + A_BYTES, s_side, wave, lane);
+    gcommit_side<T, BR>(r0.avg, s_stage + A_BYTES, s_side, wave, lane);
     gbarrier();
 
     floatx4 acc[MS][NS];
@@ -467,49 +486,60 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     const int wm = wave % WM, wn = wave / WM;
     const int l16 = lane & 15, kg = lane >> 4;
     // (tap, chunk) of step s + 1 and s + 2
-    int ta = tap1, ca = c1;
+    int ca = c1;
     int tb = tap1, cb = c1 + 1;
     if (cb == cpt) { cb = 0; ++tb; }
-    gload_desc<BR>(s_desc, prow, KT, tb < KT ? tb : tap0, dB);
+    gload_desc<BR>(s_desc, prow, KT, tb < KT ? tb : tap0, dsc);
+    gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, rB);
     int b_cur = 0;
 
     for (int s = 0; s < n; ++s) {
         unsigned char* cur = s_stage + b_cur * STAGE;
         const int b1 = b_cur == GNST - 1 ? 0 : b_cur + 1;
         const int b2 = b1 == GNST - 1 ? 0 : b1 + 1;
-        if (s + 1 < n) gissue_side<T, BR>(dA, pq, ca * GKC, in_hi, C_in, bs, s_side, wave);
+        // every fragment of the step is read first, so that the LDS latency
+        // runs under the DMA issue of step s + 2 instead of between MFMAs
+        frag af[2][NS], bf[2][MS];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int ns = 0; ns < NS; ++ns)
+                af[ks][ns] = *reinterpret_cast<const frag*>(cur + gsw(wn * NS * 16 + ns * 16 + l16, ks * 4 + kg));
+#pragma unroll
+            for (int ms = 0; ms < MS; ++ms)
+                bf[ks][ms] =
+                    *reinterpret_cast<const frag*>(cur + A_BYTES + gsw(wm * MS * 16 + ms * 16 + l16, ks * 4 + kg));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (s + 1 < n) gissue_side<T, BR>(rA, ca * GKC, C_in, bs, s_side, wave);
         if (s + 2 < n) {
             gissue_a<T, AR>(wrow, s_stage + b2 * STAGE, tb * C_in + cb * GKC, wave);
-            gissue_b<T, BR>(dB, pq, cb * GKC, in_hi, in_lo, zrow, C_in, s_stage + b2 * STAGE + A_BYTES, wave);
+            gissue_b<T, BR>(rB, cb * GKC, s_stage + b2 * STAGE + A_BYTES, wave);
         } else {
             gissue_pad<T, AR + BR>(zrow, s_stage + b2 * STAGE, wave, lane);
         }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            frag af[NS], bf[MS];
-#pragma unroll
-            for (int ns = 0; ns < NS; ++ns)
-                af[ns] = *reinterpret_cast<const frag*>(cur + gsw(wn * NS * 16 + ns * 16 + l16, ks * 4 + kg));
-#pragma unroll
-            for (int ms = 0; ms < MS; ++ms)
-                bf[ms] = *reinterpret_cast<const frag*>(cur + A_BYTES + gsw(wm * MS * 16 + ms * 16 + l16, ks * 4 + kg));
+        for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
             for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-                for (int ns = 0; ns < NS; ++ns) acc[ms][ns] = mf::mma(af[ns], bf[ms], acc[ms][ns]);
-        }
+                for (int ns = 0; ns < NS; ++ns) acc[ms][ns] = mf::mma(af[ks][ns], bf[ks][ms], acc[ms][ns]);
+        __builtin_amdgcn_sched_barrier(0);
         // step s + 1 has landed once only step s + 2's DMAs can be outstanding
         __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-        if (s + 1 < n) gcommit_side<T, BR>(dA, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
+        if (s + 1 < n) gcommit_side<T, BR>(rA.avg, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
         gbarrier();
         b_cur = b1;
-        ta = tb; ca = cb;
-#pragma unroll
-        for (int j = 0; j < BR; ++j) dA[j] = dB[j];
-        if (++cb == cpt) {  // a new tap: its descriptors (read a step before they are used)
+        ca = cb;
+        rA = rB;
+        if (++cb == cpt) {  // a new tap: its sources (read a step before they are used)
             cb = 0;
             ++tb;
-            if (tb < KT) gload_desc<BR>(s_desc, prow, KT, tb, dB);
+            if (tb < KT) {
+                gload_desc<BR>(s_desc, prow, KT, tb, dsc);
+                gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, rB);
+            }
         }
     }
     __builtin_amdgcn_s_waitcnt(0);  // the padding DMAs
@@ -651,7 +681,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     // every low-tile source is a plain copy.  Measured, the extra pass pays at
     // 128 input channels (about 5 us less at 25-75 % low blocks) and costs 1-4 us
     // at 64, 256 and 512, so it is taken there only.
-    p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && a.C_in > 64 && a.C_in <= 128;
+    p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG;
     p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 4)
                                 : 0;
     p.pad_bytes = p.pad_low ? ground256((size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * 2) : 0;
@@ -690,7 +720,7 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
         Geo pg = g;
         pg.C = a.C_in;
         e = launch_pad_rows(std::is_same<T, f16>::value ? 1 : 2, pg, a.in_hi, a.in_lo, mask, nullptr, lp, a.hi_cap,
-                            a.lo_cap, st);
+                            a.lo_cap, PM_AVG, st);
         if (e != hipSuccess) return e;
         gp.lo_pad = lp;
     }

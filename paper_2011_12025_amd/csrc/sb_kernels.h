@@ -36,8 +36,9 @@ struct ConvArgs {
 
 hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask,
                         void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t st);
+// pm: how the halo is filled (PM_AVG, PM_STRIDED, PM_ZERO of sb_pixel.h)
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
-                      const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, hipStream_t st);
+                      const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
                           const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st);
 // Device memory that a launch needs beyond its inputs and outputs, supplied
@@ -62,7 +63,7 @@ bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const v
 hipError_t launch_split_rows(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap,
                              void* lo, int lo_cap, hipStream_t st);
 hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp,
-                           void* lp, int hi_cap, int lo_cap, hipStream_t st);
+                           void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
 hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
                                int hi_cap, int lo_cap, void* y, hipStream_t st);
 

@@ -32,6 +32,14 @@ __device__ __forceinline__ Src<T> src_avg(const T* p, int d1, int d2) {
     return Src<T>{p, 1, d1, d2};
 }
 
+// How BlockPad fills a halo (the `pm` argument below): PM_AVG is BlockPad
+// with average sampling (a high neighbour's 2x2 cell averaged into a low
+// block's halo), PM_STRIDED takes that cell's top-left pixel instead
+// (strided subsampling), PM_ZERO pads every block with zeros.  A call's
+// flags carry it in bits 1-2 (SB_FLAG_PAD_STRIDED, SB_FLAG_PAD_ZERO).
+constexpr int PM_AVG = 0, PM_STRIDED = 1, PM_ZERO = 2;
+__host__ __device__ __forceinline__ int pad_mode(int flags) { return (flags >> 1) & 3; }
+
 // Element (s, c, y, x) of a block stack of extent `ext` with C channels.
 template <typename T, int L>
 __device__ __forceinline__ const T* stack_at(const T* base, int s, int C, int ext, int y, int x, int c) {
@@ -55,13 +63,14 @@ __device__ __forceinline__ const T* map_at(const T* base, int n, int C, int H, i
 // image or for a neighbour beyond its stack's capacity.
 template <typename T, int L>
 __device__ __forceinline__ Src<T> packed_src(const T* __restrict__ hi, const T* __restrict__ lo, int C, int bs,
-                                             const Neigh& nb, int hi_cap, int lo_cap, int uu, int vv, int c) {
+                                             const Neigh& nb, int hi_cap, int lo_cap, int uu, int vv, int c,
+                                             int pm = PM_AVG) {
     const int own_high = (nb.high >> 4) & 1;
     const int lb = bs >> 1, e = own_high ? bs : lb;
     const int dy = uu < 0 ? -1 : (uu >= e ? 1 : 0);
     const int dx = vv < 0 ? -1 : (vv >= e ? 1 : 0);
     const int d = (dy + 1) * 3 + (dx + 1);
-    if (!((nb.valid >> d) & 1)) return src_zero<T>();
+    if (!((nb.valid >> d) & 1) || (pm == PM_ZERO && d != 4)) return src_zero<T>();
     const int nhigh = (nb.high >> d) & 1;
     const int ns = neigh_slot(nb, d);
     if (ns >= (nhigh ? hi_cap : lo_cap)) return src_zero<T>();
@@ -69,6 +78,7 @@ __device__ __forceinline__ Src<T> packed_src(const T* __restrict__ hi, const T* 
     if (nhigh == own_high) return src_copy<T>(stack_at<T, L>(nhigh ? hi : lo, ns, C, e, u2, v2, c));
     if (own_high) return src_copy<T>(stack_at<T, L>(lo, ns, C, lb, u2 >> 1, v2 >> 1, c));
     const int px = (L == NHWC) ? C : 1;
+    if (pm == PM_STRIDED) return src_copy<T>(stack_at<T, L>(hi, ns, C, bs, 2 * u2, 2 * v2, c));
     return src_avg<T>(stack_at<T, L>(hi, ns, C, bs, 2 * u2, 2 * v2, c), px, px * bs);
 }
 
@@ -79,24 +89,32 @@ __device__ __forceinline__ Src<T> packed_src(const T* __restrict__ hi, const T* 
 // the low-resolution coordinate, whatever the neighbour's resolution (a high
 // neighbour's 2x2 average and a low neighbour's own value are both that
 // cell's average).  Zero outside the image.
+//
+// With strided sampling a low block's halo pixel whose cell lies in a high
+// neighbour is that cell's top-left image pixel; with zero padding every
+// halo pixel is zero.
 template <typename T, int L>
 __device__ __forceinline__ Src<T> dense_src(const T* __restrict__ x, int n, int C, int H, int W, int bs, int gy,
-                                            int gx, const Neigh& nb, int uu, int vv, int c) {
+                                            int gx, const Neigh& nb, int uu, int vv, int c, int pm = PM_AVG) {
     const int own_high = (nb.high >> 4) & 1;
     const int px = (L == NHWC) ? C : 1;
     const int row = px * W;
+    const int e = own_high ? bs : (bs >> 1);
+    const int dy = uu < 0 ? -1 : (uu >= e ? 1 : 0);
+    const int dx = vv < 0 ? -1 : (vv >= e ? 1 : 0);
+    const int d = (dy + 1) * 3 + (dx + 1);
+    if (pm == PM_ZERO && d != 4) return src_zero<T>();
     if (own_high) {
         const int Y = gy * bs + uu, X = gx * bs + vv;
         if (Y < 0 || Y >= H || X < 0 || X >= W) return src_zero<T>();
-        const int dy = uu < 0 ? -1 : (uu >= bs ? 1 : 0);
-        const int dx = vv < 0 ? -1 : (vv >= bs ? 1 : 0);
-        const int d = (dy + 1) * 3 + (dx + 1);
         if ((nb.high >> d) & 1) return src_copy<T>(map_at<T, L>(x, n, C, H, W, Y, X, c));
         return src_avg<T>(map_at<T, L>(x, n, C, H, W, Y & ~1, X & ~1, c), px, row);
     }
     const int lb = bs >> 1;
     const int Yl = gy * lb + uu, Xl = gx * lb + vv;
     if (Yl < 0 || 2 * Yl >= H || Xl < 0 || 2 * Xl >= W) return src_zero<T>();
+    if (pm == PM_STRIDED && d != 4 && ((nb.high >> d) & 1))
+        return src_copy<T>(map_at<T, L>(x, n, C, H, W, 2 * Yl, 2 * Xl, c));
     return src_avg<T>(map_at<T, L>(x, n, C, H, W, 2 * Yl, 2 * Xl, c), px, row);
 }
 

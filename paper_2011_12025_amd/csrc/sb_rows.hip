@@ -256,14 +256,14 @@ constexpr int PADM = 5;   // vectors per lane and pass (up to four loads each)
 template <typename T>
 __device__ __forceinline__ const T* pad_row_source(const T* __restrict__ hi, const T* __restrict__ lo, int C, int bs,
                                                    const Neigh& nb, bool high, int hi_cap, int lo_cap, int u,
-                                                   int& kind) {
+                                                   int pm, int& kind) {
     const int lb = bs >> 1, e = high ? bs : lb;
     const int r = u - 1;
     const int dy = r < 0 ? 0 : (r >= e ? 2 : 1), dn = dy * 3 + 1;
     const int nhigh = (nb.high >> dn) & 1;
     const int ns = neigh_slot(nb, dn);
     kind = 0;
-    if (!((nb.valid >> dn) & 1) || ns >= (nhigh ? hi_cap : lo_cap)) return nullptr;
+    if (!((nb.valid >> dn) & 1) || ns >= (nhigh ? hi_cap : lo_cap) || (pm == PM_ZERO && dy != 1)) return nullptr;
     const int u2 = r - (dy - 1) * e;
     if (nhigh == (int)high) {
         kind = 1;
@@ -273,7 +273,7 @@ __device__ __forceinline__ const T* pad_row_source(const T* __restrict__ hi, con
         kind = 2;
         return lo + ((size_t)(ns * lb + (u2 >> 1)) * lb) * C;
     }
-    kind = 3;
+    kind = pm == PM_STRIDED ? 4 : 3;  // every other pixel of the even row, averaged with the next ones or not
     return hi + ((size_t)(ns * bs + 2 * u2) * bs) * C;
 }
 
@@ -281,7 +281,7 @@ template <typename T, bool ONE>
 __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, const T* __restrict__ lo, int C,
                                                  const uint8_t* __restrict__ mask, int bs, int B, int GH, int GW,
                                                  int per_wave, T* __restrict__ hp, T* __restrict__ lp, int hi_cap,
-                                                 int lo_cap) {
+                                                 int lo_cap, int pm) {
     constexpr int V = 16 / (int)sizeof(T);
     const int lane = lane_id();
     const int CV = C / V, lb = bs >> 1, ph = lb + 2, ex = bs - lb;
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
         if (s >= (high ? hi_cap : lo_cap) || (high && !hp)) continue;
         const int e = high ? bs : lb, pe = e + 2, nv = pe * CV;
         int kind;
-        const T* row = pad_row_source<T>(hi, lo, C, bs, nb, high, hi_cap, lo_cap, u, kind);
+        const T* row = pad_row_source<T>(hi, lo, C, bs, nb, high, hi_cap, lo_cap, u, pm, kind);
         T* d = (high ? hp : lp) + ((size_t)(s * pe + u) * pe) * C;
         for (int ib = 0; ib < nv; ib += 64 * PADM) {
             uint4 v[PADM][4];
@@ -358,7 +358,8 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
                     bool avg = false;
                     int d1c = C, d2c = bs * C;
                     if (w == 0 || w == pe - 1) {
-                        const Src<T> sp = packed_src<T, NHWC>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, w - 1, c);
+                        const Src<T> sp =
+                            packed_src<T, NHWC>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, w - 1, c, pm);
                         src = sp.p;
                         avg = sp.avg;
                         d1c = sp.d1;
@@ -367,9 +368,9 @@ __global__ __launch_bounds__(WG, 4) void k_pad_rows(const T* __restrict__ hi, co
                         src = row + (w - 1) * C + c;
                     } else if (kind == 2) {
                         src = row + ((w - 1) >> 1) * C + c;
-                    } else if (kind == 3) {
+                    } else if (kind >= 3) {
                         src = row + 2 * (w - 1) * C + c;
-                        avg = true;
+                        avg = kind == 3;
                     }
                     if (!src) {
                         mode[m] = 0;
@@ -424,13 +425,13 @@ hipError_t combine_rows(const Geo& g, const void* hi, const void* lo, const uint
 
 template <typename T, bool ONE>
 hipError_t pad_rows(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                    int hi_cap, int lo_cap, hipStream_t st) {
+                    int hi_cap, int lo_cap, int pm, hipStream_t st) {
     const long long jobs = g.B * (g.bs / 2 + 2) + (hp ? (long long)hi_cap * (g.bs - g.bs / 2) : 0LL);
     const int grid = rows_grid(jobs);
     const long long waves = (long long)grid * RW_WAVES;
     const int per_wave = (int)((jobs + waves - 1) / waves);
     hipLaunchKernelGGL((k_pad_rows<T, ONE>), dim3(grid), dim3(WG), 0, st, (const T*)hi, (const T*)lo, g.C, mask,
-                       g.bs, (int)g.B, g.GH, g.GW, per_wave, (T*)hp, (T*)lp, hi_cap, lo_cap);
+                       g.bs, (int)g.B, g.GH, g.GW, per_wave, (T*)hp, (T*)lp, hi_cap, lo_cap, pm);
     return hipGetLastError();
 }
 
@@ -448,9 +449,9 @@ hipError_t combine_rows_t(const Geo& g, const void* hi, const void* lo, const ui
 }
 template <typename T>
 hipError_t pad_rows_t(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                      int hi_cap, int lo_cap, hipStream_t st) {
-    return g.B <= 1024 ? pad_rows<T, true>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st)
-                       : pad_rows<T, false>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+                      int hi_cap, int lo_cap, int pm, hipStream_t st) {
+    return g.B <= 1024 ? pad_rows<T, true>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st)
+                       : pad_rows<T, false>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
 }
 
 inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -485,11 +486,11 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
 }
 
 hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp,
-                           void* lp, int hi_cap, int lo_cap, hipStream_t st) {
+                           void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st) {
     switch (dtype) {
-    case 0: return pad_rows_t<float>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
-    case 1: return pad_rows_t<f16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
-    default: return pad_rows_t<bf16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, st);
+    case 0: return pad_rows_t<float>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    case 1: return pad_rows_t<f16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    default: return pad_rows_t<bf16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     }
 }
 

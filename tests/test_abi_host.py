@@ -85,18 +85,26 @@ def test_conv_and_layer_validation(lib):
                               ctypes.c_void_p(0x78000000), 1, 0, None)
     assert r == -2 and "256" in lib.segblocks_last_error().decode()
     # missing weight
-    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, NULL, NULL, 8, ctypes.c_void_p(0x50000000), NULL, 0,
-                            None)
+    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, NULL, NULL, 8, 0, ctypes.c_void_p(0x50000000), NULL,
+                            0, None)
     assert r == -1 and "weight" in lib.segblocks_last_error().decode()
     # output aliasing the input
-    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, ctypes.c_void_p(0x60000000), NULL, 8, FAKE, NULL, 0,
-                            None)
+    r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, ctypes.c_void_p(0x60000000), NULL, 8, 0, FAKE, NULL,
+                            0, None)
     assert r == -1 and "overlap" in lib.segblocks_last_error().decode()
     # unknown flag on the fused-pad convolution
-    r = lib.segblocks_block_conv3x3(FAKE, FAKE2, 1, 1, 1, 8, 32, 32, ctypes.c_void_p(0x30000000), 16,
-                                    ctypes.c_void_p(0x60000000), NULL, 8, 4, NULL, NULL,
-                                    ctypes.c_void_p(0x70000000), ctypes.c_void_p(0x78000000), 1, 3, NULL, 0, None)
-    assert r == -1 and "flags" in lib.segblocks_last_error().decode()
+    for flags, msg in [(8, "unknown flags"), (6, "exclude each other")]:
+        r = lib.segblocks_block_conv3x3(FAKE, FAKE2, 1, 1, 1, 8, 32, 32, ctypes.c_void_p(0x30000000), 16,
+                                        ctypes.c_void_p(0x60000000), NULL, 8, flags, NULL, NULL,
+                                        ctypes.c_void_p(0x70000000), ctypes.c_void_p(0x78000000), 1, 3, NULL, 0, None)
+        assert r == -1 and msg in lib.segblocks_last_error().decode()
+        r = lib.segblocks_layer(FAKE, 1, 1, 1, 8, 32, 32, FAKE2, 16, ctypes.c_void_p(0x60000000), NULL, 8, flags,
+                                ctypes.c_void_p(0x50000000), NULL, 0, None)
+        assert r == -1 and msg in lib.segblocks_last_error().decode()
+    # pad_ex: sampling outside the three choices
+    r = lib.segblocks_pad_ex(FAKE, FAKE2, 1, 1, 1, 8, 32, 32, ctypes.c_void_p(0x30000000), 16,
+                             ctypes.c_void_p(0x40000000), ctypes.c_void_p(0x48000000), 1, 3, 3, None)
+    assert r == -1 and "sampling" in lib.segblocks_last_error().decode()
 
 
 def test_pad_combine_count_validation(lib):
@@ -117,10 +125,11 @@ def _ws_query(lib, fn, *args):
 
 
 def test_workspace_size_queries(lib):
-    """The sizes depend on the route the shapes take: none for the resident
-    convolution (64 channels, blocks of 32), split-K partials for the deep
-    stages, the packed stacks for a fused layer with 512 channels."""
-    r, n = _ws_query(lib, "segblocks_block_conv3x3_workspace_size", 1, 1, 1, 64, 256, 512, 32, 64, 128, 128)
+    """The sizes depend on the route the shapes take: none for a fused layer
+    on the resident convolution (64 channels, blocks of 32), split-K partials
+    for the deep stages, the packed stacks for a fused layer with 512
+    channels."""
+    r, n = _ws_query(lib, "segblocks_layer_workspace_size", 1, 1, 1, 64, 256, 512, 32, 64)
     assert r == 0 and n == 0
     r, n = _ws_query(lib, "segblocks_block_conv_ex_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 1, 128, 128)
     assert r == 0 and n > 0 and n % 256 == 0
@@ -157,7 +166,7 @@ def test_calls_reject_missing_or_small_workspace(lib):
     assert "overlap" in lib.segblocks_last_error().decode()
     # the fused layer with 512 channels takes its packed stacks from the workspace
     _, lneed = _ws_query(lib, "segblocks_layer_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512)
-    largs = [P(base), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL, 512,
+    largs = [P(base), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL, 512, 0,
              P(base + 0x4000000)]
     assert lib.segblocks_layer(*largs, P(ws), lneed // 2, None) == b.SB_ENOMEM
     # block_conv3x3 at a deep-stage shape
