@@ -71,6 +71,8 @@ def _L():
                                        ctypes.c_int, _fp, ctypes.c_int, _dp]
         lib.orc_conv_dense.argtypes = [_fp] + [ctypes.c_int] * 4 + [_fp] + [ctypes.c_int] * 3 + [_fp, ctypes.c_int, _dp]
         lib.orc_maxpool.argtypes = [_fp] + [ctypes.c_int] * 7 + [_fp]
+        lib.orc_policy_scores.argtypes = [_fp] + [ctypes.c_int] * 6 + [_dp]
+        lib.orc_policy_select.argtypes = [_dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _u8p]
         _lib = lib
     return _lib
 
@@ -322,3 +324,40 @@ def encoder(x, mask, image_block: int, weights: dict, dtype: str):
             hi, lo = block_conv_ex(h1[0], h1[1], mask, bs, H, W, weights[p + "c2.w"], weights[p + "c2.b"], 1, dtype,
                                    relu=True, residual=sc)
     return combine(hi, lo, mask, bs, H, W)
+
+
+# ---------------------------------------------------------------------------
+# Heuristic downsampling policy (test infrastructure)
+# ---------------------------------------------------------------------------
+
+def policy_scores(x, bs: int, dtype: str):
+    """Per-block detail score [N, H/bs, W/bs] (fp64): the block's pixels'
+    Euclidean distance over channels to its low-resolution version, averaged."""
+    x = _f32(x)
+    N, C, H, W = x.shape
+    if bs < 2 or bs % 2 or H % bs or W % bs:
+        raise ValueError("block size must be even and divide H and W")
+    out = np.zeros((N, H // bs, W // bs), np.float64)
+    _L().orc_policy_scores(_ptr(x, _fp), N, C, H, W, bs, _DT[dtype], _ptr(out, _dp))
+    return out
+
+
+def policy_k(tau_high: float, blocks_per_image: int) -> int:
+    """High-resolution blocks per image for a target fraction tau."""
+    return int(np.floor(tau_high * blocks_per_image + 0.5))
+
+
+def policy_select(scores, tau_high: float):
+    """Mask [N, GH, GW] (1 = high): per image the round(tau * GH * GW) blocks
+    with the highest scores, equal scores ranked by block id."""
+    sc = np.ascontiguousarray(scores, dtype=np.float64)
+    N, GH, GW = sc.shape
+    mask = np.zeros((N, GH, GW), np.uint8)
+    _L().orc_policy_select(_ptr(sc, _dp), N, GH * GW, policy_k(tau_high, GH * GW), _ptr(mask, _u8p))
+    return mask
+
+
+def policy(x, bs: int, tau_high: float, dtype: str):
+    """The heuristic policy: (mask, scores)."""
+    sc = policy_scores(x, bs, dtype)
+    return policy_select(sc, tau_high), sc

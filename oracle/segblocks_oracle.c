@@ -399,3 +399,56 @@ void orc_combine(const float* hi, const float* lo, int N, int C, int H, int W,
         if (mask[k]) ++nh; else ++nl;
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Heuristic downsampling policy (the earlier short paper's policy, which    */
+/* the ablation on execution policies compares with): a block's score is     */
+/* how much detail its low-resolution version loses.                         */
+/* ------------------------------------------------------------------------ */
+
+/* x[N][C][H][W] -> score[N][GH][GW] (fp64): for every pixel of the block the
+ * Euclidean distance over the channels between the pixel and the block's
+ * low-resolution version at that pixel (the 2x2 average of its cell, as
+ * BlockSample computes and rounds it, nearest-upsampled), averaged over the
+ * block's bs*bs pixels. */
+void orc_policy_scores(const float* x, int N, int C, int H, int W, int bs, int dtype, double* score)
+{
+    const int GH = H / bs, GW = W / bs;
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        double total = 0.0;
+        for (int i = 0; i < bs; ++i)
+        for (int j = 0; j < bs; ++j) {
+            const int Y = gy * bs + i, X = gx * bs + j;
+            const int Y0 = Y & ~1, X0 = X & ~1;     /* the 2x2 cell containing the pixel */
+            double d2 = 0.0;
+            for (int c = 0; c < C; ++c) {
+                const float* img = x + ((long)n * C + c) * H * (long)W;
+                const float m = orc_avg4(img[(long)Y0 * W + X0], img[(long)Y0 * W + X0 + 1],
+                                         img[(long)(Y0 + 1) * W + X0], img[(long)(Y0 + 1) * W + X0 + 1], dtype);
+                const double d = (double)img[(long)Y * W + X] - (double)m;
+                d2 += d * d;
+            }
+            total += sqrt(d2);
+        }
+        score[((long)n * GH + gy) * GW + gx] = total / ((double)bs * bs);
+    }
+}
+
+/* score[N][B] -> mask[N][B]: per image, the k blocks with the highest scores
+ * are high resolution (1), the others low (0); equal scores are ranked by
+ * block id, lower first. */
+void orc_policy_select(const double* score, int N, int B, int k, uint8_t* mask)
+{
+    for (int n = 0; n < N; ++n)
+        for (int b = 0; b < B; ++b) {
+            const double s = score[(long)n * B + b];
+            int rank = 0;  /* blocks ahead of b in the order */
+            for (int j = 0; j < B; ++j) {
+                const double t = score[(long)n * B + j];
+                if (t > s || (t == s && j < b)) ++rank;
+            }
+            mask[(long)n * B + b] = rank < k ? 1 : 0;
+        }
+}
