@@ -253,6 +253,24 @@ int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_i
 int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
                                    int C_out, size_t* bytes);
 
+/* Heuristic downsampling policy (the policy of the short paper SegBlocks
+ * extends, compared with in Experiments > Ablation studies, execution
+ * policies): it selects the blocks where half resolution loses the most
+ * detail.  x [N,C,H,W] (the image or a feature map) ->
+ *   score [N][H/bs][W/bs] (fp32, device): for every pixel of the block the
+ *     Euclidean distance over the channels between the pixel and the
+ *     block's low-resolution version there (the BlockSample 2x2 average of
+ *     its cell), averaged over the block's pixels;
+ *   mask [N][H/bs][W/bs] (uint8, device): per image the
+ *     k = floor(tau_high * GH * GW + 0.5) blocks with the highest scores are
+ *     high resolution (1), the rest low (0); equal scores rank by block id,
+ *     lower first.
+ * tau_high in [0, 1] is the high-resolution fraction (the paper's target
+ * tau).  At most 8192 blocks per image.  Any dtype and layout. */
+int segblocks_policy_heuristic(const void* x, int dtype, int layout, int N, int C, int H, int W,
+                               int bs, double tau_high, float* score, uint8_t* mask,
+                               hipStream_t stream);
+
 /* Dense convolution around the block stages (the encoder's 7x7/2 stem):
  * x [N,C_in,H,W] -> y [N,C_out,Ho,Wo], Ho = (H + 2 pad - K) / stride + 1,
  *   y = bias + sum w * x (zero padding), then max(0, .) if SB_FLAG_RELU.

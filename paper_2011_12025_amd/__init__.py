@@ -20,7 +20,7 @@ from . import _binding as _b
 
 __all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "block_conv_ex", "layer", "conv2d",
            "maxpool", "layout_of", "block_conv3x3_workspace_size", "block_conv_ex_workspace_size",
-           "layer_workspace_size"]
+           "layer_workspace_size", "policy_heuristic"]
 
 _DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
 
@@ -324,3 +324,23 @@ def maxpool(x: torch.Tensor, k: int = 3, stride: int = 2, padding: int = 1, out=
     y = _empty((N, C, Ho, Wo), x, layout) if out is None else out
     _b.call("segblocks_maxpool", _ptr(x), _dt(x), layout, N, C, H, W, k, stride, padding, _ptr(y), _stream(x))
     return y
+
+
+def policy_heuristic(x: torch.Tensor, bs: int, tau_high: float, layout=None, out=None):
+    """Heuristic downsampling policy: returns (mask [N, H/bs, W/bs] uint8,
+    1 = high resolution, score [N, H/bs, W/bs] float32).  Per image the
+    round(tau_high * blocks) blocks whose low-resolution version loses the
+    most detail are high resolution."""
+    layout = layout_of(x) if layout is None else layout
+    _check_layout(layout, x)
+    N, C, H, W = x.shape
+    if H % bs or W % bs:
+        raise ValueError("bs must divide H and W")
+    if out is None:
+        mask = torch.empty((N, H // bs, W // bs), dtype=torch.uint8, device=x.device)
+        score = torch.empty((N, H // bs, W // bs), dtype=torch.float32, device=x.device)
+    else:
+        mask, score = out
+    _b.call("segblocks_policy_heuristic", _ptr(x), _dt(x), layout, N, C, H, W, bs, float(tau_high), _ptr(score),
+            _ptr(mask), _stream(x))
+    return mask, score

@@ -23,7 +23,8 @@ SB_PAD_AVG, SB_PAD_STRIDED, SB_PAD_ZERO = 0, 1, 2
 EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_pad_ex", "segblocks_conv3x3", "segblocks_combine",
            "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
            "segblocks_maxpool", "segblocks_block_conv3x3_workspace_size", "segblocks_block_conv_ex_workspace_size",
-           "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_last_error"]
+           "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_policy_heuristic",
+           "segblocks_last_error"]
 
 SB_OK, SB_EINVAL, SB_ESHAPE, SB_EHIP, SB_ENOMEM = 0, -1, -2, -3, -4
 
@@ -45,6 +46,7 @@ _SIGS = {
                                 _I, _I, _P, _Z, _P],
     "segblocks_block_conv_ex_noalloc": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P,
                                         _P, _I, _I, _P],
+    "segblocks_policy_heuristic": [_P, _I, _I, _I, _I, _I, _I, _I, ctypes.c_double, _P, _P, _P],
     "segblocks_block_conv3x3_workspace_size": [_I] * 10 + [_ZP],
     "segblocks_block_conv_ex_workspace_size": [_I] * 12 + [_ZP],
     "segblocks_layer_workspace_size": [_I] * 8 + [_ZP],

@@ -4,6 +4,7 @@
 // comes from the caller's workspace argument, whose size the *_workspace_size
 // queries give; nothing touches the GPU before every argument, the workspace
 // included, has been checked.
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 
@@ -466,6 +467,25 @@ int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H
     *bytes = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
     g_err.clear();
     return SB_OK;
+}
+
+int segblocks_policy_heuristic(const void* x, int dtype, int layout, int N, int C, int H, int W, int bs,
+                               double tau_high, float* score, uint8_t* mask, hipStream_t stream) {
+    const char* fn = "segblocks_policy_heuristic";
+    static const uint8_t any = 0;
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, &any, bs, g))) return s;
+    if (!x || !score || !mask) return fail(SB_EINVAL, fn, "x, score or mask is NULL");
+    if (!(tau_high >= 0.0 && tau_high <= 1.0)) return fail(SB_EINVAL, fn, "tau_high must be in [0, 1]");
+    const int per = g.GH * g.GW;
+    if (per > sb::policy_max_blocks())
+        return fail(SB_ESHAPE, fn, "at most %d blocks per image (got %d)", sb::policy_max_blocks(), per);
+    const long long es = esize(dtype);
+    const Range rx{x, (long long)N * C * H * W * es}, rs{score, g.B * 4}, rm{mask, g.B};
+    if (any_overlap({rs, rm}, {rx})) return fail(SB_EINVAL, fn, "score or mask overlaps x, or each other");
+    const int khigh = (int)floor(tau_high * per + 0.5);
+    return hip_status(fn, sb::launch_policy(dtype, layout, x, N, C, H, W, bs, score, khigh, mask, stream));
 }
 
 int segblocks_conv2d(const void* x, int dtype, int layout, int N, int C_in, int H, int W, const void* weight,

@@ -87,6 +87,12 @@ hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W
 hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, int K, int S, int P, void* y,
                           hipStream_t st);
 
+// Heuristic downsampling policy: per-block scores [N*GH*GW] (fp32), then the
+// mask with khigh high blocks per image (at most policy_max_blocks() per image).
+int policy_max_blocks();
+hipError_t launch_policy(int dtype, int layout, const void* x, int N, int C, int H, int W, int bs, float* score,
+                         int khigh, uint8_t* mask, hipStream_t st);
+
 // Persistent convolution with LDS-resident weights (channels-last fp16/bf16,
 // C_in <= 64, blocks of 32 or 64); conv_res_fits tells whether it applies,
 // conv_res_fits_shape the same without the pointer alignment.
