@@ -71,6 +71,12 @@ def _L():
                                        ctypes.c_int, _fp, ctypes.c_int, _dp]
         lib.orc_conv_dense.argtypes = [_fp] + [ctypes.c_int] * 4 + [_fp] + [ctypes.c_int] * 3 + [_fp, ctypes.c_int, _dp]
         lib.orc_maxpool.argtypes = [_fp] + [ctypes.c_int] * 7 + [_fp]
+        lib.orc_combine_bwd.argtypes = [_fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp, _fp]
+        lib.orc_split_bwd.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p, ctypes.c_int, ctypes.c_int, _fp]
+        lib.orc_pad_bwd.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p] + [ctypes.c_int] * 3 + [_fp, _fp]
+        lib.orc_conv3x3_bwd_data.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, _fp, ctypes.c_int, _dp]
+        lib.orc_conv3x3_bwd_weight.argtypes = [_fp, _fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                               _dp, _dp]
         lib.orc_policy_scores.argtypes = [_fp] + [ctypes.c_int] * 6 + [_dp]
         lib.orc_policy_select.argtypes = [_dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _u8p]
         _lib = lib
@@ -361,3 +367,101 @@ def policy(x, bs: int, tau_high: float, dtype: str):
     """The heuristic policy: (mask, scores)."""
     sc = policy_scores(x, bs, dtype)
     return policy_select(sc, tau_high), sc
+
+
+# ---------------------------------------------------------------------------
+# Backward pass of the block modules and the block convolution
+# ---------------------------------------------------------------------------
+
+def _counts(mask):
+    m = np.asarray(mask) != 0
+    return int(m.sum()), int(m.size - m.sum())
+
+
+def combine_backward(dy, mask, bs: int, dtype: str):
+    """BlockCombine transposed: dy[N,C,H,W] -> (dhi, dlo); a low pixel gets the
+    fp32 sum of its 2x2 cell's gradients, rounded."""
+    dy = _f32(dy)
+    N, C, H, W = dy.shape
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    _check_shape(mask, N, H, W, bs)
+    nh, nl = _counts(mask)
+    dhi = np.zeros((nh, C, bs, bs), np.float32)
+    dlo = np.zeros((nl, C, bs // 2, bs // 2), np.float32)
+    _L().orc_combine_bwd(_ptr(dy, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype], _ptr(dhi, _fp),
+                         _ptr(dlo, _fp))
+    return dhi, dlo
+
+
+def split_backward(dhi, dlo, mask, bs: int, H: int, W: int, dtype: str):
+    """BlockSample transposed: (dhi, dlo) -> dx[N,C,H,W]."""
+    dhi, dlo = _f32(dhi), _f32(dlo)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    N = mask.shape[0]
+    _check_shape(mask, N, H, W, bs)
+    C = dhi.shape[1] if dhi.shape[0] else dlo.shape[1]
+    dx = np.zeros((N, C, H, W), np.float32)
+    _L().orc_split_bwd(_ptr(dhi, _fp), _ptr(dlo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype], _ptr(dx, _fp))
+    return dx
+
+
+def pad_backward(dhp, dlp, mask, bs: int, H: int, W: int, dtype: str, sampling: str = "avg"):
+    """BlockPad transposed: (dhp, dlp) -> (dhi, dlo), accumulated in fp64, rounded."""
+    dhp, dlp = _f32(dhp), _f32(dlp)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    N = mask.shape[0]
+    _check_shape(mask, N, H, W, bs)
+    C = dhp.shape[1] if dhp.shape[0] else dlp.shape[1]
+    nh, nl = dhp.shape[0], dlp.shape[0]
+    dhi = np.zeros((nh, C, bs, bs), np.float32)
+    dlo = np.zeros((nl, C, bs // 2, bs // 2), np.float32)
+    _L().orc_pad_bwd(_ptr(dhp, _fp), _ptr(dlp, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
+                     SAMPLING[sampling], _ptr(dhi, _fp), _ptr(dlo, _fp))
+    return dhi, dlo
+
+
+def conv3x3_backward_data(dO, w):
+    """Gradient of conv3x3_valid with respect to the padded input (fp64, unrounded)."""
+    dO, w = _f32(dO), _f32(w)
+    S, Cout, E, E2 = dO.shape
+    Cout2, Cin, k1, k2 = w.shape
+    assert E == E2 and Cout2 == Cout and (k1, k2) == (3, 3)
+    dP = np.zeros((S, Cin, E + 2, E + 2), np.float64)
+    if S:
+        _L().orc_conv3x3_bwd_data(_ptr(dO, _fp), S, Cout, E, _ptr(w, _fp), Cin, _ptr(dP, _dp))
+    return dP
+
+
+def conv3x3_backward_weight(stacks, with_bias: bool = True):
+    """Gradient with respect to weight and bias over several (P, dO) stacks
+    (padded input, output gradient): (dw [Cout,Cin,3,3], db [Cout]) in fp64."""
+    dw = db = None
+    for P, dO in stacks:
+        P, dO = _f32(P), _f32(dO)
+        S, Cin, pe, _ = P.shape
+        S2, Cout, E, _ = dO.shape
+        assert S2 == S and pe == E + 2
+        if dw is None:
+            dw = np.zeros((Cout, Cin, 3, 3), np.float64)
+            db = np.zeros(Cout, np.float64)
+        if S:
+            _L().orc_conv3x3_bwd_weight(_ptr(P, _fp), _ptr(dO, _fp), S, Cin, Cout, E, _ptr(dw, _dp),
+                                        _ptr(db, _dp) if with_bias else None)
+    return dw, (db if with_bias else None)
+
+
+def layer_backward(x, mask, bs: int, w, b, dy, dtype: str, sampling: str = "avg"):
+    """Gradients of one block-conv layer y = combine(conv3x3(pad(split(x)))):
+    (dx, dw, db).  Every stored gradient is rounded to the storage type where
+    the GPU stores it (output-block gradients, padded-stack gradients, block
+    gradients, dx); dw and db are returned unrounded (fp64)."""
+    x = _f32(x)
+    N, C, H, W = x.shape
+    hi, lo = split(x, mask, bs, dtype)
+    hp, lp = pad(hi, lo, mask, bs, H, W, dtype, sampling)
+    dho, dlo_o = combine_backward(dy, mask, bs, dtype)
+    dw, db = conv3x3_backward_weight([(hp, dho), (lp, dlo_o)], with_bias=b is not None)
+    dhp = round_to(conv3x3_backward_data(dho, w), dtype)
+    dlp = round_to(conv3x3_backward_data(dlo_o, w), dtype)
+    dhi, dlo = pad_backward(dhp, dlp, mask, bs, H, W, dtype, sampling)
+    return split_backward(dhi, dlo, mask, bs, H, W, dtype), dw, db

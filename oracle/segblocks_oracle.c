@@ -452,3 +452,202 @@ void orc_policy_select(const double* score, int N, int B, int k, uint8_t* mask)
             mask[(long)n * B + b] = rank < k ? 1 : 0;
         }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Backward pass of the block modules and of the block convolution: the     */
+/* transposes of the linear maps above (the paper notes the modules serve    */
+/* training as well as inference).  Gradients are stored in the storage      */
+/* type like the forward values.                                             */
+/* ------------------------------------------------------------------------ */
+
+/* BlockCombine transposed: dy[N][C][H][W] -> dhi[nh][C][bs][bs] (copy of the
+ * block's gradient) and dlo[nl][C][lb][lb] (the sum of the 2x2 cell of
+ * gradients that the low pixel was copied to), summed in fp32 as
+ * ((a + b) + (c + d)) with a, b the top pixels, rounded once. */
+void orc_combine_bwd(const float* dy, int N, int C, int H, int W, const uint8_t* mask, int bs, int dtype,
+                     float* dhi, float* dlo)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    long nh = 0, nl = 0;
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        for (int c = 0; c < C; ++c) {
+            const float* img = dy + ((long)n * C + c) * H * W;
+            if (mask[k]) {
+                for (int i = 0; i < bs; ++i)
+                    for (int j = 0; j < bs; ++j)
+                        dhi[((nh * C + c) * bs + i) * (long)bs + j] = img[(long)(gy * bs + i) * W + gx * bs + j];
+            } else {
+                for (int i = 0; i < lb; ++i)
+                    for (int j = 0; j < lb; ++j) {
+                        const long r0 = (long)(gy * bs + 2 * i) * W + gx * bs + 2 * j;
+                        const float sum = (img[r0] + img[r0 + 1]) + (img[r0 + W] + img[r0 + W + 1]);
+                        dlo[((nl * C + c) * lb + i) * (long)lb + j] = (float)orc_round((double)sum, dtype);
+                    }
+            }
+        }
+        if (mask[k]) ++nh; else ++nl;
+    }
+}
+
+/* BlockSample transposed: dhi, dlo -> dx[N][C][H][W]: a high block's
+ * gradient copied back; a low pixel's gradient times 0.25 (its share of the
+ * average) on each pixel of its cell, rounded. */
+void orc_split_bwd(const float* dhi, const float* dlo, int N, int C, int H, int W, const uint8_t* mask, int bs,
+                   int dtype, float* dx)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    long nh = 0, nl = 0;
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        for (int c = 0; c < C; ++c) {
+            float* img = dx + ((long)n * C + c) * H * W;
+            for (int i = 0; i < bs; ++i)
+                for (int j = 0; j < bs; ++j) {
+                    float v;
+                    if (mask[k]) v = dhi[((nh * C + c) * bs + i) * (long)bs + j];
+                    else v = (float)orc_round(0.25 * (double)dlo[((nl * C + c) * lb + (i >> 1)) * (long)lb + (j >> 1)],
+                                              dtype);
+                    img[(long)(gy * bs + i) * W + gx * bs + j] = v;
+                }
+        }
+        if (mask[k]) ++nh; else ++nl;
+    }
+}
+
+/* BlockPad transposed: dhp[nh][C][bs+2][bs+2], dlp[nl][C][lb+2][lb+2]
+ * -> dhi, dlo.  Every padded pixel hands its gradient back to the pixels
+ * orc_pad_ex read it from: the block's own pixel (interior), the neighbour's
+ * pixel at equal resolution, the low neighbour's pixel a high block's halo
+ * nearest-upsampled, the 2x2 cell of a high neighbour a low block's halo
+ * averaged (a quarter to each; all of it to the top-left pixel with strided
+ * sampling); zero-padding and the image border read nothing.  Accumulated in
+ * fp64 in block order, then rounded. */
+void orc_pad_bwd(const float* dhp, const float* dlp, int N, int C, int H, int W, const uint8_t* mask, int bs,
+                 int dtype, int sampling, float* dhi, float* dlo)
+{
+    const int GH = H / bs, GW = W / bs, lb = bs / 2;
+    const long B = (long)N * GH * GW;
+    int32_t* slot = (int32_t*)malloc(sizeof(int32_t) * (size_t)(B > 0 ? B : 1));
+    int32_t counts[2];
+    orc_plan(mask, B, slot, NULL, NULL, counts);
+    const long nhi = (long)counts[0] * C * bs * bs, nlo = (long)counts[1] * C * lb * lb;
+    double* ah = (double*)calloc((size_t)(nhi > 0 ? nhi : 1), sizeof(double));
+    double* al = (double*)calloc((size_t)(nlo > 0 ? nlo : 1), sizeof(double));
+    for (int n = 0; n < N; ++n)
+    for (int gy = 0; gy < GH; ++gy)
+    for (int gx = 0; gx < GW; ++gx) {
+        const long k = ((long)n * GH + gy) * GW + gx;
+        const int high = mask[k] != 0;
+        const int e = high ? bs : lb, pe = e + 2;
+        const float* g = high ? dhp + (long)slot[k] * C * pe * pe : dlp + (long)slot[k] * C * pe * pe;
+        for (int c = 0; c < C; ++c)
+        for (int u = -1; u <= e; ++u)
+        for (int v = -1; v <= e; ++v) {
+            const double gv = (double)g[((long)c * pe + (u + 1)) * pe + (v + 1)];
+            const int dy = u < 0 ? -1 : (u >= e ? 1 : 0);
+            const int dx = v < 0 ? -1 : (v >= e ? 1 : 0);
+            if (dy == 0 && dx == 0) {
+                double* own = high ? ah + (long)slot[k] * C * bs * bs : al + (long)slot[k] * C * lb * lb;
+                own[((long)c * e + u) * e + v] += gv;
+                continue;
+            }
+            if (sampling == ORC_PAD_ZERO) continue;
+            const int ny = gy + dy, nx = gx + dx;
+            if (ny < 0 || ny >= GH || nx < 0 || nx >= GW) continue;
+            const long nk = ((long)n * GH + ny) * GW + nx;
+            const int nhigh = mask[nk] != 0;
+            const int u2 = u - dy * e, v2 = v - dx * e;
+            if (nhigh && high) {
+                ah[(((long)slot[nk] * C + c) * bs + u2) * bs + v2] += gv;
+            } else if (!nhigh && !high) {
+                al[(((long)slot[nk] * C + c) * lb + u2) * lb + v2] += gv;
+            } else if (high) {
+                al[(((long)slot[nk] * C + c) * lb + (u2 >> 1)) * lb + (v2 >> 1)] += gv;
+            } else {
+                double* q = ah + ((long)slot[nk] * C + c) * bs * bs;
+                const int r = 2 * u2, s = 2 * v2;
+                if (sampling == ORC_PAD_STRIDED) {
+                    q[r * bs + s] += gv;
+                } else {
+                    q[r * bs + s] += 0.25 * gv;
+                    q[r * bs + s + 1] += 0.25 * gv;
+                    q[(r + 1) * bs + s] += 0.25 * gv;
+                    q[(r + 1) * bs + s + 1] += 0.25 * gv;
+                }
+            }
+        }
+    }
+    orc_round_array(ah, dhi, nhi, dtype);
+    orc_round_array(al, dlo, nlo, dtype);
+    free(ah);
+    free(al);
+    free(slot);
+}
+
+/* Gradient of the 3x3 valid block convolution with respect to its padded
+ * input: dO[S][Cout][E][E], w[Cout][Cin][3][3] -> dP[S][Cin][E+2][E+2] (fp64):
+ *   dP[s][ci][u][v] = sum_co sum_ky sum_kx w[co][ci][ky][kx] * dO[s][co][u-ky][v-kx]
+ * over the (u-ky, v-kx) inside the block, in the order co, ky, kx. */
+void orc_conv3x3_bwd_data(const float* dO, long S, int Cout, int E, const float* w, int Cin, double* dP)
+{
+    const int pe = E + 2;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (long s = 0; s < S; ++s)
+    for (int ci = 0; ci < Cin; ++ci)
+    for (int u = 0; u < pe; ++u)
+    for (int v = 0; v < pe; ++v) {
+        double acc = 0.0;
+        for (int co = 0; co < Cout; ++co) {
+            const float* g = dO + ((s * Cout + co) * E) * (long)E;
+            const float* wk = w + ((long)co * Cin + ci) * 9;
+            for (int ky = 0; ky < 3; ++ky) {
+                const int i = u - ky;
+                if (i < 0 || i >= E) continue;
+                for (int kx = 0; kx < 3; ++kx) {
+                    const int j = v - kx;
+                    if (j < 0 || j >= E) continue;
+                    acc += (double)wk[ky * 3 + kx] * (double)g[i * E + j];
+                }
+            }
+        }
+        dP[((s * Cin + ci) * pe + u) * (long)pe + v] = acc;
+    }
+}
+
+/* Gradient with respect to the weights and the bias, accumulated over one
+ * stack (call once per stack and add): P[S][Cin][E+2][E+2], dO[S][Cout][E][E]
+ *   dw[co][ci][ky][kx] += sum_s sum_i sum_j dO[s][co][i][j] * P[s][ci][i+ky][j+kx]
+ *   db[co]             += sum_s sum_i sum_j dO[s][co][i][j]        (db may be NULL)
+ * in fp64, in the order s, i, j. */
+void orc_conv3x3_bwd_weight(const float* P, const float* dO, long S, int Cin, int Cout, int E, double* dw, double* db)
+{
+    const int pe = E + 2;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int co = 0; co < Cout; ++co)
+    for (int ci = 0; ci < Cin; ++ci)
+    for (int t = 0; t < 9; ++t) {
+        const int ky = t / 3, kx = t % 3;
+        double acc = 0.0;
+        for (long s = 0; s < S; ++s) {
+            const float* g = dO + ((s * Cout + co) * E) * (long)E;
+            const float* p = P + ((s * Cin + ci) * pe) * (long)pe;
+            for (int i = 0; i < E; ++i)
+                for (int j = 0; j < E; ++j) acc += (double)g[i * E + j] * (double)p[(i + ky) * pe + (j + kx)];
+        }
+        dw[((long)co * Cin + ci) * 9 + t] += acc;
+    }
+    if (db)
+        for (int co = 0; co < Cout; ++co) {
+            double acc = 0.0;
+            for (long s = 0; s < S; ++s) {
+                const float* g = dO + ((s * Cout + co) * E) * (long)E;
+                for (int i = 0; i < E * E; ++i) acc += (double)g[i];
+            }
+            db[co] += acc;
+        }
+}
