@@ -253,6 +253,76 @@ int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_i
 int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
                                    int C_out, size_t* bytes);
 
+/* ------------------------------------------------------------------------
+ * Backward pass (the block modules and the block convolution are linear maps;
+ * these are their transposes, for training through the block-conv path).
+ * For y = combine(conv3x3(pad(split(x)))) and an output gradient dy:
+ *   (dho, dlo_o) = segblocks_combine_backward(dy)
+ *   dw, db       = segblocks_conv3x3_backward_weight(hp, lp, dho, dlo_o)
+ *   (dhp, dlp)   = segblocks_conv3x3_backward_data(dho, dlo_o, w)
+ *   (dhi, dlo)   = segblocks_pad_backward(dhp, dlp)
+ *   dx           = segblocks_split_backward(dhi, dlo)
+ * Shapes, layouts, masks and capacities follow the forward calls; every
+ * gradient is stored in `dtype` with fp32 arithmetic.  Blocks past a stack's
+ * capacity are skipped as in the forward calls.
+ * ------------------------------------------------------------------------ */
+
+/* BlockCombine transposed: dy [N,C,H,W] -> dhi [nh,C,bs,bs] (the block's
+ * gradient copied), dlo [nl,C,lb,lb] (the fp32 sum ((a + b) + (c + d)) of the
+ * 2x2 cell of gradients each low pixel was copied to, rounded once). */
+int segblocks_combine_backward(const void* dy, int dtype, int layout, int N, int C, int H, int W,
+                               const uint8_t* mask, int bs, void* dhi, int hi_cap, void* dlo,
+                               int lo_cap, hipStream_t stream);
+
+/* BlockSample transposed: dhi, dlo -> dx [N,C,H,W]: a high block's gradient
+ * copied back, a low pixel's gradient times 0.25 on each pixel of its cell. */
+int segblocks_split_backward(const void* dhi, const void* dlo, int dtype, int layout, int N, int C,
+                             int H, int W, const uint8_t* mask, int bs, int hi_cap, int lo_cap,
+                             void* dx, hipStream_t stream);
+
+/* BlockPad transposed (sampling as in segblocks_pad_ex): dhp [nh,C,bs+2,bs+2],
+ * dlp [nl,C,lb+2,lb+2] -> dhi, dlo.  Each block pixel receives the gradient
+ * of every padded pixel that was read from it: its own interior pixel, the
+ * halo pixels of neighbours at the same resolution, the halo pixels of a high
+ * neighbour it was nearest-upsampled into, and a quarter of each low
+ * neighbour's halo pixel averaged from its 2x2 cell (all of it at the cell's
+ * top-left pixel with SB_PAD_STRIDED; nothing with SB_PAD_ZERO).  Summed in
+ * fp32 in a fixed order (no atomics), rounded once. */
+int segblocks_pad_backward(const void* dhp, const void* dlp, int dtype, int layout, int N, int C,
+                           int H, int W, const uint8_t* mask, int bs, int sampling, void* dhi,
+                           void* dlo, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* Gradient of segblocks_conv3x3 with respect to its padded input:
+ *   dP[s,ci,u,v] = sum_{co,ky,kx} w[co,ci,ky,kx] * dO[s,co,u-ky,v-kx]
+ * dho [nh,C_out,bs,bs], dlo [nl,C_out,lb,lb] -> dhp [nh,C_in,bs+2,bs+2],
+ * dlp [nl,C_in,lb+2,lb+2]; weight as in segblocks_conv3x3.  Needs a
+ * workspace (the gradients padded by two zeros, the transposed filters):
+ * segblocks_conv3x3_backward_data_workspace_size. */
+int segblocks_conv3x3_backward_data(const void* dho, const void* dlo, int dtype, int layout, int N,
+                                    int C_in, int H, int W, const uint8_t* mask, int bs,
+                                    const void* weight, int C_out, void* dhp, void* dlp, int hi_cap,
+                                    int lo_cap, void* workspace, size_t ws_bytes, hipStream_t stream);
+int segblocks_conv3x3_backward_data_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
+                                                   int bs, int C_out, int hi_cap, int lo_cap,
+                                                   size_t* bytes);
+
+/* Gradient of segblocks_conv3x3 with respect to its weight and bias over both
+ * stacks:
+ *   dw[co,ci,ky,kx] = sum_{s,i,j} dO[s,co,i,j] * P[s,ci,i+ky,j+kx],  db[co] = sum dO[s,co,i,j]
+ * hp, lp: the padded inputs of the forward call; dho, dlo: the output
+ * gradients; dweight in the call's weight format, dbias [C_out] or NULL.
+ * fp32 partial sums per range of block rows in the workspace, added in a
+ * fixed order: segblocks_conv3x3_backward_weight_workspace_size (with_bias
+ * != 0 when dbias is given). */
+int segblocks_conv3x3_backward_weight(const void* hp, const void* lp, const void* dho, const void* dlo,
+                                      int dtype, int layout, int N, int C_in, int H, int W,
+                                      const uint8_t* mask, int bs, int C_out, void* dweight,
+                                      void* dbias, int hi_cap, int lo_cap, void* workspace,
+                                      size_t ws_bytes, hipStream_t stream);
+int segblocks_conv3x3_backward_weight_workspace_size(int dtype, int layout, int N, int C_in, int H,
+                                                     int W, int bs, int C_out, int hi_cap, int lo_cap,
+                                                     int with_bias, size_t* bytes);
+
 /* Heuristic downsampling policy (the policy of the short paper SegBlocks
  * extends, compared with in Experiments > Ablation studies, execution
  * policies): it selects the blocks where half resolution loses the most

@@ -20,7 +20,8 @@ from . import _binding as _b
 
 __all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "block_conv_ex", "layer", "conv2d",
            "maxpool", "layout_of", "block_conv3x3_workspace_size", "block_conv_ex_workspace_size",
-           "layer_workspace_size", "policy_heuristic"]
+           "layer_workspace_size", "policy_heuristic", "combine_backward", "split_backward", "pad_backward",
+           "conv3x3_backward_data", "conv3x3_backward_weight", "layer_backward"]
 
 _DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
 
@@ -344,3 +345,107 @@ def policy_heuristic(x: torch.Tensor, bs: int, tau_high: float, layout=None, out
     _b.call("segblocks_policy_heuristic", _ptr(x), _dt(x), layout, N, C, H, W, bs, float(tau_high), _ptr(score),
             _ptr(mask), _stream(x))
     return mask, score
+
+
+# ---------------------------------------------------------------------------
+# Backward pass
+# ---------------------------------------------------------------------------
+
+def combine_backward(dy: torch.Tensor, mask: torch.Tensor, bs: int, counts=None, layout=None):
+    """BlockCombine transposed: dy [N,C,H,W] -> (dhi, dlo)."""
+    mask = _mask(mask)
+    layout = layout_of(dy) if layout is None else layout
+    _check_layout(layout, dy)
+    N, C, H, W = dy.shape
+    nh, nl = counts if counts is not None else count(mask)
+    dhi = _empty((nh, C, bs, bs), dy, layout)
+    dlo = _empty((nl, C, bs // 2, bs // 2), dy, layout)
+    _b.call("segblocks_combine_backward", _ptr(dy), _dt(dy), layout, N, C, H, W, _ptr(mask), bs, _ptr(dhi), nh,
+            _ptr(dlo), nl, _stream(dy))
+    return dhi, dlo
+
+
+def split_backward(dhi: torch.Tensor, dlo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None):
+    """BlockSample transposed: (dhi, dlo) -> dx [N,C,H,W]."""
+    mask = _mask(mask)
+    ref = dhi if dhi.shape[0] else dlo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, dhi, dlo)
+    N, C = mask.shape[0], ref.shape[1]
+    dx = _empty((N, C, H, W), ref, layout)
+    _b.call("segblocks_split_backward", _ptr(dhi), _ptr(dlo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs,
+            dhi.shape[0], dlo.shape[0], _ptr(dx), _stream(ref))
+    return dx
+
+
+def pad_backward(dhp: torch.Tensor, dlp: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, layout=None,
+                 sampling: str = "avg"):
+    """BlockPad transposed: (dhp, dlp) -> (dhi, dlo)."""
+    mask = _mask(mask)
+    ref = dhp if dhp.shape[0] else dlp
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, dhp, dlp)
+    N, C = mask.shape[0], ref.shape[1]
+    dhi = _empty((dhp.shape[0], C, bs, bs), ref, layout)
+    dlo = _empty((dlp.shape[0], C, bs // 2, bs // 2), ref, layout)
+    _b.call("segblocks_pad_backward", _ptr(dhp), _ptr(dlp), _dt(ref), layout, N, C, H, W, _ptr(mask), bs,
+            _SAMPLING[sampling], _ptr(dhi), _ptr(dlo), dhp.shape[0], dlp.shape[0], _stream(ref))
+    return dhi, dlo
+
+
+def conv3x3_backward_data(dho: torch.Tensor, dlo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
+                          weight: torch.Tensor, layout=None, workspace=None):
+    """Gradient of the padded-stack convolution with respect to its input: (dhp, dlp)."""
+    mask = _mask(mask)
+    ref = dho if dho.shape[0] else dlo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, dho, dlo)
+    C_out, C_in = weight.shape[0], weight.shape[1]
+    N = mask.shape[0]
+    weight = _weight(weight, layout)
+    dhp = _empty((dho.shape[0], C_in, bs + 2, bs + 2), ref, layout)
+    dlp = _empty((dlo.shape[0], C_in, bs // 2 + 2, bs // 2 + 2), ref, layout)
+    need = _query("segblocks_conv3x3_backward_data_workspace_size", _DT[ref.dtype], layout, N, C_in, H, W, bs, C_out,
+                  dho.shape[0], dlo.shape[0])
+    wp, wn, _keep = _ws(need, ref.device, workspace)
+    _b.call("segblocks_conv3x3_backward_data", _ptr(dho), _ptr(dlo), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs,
+            _ptr(weight), C_out, _ptr(dhp), _ptr(dlp), dho.shape[0], dlo.shape[0], wp, wn, _stream(ref))
+    return dhp, dlp
+
+
+def conv3x3_backward_weight(hp: torch.Tensor, lp: torch.Tensor, dho: torch.Tensor, dlo: torch.Tensor,
+                            mask: torch.Tensor, bs: int, H: int, W: int, bias: bool = True, layout=None,
+                            workspace=None):
+    """Gradients of the padded-stack convolution with respect to its weight
+    (OIHW logical shape, in the call's memory format) and bias: (dw, db)."""
+    mask = _mask(mask)
+    ref = dho if dho.shape[0] else dlo
+    pref = hp if hp.shape[0] else lp
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hp, lp, dho, dlo)
+    C_out, C_in, N = ref.shape[1], pref.shape[1], mask.shape[0]
+    dw = torch.empty((C_out, C_in, 3, 3), dtype=ref.dtype, device=ref.device, memory_format=_fmt(layout))
+    db = torch.empty((C_out,), dtype=ref.dtype, device=ref.device) if bias else None
+    need = _query("segblocks_conv3x3_backward_weight_workspace_size", _DT[ref.dtype], layout, N, C_in, H, W, bs,
+                  C_out, hp.shape[0], lp.shape[0], 1 if bias else 0)
+    wp, wn, _keep = _ws(need, ref.device, workspace)
+    _b.call("segblocks_conv3x3_backward_weight", _ptr(hp), _ptr(lp), _ptr(dho), _ptr(dlo), _dt(ref), layout, N, C_in,
+            H, W, _ptr(mask), bs, C_out, _ptr(dw), _ptr(db), hp.shape[0], lp.shape[0], wp, wn, _stream(ref))
+    return dw, db
+
+
+def layer_backward(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.Tensor, dy: torch.Tensor,
+                   bias: bool = True, sampling: str = "avg"):
+    """Gradients (dx, dw, db) of y = layer(x) for an output gradient dy: the
+    forward stacks are recomputed (split, pad), then combine, convolution,
+    pad and split are run transposed.  Every step is a library call."""
+    layout = layout_of(x)
+    N, C, H, W = x.shape
+    nh, nl = count(mask)
+    hi, lo = split(x, mask, bs, counts=(nh, nl))
+    hp, lp = pad(hi, lo, mask, bs, H, W, sampling=sampling)
+    dho, dlo_o = combine_backward(dy, mask, bs, counts=(nh, nl), layout=layout)
+    dw, db = conv3x3_backward_weight(hp, lp, dho, dlo_o, mask, bs, H, W, bias=bias, layout=layout)
+    dhp, dlp = conv3x3_backward_data(dho, dlo_o, mask, bs, H, W, weight, layout=layout)
+    dhi, dlo = pad_backward(dhp, dlp, mask, bs, H, W, layout=layout, sampling=sampling)
+    return split_backward(dhi, dlo, mask, bs, H, W, layout=layout), dw, db

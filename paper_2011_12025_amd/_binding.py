@@ -24,6 +24,9 @@ EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_pad
            "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
            "segblocks_maxpool", "segblocks_block_conv3x3_workspace_size", "segblocks_block_conv_ex_workspace_size",
            "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_policy_heuristic",
+           "segblocks_combine_backward", "segblocks_split_backward", "segblocks_pad_backward",
+           "segblocks_conv3x3_backward_data", "segblocks_conv3x3_backward_data_workspace_size",
+           "segblocks_conv3x3_backward_weight", "segblocks_conv3x3_backward_weight_workspace_size",
            "segblocks_last_error"]
 
 SB_OK, SB_EINVAL, SB_ESHAPE, SB_EHIP, SB_ENOMEM = 0, -1, -2, -3, -4
@@ -47,6 +50,15 @@ _SIGS = {
     "segblocks_block_conv_ex_noalloc": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P,
                                         _P, _I, _I, _P],
     "segblocks_policy_heuristic": [_P, _I, _I, _I, _I, _I, _I, _I, ctypes.c_double, _P, _P, _P],
+    "segblocks_combine_backward": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _I, _P],
+    "segblocks_split_backward": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P],
+    "segblocks_pad_backward": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P, _I, _I, _P],
+    "segblocks_conv3x3_backward_data": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _P, _I, _I, _P, _Z,
+                                        _P],
+    "segblocks_conv3x3_backward_data_workspace_size": [_I] * 10 + [_ZP],
+    "segblocks_conv3x3_backward_weight": [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P, _I, _I, _P,
+                                          _Z, _P],
+    "segblocks_conv3x3_backward_weight_workspace_size": [_I] * 11 + [_ZP],
     "segblocks_block_conv3x3_workspace_size": [_I] * 10 + [_ZP],
     "segblocks_block_conv_ex_workspace_size": [_I] * 12 + [_ZP],
     "segblocks_layer_workspace_size": [_I] * 8 + [_ZP],

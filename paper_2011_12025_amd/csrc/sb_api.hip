@@ -469,6 +469,146 @@ int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H
     return SB_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Backward pass
+// ---------------------------------------------------------------------------
+
+int segblocks_combine_backward(const void* dy, int dtype, int layout, int N, int C, int H, int W,
+                               const uint8_t* mask, int bs, void* dhi, int hi_cap, void* dlo, int lo_cap,
+                               hipStream_t stream) {
+    const char* fn = "segblocks_combine_backward";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (!dy) return fail(SB_EINVAL, fn, "dy is NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "dhi", dhi, hi_cap)) ||
+        (s = check_stack(fn, "dlo", dlo, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range ry{dy, (long long)N * C * H * W * es}, rm{mask, g.B};
+    const Range rh{dhi, hi_cap * (long long)C * bs * bs * es}, rl{dlo, lo_cap * (long long)C * lb * lb * es};
+    if (any_overlap({rh, rl}, {ry, rm})) return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_split(dtype, layout, g, dy, mask, dhi, hi_cap, dlo, lo_cap, stream, true));
+}
+
+int segblocks_split_backward(const void* dhi, const void* dlo, int dtype, int layout, int N, int C, int H, int W,
+                             const uint8_t* mask, int bs, int hi_cap, int lo_cap, void* dx, hipStream_t stream) {
+    const char* fn = "segblocks_split_backward";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (!dx) return fail(SB_EINVAL, fn, "dx is NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "dhi", dhi, hi_cap)) ||
+        (s = check_stack(fn, "dlo", dlo, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rh{dhi, hi_cap * (long long)C * bs * bs * es}, rl{dlo, lo_cap * (long long)C * lb * lb * es};
+    const Range rx{dx, (long long)N * C * H * W * es};
+    if (any_overlap({rx}, {rh, rl, Range{mask, g.B}})) return fail(SB_EINVAL, fn, "dx overlaps an input");
+    return hip_status(fn, sb::launch_combine(dtype, layout, g, dhi, dlo, mask, hi_cap, lo_cap, dx, stream, true));
+}
+
+int segblocks_pad_backward(const void* dhp, const void* dlp, int dtype, int layout, int N, int C, int H, int W,
+                           const uint8_t* mask, int bs, int sampling, void* dhi, void* dlo, int hi_cap, int lo_cap,
+                           hipStream_t stream) {
+    const char* fn = "segblocks_pad_backward";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (sampling != SB_PAD_AVG && sampling != SB_PAD_STRIDED && sampling != SB_PAD_ZERO)
+        return fail(SB_EINVAL, fn, "bad sampling %d", sampling);
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "dhp", dhp, hi_cap)) ||
+        (s = check_stack(fn, "dlp", dlp, lo_cap)) || (s = check_stack(fn, "dhi", dhi, hi_cap)) ||
+        (s = check_stack(fn, "dlo", dlo, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rhp{dhp, hi_cap * (long long)C * (bs + 2) * (bs + 2) * es};
+    const Range rlp{dlp, lo_cap * (long long)C * (lb + 2) * (lb + 2) * es};
+    const Range rh{dhi, hi_cap * (long long)C * bs * bs * es}, rl{dlo, lo_cap * (long long)C * lb * lb * es};
+    if (any_overlap({rh, rl}, {rhp, rlp, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_pad_bwd(dtype, layout, g, dhp, dlp, mask, dhi, dlo, hi_cap, lo_cap, sampling,
+                                             stream));
+}
+
+int segblocks_conv3x3_backward_data_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
+                                                   int C_out, int hi_cap, int lo_cap, size_t* bytes) {
+    const char* fn = "segblocks_conv3x3_backward_data_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
+        return s;
+    *bytes = sb::dgrad_ws_bytes(dtype, g, C_in, C_out, hi_cap, lo_cap);
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_conv3x3_backward_data(const void* dho, const void* dlo, int dtype, int layout, int N, int C_in, int H,
+                                    int W, const uint8_t* mask, int bs, const void* weight, int C_out, void* dhp,
+                                    void* dlp, int hi_cap, int lo_cap, void* workspace, size_t ws_bytes,
+                                    hipStream_t stream) {
+    const char* fn = "segblocks_conv3x3_backward_data";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs + 4, weight))) return s;
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "dho", dho, hi_cap)) ||
+        (s = check_stack(fn, "dlo", dlo, lo_cap)) || (s = check_stack(fn, "dhp", dhp, hi_cap)) ||
+        (s = check_stack(fn, "dlp", dlp, lo_cap)))
+        return s;
+    const size_t need = sb::dgrad_ws_bytes(dtype, g, C_in, C_out, hi_cap, lo_cap);
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rho{dho, hi_cap * (long long)C_out * bs * bs * es}, rlo{dlo, lo_cap * (long long)C_out * lb * lb * es};
+    const Range rw{weight, (long long)C_out * C_in * 9 * es};
+    const Range rhp{dhp, hi_cap * (long long)C_in * (bs + 2) * (bs + 2) * es};
+    const Range rlp{dlp, lo_cap * (long long)C_in * (lb + 2) * (lb + 2) * es};
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({rhp, rlp, rws}, {rho, rlo, rw, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    return hip_status(fn, sb::launch_dgrad(dtype, layout, g, dho, dlo, mask, weight, C_in, C_out, dhp, dlp, hi_cap,
+                                           lo_cap, sb::Ws{workspace, ws_bytes}, stream));
+}
+
+int segblocks_conv3x3_backward_weight_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
+                                                     int C_out, int hi_cap, int lo_cap, int with_bias, size_t* bytes) {
+    const char* fn = "segblocks_conv3x3_backward_weight_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
+        return s;
+    *bytes = sb::wgrad_ws_bytes(g, C_in, C_out, hi_cap, lo_cap, with_bias != 0);
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_conv3x3_backward_weight(const void* hp, const void* lp, const void* dho, const void* dlo, int dtype,
+                                      int layout, int N, int C_in, int H, int W, const uint8_t* mask, int bs,
+                                      int C_out, void* dweight, void* dbias, int hi_cap, int lo_cap, void* workspace,
+                                      size_t ws_bytes, hipStream_t stream) {
+    const char* fn = "segblocks_conv3x3_backward_weight";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, dweight))) return s;
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hp", hp, hi_cap)) ||
+        (s = check_stack(fn, "lp", lp, lo_cap)) || (s = check_stack(fn, "dho", dho, hi_cap)) ||
+        (s = check_stack(fn, "dlo", dlo, lo_cap)))
+        return s;
+    const size_t need = sb::wgrad_ws_bytes(g, C_in, C_out, hi_cap, lo_cap, dbias != nullptr);
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
+    const long long es = esize(dtype), lb = bs / 2;
+    const Range rhp{hp, hi_cap * (long long)C_in * (bs + 2) * (bs + 2) * es};
+    const Range rlp{lp, lo_cap * (long long)C_in * (lb + 2) * (lb + 2) * es};
+    const Range rho{dho, hi_cap * (long long)C_out * bs * bs * es}, rlo{dlo, lo_cap * (long long)C_out * lb * lb * es};
+    const Range rw{dweight, (long long)C_out * C_in * 9 * es}, rb{dbias, dbias ? C_out * es : 0};
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({rw, rb, rws}, {rhp, rlp, rho, rlo, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    return hip_status(fn, sb::launch_wgrad(dtype, layout, g, hp, lp, dho, dlo, mask, C_in, C_out, dweight, dbias,
+                                           hi_cap, lo_cap, sb::Ws{workspace, ws_bytes}, stream));
+}
+
 int segblocks_policy_heuristic(const void* x, int dtype, int layout, int N, int C, int H, int W, int bs,
                                double tau_high, float* score, uint8_t* mask, hipStream_t stream) {
     const char* fn = "segblocks_policy_heuristic";

@@ -1,0 +1,538 @@
+// Backward pass of the block-conv layer y = combine(conv3x3(pad(split(x)))):
+// the transposes of the block modules and the gradients of the block
+// convolution.  BlockCombine and BlockSample transposed are the split and
+// combine kernels run with their backward flag (sb_rows.hip, sb_gather.hip).
+// Here:
+//
+//   k_pad_bwd     BlockPad transposed.  A block pixel gathers every padded
+//                 pixel that read it, in the image frame: the full-resolution
+//                 map Z that the high stacks' padded windows tile (with one
+//                 pixel of overlap), and its half-resolution pool P that the
+//                 low stacks' windows tile; Z's gradient takes P's through the
+//                 2x2 average (a quarter each; all of it at the cell's
+//                 top-left pixel with strided sampling), and BlockCombine's
+//                 transpose hands Z's gradient to the block (copy for a high
+//                 block, the sum of the cell for a low one).  No atomics: the
+//                 sums run in a fixed order, so results do not depend on
+//                 timing.
+//   dgrad         the gradient of the valid 3x3 convolution of a padded block
+//                 is a valid 3x3 convolution of the output gradient padded by
+//                 two zeros, with the filters transposed (in <-> out) and
+//                 rotated by 180 degrees: run on the general block
+//                 convolution kernel over a stack of such padded gradients.
+//   k_wgrad       the weight and bias gradients: sums over every output pixel
+//                 of both stacks of outer products of the output gradient and
+//                 the padded input around the pixel.  Workgroups take 64
+//                 output x 64 input channels over a range of block rows and
+//                 keep 4 x 4 x 9 fp32 sums per thread; their partial sums go
+//                 to the workspace and k_wgrad_reduce adds them in chunk order.
+#include <type_traits>
+
+#include "sb_common.h"
+#include "sb_kernels.h"
+#include "sb_pixel.h"
+
+namespace sb {
+
+namespace {
+
+constexpr int BPIECE = WG;
+
+__device__ __forceinline__ void bcoords(int k, int GH, int GW, int& n, int& gy, int& gx) {
+    const int per = GH * GW;
+    n = k / per;
+    const int rem = k - n * per;
+    gy = rem / GW;
+    gx = rem - gy * GW;
+}
+
+// Gradient that the padded windows of one class put on pixel (r, c) of the
+// block (gy, gx) frame at extent e (block-local, 0 <= r, c < e): the windows
+// of the block itself and of the neighbours whose one-pixel halo overlaps the
+// pixel, counted only where that window belongs to the class `want_high`.
+template <typename T, int L, int V>
+__device__ __forceinline__ void window_sum(const T* __restrict__ pad, int C, int e, const Neigh& nb, int cap,
+                                           bool want_high, int r, int c, int ch, float (&acc)[V]) {
+    const int pe = e + 2;
+#pragma unroll
+    for (int dy = -1; dy <= 1; ++dy) {
+        if ((dy == -1 && r != 0) || (dy == 1 && r != e - 1)) continue;
+#pragma unroll
+        for (int dx = -1; dx <= 1; ++dx) {
+            if ((dx == -1 && c != 0) || (dx == 1 && c != e - 1)) continue;
+            const int d = (dy + 1) * 3 + (dx + 1);
+            if (!((nb.valid >> d) & 1) || (((nb.high >> d) & 1) != (want_high ? 1u : 0u))) continue;
+            const int s = neigh_slot(nb, d);
+            if (s >= cap) continue;
+            const Vec<T, V> v = vload<T, V>(stack_at<T, L>(pad, s, C, pe, r - dy * e + 1, c - dx * e + 1, ch));
+#pragma unroll
+            for (int q = 0; q < V; ++q) acc[q] += to_f32(v.e[q]);
+        }
+    }
+}
+
+template <typename T, int L, int V>
+__global__ __launch_bounds__(WG) void k_pad_bwd(const T* __restrict__ dhp, const T* __restrict__ dlp, int C, int H,
+                                                int W, const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
+                                                T* __restrict__ dhi, T* __restrict__ dlo, int hi_cap, int lo_cap,
+                                                int pm) {
+    const int w = (int)blockIdx.x;
+    bool high;
+    int slot, piece;
+    if (w < hi_cap * Gh) {
+        high = true;
+        slot = w / Gh;
+        piece = w - slot * Gh;
+    } else {
+        high = false;
+        slot = (w - hi_cap * Gh) / Gl;
+        piece = (w - hi_cap * Gh) - slot * Gl;
+    }
+    WaveMask wm;
+    wm.init(mask, B);
+    const int k = wm.find_nth(slot, high);
+    if (k < 0) return;
+    const int GH = H / bs, GW = W / bs, lb = bs >> 1;
+    int n, gy, gx;
+    bcoords(k, GH, GW, n, gy, gx);
+    const int e = high ? bs : lb;
+    const Neigh nb = wave_neighbourhood<true>(wm, GH, GW, n, gy, gx);
+    const int it = piece * BPIECE + (int)threadIdx.x;
+    if (it >= e * e * C / V) return;
+    int r, j, c;
+    if constexpr (L == NHWC) {
+        const int cv = C / V, pix = it / cv;
+        c = (it - pix * cv) * V;
+        r = pix / e;
+        j = pix - r * e;
+    } else {
+        static_assert(L == NHWC || V == 1, "NCHW moves single elements");
+        const int row = it / e;
+        j = it - row * e;
+        c = row / e;
+        r = row - c * e;
+    }
+    float acc[V];
+#pragma unroll
+    for (int q = 0; q < V; ++q) acc[q] = 0.0f;
+    if (pm == PM_ZERO) {  // every block was padded on its own: its interior only
+        const Vec<T, V> v = vload<T, V>(stack_at<T, L>(high ? dhp : dlp, slot, C, e + 2, r + 1, j + 1, c));
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc[q] = to_f32(v.e[q]);
+    } else if (high) {
+        // Z at this pixel: the high windows over it
+        window_sum<T, L, V>(dhp, C, bs, nb, hi_cap, true, r, j, c, acc);
+        // P at its cell: the low windows over it, through the 2x2 average (or the stride)
+        if (pm == PM_AVG || ((r | j) & 1) == 0) {
+            float h[V];
+#pragma unroll
+            for (int q = 0; q < V; ++q) h[q] = 0.0f;
+            window_sum<T, L, V>(dlp, C, lb, nb, lo_cap, false, r >> 1, j >> 1, c, h);
+            const float f = pm == PM_AVG ? 0.25f : 1.0f;
+#pragma unroll
+            for (int q = 0; q < V; ++q) acc[q] += f * h[q];
+        }
+    } else {
+        // the four pixels of the cell in Z: the high windows over them
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) window_sum<T, L, V>(dhp, C, bs, nb, hi_cap, true, 2 * r + a, 2 * j + b, c, acc);
+        // P at the cell, whose quarters (or whole, strided) come back through the four pixels
+        window_sum<T, L, V>(dlp, C, lb, nb, lo_cap, false, r, j, c, acc);
+    }
+    Vec<T, V> o;
+#pragma unroll
+    for (int q = 0; q < V; ++q) o.e[q] = from_f32<T>(acc[q]);
+    T* dst;
+    if constexpr (L == NHWC) dst = (high ? dhi : dlo) + ((((size_t)slot * e + r) * e + j) * C + c);
+    else                     dst = (high ? dhi : dlo) + ((((size_t)slot * C + c) * e + r) * e + j);
+    vstore<T, V>(dst, o);
+}
+
+// ---------------------------------------------------------------------------
+// dgrad helpers: the output gradient padded by two zeros, the transposed and
+// rotated filters, and the all-high / all-low masks that let the general
+// block convolution run over one stack at a time.
+// ---------------------------------------------------------------------------
+template <typename T, int L>
+__global__ __launch_bounds__(WG) void k_pad2(const T* __restrict__ src, int S, int C, int e, T* __restrict__ dst) {
+    const int pe = e + 4;
+    const long long total = (long long)S * C * pe * pe;
+    for (long long i = (long long)blockIdx.x * WG + threadIdx.x; i < total; i += (long long)gridDim.x * WG) {
+        int s, c, u, v;
+        if constexpr (L == NHWC) {
+            c = (int)(i % C);
+            long long p = i / C;
+            v = (int)(p % pe);
+            p /= pe;
+            u = (int)(p % pe);
+            s = (int)(p / pe);
+        } else {
+            v = (int)(i % pe);
+            long long p = i / pe;
+            u = (int)(p % pe);
+            p /= pe;
+            c = (int)(p % C);
+            s = (int)(p / C);
+        }
+        const int a = u - 2, b = v - 2;
+        T val = from_f32<T>(0.0f);
+        if (a >= 0 && a < e && b >= 0 && b < e) {
+            if constexpr (L == NHWC) val = src[(((size_t)s * e + a) * e + b) * C + c];
+            else                     val = src[(((size_t)s * C + c) * e + a) * e + b];
+        }
+        dst[i] = val;
+    }
+}
+
+// w [Cout][Cin][3][3] in the call's format -> wt [Cin][Cout][3][3], rotated
+template <typename T, int L>
+__global__ __launch_bounds__(WG) void k_wflip(const T* __restrict__ w, int Cout, int Cin, T* __restrict__ wt) {
+    const int total = Cout * Cin * 9;
+    for (int i = (int)(blockIdx.x * WG + threadIdx.x); i < total; i += (int)(gridDim.x * WG)) {
+        // i indexes wt in its memory order
+        int ci, co, t;
+        if constexpr (L == NHWC) {  // [Cin][3][3][Cout]
+            co = i % Cout;
+            t = (i / Cout) % 9;
+            ci = i / (Cout * 9);
+        } else {                    // [Cin][Cout][3][3]
+            t = i % 9;
+            co = (i / 9) % Cout;
+            ci = i / (9 * Cout);
+        }
+        const int ts = 8 - t;       // (2 - ky, 2 - kx)
+        size_t src;
+        if constexpr (L == NHWC) src = ((size_t)co * 9 + ts) * Cin + ci;
+        else                     src = ((size_t)co * Cin + ci) * 9 + ts;
+        wt[i] = w[src];
+    }
+}
+
+__global__ __launch_bounds__(WG) void k_fill8(uint8_t* __restrict__ p, long long n, uint8_t v) {
+    for (long long i = (long long)blockIdx.x * WG + threadIdx.x; i < n; i += (long long)gridDim.x * WG) p[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// wgrad
+// ---------------------------------------------------------------------------
+constexpr int WG_CO = 64, WG_CI = 64;  // output / input channels of a workgroup
+constexpr int WG_PX = 32;              // output pixels of a row strip
+
+// Number of high blocks of the mask (every thread of the workgroup gets it).
+__device__ __forceinline__ int count_high(const uint8_t* __restrict__ mask, int B, int* s_red) {
+    int c = 0;
+    for (int i = (int)threadIdx.x; i < B; i += WG) c += mask[i] != 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = c;
+    __syncthreads();
+    int t = 0;
+#pragma unroll
+    for (int w = 0; w < WG / 64; ++w) t += s_red[w];
+    __syncthreads();
+    return t;
+}
+
+// Element (s, c, y, x) of a stack of extent ext as fp32 (0 outside the channel range).
+template <typename T, int L>
+__device__ __forceinline__ float stk(const T* __restrict__ base, int s, int C, int ext, int y, int x, int c) {
+    if (c >= C) return 0.0f;
+    if constexpr (L == NHWC) return to_f32(base[(((size_t)s * ext + y) * ext + x) * C + c]);
+    else                     return to_f32(base[(((size_t)s * C + c) * ext + y) * ext + x]);
+}
+
+// grid: (chunk, co block, ci block).  A chunk is a range of block rows of the
+// concatenation [high stack rows, low stack rows] (high_rows = nh * bs).
+template <typename T, int L>
+__global__ __launch_bounds__(WG) void k_wgrad(const T* __restrict__ hp, const T* __restrict__ lp,
+                                              const T* __restrict__ dho, const T* __restrict__ dlo,
+                                              const uint8_t* __restrict__ mask, int B, int bs, int C_in, int C_out,
+                                              int hi_cap, int lo_cap, int rows_per_chunk, float* __restrict__ part,
+                                              float* __restrict__ part_b) {
+    __shared__ float s_o[WG_PX][WG_CO];             // output-gradient strip (pixels x co)
+    __shared__ float s_p[3][WG_PX + 2][WG_CI + 1];  // three padded input rows (pixels x ci)
+    __shared__ int s_red[WG / 64];
+    const int tid = (int)threadIdx.x;
+    const int co0 = (int)blockIdx.y * WG_CO, ci0 = (int)blockIdx.z * WG_CI;
+    const int tco = (tid >> 4) * 4, tci = (tid & 15) * 4;  // this thread's 4 co x 4 ci
+    const int nh_all = count_high(mask, B, s_red);
+    const int nh = min(nh_all, hi_cap), nl = min(B - nh_all, lo_cap);
+    const int lb = bs >> 1;
+    const long long rows_h = (long long)nh * bs, rows = rows_h + (long long)nl * lb;
+    float acc[4][4][9];
+    float accb[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        accb[a] = 0.0f;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int t = 0; t < 9; ++t) acc[a][b][t] = 0.0f;
+    }
+    const long long r0 = (long long)blockIdx.x * rows_per_chunk;
+    const long long r1 = min(rows, r0 + rows_per_chunk);
+    for (long long rr = r0; rr < r1; ++rr) {
+        const bool high = rr < rows_h;
+        const int e = high ? bs : lb;
+        const long long q = high ? rr : rr - rows_h;
+        const int s = (int)(q / e), i = (int)(q - (long long)s * e);
+        const T* P = high ? hp : lp;
+        const T* O = high ? dho : dlo;
+        for (int x = 0; x < e; x += WG_PX) {  // strips of up to WG_PX output pixels
+            const int np = min(WG_PX, e - x);
+            __syncthreads();
+            for (int idx = tid; idx < np * WG_CO; idx += WG) {
+                const int p = idx / WG_CO, co = idx - p * WG_CO;
+                s_o[p][co] = stk<T, L>(O, s, C_out, e, i, x + p, co0 + co);
+            }
+            for (int idx = tid; idx < 3 * (np + 2) * WG_CI; idx += WG) {
+                const int ky = idx / ((np + 2) * WG_CI);
+                const int rem = idx - ky * (np + 2) * WG_CI;
+                const int p = rem / WG_CI, ci = rem - p * WG_CI;
+                s_p[ky][p][ci] = stk<T, L>(P, s, C_in, e + 2, i + ky, x + p, ci0 + ci);
+            }
+            __syncthreads();
+            for (int p = 0; p < np; ++p) {
+                float o[4];
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+                    o[a] = s_o[p][tco + a];
+                    accb[a] += o[a];
+                }
+#pragma unroll
+                for (int t = 0; t < 9; ++t) {
+                    const int ky = t / 3, kx = t - ky * 3;
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const float pv = s_p[ky][p + kx][tci + b];
+#pragma unroll
+                        for (int a = 0; a < 4; ++a) acc[a][b][t] += o[a] * pv;
+                    }
+                }
+            }
+        }
+    }
+    // partial sums of this chunk: part[chunk][co][t][ci] over the full channel ranges
+    float* pc = part + (size_t)blockIdx.x * C_out * 9 * C_in;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const int co = co0 + tco + a;
+        if (co >= C_out) continue;
+#pragma unroll
+        for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int ci = ci0 + tci + b;
+                if (ci < C_in) pc[((size_t)co * 9 + t) * C_in + ci] = acc[a][b][t];
+            }
+        if (part_b && blockIdx.z == 0 && (tid & 15) == 0) part_b[(size_t)blockIdx.x * C_out + co] = accb[a];
+    }
+}
+
+// dw (call's format) and db from the chunk partial sums, added in chunk order.
+template <typename T, int L>
+__global__ __launch_bounds__(WG) void k_wgrad_reduce(const float* __restrict__ part, const float* __restrict__ part_b,
+                                                     int chunks, int C_in, int C_out, T* __restrict__ dw,
+                                                     T* __restrict__ db) {
+    const int total = C_out * 9 * C_in;
+    const int i = (int)(blockIdx.x * WG + threadIdx.x);
+    if (i < total) {
+        float s = 0.0f;
+        for (int q = 0; q < chunks; ++q) s += part[(size_t)q * total + i];
+        const int ci = i % C_in, t = (i / C_in) % 9, co = i / (9 * C_in);
+        size_t o;
+        if constexpr (L == NHWC) o = i;  // [Cout][3][3][Cin]
+        else                     o = ((size_t)co * C_in + ci) * 9 + t;
+        dw[o] = from_f32<T>(s);
+    }
+    if (db && i < C_out) {
+        float s = 0.0f;
+        for (int q = 0; q < chunks; ++q) s += part_b[(size_t)q * C_out + i];
+        db[i] = from_f32<T>(s);
+    }
+}
+
+inline size_t r256(size_t b) { return (b + 255) / 256 * 256; }
+inline int esz(int dtype) { return dtype == 0 ? 4 : 2; }
+
+struct DgradLayout {
+    size_t qh, ql, wt, masks, total;
+};
+
+DgradLayout dgrad_layout(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+    const size_t es = esz(dtype), lb = g.bs / 2;
+    DgradLayout D;
+    D.qh = r256((size_t)hi_cap * C_out * (g.bs + 4) * (g.bs + 4) * es);
+    D.ql = r256((size_t)lo_cap * C_out * (lb + 4) * (lb + 4) * es);
+    D.wt = r256((size_t)C_in * C_out * 9 * es);
+    D.masks = r256((size_t)g.B * 2);
+    D.total = D.qh + D.ql + D.wt + D.masks;
+    return D;
+}
+
+struct WgradPlan {
+    int chunks, rows_per_chunk, tiles_co, tiles_ci;
+    size_t part, part_b, total;
+};
+
+WgradPlan wgrad_plan(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
+    WgradPlan p;
+    p.tiles_co = (C_out + WG_CO - 1) / WG_CO;
+    p.tiles_ci = (C_in + WG_CI - 1) / WG_CI;
+    // rows by capacity (the counts are on the device): aim at about 2 workgroups per CU
+    const long long rows = (long long)hi_cap * g.bs + (long long)lo_cap * (g.bs / 2);
+    const long long want = (2LL * device_cus() + p.tiles_co * p.tiles_ci - 1) / (p.tiles_co * p.tiles_ci);
+    const long long per = rows > 0 ? (rows + want - 1) / want : 1;
+    p.rows_per_chunk = (int)(per > 0 ? per : 1);
+    p.chunks = rows > 0 ? (int)((rows + p.rows_per_chunk - 1) / p.rows_per_chunk) : 1;
+    p.part = r256((size_t)p.chunks * C_out * 9 * C_in * 4);
+    p.part_b = bias ? r256((size_t)p.chunks * C_out * 4) : 0;
+    p.total = p.part + p.part_b;
+    return p;
+}
+
+template <typename T>
+hipError_t pad_bwd_t(int layout, const Geo& g, const void* dhp, const void* dlp, const uint8_t* mask, void* dhi,
+                     void* dlo, int hi_cap, int lo_cap, int pm, hipStream_t st) {
+    constexpr int VM = 16 / (int)sizeof(T);
+    const bool al = ((reinterpret_cast<uintptr_t>(dhp) | reinterpret_cast<uintptr_t>(dlp) |
+                      reinterpret_cast<uintptr_t>(dhi) | reinterpret_cast<uintptr_t>(dlo)) & 15) == 0;
+    const int lb = g.bs / 2;
+    auto run = [&](auto kern, int V) -> hipError_t {
+        const int Gh = (int)(((long long)g.bs * g.bs * g.C / V + BPIECE - 1) / BPIECE);
+        const int Gl = (int)(((long long)lb * lb * g.C / V + BPIECE - 1) / BPIECE);
+        const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
+        if (blocks == 0) return hipSuccess;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)dhp, (const T*)dlp, g.C, g.H, g.W,
+                           mask, g.bs, (int)g.B, Gh, Gl, (T*)dhi, (T*)dlo, hi_cap, lo_cap, pm);
+        return hipGetLastError();
+    };
+    if (layout == NHWC) {
+        if (al && g.C % VM == 0) return run(k_pad_bwd<T, NHWC, VM>, VM);
+        return run(k_pad_bwd<T, NHWC, 1>, 1);
+    }
+    return run(k_pad_bwd<T, NCHW, 1>, 1);
+}
+
+template <typename T, int L>
+hipError_t dgrad_t(const Geo& g, const void* dho, const void* dlo, const uint8_t* mask, const void* w, int C_in,
+                   int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws, hipStream_t st) {
+    (void)mask;
+    const DgradLayout D = dgrad_layout(sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2), g, C_in, C_out,
+                                       hi_cap, lo_cap);
+    if (ws.bytes < D.total || !ws.p) return hipErrorInvalidValue;
+    char* base = (char*)ws.p;
+    T* qh = (T*)base;
+    T* ql = (T*)(base + D.qh);
+    T* wt = (T*)(base + D.qh + D.ql);
+    uint8_t* ones = (uint8_t*)(base + D.qh + D.ql + D.wt);
+    uint8_t* zeros = ones + g.B;
+    const int lb = g.bs / 2;
+    const int grid = device_cus() * 4;
+    hipLaunchKernelGGL((k_fill8), dim3(grid), dim3(WG), 0, st, ones, g.B, (uint8_t)1);
+    hipLaunchKernelGGL((k_fill8), dim3(grid), dim3(WG), 0, st, zeros, g.B, (uint8_t)0);
+    hipLaunchKernelGGL((k_wflip<T, L>), dim3((C_in * C_out * 9 + WG - 1) / WG), dim3(WG), 0, st, (const T*)w, C_out,
+                       C_in, wt);
+    if (hi_cap > 0)
+        hipLaunchKernelGGL((k_pad2<T, L>), dim3(grid), dim3(WG), 0, st, (const T*)dho, hi_cap, C_out, g.bs, qh);
+    if (lo_cap > 0)
+        hipLaunchKernelGGL((k_pad2<T, L>), dim3(grid), dim3(WG), 0, st, (const T*)dlo, lo_cap, C_out, lb, ql);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int dt = sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2);
+    // the high stack: every block of the grid taken as high, extent bs + 2 (the padded gradient)
+    if (hi_cap > 0) {
+        Geo gh = g;
+        gh.bs = g.bs + 2;
+        gh.H = g.GH * gh.bs;
+        gh.W = g.GW * gh.bs;
+        const ConvArgs a{qh, nullptr, wt, nullptr, nullptr, nullptr, dhp, nullptr, C_out, C_in, 0, hi_cap, 0};
+        if ((e = launch_conv(dt, L, SRC_PADDED, DST_PACKED, gh, ones, a, Ws{nullptr, 0}, st)) != hipSuccess) return e;
+    }
+    // the low stack: every block taken as low, low extent lb + 2
+    if (lo_cap > 0) {
+        Geo gl = g;
+        gl.bs = g.bs + 4;
+        gl.H = g.GH * gl.bs;
+        gl.W = g.GW * gl.bs;
+        const ConvArgs a{nullptr, ql, wt, nullptr, nullptr, nullptr, nullptr, dlp, C_out, C_in, 0, 0, lo_cap};
+        if ((e = launch_conv(dt, L, SRC_PADDED, DST_PACKED, gl, zeros, a, Ws{nullptr, 0}, st)) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <typename T, int L>
+hipError_t wgrad_t(const Geo& g, const void* hp, const void* lp, const void* dho, const void* dlo,
+                   const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap, int lo_cap, Ws ws,
+                   hipStream_t st) {
+    const WgradPlan p = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, db != nullptr);
+    if (ws.bytes < p.total || !ws.p) return hipErrorInvalidValue;
+    float* part = (float*)ws.p;
+    float* part_b = db ? (float*)((char*)ws.p + p.part) : nullptr;
+    hipLaunchKernelGGL((k_wgrad<T, L>), dim3((unsigned)p.chunks, (unsigned)p.tiles_co, (unsigned)p.tiles_ci),
+                       dim3(WG), 0, st, (const T*)hp, (const T*)lp, (const T*)dho, (const T*)dlo, mask, (int)g.B,
+                       g.bs, C_in, C_out, hi_cap, lo_cap, p.rows_per_chunk, part, part_b);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int total = C_out * 9 * C_in;
+    hipLaunchKernelGGL((k_wgrad_reduce<T, L>), dim3((unsigned)((total + WG - 1) / WG)), dim3(WG), 0, st,
+                       (const float*)part, (const float*)part_b, p.chunks, C_in, C_out, (T*)dw, (T*)db);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pad_bwd(int dtype, int layout, const Geo& g, const void* dhp, const void* dlp, const uint8_t* mask,
+                          void* dhi, void* dlo, int hi_cap, int lo_cap, int pm, hipStream_t st) {
+    switch (dtype) {
+    case 0: return pad_bwd_t<float>(layout, g, dhp, dlp, mask, dhi, dlo, hi_cap, lo_cap, pm, st);
+    case 1: return pad_bwd_t<f16>(layout, g, dhp, dlp, mask, dhi, dlo, hi_cap, lo_cap, pm, st);
+    default: return pad_bwd_t<bf16>(layout, g, dhp, dlp, mask, dhi, dlo, hi_cap, lo_cap, pm, st);
+    }
+}
+
+size_t dgrad_ws_bytes(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+    return dgrad_layout(dtype, g, C_in, C_out, hi_cap, lo_cap).total;
+}
+
+hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, const void* dlo, const uint8_t* mask,
+                        const void* w, int C_in, int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws,
+                        hipStream_t st) {
+    if (layout == NHWC) {
+        switch (dtype) {
+        case 0: return dgrad_t<float, NHWC>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+        case 1: return dgrad_t<f16, NHWC>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+        default: return dgrad_t<bf16, NHWC>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+        }
+    }
+    switch (dtype) {
+    case 0: return dgrad_t<float, NCHW>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+    case 1: return dgrad_t<f16, NCHW>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+    default: return dgrad_t<bf16, NCHW>(g, dho, dlo, mask, w, C_in, C_out, dhp, dlp, hi_cap, lo_cap, ws, st);
+    }
+}
+
+size_t wgrad_ws_bytes(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
+    return wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias).total;
+}
+
+hipError_t launch_wgrad(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const void* dho,
+                        const void* dlo, const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap,
+                        int lo_cap, Ws ws, hipStream_t st) {
+    if (layout == NHWC) {
+        switch (dtype) {
+        case 0: return wgrad_t<float, NHWC>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+        case 1: return wgrad_t<f16, NHWC>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+        default: return wgrad_t<bf16, NHWC>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+        }
+    }
+    switch (dtype) {
+    case 0: return wgrad_t<float, NCHW>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+    case 1: return wgrad_t<f16, NCHW>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+    default: return wgrad_t<bf16, NCHW>(g, hp, lp, dho, dlo, mask, C_in, C_out, dw, db, hi_cap, lo_cap, ws, st);
+    }
+}
+
+}  // namespace sb

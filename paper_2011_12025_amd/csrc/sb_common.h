@@ -116,6 +116,26 @@ __device__ __forceinline__ Vec<T, V> vavg4(const Vec<T, V>& a, const Vec<T, V>& 
     return r;
 }
 
+// The transposes for the backward pass: the 2x2 cell sum ((a + b) + (c + d))
+// (BlockCombine's nearest upsampling transposed) and a quarter of a value
+// (BlockSample's average transposed), in fp32, rounded once.
+template <typename T, int V>
+__device__ __forceinline__ Vec<T, V> vsum4(const Vec<T, V>& a, const Vec<T, V>& b,
+                                           const Vec<T, V>& c, const Vec<T, V>& d) {
+    Vec<T, V> r;
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        r.e[i] = from_f32<T>((to_f32(a.e[i]) + to_f32(b.e[i])) + (to_f32(c.e[i]) + to_f32(d.e[i])));
+    return r;
+}
+template <typename T, int V>
+__device__ __forceinline__ Vec<T, V> vquarter(const Vec<T, V>& a) {
+    Vec<T, V> r;
+#pragma unroll
+    for (int i = 0; i < V; ++i) r.e[i] = from_f32<T>(to_f32(a.e[i]) * 0.25f);
+    return r;
+}
+
 // ---------------------------------------------------------------------------
 // Wavefront primitives and the block plan
 //

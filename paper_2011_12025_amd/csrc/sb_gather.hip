@@ -81,10 +81,12 @@ __device__ __forceinline__ bool slot_piece(int w, int hi_cap, int Gh, int Gl, bo
 // ---------------------------------------------------------------------------
 // split: x[N,C,H,W] -> hi[nh,C,bs,bs], lo[nl,C,lb,lb]
 // ---------------------------------------------------------------------------
+// bwd != 0: BlockCombine transposed (a low block gets the sums of its cells)
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, int H, int W,
                                               const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
-                                              T* __restrict__ hi, int hi_cap, T* __restrict__ lo, int lo_cap) {
+                                              T* __restrict__ hi, int hi_cap, T* __restrict__ lo, int lo_cap,
+                                              int bwd) {
     bool high;
     int slot, piece;
     slot_piece((int)blockIdx.x, hi_cap, Gh, Gl, high, slot, piece);
@@ -110,8 +112,9 @@ __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, in
     if constexpr (L == NHWC) {
         const T* p = map_at<T, L>(x, n, C, H, W, Y, X, c);
         const size_t down = (size_t)W * C;
-        vstore<T, V>(dst, vavg4<T, V>(vload<T, V>(p), vload<T, V>(p + C), vload<T, V>(p + down),
-                                      vload<T, V>(p + down + C)));
+        const Vec<T, V> a = vload<T, V>(p), b = vload<T, V>(p + C), c2 = vload<T, V>(p + down),
+                        d = vload<T, V>(p + down + C);
+        vstore<T, V>(dst, bwd ? vsum4<T, V>(a, b, c2, d) : vavg4<T, V>(a, b, c2, d));
     } else {
         // V low pixels along the row come from 2V input pixels of two rows
         const T* p = map_at<T, L>(x, n, C, H, W, Y, X, c);
@@ -119,9 +122,11 @@ __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, in
         const Vec<T, V> b0 = vload<T, V>(p + W), b1 = vload<T, V>(p + W + V);
         Vec<T, V> o;
 #pragma unroll
-        for (int q = 0; q < V; ++q)
-            o.e[q] = avg4(pick2(t0, t1, 2 * q), pick2(t0, t1, 2 * q + 1), pick2(b0, b1, 2 * q),
-                          pick2(b0, b1, 2 * q + 1));
+        for (int q = 0; q < V; ++q) {
+            const T a = pick2(t0, t1, 2 * q), b = pick2(t0, t1, 2 * q + 1), c2 = pick2(b0, b1, 2 * q),
+                    d = pick2(b0, b1, 2 * q + 1);
+            o.e[q] = bwd ? from_f32<T>((to_f32(a) + to_f32(b)) + (to_f32(c2) + to_f32(d))) : avg4(a, b, c2, d);
+        }
         vstore<T, V>(dst, o);
     }
 }
@@ -165,9 +170,10 @@ __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* _
 // combine: hi, lo -> y[N,C,H,W]
 // ---------------------------------------------------------------------------
 template <typename T, int L, int V>
+// bwd != 0: BlockSample transposed (a low value is spread as quarters)
 __global__ __launch_bounds__(WG) void k_combine(const T* __restrict__ hi, const T* __restrict__ lo, int C, int H,
                                                 int W, const uint8_t* __restrict__ mask, int bs, int B, int G,
-                                                int hi_cap, int lo_cap, T* __restrict__ y) {
+                                                int hi_cap, int lo_cap, T* __restrict__ y, int bwd) {
     const int k = (int)blockIdx.x / G;
     const int piece = (int)blockIdx.x - k * G;
     const int GH = H / bs, GW = W / bs, lb = bs >> 1;
@@ -198,6 +204,7 @@ __global__ __launch_bounds__(WG) void k_combine(const T* __restrict__ hi, const 
 #pragma unroll
         for (int q = 0; q < V; ++q) val.e[q] = h.e[q >> 1];
     }
+    if (bwd && !high && !skip) val = vquarter<T, V>(val);
     T* dst;
     if constexpr (L == NHWC) dst = y + (((size_t)n * H + gy * bs + r) * W + (size_t)gx * bs + j) * C + c;
     else                     dst = y + (((size_t)n * C + c) * H + gy * bs + r) * (size_t)W + (size_t)gx * bs + j;
@@ -212,13 +219,13 @@ inline int pieces(long long vectors) { return (int)((vectors + PIECE - 1) / PIEC
 
 template <typename T, int L, int V>
 hipError_t run_split(const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap, void* lo,
-                     int lo_cap, hipStream_t st) {
+                     int lo_cap, int bwd, hipStream_t st) {
     const int lb = g.bs / 2;
     const int Gh = pieces((long long)g.bs * g.bs * g.C / V), Gl = pieces((long long)lb * lb * g.C / V);
     const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((k_split<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)x, g.C, g.H, g.W,
-                       mask, g.bs, (int)g.B, Gh, Gl, (T*)hi, hi_cap, (T*)lo, lo_cap);
+                       mask, g.bs, (int)g.B, Gh, Gl, (T*)hi, hi_cap, (T*)lo, lo_cap, bwd);
     return hipGetLastError();
 }
 
@@ -236,25 +243,25 @@ hipError_t run_pad(const Geo& g, const void* hi, const void* lo, const uint8_t* 
 
 template <typename T, int L, int V>
 hipError_t run_combine(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, int hi_cap, int lo_cap,
-                       void* y, hipStream_t st) {
+                       void* y, int bwd, hipStream_t st) {
     const int G = pieces((long long)g.bs * g.bs * g.C / V);
     const long long blocks = g.B * G;
     hipLaunchKernelGGL((k_combine<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)hi, (const T*)lo,
-                       g.C, g.H, g.W, mask, g.bs, (int)g.B, G, hi_cap, lo_cap, (T*)y);
+                       g.C, g.H, g.W, mask, g.bs, (int)g.B, G, hi_cap, lo_cap, (T*)y, bwd);
     return hipGetLastError();
 }
 
 template <typename T>
 hipError_t split_t(int layout, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap, void* lo,
-                   int lo_cap, hipStream_t st) {
+                   int lo_cap, int bwd, hipStream_t st) {
     constexpr int VM = 16 / (int)sizeof(T);
     const bool al = aligned16(x) && aligned16(hi) && aligned16(lo);
     if (layout == NHWC) {
-        if (al && g.C % VM == 0) return run_split<T, NHWC, VM>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
-        return run_split<T, NHWC, 1>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
+        if (al && g.C % VM == 0) return run_split<T, NHWC, VM>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+        return run_split<T, NHWC, 1>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
     }
-    if (al && (g.bs / 2) % VM == 0) return run_split<T, NCHW, VM>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
-    return run_split<T, NCHW, 1>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
+    if (al && (g.bs / 2) % VM == 0) return run_split<T, NCHW, VM>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+    return run_split<T, NCHW, 1>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
 }
 
 template <typename T>
@@ -271,26 +278,27 @@ hipError_t pad_t(int layout, const Geo& g, const void* hi, const void* lo, const
 
 template <typename T>
 hipError_t combine_t(int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, int hi_cap,
-                     int lo_cap, void* y, hipStream_t st) {
+                     int lo_cap, void* y, int bwd, hipStream_t st) {
     constexpr int VM = 16 / (int)sizeof(T);
     const bool al = aligned16(hi) && aligned16(lo) && aligned16(y);
     if (layout == NHWC) {
-        if (al && g.C % VM == 0) return run_combine<T, NHWC, VM>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
-        return run_combine<T, NHWC, 1>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
+        if (al && g.C % VM == 0) return run_combine<T, NHWC, VM>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+        return run_combine<T, NHWC, 1>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
     }
-    if (al && g.bs % VM == 0) return run_combine<T, NCHW, VM>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
-    return run_combine<T, NCHW, 1>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
+    if (al && g.bs % VM == 0) return run_combine<T, NCHW, VM>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+    return run_combine<T, NCHW, 1>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
 }
 
 }  // namespace
 
 hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask, void* hi,
-                        int hi_cap, void* lo, int lo_cap, hipStream_t st) {
-    if (rows_fit(dtype, layout, g, {x, hi, lo})) return launch_split_rows(dtype, g, x, mask, hi, hi_cap, lo, lo_cap, st);
+                        int hi_cap, void* lo, int lo_cap, hipStream_t st, bool bwd) {
+    if (rows_fit(dtype, layout, g, {x, hi, lo}))
+        return launch_split_rows(dtype, g, x, mask, hi, hi_cap, lo, lo_cap, st, bwd);
     switch (dtype) {
-    case 0: return split_t<float>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, st);
-    case 1: return split_t<f16>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, st);
-    default: return split_t<bf16>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, st);
+    case 0: return split_t<float>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+    case 1: return split_t<f16>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+    default: return split_t<bf16>(layout, g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
     }
 }
 
@@ -306,12 +314,13 @@ hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const
 }
 
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
-                          int hi_cap, int lo_cap, void* y, hipStream_t st) {
-    if (rows_fit(dtype, layout, g, {hi, lo, y})) return launch_combine_rows(dtype, g, hi, lo, mask, hi_cap, lo_cap, y, st);
+                          int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd) {
+    if (rows_fit(dtype, layout, g, {hi, lo, y}))
+        return launch_combine_rows(dtype, g, hi, lo, mask, hi_cap, lo_cap, y, st, bwd);
     switch (dtype) {
-    case 0: return combine_t<float>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, st);
-    case 1: return combine_t<f16>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, st);
-    default: return combine_t<bf16>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, st);
+    case 0: return combine_t<float>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+    case 1: return combine_t<f16>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+    default: return combine_t<bf16>(layout, g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
     }
 }
 

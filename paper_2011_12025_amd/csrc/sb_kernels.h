@@ -34,13 +34,16 @@ struct ConvArgs {
     int C_in, C_out, flags, hi_cap, lo_cap;
 };
 
+// bwd: the transposes for the backward pass instead: split of a gradient map
+// is BlockCombine transposed (low blocks get 2x2 sums), combine of gradient
+// stacks is BlockSample transposed (low values spread as quarters).
 hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask,
-                        void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t st);
+                        void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t st, bool bwd = false);
 // pm: how the halo is filled (PM_AVG, PM_STRIDED, PM_ZERO of sb_pixel.h)
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
                       const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
-                          const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st);
+                          const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd = false);
 // Device memory that a launch needs beyond its inputs and outputs, supplied
 // by the caller (at least the bytes that the matching *_ws_bytes function
 // returns for the same shapes, 256-byte aligned).
@@ -61,11 +64,11 @@ size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo&
 // launch_pad_rows with hp == nullptr pads the low blocks only (into lp).
 bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const void*> ptrs);
 hipError_t launch_split_rows(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap,
-                             void* lo, int lo_cap, hipStream_t st);
+                             void* lo, int lo_cap, hipStream_t st, bool bwd = false);
 hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp,
                            void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
 hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
-                               int hi_cap, int lo_cap, void* y, hipStream_t st);
+                               int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd = false);
 
 // Encoder kernels (channels-last fp16/bf16): block convolution K x K
 // (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
@@ -86,6 +89,22 @@ hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W
                          int C_out, int K, int S, int P, int flags, void* y, hipStream_t st);
 hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, int K, int S, int P, void* y,
                           hipStream_t st);
+
+// Backward pass (sb_backward.hip): BlockPad transposed, the block
+// convolution's gradient with respect to its padded input (dgrad, on the
+// general kernel; workspace: dgrad_ws_bytes) and to its weights and bias
+// (wgrad; workspace: wgrad_ws_bytes).  BlockCombine / BlockSample transposed
+// are launch_split / launch_combine with bwd.
+hipError_t launch_pad_bwd(int dtype, int layout, const Geo& g, const void* dhp, const void* dlp, const uint8_t* mask,
+                          void* dhi, void* dlo, int hi_cap, int lo_cap, int pm, hipStream_t st);
+size_t dgrad_ws_bytes(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap);
+hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, const void* dlo, const uint8_t* mask,
+                        const void* w, int C_in, int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws,
+                        hipStream_t st);
+size_t wgrad_ws_bytes(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias);
+hipError_t launch_wgrad(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const void* dho,
+                        const void* dlo, const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap,
+                        int lo_cap, Ws ws, hipStream_t st);
 
 // Heuristic downsampling policy: per-block scores [N*GH*GW] (fp32), then the
 // mask with khigh high blocks per image (at most policy_max_blocks() per image).

@@ -52,6 +52,25 @@ __device__ __forceinline__ uint4 avg_raw(uint4 a, uint4 b, uint4 c, uint4 d) {
     return vavg4<T, V>(va, vb, vc, vd).raw;
 }
 
+template <typename T>
+__device__ __forceinline__ uint4 sum_raw(uint4 a, uint4 b, uint4 c, uint4 d) {
+    constexpr int V = 16 / (int)sizeof(T);
+    Vec<T, V> va, vb, vc, vd;
+    va.raw = a;
+    vb.raw = b;
+    vc.raw = c;
+    vd.raw = d;
+    return vsum4<T, V>(va, vb, vc, vd).raw;
+}
+
+template <typename T>
+__device__ __forceinline__ uint4 quarter_raw(uint4 a) {
+    constexpr int V = 16 / (int)sizeof(T);
+    Vec<T, V> va;
+    va.raw = a;
+    return vquarter<T, V>(va).raw;
+}
+
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 // The block plan of a workgroup: the LDS table for masks of up to 1024
@@ -98,7 +117,8 @@ constexpr int MAXM = 4;
 // ---------------------------------------------------------------------------
 // split: x -> hi, lo
 // ---------------------------------------------------------------------------
-template <typename T, bool ONE>
+// BWD: the transpose of BlockCombine instead (a low block gets its cells' sums)
+template <typename T, bool ONE, bool BWD>
 __global__ __launch_bounds__(WG) void k_split_rows(const T* __restrict__ x, int C, int H, int W,
                                                    const uint8_t* __restrict__ mask, int bs, int B, int GH, int GW,
                                                    T* __restrict__ hi, int hi_cap, T* __restrict__ lo, int lo_cap) {
@@ -162,7 +182,8 @@ __global__ __launch_bounds__(WG) void k_split_rows(const T* __restrict__ x, int 
                     const int cell = cb + lane + 64 * m;
                     if (cell < cells) {
                         const int j = cell / CV, c = (cell - j * CV) * V;
-                        st_nt16(d + j * C + c, avg_raw<T>(v[m][0], v[m][1], v[m][2], v[m][3]));
+                        st_nt16(d + j * C + c, BWD ? sum_raw<T>(v[m][0], v[m][1], v[m][2], v[m][3])
+                                                   : avg_raw<T>(v[m][0], v[m][1], v[m][2], v[m][3]));
                     }
                 }
             }
@@ -173,7 +194,8 @@ __global__ __launch_bounds__(WG) void k_split_rows(const T* __restrict__ x, int 
 // ---------------------------------------------------------------------------
 // combine: hi, lo -> y (blocks past a stack's capacity are written as zeros)
 // ---------------------------------------------------------------------------
-template <typename T, bool ONE>
+// BWD: the transpose of BlockSample instead (a low value is spread as quarters)
+template <typename T, bool ONE, bool BWD>
 __global__ __launch_bounds__(WG) void k_combine_rows(const T* __restrict__ hi, const T* __restrict__ lo, int C,
                                                      int H, int W, const uint8_t* __restrict__ mask, int bs, int B,
                                                      int GH, int GW, int hi_cap, int lo_cap, T* __restrict__ y) {
@@ -215,6 +237,7 @@ __global__ __launch_bounds__(WG) void k_combine_rows(const T* __restrict__ hi, c
                         v[m][3] = ld_nt16(s1 + o + C);
                     } else {
                         v[m][0] = ld_nt16(s0 + j * C + c);
+                        if (BWD) v[m][0] = quarter_raw<T>(v[m][0]);
                         v[m][1] = v[m][2] = v[m][3] = v[m][0];
                     }
                 }
@@ -405,20 +428,20 @@ int rows_grid(long long waves) {
     return (int)(wgs < cap ? wgs : cap);
 }
 
-template <typename T, bool ONE>
+template <typename T, bool ONE, bool BWD>
 hipError_t split_rows(const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap, void* lo, int lo_cap,
                       hipStream_t st) {
     const long long jobs = g.B * (g.bs / 2);
-    hipLaunchKernelGGL((k_split_rows<T, ONE>), dim3(rows_grid(jobs)), dim3(WG), 0, st, (const T*)x, g.C, g.H, g.W,
-                       mask, g.bs, (int)g.B, g.GH, g.GW, (T*)hi, hi_cap, (T*)lo, lo_cap);
+    hipLaunchKernelGGL((k_split_rows<T, ONE, BWD>), dim3(rows_grid(jobs)), dim3(WG), 0, st, (const T*)x, g.C, g.H,
+                       g.W, mask, g.bs, (int)g.B, g.GH, g.GW, (T*)hi, hi_cap, (T*)lo, lo_cap);
     return hipGetLastError();
 }
 
-template <typename T, bool ONE>
+template <typename T, bool ONE, bool BWD>
 hipError_t combine_rows(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, int hi_cap, int lo_cap,
                         void* y, hipStream_t st) {
     const long long jobs = g.B * (g.bs / 2);
-    hipLaunchKernelGGL((k_combine_rows<T, ONE>), dim3(rows_grid(jobs)), dim3(WG), 0, st, (const T*)hi,
+    hipLaunchKernelGGL((k_combine_rows<T, ONE, BWD>), dim3(rows_grid(jobs)), dim3(WG), 0, st, (const T*)hi,
                        (const T*)lo, g.C, g.H, g.W, mask, g.bs, (int)g.B, g.GH, g.GW, hi_cap, lo_cap, (T*)y);
     return hipGetLastError();
 }
@@ -437,15 +460,21 @@ hipError_t pad_rows(const Geo& g, const void* hi, const void* lo, const uint8_t*
 
 template <typename T>
 hipError_t split_rows_t(const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap, void* lo, int lo_cap,
-                        hipStream_t st) {
-    return g.B <= 1024 ? split_rows<T, true>(g, x, mask, hi, hi_cap, lo, lo_cap, st)
-                       : split_rows<T, false>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
+                        bool bwd, hipStream_t st) {
+    if (bwd)
+        return g.B <= 1024 ? split_rows<T, true, true>(g, x, mask, hi, hi_cap, lo, lo_cap, st)
+                           : split_rows<T, false, true>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
+    return g.B <= 1024 ? split_rows<T, true, false>(g, x, mask, hi, hi_cap, lo, lo_cap, st)
+                       : split_rows<T, false, false>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
 }
 template <typename T>
 hipError_t combine_rows_t(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, int hi_cap, int lo_cap,
-                          void* y, hipStream_t st) {
-    return g.B <= 1024 ? combine_rows<T, true>(g, hi, lo, mask, hi_cap, lo_cap, y, st)
-                       : combine_rows<T, false>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
+                          void* y, bool bwd, hipStream_t st) {
+    if (bwd)
+        return g.B <= 1024 ? combine_rows<T, true, true>(g, hi, lo, mask, hi_cap, lo_cap, y, st)
+                           : combine_rows<T, false, true>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
+    return g.B <= 1024 ? combine_rows<T, true, false>(g, hi, lo, mask, hi_cap, lo_cap, y, st)
+                       : combine_rows<T, false, false>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
 }
 template <typename T>
 hipError_t pad_rows_t(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
@@ -468,20 +497,20 @@ bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const v
 }
 
 hipError_t launch_split_rows(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* hi, int hi_cap,
-                             void* lo, int lo_cap, hipStream_t st) {
+                             void* lo, int lo_cap, hipStream_t st, bool bwd) {
     switch (dtype) {
-    case 0: return split_rows_t<float>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
-    case 1: return split_rows_t<f16>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
-    default: return split_rows_t<bf16>(g, x, mask, hi, hi_cap, lo, lo_cap, st);
+    case 0: return split_rows_t<float>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+    case 1: return split_rows_t<f16>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
+    default: return split_rows_t<bf16>(g, x, mask, hi, hi_cap, lo, lo_cap, bwd, st);
     }
 }
 
 hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
-                               int hi_cap, int lo_cap, void* y, hipStream_t st) {
+                               int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd) {
     switch (dtype) {
-    case 0: return combine_rows_t<float>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
-    case 1: return combine_rows_t<f16>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
-    default: return combine_rows_t<bf16>(g, hi, lo, mask, hi_cap, lo_cap, y, st);
+    case 0: return combine_rows_t<float>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+    case 1: return combine_rows_t<f16>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
+    default: return combine_rows_t<bf16>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
     }
 }
 
