@@ -77,6 +77,10 @@ def _L():
         lib.orc_conv3x3_bwd_data.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, _fp, ctypes.c_int, _dp]
         lib.orc_conv3x3_bwd_weight.argtypes = [_fp, _fp, ctypes.c_long, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                                _dp, _dp]
+        lib.orc_pad_halo.argtypes = [_fp, _fp] + [ctypes.c_int] * 4 + [_u8p] + [ctypes.c_int] * 4 + [_fp, _fp]
+        lib.orc_conv_block_general.argtypes = [_fp, ctypes.c_long] + [ctypes.c_int] * 3 + [_fp] + \
+            [ctypes.c_int] * 3 + [_fp, ctypes.c_int, _dp]
+        lib.orc_maxpool_block.argtypes = [_fp, ctypes.c_long] + [ctypes.c_int] * 5 + [_fp]
         lib.orc_policy_scores.argtypes = [_fp] + [ctypes.c_int] * 6 + [_dp]
         lib.orc_policy_select.argtypes = [_dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _u8p]
         _lib = lib
@@ -317,6 +321,11 @@ def encoder(x, mask, image_block: int, weights: dict, dtype: str):
     N, C, H, W = h.shape
     bs = image_block // 4
     hi, lo = split(h, mask, bs, dtype)
+    return _stages(hi, lo, mask, bs, H, W, weights, dtype)
+
+
+def _stages(hi, lo, mask, bs: int, H: int, W: int, weights: dict, dtype: str):
+    """The four stages of two basic blocks on the stacks, then BlockCombine."""
     for si, (width, stride) in enumerate(zip(ENCODER_WIDTHS, ENCODER_STRIDES)):
         for bi in range(2):
             st = stride if bi == 0 else 1
@@ -465,3 +474,80 @@ def layer_backward(x, mask, bs: int, w, b, dy, dtype: str, sampling: str = "avg"
     dlp = round_to(conv3x3_backward_data(dlo_o, w), dtype)
     dhi, dlo = pad_backward(dhp, dlp, mask, bs, H, W, dtype, sampling)
     return split_backward(dhi, dlo, mask, bs, H, W, dtype), dw, db
+
+
+# ---------------------------------------------------------------------------
+# Wider halos: blockwise layers beyond 3x3 (test infrastructure)
+# ---------------------------------------------------------------------------
+
+def pad_halo(hi, lo, mask, bs: int, H: int, W: int, dtype: str, halo: int, sampling: str = "avg"):
+    """BlockPad with a halo of `halo` pixels (1 <= halo <= bs/2):
+    (hp [nh,C,bs+2h,bs+2h], lp [nl,C,bs/2+2h,bs/2+2h])."""
+    hi, lo = _f32(hi), _f32(lo)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    N = mask.shape[0]
+    _check_shape(mask, N, H, W, bs)
+    if not 1 <= halo <= bs // 2:
+        raise ValueError("halo must be between 1 and bs/2")
+    C = hi.shape[1] if hi.shape[0] else lo.shape[1]
+    hp = np.zeros((hi.shape[0], C, bs + 2 * halo, bs + 2 * halo), np.float32)
+    lp = np.zeros((lo.shape[0], C, bs // 2 + 2 * halo, bs // 2 + 2 * halo), np.float32)
+    _L().orc_pad_halo(_ptr(hi, _fp), _ptr(lo, _fp), N, C, H, W, _ptr(mask, _u8p), bs, _DT[dtype],
+                      SAMPLING[sampling], halo, _ptr(hp, _fp), _ptr(lp, _fp))
+    return hp, lp
+
+
+def conv_block_general(P, halo: int, w, stride: int = 1, dilation: int = 1, b=None):
+    """K x K (odd K) convolution at `stride` and `dilation` of a stack padded
+    by `halo`, centred on block pixel (stride*i, stride*j); fp64, unrounded."""
+    P, w = _f32(P), _f32(w)
+    S, Cin, pe, _ = P.shape
+    Cout, Cin2, K, _ = w.shape
+    E = pe - 2 * halo
+    assert Cin2 == Cin and K % 2 == 1 and dilation * (K - 1) // 2 <= halo and E % stride == 0
+    out = np.zeros((S, Cout, E // stride, E // stride), np.float64)
+    bp = None
+    if b is not None:
+        b = _f32(b)
+        bp = _ptr(b, _fp)
+    if S:
+        _L().orc_conv_block_general(_ptr(P, _fp), S, Cin, E, halo, _ptr(w, _fp), K, stride, dilation, bp, Cout,
+                                    _ptr(out, _dp))
+    return out
+
+
+def maxpool_block(P, halo: int, k: int, stride: int):
+    """k x k max-pooling at `stride` of a stack padded by `halo` (halo values
+    take part)."""
+    P = _f32(P)
+    S, C, pe, _ = P.shape
+    E = pe - 2 * halo
+    assert k % 2 == 1 and (k - 1) // 2 <= halo and E % stride == 0
+    out = np.zeros((S, C, E // stride, E // stride), np.float32)
+    if S:
+        _L().orc_maxpool_block(_ptr(P, _fp), S, C, E, halo, k, stride, _ptr(out, _fp))
+    return out
+
+
+def blockwise_stem(x, mask, image_block: int, w, b, dtype: str):
+    """The encoder's stem on image blocks: 7x7/2 convolution with a 3-pixel
+    BlockPad, bias, ReLU (rounded), then 3x3/2 max-pooling with a 1-pixel
+    BlockPad: (hi, lo) stacks at stride 4 (block side image_block / 4)."""
+    x = _f32(x)
+    N, C, H, W = x.shape
+    hi, lo = split(x, mask, image_block, dtype)
+    hp, lp = pad_halo(hi, lo, mask, image_block, H, W, dtype, 3)
+    sh = round_to(np.maximum(conv_block_general(hp, 3, w, 2, 1, b), 0.0), dtype)
+    sl = round_to(np.maximum(conv_block_general(lp, 3, w, 2, 1, b), 0.0), dtype)
+    bs2, H2, W2 = image_block // 2, H // 2, W // 2
+    ph, pl = pad_halo(sh, sl, mask, bs2, H2, W2, dtype, 1)
+    return maxpool_block(ph, 1, 3, 2), maxpool_block(pl, 1, 3, 2)
+
+
+def encoder_blockwise(x, mask, image_block: int, weights: dict, dtype: str):
+    """The ResNet-18 encoder with the blocks kept from the image on: the
+    stem and its max-pool run blockwise (blockwise_stem), then the stages as
+    in encoder()."""
+    N, C, H, W = np.asarray(x).shape
+    hi, lo = blockwise_stem(x, mask, image_block, weights["stem.w"], weights["stem.b"], dtype)
+    return _stages(hi, lo, mask, image_block // 4, H // 4, W // 4, weights, dtype)

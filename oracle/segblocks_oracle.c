@@ -175,8 +175,13 @@ void orc_split(const float* x, int N, int C, int H, int W, const uint8_t* mask,
 #define ORC_PAD_STRIDED 1
 #define ORC_PAD_ZERO 2
 
-void orc_pad_ex(const float* hi, const float* lo, int N, int C, int H, int W,
-                const uint8_t* mask, int bs, int dtype, int sampling, float* hp, float* lp)
+/* The same with a halo of p pixels (1 <= p <= bs/2, so that every halo pixel
+ * lies in the adjacent block): padded extent e + 2p, halo coordinates
+ * u, v in [-p, e + p), the neighbour in the direction of the pixel as above.
+ * Wider halos serve kernels larger than 3x3 (a 7x7 stem needs 3 pixels) and
+ * dilated kernels; p = 1 is BlockPad itself. */
+void orc_pad_halo(const float* hi, const float* lo, int N, int C, int H, int W,
+                  const uint8_t* mask, int bs, int dtype, int sampling, int p, float* hp, float* lp)
 {
     const int GH = H / bs, GW = W / bs, lb = bs / 2;
     const long B = (long)N * GH * GW;
@@ -190,14 +195,14 @@ void orc_pad_ex(const float* hi, const float* lo, int N, int C, int H, int W,
         const long k = ((long)n * GH + gy) * GW + gx;
         const int high = mask[k] != 0;
         const int e = high ? bs : lb;          /* own extent */
-        const int pe = e + 2;                  /* padded extent */
+        const int pe = e + 2 * p;              /* padded extent */
         const float* own = high ? hi + (long)slot[k] * C * bs * bs
                                 : lo + (long)slot[k] * C * lb * lb;
         float* out = high ? hp + (long)slot[k] * C * pe * pe
                           : lp + (long)slot[k] * C * pe * pe;
         for (int c = 0; c < C; ++c)
-        for (int u = -1; u <= e; ++u)
-        for (int v = -1; v <= e; ++v) {
+        for (int u = -p; u < e + p; ++u)
+        for (int v = -p; v < e + p; ++v) {
             const int dy = u < 0 ? -1 : (u >= e ? 1 : 0);
             const int dx = v < 0 ? -1 : (v >= e ? 1 : 0);
             float val;
@@ -230,10 +235,16 @@ void orc_pad_ex(const float* hi, const float* lo, int N, int C, int H, int W,
                     }
                 }
             }
-            out[((long)c * pe + (u + 1)) * pe + (v + 1)] = val;
+            out[((long)c * pe + (u + p)) * pe + (v + p)] = val;
         }
     }
     free(slot);
+}
+
+void orc_pad_ex(const float* hi, const float* lo, int N, int C, int H, int W,
+                const uint8_t* mask, int bs, int dtype, int sampling, float* hp, float* lp)
+{
+    orc_pad_halo(hi, lo, N, C, H, W, mask, bs, dtype, sampling, 1, hp, lp);
 }
 
 /* BlockPad with average sampling, the module as the paper uses it. */
@@ -650,4 +661,59 @@ void orc_conv3x3_bwd_weight(const float* P, const float* dO, long S, int Cin, in
             }
             db[co] += acc;
         }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Layers beyond 3x3 on block stacks: every padded layer of the network can  */
+/* run blockwise once BlockPad supplies a halo as wide as the kernel reaches */
+/* (the blocks then persist from the image to the last stage).              */
+/* ------------------------------------------------------------------------ */
+
+/* P[S][Cin][E+2p][E+2p] (halo p), w[Cout][Cin][K][K] (K odd), stride st
+ * dividing E, dilation dl with dl*(K-1)/2 <= p, bias or NULL
+ * -> out[S][Cout][E/st][E/st] (fp64):
+ *    out[i][j] = bias + sum_ci sum_ky sum_kx w * P[st*i + dl*ky + o][st*j + dl*kx + o],
+ *    o = p - dl*(K-1)/2,
+ * i.e. the kernel centred on block pixel (st*i, st*j); order ci, ky, kx. */
+void orc_conv_block_general(const float* P, long S, int Cin, int E, int p, const float* w, int K, int st, int dl,
+                            const float* bias, int Cout, double* out)
+{
+    const int pe = E + 2 * p, Eo = E / st, o = p - dl * (K - 1) / 2;
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (long s = 0; s < S; ++s)
+    for (int co = 0; co < Cout; ++co)
+    for (int i = 0; i < Eo; ++i)
+    for (int j = 0; j < Eo; ++j) {
+        double acc = 0.0;
+        for (int ci = 0; ci < Cin; ++ci) {
+            const float* q = P + ((s * Cin + ci) * pe) * (long)pe;
+            const float* wk = w + ((long)co * Cin + ci) * K * K;
+            for (int ky = 0; ky < K; ++ky)
+                for (int kx = 0; kx < K; ++kx)
+                    acc += (double)wk[ky * K + kx] * (double)q[(st * i + dl * ky + o) * pe + (st * j + dl * kx + o)];
+        }
+        if (bias) acc += (double)bias[co];
+        out[((s * Cout + co) * Eo + i) * (long)Eo + j] = acc;
+    }
+}
+
+/* P[S][C][E+2p][E+2p] -> out[S][C][E/st][E/st]: maximum over the K x K window
+ * centred on block pixel (st*i, st*j) (o = p - (K-1)/2), halo values included
+ * (zeros at the image border, which never exceed a ReLU output). */
+void orc_maxpool_block(const float* P, long S, int C, int E, int p, int K, int st, float* out)
+{
+    const int pe = E + 2 * p, Eo = E / st, o = p - (K - 1) / 2;
+    for (long s = 0; s < S; ++s)
+    for (int c = 0; c < C; ++c)
+    for (int i = 0; i < Eo; ++i)
+    for (int j = 0; j < Eo; ++j) {
+        const float* q = P + ((s * C + c) * pe) * (long)pe;
+        float m = -INFINITY;
+        for (int ky = 0; ky < K; ++ky)
+            for (int kx = 0; kx < K; ++kx) {
+                const float v = q[(st * i + ky + o) * pe + (st * j + kx + o)];
+                if (v > m) m = v;
+            }
+        out[((s * C + c) * Eo + i) * (long)Eo + j] = m;
+    }
 }
