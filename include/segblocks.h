@@ -254,6 +254,42 @@ int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H
                                    int C_out, size_t* bytes);
 
 /* ------------------------------------------------------------------------
+ * Wider halos (paper: Method > Block modules -- BlockPad replaces the zero
+ * padding of every padded layer and the blocks shrink with the map, so a
+ * network can keep its blocks from the image on).  A K x K layer needs a
+ * halo of (K-1)/2 pixels, a dilated one dilation*(K-1)/2.
+ * ------------------------------------------------------------------------ */
+
+/* BlockPad with a halo of `halo` pixels, 1 <= halo <= bs/2 (every halo pixel
+ * then lies in the adjacent block, taken by the rules of segblocks_pad_ex):
+ * hi [nh,C,bs,bs], lo [nl,C,lb,lb] -> hi_pad [nh,C,bs+2h,bs+2h],
+ * lo_pad [nl,C,lb+2h,lb+2h].  halo = 1 is segblocks_pad_ex. */
+int segblocks_pad_halo(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H,
+                       int W, const uint8_t* mask, int bs, int halo, int sampling, void* hi_pad,
+                       void* lo_pad, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* K x K convolution (K odd) at stride 1 or 2 with dilation on stacks padded
+ * by `halo` >= dilation*(K-1)/2 (e.g. the 7x7/2 stem on image blocks with a
+ * 3-pixel halo):
+ *   out[s,co,i,j] = bias[co] + sum w[co,ci,ky,kx] *
+ *                   pad[s,ci, st*i + dil*ky + o, st*j + dil*kx + o],  o = halo - dil*(K-1)/2
+ * -> hi_out [nh,C_out,bs/st,bs/st], lo_out [nl,C_out,lb/st,lb/st];
+ * weight [C_out][C_in][K][K] in the call's memory format (OHWI for
+ * SB_NHWC), bias [C_out] or NULL, flags: SB_FLAG_RELU.  H, W, bs describe
+ * the unpadded map.  fp32 sums, one rounding. */
+int segblocks_conv_halo(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C_in,
+                        int H, int W, const uint8_t* mask, int bs, int halo, const void* weight,
+                        const void* bias, int C_out, int ksize, int stride, int dilation, int flags,
+                        void* hi_out, void* lo_out, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* K x K max-pooling (K odd) at stride 1 or 2 of stacks padded by
+ * halo >= (K-1)/2; the halo values take part (zeros at the image border,
+ * which never exceed a ReLU output).  Same shapes as segblocks_conv_halo. */
+int segblocks_maxpool_halo(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C,
+                           int H, int W, const uint8_t* mask, int bs, int halo, int ksize, int stride,
+                           void* hi_out, void* lo_out, int hi_cap, int lo_cap, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Backward pass (the block modules and the block convolution are linear maps;
  * these are their transposes, for training through the block-conv path).
  * For y = combine(conv3x3(pad(split(x)))) and an output gradient dy:

@@ -21,7 +21,8 @@ from . import _binding as _b
 __all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "block_conv_ex", "layer", "conv2d",
            "maxpool", "layout_of", "block_conv3x3_workspace_size", "block_conv_ex_workspace_size",
            "layer_workspace_size", "policy_heuristic", "combine_backward", "split_backward", "pad_backward",
-           "conv3x3_backward_data", "conv3x3_backward_weight", "layer_backward"]
+           "conv3x3_backward_data", "conv3x3_backward_weight", "layer_backward", "pad_halo", "conv_halo",
+           "maxpool_halo"]
 
 _DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
 
@@ -449,3 +450,57 @@ def layer_backward(x: torch.Tensor, mask: torch.Tensor, bs: int, weight: torch.T
     dhp, dlp = conv3x3_backward_data(dho, dlo_o, mask, bs, H, W, weight, layout=layout)
     dhi, dlo = pad_backward(dhp, dlp, mask, bs, H, W, layout=layout, sampling=sampling)
     return split_backward(dhi, dlo, mask, bs, H, W, layout=layout), dw, db
+
+
+# ---------------------------------------------------------------------------
+# Wider halos: layers beyond 3x3 on block stacks
+# ---------------------------------------------------------------------------
+
+def pad_halo(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, halo: int,
+             layout=None, sampling: str = "avg"):
+    """BlockPad with a halo of `halo` pixels: (hi_pad, lo_pad)."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hi, lo)
+    C, N = ref.shape[1], mask.shape[0]
+    hp = _empty((hi.shape[0], C, bs + 2 * halo, bs + 2 * halo), ref, layout)
+    lp = _empty((lo.shape[0], C, bs // 2 + 2 * halo, bs // 2 + 2 * halo), ref, layout)
+    _b.call("segblocks_pad_halo", _ptr(hi), _ptr(lo), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, halo,
+            _SAMPLING[sampling], _ptr(hp), _ptr(lp), hi.shape[0], lo.shape[0], _stream(ref))
+    return hp, lp
+
+
+def conv_halo(hp: torch.Tensor, lp: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, halo: int,
+              weight: torch.Tensor, bias=None, stride: int = 1, dilation: int = 1, relu: bool = False, layout=None):
+    """K x K (K = weight.shape[2], odd) convolution at `stride` / `dilation` of
+    stacks padded by `halo`: (hi_out, lo_out) with sides bs/stride, bs/(2 stride)."""
+    mask = _mask(mask)
+    ref = hp if hp.shape[0] else lp
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hp, lp)
+    k = weight.shape[2]
+    C_in, C_out, N = ref.shape[1], weight.shape[0], mask.shape[0]
+    weight = _weight(weight, layout, k)
+    bias = None if bias is None else bias.contiguous()
+    ho = _empty((hp.shape[0], C_out, bs // stride, bs // stride), ref, layout)
+    lo = _empty((lp.shape[0], C_out, bs // 2 // stride, bs // 2 // stride), ref, layout)
+    _b.call("segblocks_conv_halo", _ptr(hp), _ptr(lp), _dt(ref), layout, N, C_in, H, W, _ptr(mask), bs, halo,
+            _ptr(weight), _ptr(bias), C_out, k, stride, dilation, _b.SB_FLAG_RELU if relu else 0, _ptr(ho), _ptr(lo),
+            hp.shape[0], lp.shape[0], _stream(ref))
+    return ho, lo
+
+
+def maxpool_halo(hp: torch.Tensor, lp: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int, halo: int,
+                 k: int = 3, stride: int = 2, layout=None):
+    """k x k max-pooling at `stride` of stacks padded by `halo`: (hi_out, lo_out)."""
+    mask = _mask(mask)
+    ref = hp if hp.shape[0] else lp
+    layout = layout_of(ref) if layout is None else layout
+    _check_layout(layout, hp, lp)
+    C, N = ref.shape[1], mask.shape[0]
+    ho = _empty((hp.shape[0], C, bs // stride, bs // stride), ref, layout)
+    lo = _empty((lp.shape[0], C, bs // 2 // stride, bs // 2 // stride), ref, layout)
+    _b.call("segblocks_maxpool_halo", _ptr(hp), _ptr(lp), _dt(ref), layout, N, C, H, W, _ptr(mask), bs, halo, k,
+            stride, _ptr(ho), _ptr(lo), hp.shape[0], lp.shape[0], _stream(ref))
+    return ho, lo

@@ -27,7 +27,7 @@ EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_pad
            "segblocks_combine_backward", "segblocks_split_backward", "segblocks_pad_backward",
            "segblocks_conv3x3_backward_data", "segblocks_conv3x3_backward_data_workspace_size",
            "segblocks_conv3x3_backward_weight", "segblocks_conv3x3_backward_weight_workspace_size",
-           "segblocks_last_error"]
+           "segblocks_pad_halo", "segblocks_conv_halo", "segblocks_maxpool_halo", "segblocks_last_error"]
 
 SB_OK, SB_EINVAL, SB_ESHAPE, SB_EHIP, SB_ENOMEM = 0, -1, -2, -3, -4
 
@@ -59,6 +59,10 @@ _SIGS = {
     "segblocks_conv3x3_backward_weight": [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P, _I, _I, _P,
                                           _Z, _P],
     "segblocks_conv3x3_backward_weight_workspace_size": [_I] * 11 + [_ZP],
+    "segblocks_pad_halo": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _I, _I, _P],
+    "segblocks_conv_halo": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P, _I, _I, _I, _I, _I, _P, _P, _I, _I,
+                            _P],
+    "segblocks_maxpool_halo": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _I, _P],
     "segblocks_block_conv3x3_workspace_size": [_I] * 10 + [_ZP],
     "segblocks_block_conv_ex_workspace_size": [_I] * 12 + [_ZP],
     "segblocks_layer_workspace_size": [_I] * 8 + [_ZP],

@@ -470,6 +470,93 @@ int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H
 }
 
 // ---------------------------------------------------------------------------
+// Wider halos: layers beyond 3x3 on block stacks
+// ---------------------------------------------------------------------------
+
+int segblocks_pad_halo(const void* hi, const void* lo, int dtype, int layout, int N, int C, int H, int W,
+                       const uint8_t* mask, int bs, int halo, int sampling, void* hi_pad, void* lo_pad, int hi_cap,
+                       int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_pad_halo";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (halo < 1 || halo > bs / 2) return fail(SB_ESHAPE, fn, "halo must be between 1 and bs/2 = %d (got %d)", bs / 2, halo);
+    if (sampling != SB_PAD_AVG && sampling != SB_PAD_STRIDED && sampling != SB_PAD_ZERO)
+        return fail(SB_EINVAL, fn, "bad sampling %d", sampling);
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
+        (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2, ph = bs + 2 * halo, pl = lb + 2 * halo;
+    const Range rh{hi, hi_cap * (long long)C * bs * bs * es}, rl{lo, lo_cap * (long long)C * lb * lb * es};
+    const Range rhp{hi_pad, hi_cap * (long long)C * ph * ph * es}, rlp{lo_pad, lo_cap * (long long)C * pl * pl * es};
+    if (any_overlap({rhp, rlp}, {rh, rl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_pad(dtype, layout, g, hi, lo, mask, hi_pad, lo_pad, hi_cap, lo_cap, sampling,
+                                         stream, halo));
+}
+
+int segblocks_conv_halo(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C_in, int H, int W,
+                        const uint8_t* mask, int bs, int halo, const void* weight, const void* bias, int C_out,
+                        int ksize, int stride, int dilation, int flags, void* hi_out, void* lo_out, int hi_cap,
+                        int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_conv_halo";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if (ksize < 1 || ksize % 2 == 0) return fail(SB_EINVAL, fn, "ksize must be odd (got %d)", ksize);
+    if (stride != 1 && stride != 2) return fail(SB_EINVAL, fn, "stride must be 1 or 2 (got %d)", stride);
+    if (dilation < 1) return fail(SB_EINVAL, fn, "dilation must be >= 1 (got %d)", dilation);
+    if (halo < 1 || halo > bs / 2) return fail(SB_ESHAPE, fn, "halo must be between 1 and bs/2 (got %d)", halo);
+    if (dilation * (ksize - 1) / 2 > halo)
+        return fail(SB_ESHAPE, fn, "the kernel reaches %d pixels beyond the block, the halo is %d",
+                    dilation * (ksize - 1) / 2, halo);
+    if ((bs / 2) % stride) return fail(SB_ESHAPE, fn, "stride %d does not divide the low block side %d", stride, bs / 2);
+    if (flags & ~SB_FLAG_RELU) return fail(SB_EINVAL, fn, "unknown flags 0x%x", flags);
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
+        (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2, ph = bs + 2 * halo, pl = lb + 2 * halo;
+    const long long bo = bs / stride, lo_e = lb / stride;
+    const Range rhp{hi_pad, hi_cap * (long long)C_in * ph * ph * es}, rlp{lo_pad, lo_cap * (long long)C_in * pl * pl * es};
+    const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
+    const Range rho{hi_out, hi_cap * (long long)C_out * bo * bo * es};
+    const Range rlo{lo_out, lo_cap * (long long)C_out * lo_e * lo_e * es};
+    if (any_overlap({rho, rlo}, {rhp, rlp, rw, rb, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_conv_halo(dtype, layout, g, hi_pad, lo_pad, mask, halo, weight, bias, C_in, C_out,
+                                               ksize, stride, dilation, flags, hi_out, lo_out, hi_cap, lo_cap, stream));
+}
+
+int segblocks_maxpool_halo(const void* hi_pad, const void* lo_pad, int dtype, int layout, int N, int C, int H, int W,
+                           const uint8_t* mask, int bs, int halo, int ksize, int stride, void* hi_out, void* lo_out,
+                           int hi_cap, int lo_cap, hipStream_t stream) {
+    const char* fn = "segblocks_maxpool_halo";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C, H, W, mask, bs, g))) return s;
+    if (ksize < 1 || ksize % 2 == 0) return fail(SB_EINVAL, fn, "ksize must be odd (got %d)", ksize);
+    if (stride != 1 && stride != 2) return fail(SB_EINVAL, fn, "stride must be 1 or 2 (got %d)", stride);
+    if (halo < 1 || halo > bs / 2 || (ksize - 1) / 2 > halo)
+        return fail(SB_ESHAPE, fn, "halo %d must cover the window (%d) and be at most bs/2", halo, (ksize - 1) / 2);
+    if ((bs / 2) % stride) return fail(SB_ESHAPE, fn, "stride %d does not divide the low block side %d", stride, bs / 2);
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi_pad", hi_pad, hi_cap)) ||
+        (s = check_stack(fn, "lo_pad", lo_pad, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2, ph = bs + 2 * halo, pl = lb + 2 * halo;
+    const long long bo = bs / stride, lo_e = lb / stride;
+    const Range rhp{hi_pad, hi_cap * (long long)C * ph * ph * es}, rlp{lo_pad, lo_cap * (long long)C * pl * pl * es};
+    const Range rho{hi_out, hi_cap * (long long)C * bo * bo * es}, rlo{lo_out, lo_cap * (long long)C * lo_e * lo_e * es};
+    if (any_overlap({rho, rlo}, {rhp, rlp, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers overlap inputs or each other");
+    return hip_status(fn, sb::launch_maxpool_halo(dtype, layout, g, hi_pad, lo_pad, mask, halo, ksize, stride, hi_out,
+                                                  lo_out, hi_cap, lo_cap, stream));
+}
+
+// ---------------------------------------------------------------------------
 // Backward pass
 // ---------------------------------------------------------------------------
 

@@ -137,7 +137,8 @@ __global__ __launch_bounds__(WG) void k_split(const T* __restrict__ x, int C, in
 template <typename T, int L, int V>
 __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* __restrict__ lo, int C, int H, int W,
                                             const uint8_t* __restrict__ mask, int bs, int B, int Gh, int Gl,
-                                            T* __restrict__ hp, T* __restrict__ lp, int hi_cap, int lo_cap, int pm) {
+                                            T* __restrict__ hp, T* __restrict__ lp, int hi_cap, int lo_cap, int pm,
+                                            int halo) {
     bool high;
     int slot, piece;
     slot_piece((int)blockIdx.x, hi_cap, Gh, Gl, high, slot, piece);
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* _
     const int GH = H / bs, GW = W / bs, lb = bs >> 1;
     int n, gy, gx;
     block_coords(k, GH, GW, n, gy, gx);
-    const int e = high ? bs : lb, pe = e + 2;
+    const int e = high ? bs : lb, pe = e + 2 * halo;
     const int items = pe * pe * C / V;
     const int it = piece * PIECE + (int)threadIdx.x;
     const Neigh nb = wave_neighbourhood<true>(wm, GH, GW, n, gy, gx);
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(WG) void k_pad(const T* __restrict__ hi, const T* _
     item_coords<L, V>(it, pe, C, u, v, c);
     T* dst = (high ? hp : lp) + (size_t)slot * C * pe * pe + (size_t)it * V;
     if constexpr (L == NHWC || V == 1) {
-        const Src<T> s = packed_src<T, L>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - 1, v - 1, c, pm);
+        const Src<T> s = packed_src<T, L>(hi, lo, C, bs, nb, hi_cap, lo_cap, u - halo, v - halo, c, pm);
         SrcBatch<T, V, 1> b;
         b.issue(0, s);
         vstore<T, V>(dst, b.value(0));
@@ -231,13 +232,13 @@ hipError_t run_split(const Geo& g, const void* x, const uint8_t* mask, void* hi,
 
 template <typename T, int L, int V>
 hipError_t run_pad(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                   int hi_cap, int lo_cap, int pm, hipStream_t st) {
-    const int ph = g.bs + 2, pl = g.bs / 2 + 2;
+                   int hi_cap, int lo_cap, int pm, int halo, hipStream_t st) {
+    const int ph = g.bs + 2 * halo, pl = g.bs / 2 + 2 * halo;
     const int Gh = pieces((long long)ph * ph * g.C / V), Gl = pieces((long long)pl * pl * g.C / V);
     const long long blocks = (long long)hi_cap * Gh + (long long)lo_cap * Gl;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((k_pad<T, L, V>), dim3((unsigned)blocks), dim3(WG), 0, st, (const T*)hi, (const T*)lo, g.C,
-                       g.H, g.W, mask, g.bs, (int)g.B, Gh, Gl, (T*)hp, (T*)lp, hi_cap, lo_cap, pm);
+                       g.H, g.W, mask, g.bs, (int)g.B, Gh, Gl, (T*)hp, (T*)lp, hi_cap, lo_cap, pm, halo);
     return hipGetLastError();
 }
 
@@ -266,14 +267,14 @@ hipError_t split_t(int layout, const Geo& g, const void* x, const uint8_t* mask,
 
 template <typename T>
 hipError_t pad_t(int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
-                 int hi_cap, int lo_cap, int pm, hipStream_t st) {
+                 int hi_cap, int lo_cap, int pm, int halo, hipStream_t st) {
     constexpr int VM = 16 / (int)sizeof(T);
     const bool al = aligned16(hi) && aligned16(lo) && aligned16(hp) && aligned16(lp);
     if (layout == NHWC) {
-        if (al && g.C % VM == 0) return run_pad<T, NHWC, VM>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
-        return run_pad<T, NHWC, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+        if (al && g.C % VM == 0) return run_pad<T, NHWC, VM>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
+        return run_pad<T, NHWC, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
     }
-    return run_pad<T, NCHW, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    return run_pad<T, NCHW, 1>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
 }
 
 template <typename T>
@@ -303,13 +304,13 @@ hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, cons
 }
 
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
-                      void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st) {
-    if (rows_fit(dtype, layout, g, {hi, lo, hp, lp}))
+                      void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st, int halo) {
+    if (halo == 1 && rows_fit(dtype, layout, g, {hi, lo, hp, lp}))
         return launch_pad_rows(dtype, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     switch (dtype) {
-    case 0: return pad_t<float>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
-    case 1: return pad_t<f16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
-    default: return pad_t<bf16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
+    case 0: return pad_t<float>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
+    case 1: return pad_t<f16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
+    default: return pad_t<bf16>(layout, g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, halo, st);
     }
 }
 

@@ -39,9 +39,11 @@ struct ConvArgs {
 // stacks is BlockSample transposed (low values spread as quarters).
 hipError_t launch_split(int dtype, int layout, const Geo& g, const void* x, const uint8_t* mask,
                         void* hi, int hi_cap, void* lo, int lo_cap, hipStream_t st, bool bwd = false);
-// pm: how the halo is filled (PM_AVG, PM_STRIDED, PM_ZERO of sb_pixel.h)
+// pm: how the halo is filled (PM_AVG, PM_STRIDED, PM_ZERO of sb_pixel.h);
+// halo: its width in pixels (1 <= halo <= bs/2)
 hipError_t launch_pad(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
-                      const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
+                      const uint8_t* mask, void* hp, void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st,
+                      int halo = 1);
 hipError_t launch_combine(int dtype, int layout, const Geo& g, const void* hi, const void* lo,
                           const uint8_t* mask, int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd = false);
 // Device memory that a launch needs beyond its inputs and outputs, supplied
@@ -105,6 +107,16 @@ size_t wgrad_ws_bytes(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap,
 hipError_t launch_wgrad(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const void* dho,
                         const void* dlo, const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap,
                         int lo_cap, Ws ws, hipStream_t st);
+
+// Layers beyond 3x3 on stacks padded with a halo of `halo` pixels
+// (sb_halo.hip): K x K convolution (K odd) at stride st with dilation dl, and
+// K x K max-pooling; g.C is the channel count of the max-pooling.
+hipError_t launch_conv_halo(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const uint8_t* mask,
+                            int halo, const void* w, const void* bias, int C_in, int C_out, int K, int st, int dl,
+                            int flags, void* ho, void* lo, int hi_cap, int lo_cap, hipStream_t s);
+hipError_t launch_maxpool_halo(int dtype, int layout, const Geo& g, const void* hp, const void* lp,
+                               const uint8_t* mask, int halo, int K, int st, void* ho, void* lo, int hi_cap,
+                               int lo_cap, hipStream_t s);
 
 // Heuristic downsampling policy: per-block scores [N*GH*GW] (fp32), then the
 // mask with khigh high blocks per image (at most policy_max_blocks() per image).

@@ -13,7 +13,7 @@ from __future__ import annotations
 import torch
 
 from . import (block_conv3x3, block_conv3x3_workspace_size, block_conv_ex, block_conv_ex_workspace_size, combine,
-               conv2d, count, maxpool, split)
+               conv2d, conv_halo, count, maxpool, maxpool_halo, pad_halo, split)
 from ._binding import SB_NHWC
 
 WIDTHS = (64, 128, 256, 512)
@@ -24,10 +24,14 @@ class BlockEncoder:
     """weights: name -> OIHW tensor as drawn by inputs.encoder_weights (any
     device); they are moved to `device` as channels_last (OHWI memory)."""
 
-    def __init__(self, weights: dict, image_block: int, device="cuda"):
+    def __init__(self, weights: dict, image_block: int, device="cuda", blockwise_stem: bool = False):
         if image_block % 64:
             raise ValueError("the image block must be a multiple of 64 pixels (block side >= 2 at stride 32)")
         self.image_block = image_block
+        # blockwise_stem: split the image itself and run the 7x7/2 stem (3-pixel
+        # BlockPad) and the 3x3/2 max-pool (1-pixel BlockPad) on the blocks, so
+        # that the blocks persist from the image to the last stage
+        self.blockwise_stem = blockwise_stem
         cl = torch.channels_last
         self.w = {k: (v.to(device).contiguous(memory_format=cl) if v.dim() == 4 else v.to(device).contiguous())
                   for k, v in weights.items()}
@@ -57,12 +61,30 @@ class BlockEncoder:
                 cin = width
         return need
 
+    def stem_blocks(self, x: torch.Tensor, mask: torch.Tensor, counts):
+        """The blockwise stem: image blocks -> stacks at stride 4."""
+        N, C, H, W = x.shape
+        blk = self.image_block
+        hi, lo = split(x, mask, blk, counts=counts)
+        hp, lp = pad_halo(hi, lo, mask, blk, H, W, 3)
+        sh, sl = conv_halo(hp, lp, mask, blk, H, W, 3, self.w["stem.w"], self.w["stem.b"], stride=2, relu=True)
+        ph, pl = pad_halo(sh, sl, mask, blk // 2, H // 2, W // 2, 1)
+        return maxpool_halo(ph, pl, mask, blk // 2, H // 2, W // 2, 1, 3, 2)
+
     def stages(self, h: torch.Tensor, mask: torch.Tensor, counts=None) -> torch.Tensor:
+        """h: the stage-1 map [N, 64, H/4, W/4] -> [N, 512, H/32, W/32]."""
         N, C, H, W = h.shape
+        hi, lo = split(h, mask, self.image_block // 4, counts=counts)
+        return self.stages_on_stacks(hi, lo, mask, H, W)
+
+    def stages_on_stacks(self, hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, H: int, W: int):
+        """The four stages on the stage-1 stacks (H x W: the stage-1 map), then
+        BlockCombine."""
+        N = mask.shape[0]
         bs = self.image_block // 4
-        hi, lo = split(h, mask, bs, counts=counts)
-        nbytes = self.workspace_bytes(N, H, W, h.dtype, (hi.shape[0], lo.shape[0]))
-        ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=h.device) if nbytes else None
+        ref = hi if hi.shape[0] else lo
+        nbytes = self.workspace_bytes(N, H, W, ref.dtype, (hi.shape[0], lo.shape[0]))
+        ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=ref.device) if nbytes else None
         for si, (width, stride) in enumerate(zip(WIDTHS, STRIDES)):
             for bi in range(2):
                 st = stride if bi == 0 else 1
@@ -88,6 +110,9 @@ class BlockEncoder:
         of the mask, else taken with segblocks_count (one host sync)."""
         if counts is None:
             counts = count(mask)
+        if self.blockwise_stem:
+            hi, lo = self.stem_blocks(x, mask, counts)
+            return self.stages_on_stacks(hi, lo, mask, x.shape[2] // 4, x.shape[3] // 4)
         return self.stages(self.stem(x), mask, counts)
 
     def capture(self, x: torch.Tensor, mask: torch.Tensor, counts):
