@@ -241,10 +241,10 @@ int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, i
 /* Workspace sizes (bytes, HOST out-parameter) of segblocks_block_conv3x3,
  * segblocks_block_conv_ex and segblocks_layer for the given shapes and
  * stack capacities on the current device; the arguments mean what they mean
- * in those calls and are validated the same way.  The size is the one of
- * flags without the BlockPad alternatives, which need no more.  It assumes
- * 16-byte aligned buffers (a call with less aligned buffers takes a route that needs
- * no more).  Pure host functions: nothing is launched. */
+ * in those calls and are validated the same way.  The size covers every
+ * flag combination (a call checks only what its own route needs) and assumes
+ * 16-byte aligned buffers (a call with less aligned buffers takes a route
+ * that needs no more).  Pure host functions: nothing is launched. */
 int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
                                            int bs, int C_out, int hi_cap, int lo_cap, size_t* bytes);
 int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,

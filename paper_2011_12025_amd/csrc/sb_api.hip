@@ -435,9 +435,14 @@ int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_i
     int s;
     if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
         return s;
+    // the most any flags need: average sampling may take the resident kernel
+    // (no workspace), the BlockPad alternatives then take the GEMM
     sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, hi_cap,
                    lo_cap};
-    *bytes = sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a);
+    size_t n = sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a);
+    a.flags = SB_FLAG_PAD_STRIDED;
+    const size_t n2 = sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a);
+    *bytes = n > n2 ? n : n2;
     g_err.clear();
     return SB_OK;
 }
@@ -464,7 +469,10 @@ int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H
     int s;
     if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g))) return s;
     sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, 0, 0};
-    *bytes = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
+    size_t n = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
+    a.flags = SB_FLAG_PAD_STRIDED;
+    const size_t n2 = sb::conv_ws_bytes(dtype, layout, sb::SRC_DENSE, sb::DST_DENSE, g, a);
+    *bytes = n > n2 ? n : n2;
     g_err.clear();
     return SB_OK;
 }

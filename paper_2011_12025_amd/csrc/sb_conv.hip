@@ -537,11 +537,9 @@ hipError_t layer_via_packed(int dtype, const Geo& g, const uint8_t* mask, const 
 }  // namespace
 
 size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo& g, const ConvArgs& a) {
-    // packed stacks: the GEMM's need also where the resident kernel takes the call
-    // with average sampling, since the BlockPad alternatives go to the GEMM
+    if (conv_res_fits_shape(dtype, layout, g, a)) return 0;
     if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits_shape(dtype, layout, g, a))
         return igemm_ws_bytes(g, a, 3, 1);
-    if (conv_res_fits_shape(dtype, layout, g, a)) return 0;
     if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a))
         return packed_layout(g, a).total;
     return 0;

@@ -3,9 +3,14 @@
 // 32 or 64 (the early, bandwidth-bound layers of the network).
 //
 // One 8-wave workgroup per CU computes a 64-output-channel slice and walks a
-// static list of tiles.  A tile is a group of image rows of one block: R rows
-// of a high block or R/2 rows of a low block (R = 8 for blocks of 32, 4 for
-// blocks of 64), so every tile covers the same image area.  The padded input
+// static list of tiles.  A tile is a group of rows of one block: R rows of a
+// high block (R = 8 for blocks of 32, 4 for blocks of 64) or, from packed
+// stacks, 2R rows of a low block, so every tile has the same number of
+// output pixels and a low block has a quarter of a high block's tiles (from
+// the dense map, R/2 low rows; see res_tile).  The list holds the high
+// blocks' tiles, then the low blocks', in slot order; its length follows the
+// class counts of the mask, so the work of a launch falls with the
+// low-resolution fraction.  The padded input
 // tile (all input channels, 128 bytes per pixel) is triple-buffered in LDS
 // and the waves are specialised:
 //
@@ -108,11 +113,23 @@ struct RTile {
     float inv_pe;
 };
 
+// Tile `tile` of the class-major list: first the high blocks' tiles (Gh per
+// block, R image rows each), then the low blocks' (Gl per block, RL low rows
+// each), in slot order.  nth = high tiles in the list.  From packed or padded
+// stacks RL = 2R (the same pixels as a high tile, so a low block costs a
+// quarter of a high one); from the dense map RL = R/2 (a low tile's pixels
+// are 2x2 averages of image pixels, staged through registers, and 2R rows of
+// them take three rounds of loads where R/2 rows take one).
 template <int SRC, int DST, bool ONE>
-__device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const WaveMaskT<ONE>& wm, int R, int G,
-                                         int tile, RTile& t, Neigh& nb) {
-    const int k = tile / G;
-    const int grp = tile - k * G;
+__device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const WaveMaskT<ONE>& wm, int R, int RL,
+                                         int Gh, int Gl, int nth, int tile, RTile& t, Neigh& nb) {
+    const bool high = tile < nth;
+    const int G = high ? Gh : Gl;
+    const int q = high ? tile : tile - nth;
+    const int slot = q / G;
+    const int grp = q - slot * G;
+    const int k = wm.find_nth(slot, high);
+    if (k < 0) return false;
     const int per = g.GH * g.GW;
     t.n = k / per;
     const int rem = k - t.n * per;
@@ -120,11 +137,10 @@ __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const 
     t.gx = rem - t.gy * g.GW;
     constexpr bool NEED_SLOTS = !(SRC == SRC_DENSE && DST == DST_DENSE);
     nb = wave_neighbourhood<NEED_SLOTS>(wm, g.GH, g.GW, t.n, t.gy, t.gx);
-    t.high = (nb.high >> 4) & 1;
-    t.slot = nb.slot[4];
-    if (NEED_SLOTS && t.slot >= (t.high ? a.hi_cap : a.lo_cap)) return false;
-    t.e = t.high ? g.bs : (g.bs >> 1);
-    const int rr = t.high ? R : (R >> 1);
+    t.high = high ? 1 : 0;
+    t.slot = slot;
+    t.e = high ? g.bs : (g.bs >> 1);
+    const int rr = high ? R : RL;
     t.r0 = grp * rr;
     if (t.r0 >= t.e) return false;
     t.rows = min(rr, t.e - t.r0);
@@ -568,7 +584,7 @@ __device__ __forceinline__ void res_barrier() {
 
 template <typename T, int SRC, int DST, bool ONE, int NKS>
 __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __restrict__ mask, ConvArgs a, int R,
-                                                     int G, int ntiles, int buf_bytes, int vec_out) {
+                                                     int RL, int Gh, int Gl, int buf_bytes, int vec_out) {
     typedef typename MFR<T>::frag frag;
     extern __shared__ __align__(16) unsigned char smem[];
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -618,12 +634,19 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     // This workgroup's tiles are pos, pos + nwg, ...  Workgroups are spread
     // over the XCDs round-robin; pos numbers them XCD by XCD, so the tiles of
     // one block (which share halo rows) run on one XCD and share its L2.
+    // The tile list by class (the class counts come from the mask; slots past
+    // a stack's capacity are skipped).
+    const int nh_all = wm.count_high((int)g.B);
+    constexpr bool CAPS = !(SRC == SRC_DENSE && DST == DST_DENSE);
+    const int nh = CAPS ? min(nh_all, a.hi_cap) : nh_all;
+    const int nl = CAPS ? min((int)g.B - nh_all, a.lo_cap) : (int)g.B - nh_all;
+    const int nth = nh * Gh, ntiles = nth + nl * Gl;
     const int nwg = (int)gridDim.x;
     const int pos = (nwg & 7) ? (int)blockIdx.x : (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
     int tile = pos;
     auto next_tile = [&](RTile& t, Neigh& nb) -> bool {
         while (tile < ntiles) {
-            const bool ok = res_tile<SRC, DST, ONE>(g, a, wm, R, G, tile, t, nb);
+            const bool ok = res_tile<SRC, DST, ONE>(g, a, wm, R, RL, Gh, Gl, nth, tile, t, nb);
             tile += nwg;
             if (ok) return true;
         }
@@ -701,7 +724,17 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
                     rw_compute<T, DST, 64, 2, NKS>(g, a, t0, 2 * half + (u >> 1), 2 * (u & 1), buf, Wr, bv, cobase,
                                                    vec_out, relu);
             }
-        } else {
+        } else if (t0.rows == 2 * R) {
+            if (t0.e == 16) {  // 16 rows x 1 strip: rows 8 * half .. + 8, two at a time
+#pragma unroll 1
+                for (int r = 0; r < 8; r += 2)
+                    rw_compute<T, DST, 16, 2, NKS>(g, a, t0, 0, 8 * half + r, buf, Wr, bv, cobase, vec_out, relu);
+            } else {           // 8 rows x 2 strips: strip `half`, two rows at a time
+#pragma unroll 1
+                for (int r = 0; r < 8; r += 2)
+                    rw_compute<T, DST, 32, 2, NKS>(g, a, t0, half, r, buf, Wr, bv, cobase, vec_out, relu);
+            }
+        } else {               // R/2 rows
             if (t0.e == 16) rw_compute<T, DST, 16, 2, NKS>(g, a, t0, 0, 2 * half, buf, Wr, bv, cobase, vec_out, relu);
             else rw_compute<T, DST, 32, 2, NKS>(g, a, t0, half, 0, buf, Wr, bv, cobase, vec_out, relu);
         }
@@ -718,21 +751,24 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
 
 inline bool aligned_to(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; }
 
-// Image rows per high tile (a low tile has half as many): 8 for blocks of
-// 32, 4 for blocks of 64, so that every tile has 256 output pixels and each
-// consumer half is whole 16-pixel strips of whole rows; 0 = not supported.
+// Image rows per high tile (a low tile has twice as many rows of half the
+// width): 8 for blocks of 32, 4 for blocks of 64, so that every tile has 256
+// output pixels and each consumer half is whole 16-pixel strips of whole
+// rows; 0 = not supported.
 int res_rows(int bs) { return bs == 32 ? 8 : (bs == 64 ? 4 : 0); }
 
 int res_buf_bytes(int bs, int R) {
     const int lb = bs / 2;
-    const int px_h = (R + 2) * (bs + 2), px_l = (R / 2 + 2) * (lb + 2);
+    const int px_h = (R + 2) * (bs + 2), px_l = (2 * R + 2) * (lb + 2);
     return (px_h > px_l ? px_h : px_l) * RROW;
 }
 
 template <typename T, int SRC, int DST, bool ONE, int NKS>
 hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, hipStream_t st) {
-    const int G = g.bs / R;  // tiles per block, for both classes
-    const long long ntiles = g.B * G;
+    const int RL = SRC == SRC_DENSE ? R / 2 : 2 * R;  // rows of a low tile (see res_tile)
+    const int Gh = g.bs / R;                           // tiles per high block
+    const int Gl = (g.bs / 2) / RL;                    // tiles per low block
+    const long long ntiles = g.B * Gh;                 // at most (every block high)
     const int buf_bytes = res_buf_bytes(g.bs, R);
     const int smem = NBUF * buf_bytes;
     const int ob = 16;
@@ -743,7 +779,7 @@ hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, 
     const int cus = device_cus();
     const int nwg = (int)(ntiles < cus ? ntiles : cus);
     const dim3 grid((unsigned)nwg, (unsigned)((a.C_out + RNT - 1) / RNT));
-    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, G, (int)ntiles,
+    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, RL, Gh, Gl,
                        buf_bytes, vec_out);
     return hipGetLastError();
 }
