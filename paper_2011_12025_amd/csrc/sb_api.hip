@@ -672,7 +672,7 @@ int segblocks_conv3x3_backward_weight_workspace_size(int dtype, int layout, int 
     int s;
     if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
         return s;
-    *bytes = sb::wgrad_ws_bytes(g, C_in, C_out, hi_cap, lo_cap, with_bias != 0);
+    *bytes = sb::wgrad_ws_bytes(dtype, layout, g, C_in, C_out, hi_cap, lo_cap, with_bias != 0);
     g_err.clear();
     return SB_OK;
 }
@@ -690,7 +690,7 @@ int segblocks_conv3x3_backward_weight(const void* hp, const void* lp, const void
         (s = check_stack(fn, "lp", lp, lo_cap)) || (s = check_stack(fn, "dho", dho, hi_cap)) ||
         (s = check_stack(fn, "dlo", dlo, lo_cap)))
         return s;
-    const size_t need = sb::wgrad_ws_bytes(g, C_in, C_out, hi_cap, lo_cap, dbias != nullptr);
+    const size_t need = sb::wgrad_ws_bytes(dtype, layout, g, C_in, C_out, hi_cap, lo_cap, dbias != nullptr);
     if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype), lb = bs / 2;
     const Range rhp{hp, hi_cap * (long long)C_in * (bs + 2) * (bs + 2) * es};

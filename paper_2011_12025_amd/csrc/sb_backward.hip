@@ -20,12 +20,28 @@
 //                 two zeros, with the filters transposed (in <-> out) and
 //                 rotated by 180 degrees: run on the general block
 //                 convolution kernel over a stack of such padded gradients.
-//   k_wgrad       the weight and bias gradients: sums over every output pixel
+//   k_wgrad_mfma  the weight and bias gradients: sums over every output pixel
 //                 of both stacks of outer products of the output gradient and
-//                 the padded input around the pixel.  Workgroups take 64
-//                 output x 64 input channels over a range of block rows and
-//                 keep 4 x 4 x 9 fp32 sums per thread; their partial sums go
-//                 to the workspace and k_wgrad_reduce adds them in chunk order.
+//                 the padded input around the pixel, as a GEMM whose K is the
+//                 pixels (channels-last fp16 / bf16, channel counts multiples
+//                 of 4).  A workgroup takes 64 output x 64 input channels over
+//                 one range of pixels; its twelve waves are two sub-ranges x
+//                 three tap rows x two halves of the output channels, each
+//                 wave a 32 x (3 x 64) fp32 tile in v_mfma_f32_16x16x16
+//                 accumulators.  Operands come straight
+//                 from the stacks: a lane loads four consecutive channels of
+//                 four consecutive pixels (8 bytes each) and transposes them
+//                 in registers into the four K values of an MFMA operand, so
+//                 lane n of an operand holds channels 4n + {0..3} of the four
+//                 16-channel fragments.  The sub-ranges are added in LDS in a
+//                 fixed order and the workgroup's sum goes to the workspace.
+//   k_wgrad       the same sums on the vector ALU, 4 x 4 x 9 fp32 per thread
+//                 over block rows (every other dtype, layout and channel
+//                 count).
+//   Either way the partial sums are added in a fixed order (k_wgrad_group
+//   sums groups of 16 ranges, k_wgrad_reduce the groups in order), so
+//   results do not depend on timing.
+#include <algorithm>
 #include <type_traits>
 
 #include "sb_common.h"
@@ -331,16 +347,38 @@ __global__ __launch_bounds__(WG) void k_wgrad(const T* __restrict__ hp, const T*
     }
 }
 
-// dw (call's format) and db from the chunk partial sums, added in chunk order.
+// First stage of the partial-sum reduction when there are many chunks:
+// thread (i, group) adds chunks 16 group .. 16 group + 15 of element i in
+// order and leaves the sum in chunk 16 group (read by no other thread).
+constexpr int WR_GROUP = 16;
+__global__ __launch_bounds__(WG) void k_wgrad_group(float* __restrict__ part, int chunks, int total) {
+    const long long gid = (long long)blockIdx.x * WG + threadIdx.x;
+    const int groups = (chunks + WR_GROUP - 1) / WR_GROUP;
+    if (gid >= (long long)total * groups) return;
+    const int grp = (int)(gid / total), i = (int)(gid - (long long)grp * total);
+    const int q0 = grp * WR_GROUP, q1 = min(chunks, q0 + WR_GROUP);
+    float v[WR_GROUP];
+#pragma unroll
+    for (int u = 0; u < WR_GROUP; ++u) v[u] = q0 + u < q1 ? part[(size_t)(q0 + u) * total + i] : 0.0f;
+    float s = v[0];
+#pragma unroll
+    for (int u = 1; u < WR_GROUP; ++u)
+        if (q0 + u < q1) s += v[u];
+    part[(size_t)q0 * total + i] = s;
+}
+
+// dw (call's format) and db from the chunk partial sums, added in chunk order
+// (gstride 1), or from the group sums of k_wgrad_group in group order
+// (gstride WR_GROUP).
 template <typename T, int L>
 __global__ __launch_bounds__(WG) void k_wgrad_reduce(const float* __restrict__ part, const float* __restrict__ part_b,
-                                                     int chunks, int C_in, int C_out, T* __restrict__ dw,
+                                                     int chunks, int gstride, int C_in, int C_out, T* __restrict__ dw,
                                                      T* __restrict__ db) {
     const int total = C_out * 9 * C_in;
     const int i = (int)(blockIdx.x * WG + threadIdx.x);
     if (i < total) {
         float s = 0.0f;
-        for (int q = 0; q < chunks; ++q) s += part[(size_t)q * total + i];
+        for (int q = 0; q < chunks; q += gstride) s += part[(size_t)q * total + i];
         const int ci = i % C_in, t = (i / C_in) % 9, co = i / (9 * C_in);
         size_t o;
         if constexpr (L == NHWC) o = i;  // [Cout][3][3][Cin]
@@ -348,10 +386,221 @@ __global__ __launch_bounds__(WG) void k_wgrad_reduce(const float* __restrict__ p
         dw[o] = from_f32<T>(s);
     }
     if (db && i < C_out) {
+        // in chunk order, sixteen loads in flight at a time
         float s = 0.0f;
-        for (int q = 0; q < chunks; ++q) s += part_b[(size_t)q * C_out + i];
+        int q = 0;
+        for (; q + 16 <= chunks; q += 16) {
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) v[u] = part_b[(size_t)(q + u) * C_out + i];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) s += v[u];
+        }
+        for (; q < chunks; ++q) s += part_b[(size_t)q * C_out + i];
         db[i] = from_f32<T>(s);
     }
+}
+
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+constexpr int WM_SUB = 2;                 // pixel sub-ranges of a workgroup
+constexpr int WM_WAVES = 6 * WM_SUB;      // x three tap rows x two output-channel halves
+constexpr int WM_THREADS = 64 * WM_WAVES;
+constexpr int WM_LDS = (64 * 9 * 64 + 64) * 4;  // the workgroup's sums: [co][tap][ci] fp32, then the bias
+
+template <typename T> struct WMF;
+template <> struct WMF<f16> {
+    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+    static __device__ __forceinline__ floatx4_t mma(uint2 a, uint2 b, floatx4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(h4, a), __builtin_bit_cast(h4, b), c, 0, 0, 0);
+    }
+};
+template <> struct WMF<bf16> {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    static __device__ __forceinline__ floatx4_t mma(uint2 a, uint2 b, floatx4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0,
+                                                          0, 0);
+    }
+};
+
+// 16-bit element c (0..1) of four 32-bit words (one per pixel) as an MFMA
+// operand: pixel u's value in 16-bit slot u.
+__device__ __forceinline__ uint2 wm_gather2(const uint32_t (&v)[4], int c) {
+    const int sh = c * 16;
+    uint32_t e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = (v[u] >> sh) & 0xFFFFu;
+    return uint2{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
+}
+// 16-bit element c (0..3) of four 64-bit words (one per pixel), the same way.
+__device__ __forceinline__ uint2 wm_gather4(const uint2 (&v)[4], int c) {
+    uint32_t w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) w[u] = (c & 2) ? v[u].y : v[u].x;
+    return wm_gather2(w, c & 1);
+}
+
+// grid: (pixel range, co block, ci block).  The pixels are those of the high
+// stack then the low stack (counts from the mask, capped by the capacities),
+// in stack order; range r is [P r / R, P (r + 1) / R).
+template <typename T>
+__global__ __launch_bounds__(WM_THREADS, 1) void k_wgrad_mfma(const T* __restrict__ hp, const T* __restrict__ lp,
+                                                              const T* __restrict__ dho, const T* __restrict__ dlo,
+                                                              const uint8_t* __restrict__ mask, int B, int bs, int C_in,
+                                                              int C_out, int hi_cap, int lo_cap,
+                                                              float* __restrict__ part, float* __restrict__ part_b) {
+    typedef WMF<T> mf;
+    extern __shared__ __align__(16) float s_sum[];
+    __shared__ int s_red[WM_WAVES];
+    const int tid = (int)threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int hf = wave & 1, ky = (wave >> 1) % 3, sub = wave / 6;
+    const int co0 = (int)blockIdx.y * 64, ci0 = (int)blockIdx.z * 64;
+    const int n = lane & 15, kq = lane >> 4;
+
+    // class counts
+    int c = 0;
+    for (int i = tid; i < B; i += WM_THREADS) c += mask[i] != 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (lane == 0) s_red[wave] = c;
+    __syncthreads();
+    int nh_all = 0;
+#pragma unroll
+    for (int w = 0; w < WM_WAVES; ++w) nh_all += s_red[w];
+    const int nh = min(nh_all, hi_cap), nl = min(B - nh_all, lo_cap);
+    const int lb = bs >> 1;
+    const long long P_h = (long long)nh * bs * bs, P = P_h + (long long)nl * lb * lb;
+    const long long R = gridDim.x, r = blockIdx.x;
+    const long long pa = P * r / R, pb = P * (r + 1) / R;
+    const long long ps = pa + (pb - pa) * sub / WM_SUB, pe = pa + (pb - pa) * (sub + 1) / WM_SUB;
+
+    // this lane's channels: output channels co0 + 4 n + 2 hf + {0, 1} (the
+    // wave's half of fragments 0..3), input channels ci0 + 4 n + {0..3}
+    const int co_l = co0 + 4 * n, ci_l = ci0 + 4 * n;
+    const bool co_ok = co_l < C_out, ci_ok = ci_l < C_in;
+    floatx4_t acc[3][2][4];  // [kx][co fragment 2 hf + 0, 1][ci fragment]
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int d = 0; d < 4; ++d) acc[a][b][d] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    float bsum[2] = {0.f, 0.f};
+
+    // one step: sixteen pixels, K values 4 kq .. 4 kq + 3 from this lane
+    auto load_step = [&](int stp, uint32_t (&va)[4], uint2 (&vb)[3][4]) {
+        long long p = ps + 16LL * stp + 4 * kq;
+        bool high = p < P_h;
+        int e = high ? bs : lb;
+        const long long q = high ? p : p - P_h;
+        const long long ee = (long long)e * e;
+        int slot = (int)(q / ee);
+        const int rem = (int)(q - (long long)slot * ee);
+        int i = rem / e, j = rem - (rem / e) * e;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool ok = p < pe;
+            const T* O = high ? dho : dlo;
+            const T* X = high ? hp : lp;
+            const int pe2 = e + 2;
+            va[u] = (ok && co_ok) ? *reinterpret_cast<const uint32_t*>(
+                                        O + ((size_t)((long long)slot * e + i) * e + j) * C_out + co_l + 2 * hf)
+                                  : 0u;
+            const size_t xrow = ((size_t)((long long)slot * pe2 + i + ky) * pe2 + j) * C_in + ci_l;
+#pragma unroll
+            for (int kx = 0; kx < 3; ++kx)
+                vb[kx][u] = (ok && ci_ok) ? *reinterpret_cast<const uint2*>(X + xrow + (size_t)kx * C_in)
+                                          : uint2{0u, 0u};
+            // next pixel in stack order
+            ++p;
+            if (++j == e) {
+                j = 0;
+                if (++i == e) {
+                    i = 0;
+                    if (++slot == nh && high) {
+                        high = false;
+                        slot = 0;
+                        e = lb;
+                    }
+                }
+            }
+        }
+    };
+    auto compute_step = [&](const uint32_t (&va)[4], const uint2 (&vb)[3][4]) {
+        uint2 fa[2];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) fa[cb] = wm_gather2(va, cb);
+        if (ky == 0) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                Vec<T, 2> t;
+                t.raw = va[u];
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) bsum[cb] += to_f32(t.e[cb]);
+            }
+        }
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx)
+#pragma unroll
+            for (int cib = 0; cib < 4; ++cib) {
+                const uint2 fb = wm_gather4(vb[kx], cib);
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) acc[kx][cb][cib] = mf::mma(fa[cb], fb, acc[kx][cb][cib]);
+            }
+    };
+    // (a second register set for the next step's loads does not fit beside
+    // the accumulators at three waves per SIMD: the three waves of a SIMD
+    // overlap each other's loads instead)
+    const int steps = (int)((pe - ps + 15) / 16);
+    for (int stp = 0; stp < steps; ++stp) {
+        uint32_t va[4];
+        uint2 vb[3][4];
+        load_step(stp, va, vb);
+        compute_step(va, vb);
+    }
+
+    // bias: the four pixel groups of a lane column, in a fixed order
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+        bsum[cb] += __shfl_xor(bsum[cb], 16, 64);
+        bsum[cb] += __shfl_xor(bsum[cb], 32, 64);
+    }
+    // the sub-ranges' sums, added in LDS in sub-range order.  Lane l holds
+    // rows 4 (l >> 4) + rr of each 16 x 16 fragment, column l & 15: output
+    // channel 16 (l >> 4) + 4 rr + (2 hf + cb), input channel 4 (l & 15) + cib.
+    float* s_b = s_sum + 64 * 9 * 64;
+    for (int ph = 0; ph < WM_SUB; ++ph) {
+        if (sub == ph) {
+#pragma unroll
+            for (int kx = 0; kx < 3; ++kx)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int cib = 0; cib < 4; ++cib)
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            const int co = 16 * kq + 4 * rr + 2 * hf + cb, ci = 4 * n + cib;
+                            float* d = s_sum + (co * 9 + 3 * ky + kx) * 64 + ci;
+                            *d = ph == 0 ? acc[kx][cb][cib][rr] : *d + acc[kx][cb][cib][rr];
+                        }
+            if (ky == 0 && kq == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    float* d = s_b + 4 * n + 2 * hf + cb;
+                    *d = ph == 0 ? bsum[cb] : *d + bsum[cb];
+                }
+            }
+        }
+        __syncthreads();
+    }
+    float* pc = part + (size_t)blockIdx.x * C_out * 9 * C_in;
+    for (int idx = tid; idx < 64 * 9 * 64; idx += WM_THREADS) {
+        const int co = idx / (9 * 64), rest = idx - co * (9 * 64);
+        const int t = rest >> 6, ci = rest & 63;
+        if (co0 + co < C_out && ci0 + ci < C_in) pc[((size_t)(co0 + co) * 9 + t) * C_in + ci0 + ci] = s_sum[idx];
+    }
+    if (part_b && blockIdx.z == 0 && tid < 64 && co0 + tid < C_out)
+        part_b[(size_t)blockIdx.x * C_out + co0 + tid] = s_b[tid];
 }
 
 inline size_t r256(size_t b) { return (b + 255) / 256 * 256; }
@@ -373,14 +622,35 @@ DgradLayout dgrad_layout(int dtype, const Geo& g, int C_in, int C_out, int hi_ca
 }
 
 struct WgradPlan {
+    bool mfma;
     int chunks, rows_per_chunk, tiles_co, tiles_ci;
     size_t part, part_b, total;
 };
 
-WgradPlan wgrad_plan(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
+// The MFMA kernel takes channels-last fp16 / bf16 with channel counts that
+// are multiples of 4 (8-byte operand loads).
+bool wgrad_mfma_fits(int dtype, int layout, int C_in, int C_out) {
+    return layout == NHWC && (dtype == 1 || dtype == 2) && C_in % 4 == 0 && C_out % 4 == 0;
+}
+
+// mfma: the plan of k_wgrad_mfma (else of k_wgrad)
+WgradPlan wgrad_plan(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias, bool mfma) {
     WgradPlan p;
     p.tiles_co = (C_out + WG_CO - 1) / WG_CO;
     p.tiles_ci = (C_in + WG_CI - 1) / WG_CI;
+    p.mfma = mfma;
+    if (mfma) {
+        // pixel ranges: one workgroup per CU over the channel blocks, at least
+        // 256 pixels per range (partial sums cost 147 KB per range and block)
+        const long long px = (long long)hi_cap * g.bs * g.bs + (long long)lo_cap * (g.bs / 2) * (g.bs / 2);
+        const long long per_block = std::max(1LL, (long long)device_cus() / (p.tiles_co * p.tiles_ci));
+        p.chunks = (int)std::max(1LL, std::min(per_block, (px + 255) / 256));
+        p.rows_per_chunk = 0;
+        p.part = r256((size_t)p.chunks * C_out * 9 * C_in * 4);
+        p.part_b = bias ? r256((size_t)p.chunks * C_out * 4) : 0;
+        p.total = p.part + p.part_b;
+        return p;
+    }
     // rows by capacity (the counts are on the device): aim at about 2 workgroups per CU
     const long long rows = (long long)hi_cap * g.bs + (long long)lo_cap * (g.bs / 2);
     const long long want = (2LL * device_cus() + p.tiles_co * p.tiles_ci - 1) / (p.tiles_co * p.tiles_ci);
@@ -467,18 +737,39 @@ template <typename T, int L>
 hipError_t wgrad_t(const Geo& g, const void* hp, const void* lp, const void* dho, const void* dlo,
                    const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap, int lo_cap, Ws ws,
                    hipStream_t st) {
-    const WgradPlan p = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, db != nullptr);
+    constexpr int dt = sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2);
+    const bool al8 = ((reinterpret_cast<uintptr_t>(hp) | reinterpret_cast<uintptr_t>(lp) |
+                       reinterpret_cast<uintptr_t>(dho) | reinterpret_cast<uintptr_t>(dlo)) & 7) == 0;
+    const bool mfma = al8 && wgrad_mfma_fits(dt, L, C_in, C_out);
+    const WgradPlan p = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, db != nullptr, mfma);
     if (ws.bytes < p.total || !ws.p) return hipErrorInvalidValue;
     float* part = (float*)ws.p;
     float* part_b = db ? (float*)((char*)ws.p + p.part) : nullptr;
-    hipLaunchKernelGGL((k_wgrad<T, L>), dim3((unsigned)p.chunks, (unsigned)p.tiles_co, (unsigned)p.tiles_ci),
-                       dim3(WG), 0, st, (const T*)hp, (const T*)lp, (const T*)dho, (const T*)dlo, mask, (int)g.B,
-                       g.bs, C_in, C_out, hi_cap, lo_cap, p.rows_per_chunk, part, part_b);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e;
+    const dim3 grid((unsigned)p.chunks, (unsigned)p.tiles_co, (unsigned)p.tiles_ci);
+    if constexpr (L == NHWC && dt != 0) {
+        if (mfma) {
+            if ((e = ensure_dyn_lds((const void*)k_wgrad_mfma<T>, WM_LDS)) != hipSuccess) return e;
+            hipLaunchKernelGGL((k_wgrad_mfma<T>), grid, dim3(WM_THREADS), WM_LDS, st, (const T*)hp, (const T*)lp,
+                               (const T*)dho, (const T*)dlo, mask, (int)g.B, g.bs, C_in, C_out, hi_cap, lo_cap, part,
+                               part_b);
+        }
+    }
+    if (!mfma)
+        hipLaunchKernelGGL((k_wgrad<T, L>), grid, dim3(WG), 0, st, (const T*)hp, (const T*)lp, (const T*)dho,
+                           (const T*)dlo, mask, (int)g.B, g.bs, C_in, C_out, hi_cap, lo_cap, p.rows_per_chunk, part,
+                           part_b);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     const int total = C_out * 9 * C_in;
+    int gstride = 1;
+    if (p.chunks > 2 * WR_GROUP) {
+        const long long threads = (long long)total * ((p.chunks + WR_GROUP - 1) / WR_GROUP);
+        hipLaunchKernelGGL(k_wgrad_group, dim3((unsigned)((threads + WG - 1) / WG)), dim3(WG), 0, st, part, p.chunks,
+                           total);
+        gstride = WR_GROUP;
+    }
     hipLaunchKernelGGL((k_wgrad_reduce<T, L>), dim3((unsigned)((total + WG - 1) / WG)), dim3(WG), 0, st,
-                       (const float*)part, (const float*)part_b, p.chunks, C_in, C_out, (T*)dw, (T*)db);
+                       (const float*)part, (const float*)part_b, p.chunks, gstride, C_in, C_out, (T*)dw, (T*)db);
     return hipGetLastError();
 }
 
@@ -514,8 +805,11 @@ hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, co
     }
 }
 
-size_t wgrad_ws_bytes(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
-    return wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias).total;
+size_t wgrad_ws_bytes(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
+    // a misaligned call of the MFMA kernel's shapes takes the vector-ALU kernel
+    const size_t v = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias, false).total;
+    if (!wgrad_mfma_fits(dtype, layout, C_in, C_out)) return v;
+    return std::max(v, wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias, true).total);
 }
 
 hipError_t launch_wgrad(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const void* dho,

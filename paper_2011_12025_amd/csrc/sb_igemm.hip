@@ -675,12 +675,14 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     }
     p.splits = tiles > 0 ? S : 1;
     // A low block's halo pixels across a resolution boundary are 2x2 averages
-    // of the high neighbour: four loads per element in the K loop, which make
+    // of the high neighbour: four loads per element in every K step, which make
     // the low tiles the last to finish.  A 3 x 3 convolution with both classes
-    // can pad the low stack once instead (BlockPad of the low blocks), so that
-    // every low-tile source is a plain copy.  Measured, the extra pass pays at
-    // 128 input channels (about 5 us less at 25-75 % low blocks) and costs 1-4 us
-    // at 64, 256 and 512, so it is taken there only.
+    // pads the low stack once instead (BlockPad of the low blocks, one extra
+    // launch), so that every low-tile source is a plain copy.  Measured at the
+    // ResNet-18 stage shapes of a 1024x2048 image (128, 256 and 512 channels,
+    // 25-75 % low blocks), the extra pass is 6-12 us faster than the averages
+    // in the K loop at 25 % low blocks and at 128 channels, and within 3 us
+    // either way elsewhere.
     p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG;
     p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 4)
                                 : 0;

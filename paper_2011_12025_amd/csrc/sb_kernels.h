@@ -103,7 +103,7 @@ size_t dgrad_ws_bytes(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, 
 hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, const void* dlo, const uint8_t* mask,
                         const void* w, int C_in, int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws,
                         hipStream_t st);
-size_t wgrad_ws_bytes(const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias);
+size_t wgrad_ws_bytes(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias);
 hipError_t launch_wgrad(int dtype, int layout, const Geo& g, const void* hp, const void* lp, const void* dho,
                         const void* dlo, const uint8_t* mask, int C_in, int C_out, void* dw, void* db, int hi_cap,
                         int lo_cap, Ws ws, hipStream_t st);
