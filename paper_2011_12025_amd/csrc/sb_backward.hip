@@ -425,11 +425,10 @@ template <> struct WMF<bf16> {
 // 16-bit element c (0..1) of four 32-bit words (one per pixel) as an MFMA
 // operand: pixel u's value in 16-bit slot u.
 __device__ __forceinline__ uint2 wm_gather2(const uint32_t (&v)[4], int c) {
-    const int sh = c * 16;
-    uint32_t e[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) e[u] = (v[u] >> sh) & 0xFFFFu;
-    return uint2{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
+    // byte selector of v_perm_b32: the low (c = 0) or high (c = 1) halves of
+    // its second and first source
+    const uint32_t sel = c ? 0x07060302u : 0x05040100u;
+    return uint2{__builtin_amdgcn_perm(v[1], v[0], sel), __builtin_amdgcn_perm(v[3], v[2], sel)};
 }
 // 16-bit element c (0..3) of four 64-bit words (one per pixel), the same way.
 __device__ __forceinline__ uint2 wm_gather4(const uint2 (&v)[4], int c) {
@@ -470,9 +469,12 @@ __global__ __launch_bounds__(WM_THREADS, 1) void k_wgrad_mfma(const T* __restric
     const int nh = min(nh_all, hi_cap), nl = min(B - nh_all, lo_cap);
     const int lb = bs >> 1;
     const long long P_h = (long long)nh * bs * bs, P = P_h + (long long)nl * lb * lb;
+    // range and sub-range bounds at multiples of four pixels (a lane's four
+    // pixels then stay in one block row whenever rows are multiples of four)
     const long long R = gridDim.x, r = blockIdx.x;
-    const long long pa = P * r / R, pb = P * (r + 1) / R;
-    const long long ps = pa + (pb - pa) * sub / WM_SUB, pe = pa + (pb - pa) * (sub + 1) / WM_SUB;
+    const long long pa = (P * r / R) & ~3LL, pb = r + 1 == R ? P : (P * (r + 1) / R) & ~3LL;
+    const long long ps = sub == 0 ? pa : (pa + (pb - pa) * sub / WM_SUB) & ~3LL;
+    const long long pe = sub + 1 == WM_SUB ? pb : (pa + (pb - pa) * (sub + 1) / WM_SUB) & ~3LL;
 
     // this lane's channels: output channels co0 + 4 n + 2 hf + {0, 1} (the
     // wave's half of fragments 0..3), input channels ci0 + 4 n + {0..3}
@@ -487,43 +489,78 @@ __global__ __launch_bounds__(WM_THREADS, 1) void k_wgrad_mfma(const T* __restric
             for (int d = 0; d < 4; ++d) acc[a][b][d] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     float bsum[2] = {0.f, 0.f};
 
-    // one step: sixteen pixels, K values 4 kq .. 4 kq + 3 from this lane
+    // one step: sixteen pixels, K values 4 kq .. 4 kq + 3 from this lane.
+    // Straight-line code: a pixel past the range loads from pixel 0 and is
+    // zeroed, the stack-order walk to the next pixel uses selects.
+    const int pe32 = (int)pe, nh32 = nh;
     auto load_step = [&](int stp, uint32_t (&va)[4], uint2 (&vb)[3][4]) {
-        long long p = ps + 16LL * stp + 4 * kq;
-        bool high = p < P_h;
+        int p = (int)ps + 16 * stp + 4 * kq;
+        bool high = p < (int)P_h;
         int e = high ? bs : lb;
-        const long long q = high ? p : p - P_h;
-        const long long ee = (long long)e * e;
-        int slot = (int)(q / ee);
-        const int rem = (int)(q - (long long)slot * ee);
-        int i = rem / e, j = rem - (rem / e) * e;
+        const int q = high ? p : p - (int)P_h;
+        const int ee = e * e;
+        int slot = q / ee;
+        const int rem = q - slot * ee;
+        int i = rem / e;
+        int j = rem - i * e;
+        if (p >= pe32) {  // past the sub-range: nothing to load
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const bool ok = p < pe;
+            for (int u = 0; u < 4; ++u) {
+                va[u] = 0u;
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) vb[kx][u] = uint2{0u, 0u};
+            }
+            return;
+        }
+        if (j + 3 < e && p + 3 < pe32) {
+            // the four pixels are consecutive in one row: fixed strides
             const T* O = high ? dho : dlo;
             const T* X = high ? hp : lp;
             const int pe2 = e + 2;
-            va[u] = (ok && co_ok) ? *reinterpret_cast<const uint32_t*>(
-                                        O + ((size_t)((long long)slot * e + i) * e + j) * C_out + co_l + 2 * hf)
-                                  : 0u;
-            const size_t xrow = ((size_t)((long long)slot * pe2 + i + ky) * pe2 + j) * C_in + ci_l;
+            const T* orow = O + ((size_t)(slot * e + i) * e + j) * C_out + (co_ok ? co_l + 2 * hf : 0);
+            const T* xr = X + ((size_t)(slot * pe2 + i + ky) * pe2 + j) * C_in + (ci_ok ? ci_l : 0);
 #pragma unroll
-            for (int kx = 0; kx < 3; ++kx)
-                vb[kx][u] = (ok && ci_ok) ? *reinterpret_cast<const uint2*>(X + xrow + (size_t)kx * C_in)
-                                          : uint2{0u, 0u};
-            // next pixel in stack order
-            ++p;
-            if (++j == e) {
-                j = 0;
-                if (++i == e) {
-                    i = 0;
-                    if (++slot == nh && high) {
-                        high = false;
-                        slot = 0;
-                        e = lb;
-                    }
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t a0 = *reinterpret_cast<const uint32_t*>(orow + (size_t)u * C_out);
+                va[u] = co_ok ? a0 : 0u;
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) {
+                    const uint2 b0 = *reinterpret_cast<const uint2*>(xr + (size_t)(u + kx) * C_in);
+                    vb[kx][u] = ci_ok ? b0 : uint2{0u, 0u};
                 }
             }
+            return;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool ok = p < pe32;
+            // a pixel past the range reads pixel 0 of a non-empty stack
+            const bool hs = ok ? high : nh32 > 0;
+            const T* O = hs ? dho : dlo;
+            const T* X = hs ? hp : lp;
+            const int pe2 = e + 2;
+            const size_t opx = ok ? ((size_t)(slot * e + i) * e + j) : 0;
+            const size_t xpx = ok ? ((size_t)(slot * pe2 + i + ky) * pe2 + j) : 0;
+            const uint32_t a0 = *reinterpret_cast<const uint32_t*>(O + opx * C_out + (co_ok ? co_l + 2 * hf : 0));
+            va[u] = (ok && co_ok) ? a0 : 0u;
+            const T* xr = X + xpx * C_in + (ci_ok ? ci_l : 0);
+#pragma unroll
+            for (int kx = 0; kx < 3; ++kx) {
+                const uint2 b0 = *reinterpret_cast<const uint2*>(xr + (size_t)kx * C_in);
+                vb[kx][u] = (ok && ci_ok) ? b0 : uint2{0u, 0u};
+            }
+            // next pixel in stack order
+            ++p;
+            const bool wj = ++j == e;
+            j = wj ? 0 : j;
+            i += wj;
+            const bool wi = i == e;
+            i = wi ? 0 : i;
+            slot += wi;
+            const bool sw = high && slot == nh32;
+            high = high && !sw;
+            slot = sw ? 0 : slot;
+            e = sw ? lb : e;
         }
     };
     auto compute_step = [&](const uint32_t (&va)[4], const uint2 (&vb)[3][4]) {
@@ -594,10 +631,12 @@ __global__ __launch_bounds__(WM_THREADS, 1) void k_wgrad_mfma(const T* __restric
         __syncthreads();
     }
     float* pc = part + (size_t)blockIdx.x * C_out * 9 * C_in;
-    for (int idx = tid; idx < 64 * 9 * 64; idx += WM_THREADS) {
-        const int co = idx / (9 * 64), rest = idx - co * (9 * 64);
-        const int t = rest >> 6, ci = rest & 63;
-        if (co0 + co < C_out && ci0 + ci < C_in) pc[((size_t)(co0 + co) * 9 + t) * C_in + ci0 + ci] = s_sum[idx];
+    for (int idx = tid; idx < 64 * 9 * 16; idx += WM_THREADS) {  // four channels per store
+        const int co = idx / (9 * 16), rest = idx - co * (9 * 16);
+        const int t = rest >> 4, ci = (rest & 15) * 4;
+        if (co0 + co < C_out && ci0 + ci < C_in)
+            *reinterpret_cast<float4*>(pc + ((size_t)(co0 + co) * 9 + t) * C_in + ci0 + ci) =
+                *reinterpret_cast<const float4*>(s_sum + 4 * idx);
     }
     if (part_b && blockIdx.z == 0 && tid < 64 && co0 + tid < C_out)
         part_b[(size_t)blockIdx.x * C_out + co0 + tid] = s_b[tid];
@@ -628,9 +667,11 @@ struct WgradPlan {
 };
 
 // The MFMA kernel takes channels-last fp16 / bf16 with channel counts that
-// are multiples of 4 (8-byte operand loads).
-bool wgrad_mfma_fits(int dtype, int layout, int C_in, int C_out) {
-    return layout == NHWC && (dtype == 1 || dtype == 2) && C_in % 4 == 0 && C_out % 4 == 0;
+// are multiples of 4 (8-byte operand loads) and fewer than 2^30 pixels.
+bool wgrad_mfma_fits(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+    const long long px = (long long)hi_cap * g.bs * g.bs + (long long)lo_cap * (g.bs / 2) * (g.bs / 2);
+    return layout == NHWC && (dtype == 1 || dtype == 2) && C_in % 4 == 0 && C_out % 4 == 0 &&
+           px < (1LL << 30);  // pixel indices in 32 bits
 }
 
 // mfma: the plan of k_wgrad_mfma (else of k_wgrad)
@@ -740,7 +781,7 @@ hipError_t wgrad_t(const Geo& g, const void* hp, const void* lp, const void* dho
     constexpr int dt = sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2);
     const bool al8 = ((reinterpret_cast<uintptr_t>(hp) | reinterpret_cast<uintptr_t>(lp) |
                        reinterpret_cast<uintptr_t>(dho) | reinterpret_cast<uintptr_t>(dlo)) & 7) == 0;
-    const bool mfma = al8 && wgrad_mfma_fits(dt, L, C_in, C_out);
+    const bool mfma = al8 && wgrad_mfma_fits(dt, L, g, C_in, C_out, hi_cap, lo_cap);
     const WgradPlan p = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, db != nullptr, mfma);
     if (ws.bytes < p.total || !ws.p) return hipErrorInvalidValue;
     float* part = (float*)ws.p;
@@ -808,7 +849,7 @@ hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, co
 size_t wgrad_ws_bytes(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap, bool bias) {
     // a misaligned call of the MFMA kernel's shapes takes the vector-ALU kernel
     const size_t v = wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias, false).total;
-    if (!wgrad_mfma_fits(dtype, layout, C_in, C_out)) return v;
+    if (!wgrad_mfma_fits(dtype, layout, g, C_in, C_out, hi_cap, lo_cap)) return v;
     return std::max(v, wgrad_plan(g, C_in, C_out, hi_cap, lo_cap, bias, true).total);
 }
 
