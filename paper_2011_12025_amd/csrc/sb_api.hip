@@ -633,7 +633,7 @@ int segblocks_conv3x3_backward_data_workspace_size(int dtype, int layout, int N,
     int s;
     if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) || (s = check_caps(fn, hi_cap, lo_cap)))
         return s;
-    *bytes = sb::dgrad_ws_bytes(dtype, g, C_in, C_out, hi_cap, lo_cap);
+    *bytes = sb::dgrad_ws_bytes(dtype, layout, g, C_in, C_out, hi_cap, lo_cap);
     g_err.clear();
     return SB_OK;
 }
@@ -651,7 +651,7 @@ int segblocks_conv3x3_backward_data(const void* dho, const void* dlo, int dtype,
         (s = check_stack(fn, "dlo", dlo, lo_cap)) || (s = check_stack(fn, "dhp", dhp, hi_cap)) ||
         (s = check_stack(fn, "dlp", dlp, lo_cap)))
         return s;
-    const size_t need = sb::dgrad_ws_bytes(dtype, g, C_in, C_out, hi_cap, lo_cap);
+    const size_t need = sb::dgrad_ws_bytes(dtype, layout, g, C_in, C_out, hi_cap, lo_cap);
     if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
     const long long es = esize(dtype), lb = bs / 2;
     const Range rho{dho, hi_cap * (long long)C_out * bs * bs * es}, rlo{dlo, lo_cap * (long long)C_out * lb * lb * es};

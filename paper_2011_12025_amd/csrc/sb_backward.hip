@@ -18,8 +18,11 @@
 //   dgrad         the gradient of the valid 3x3 convolution of a padded block
 //                 is a valid 3x3 convolution of the output gradient padded by
 //                 two zeros, with the filters transposed (in <-> out) and
-//                 rotated by 180 degrees: run on the general block
-//                 convolution kernel over a stack of such padded gradients.
+//                 rotated by 180 degrees, i.e. a zero-padded "same"
+//                 convolution of the gradient padded by one: run on the
+//                 implicit GEMM (channels-last fp16 / bf16, 64k output
+//                 channels, blocks of 4k), else on the general block
+//                 convolution kernel.
 //   k_wgrad_mfma  the weight and bias gradients: sums over every output pixel
 //                 of both stacks of outer products of the output gradient and
 //                 the padded input around the pixel, as a GEMM whose K is the
@@ -167,67 +170,77 @@ __global__ __launch_bounds__(WG) void k_pad_bwd(const T* __restrict__ dhp, const
 }
 
 // ---------------------------------------------------------------------------
-// dgrad helpers: the output gradient padded by two zeros, the transposed and
-// rotated filters, and the all-high / all-low masks that let the general
-// block convolution run over one stack at a time.
+// dgrad helper
 // ---------------------------------------------------------------------------
+
+// Everything the data gradient's convolutions read, in one launch: the
+// transposed-rotated weights, the all-high / all-low masks (nm bytes each)
+// and both output-gradient stacks padded by `pad` zeros.
 template <typename T, int L>
-__global__ __launch_bounds__(WG) void k_pad2(const T* __restrict__ src, int S, int C, int e, T* __restrict__ dst) {
-    const int pe = e + 4;
-    const long long total = (long long)S * C * pe * pe;
+__global__ __launch_bounds__(WG) void k_dgrad_prep(const T* __restrict__ w, int Cout, int Cin, T* __restrict__ wt,
+                                                   uint8_t* __restrict__ ones, uint8_t* __restrict__ zeros, long long nm,
+                                                   const T* __restrict__ dho, int hi_cap, T* __restrict__ qh,
+                                                   const T* __restrict__ dlo, int lo_cap, T* __restrict__ ql, int bs,
+                                                   int pad) {
+    const long long nw = (long long)Cout * Cin * 9;
+    const int lb = bs >> 1, ph = bs + 2 * pad, pl = lb + 2 * pad;
+    const long long nqh = (long long)hi_cap * Cout * ph * ph, nql = (long long)lo_cap * Cout * pl * pl;
+    const long long total = nw + 2 * nm + nqh + nql;
     for (long long i = (long long)blockIdx.x * WG + threadIdx.x; i < total; i += (long long)gridDim.x * WG) {
+        if (i < nw) {
+            int ci, co, t;  // i indexes wt in its memory order
+            if constexpr (L == NHWC) {  // [Cin][3][3][Cout]
+                co = (int)(i % Cout);
+                t = (int)((i / Cout) % 9);
+                ci = (int)(i / (Cout * 9));
+            } else {                    // [Cin][Cout][3][3]
+                t = (int)(i % 9);
+                co = (int)((i / 9) % Cout);
+                ci = (int)(i / (9 * Cout));
+            }
+            const int ts = 8 - t;       // (2 - ky, 2 - kx)
+            size_t src;
+            if constexpr (L == NHWC) src = ((size_t)co * 9 + ts) * Cin + ci;
+            else                     src = ((size_t)co * Cin + ci) * 9 + ts;
+            wt[i] = w[src];
+            continue;
+        }
+        long long k = i - nw;
+        if (k < 2 * nm) {
+            if (k < nm) ones[k] = 1;
+            else zeros[k - nm] = 0;
+            continue;
+        }
+        k -= 2 * nm;
+        const bool hi = k < nqh;
+        if (!hi) k -= nqh;
+        const T* src = hi ? dho : dlo;
+        T* dst = hi ? qh : ql;
+        const int e = hi ? bs : lb, pe = hi ? ph : pl;
         int s, c, u, v;
         if constexpr (L == NHWC) {
-            c = (int)(i % C);
-            long long p = i / C;
-            v = (int)(p % pe);
-            p /= pe;
-            u = (int)(p % pe);
-            s = (int)(p / pe);
+            c = (int)(k % Cout);
+            long long q = k / Cout;
+            v = (int)(q % pe);
+            q /= pe;
+            u = (int)(q % pe);
+            s = (int)(q / pe);
         } else {
-            v = (int)(i % pe);
-            long long p = i / pe;
-            u = (int)(p % pe);
-            p /= pe;
-            c = (int)(p % C);
-            s = (int)(p / C);
+            v = (int)(k % pe);
+            long long q = k / pe;
+            u = (int)(q % pe);
+            q /= pe;
+            c = (int)(q % Cout);
+            s = (int)(q / Cout);
         }
-        const int a = u - 2, b = v - 2;
+        const int a = u - pad, b = v - pad;
         T val = from_f32<T>(0.0f);
         if (a >= 0 && a < e && b >= 0 && b < e) {
-            if constexpr (L == NHWC) val = src[(((size_t)s * e + a) * e + b) * C + c];
-            else                     val = src[(((size_t)s * C + c) * e + a) * e + b];
+            if constexpr (L == NHWC) val = src[(((size_t)s * e + a) * e + b) * Cout + c];
+            else                     val = src[(((size_t)s * Cout + c) * e + a) * e + b];
         }
-        dst[i] = val;
+        dst[k] = val;
     }
-}
-
-// w [Cout][Cin][3][3] in the call's format -> wt [Cin][Cout][3][3], rotated
-template <typename T, int L>
-__global__ __launch_bounds__(WG) void k_wflip(const T* __restrict__ w, int Cout, int Cin, T* __restrict__ wt) {
-    const int total = Cout * Cin * 9;
-    for (int i = (int)(blockIdx.x * WG + threadIdx.x); i < total; i += (int)(gridDim.x * WG)) {
-        // i indexes wt in its memory order
-        int ci, co, t;
-        if constexpr (L == NHWC) {  // [Cin][3][3][Cout]
-            co = i % Cout;
-            t = (i / Cout) % 9;
-            ci = i / (Cout * 9);
-        } else {                    // [Cin][Cout][3][3]
-            t = i % 9;
-            co = (i / 9) % Cout;
-            ci = i / (9 * Cout);
-        }
-        const int ts = 8 - t;       // (2 - ky, 2 - kx)
-        size_t src;
-        if constexpr (L == NHWC) src = ((size_t)co * 9 + ts) * Cin + ci;
-        else                     src = ((size_t)co * Cin + ci) * 9 + ts;
-        wt[i] = w[src];
-    }
-}
-
-__global__ __launch_bounds__(WG) void k_fill8(uint8_t* __restrict__ p, long long n, uint8_t v) {
-    for (long long i = (long long)blockIdx.x * WG + threadIdx.x; i < n; i += (long long)gridDim.x * WG) p[i] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -645,18 +658,58 @@ __global__ __launch_bounds__(WM_THREADS, 1) void k_wgrad_mfma(const T* __restric
 inline size_t r256(size_t b) { return (b + 255) / 256 * 256; }
 inline int esz(int dtype) { return dtype == 0 ? 4 : 2; }
 
+// The data gradient of each stack as a convolution of its own (the classes
+// do not mix: the padded blocks are independent).  On the implicit GEMM:
+// the output gradient padded by one zero (extent e + 2) taken as a stack of
+// blocks of that extent, every block high, zero-padded on its own
+// (SB_FLAG_PAD_ZERO), transposed-rotated weights: a "same" convolution whose
+// output is the padded block's gradient.  Otherwise the general kernel runs
+// a valid convolution over the gradient padded by two.
+struct DgradCall {
+    Geo g;
+    ConvArgs a;
+};
+DgradCall dgrad_call(const Geo& g, int e, int cap, int C_in, int C_out) {
+    DgradCall d;
+    d.g = g;
+    d.g.N = 1;
+    d.g.C = C_out;
+    d.g.bs = e + 2;
+    d.g.GH = 1;
+    d.g.GW = cap;
+    d.g.B = cap;
+    d.g.H = e + 2;
+    d.g.W = cap * (e + 2);
+    d.a = ConvArgs{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_out, C_in,
+                   PM_ZERO << 1, cap, 0};  // zero padding of each block on its own
+    return d;
+}
+bool dgrad_igemm_shape(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+    if (g.bs % 4) return false;  // even extents e + 2 for both classes
+    const DgradCall h = dgrad_call(g, g.bs, hi_cap, C_in, C_out), l = dgrad_call(g, g.bs / 2, lo_cap, C_in, C_out);
+    return (hi_cap == 0 || igemm_fits_shape(dtype, layout, h.g, h.a)) &&
+           (lo_cap == 0 || igemm_fits_shape(dtype, layout, l.g, l.a));
+}
+
 struct DgradLayout {
-    size_t qh, ql, wt, masks, total;
+    bool ig_shape;  // the implicit GEMM takes these shapes
+    size_t qh, ql, wt, masks, ig, total;
 };
 
-DgradLayout dgrad_layout(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+DgradLayout dgrad_layout(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
     const size_t es = esz(dtype), lb = g.bs / 2;
     DgradLayout D;
     D.qh = r256((size_t)hi_cap * C_out * (g.bs + 4) * (g.bs + 4) * es);
     D.ql = r256((size_t)lo_cap * C_out * (lb + 4) * (lb + 4) * es);
     D.wt = r256((size_t)C_in * C_out * 9 * es);
-    D.masks = r256((size_t)g.B * 2);
-    D.total = D.qh + D.ql + D.wt + D.masks;
+    D.masks = r256((size_t)std::max<long long>({g.B, (long long)hi_cap, (long long)lo_cap}) * 2);
+    D.ig = 0;
+    D.ig_shape = dgrad_igemm_shape(dtype, layout, g, C_in, C_out, hi_cap, lo_cap);
+    if (D.ig_shape) {
+        const DgradCall h = dgrad_call(g, g.bs, hi_cap, C_in, C_out), l = dgrad_call(g, (int)lb, lo_cap, C_in, C_out);
+        D.ig = r256(std::max(hi_cap ? igemm_ws_bytes(h.g, h.a, 3, 1) : 0, lo_cap ? igemm_ws_bytes(l.g, l.a, 3, 1) : 0));
+    }
+    D.total = D.qh + D.ql + D.wt + D.masks + D.ig;
     return D;
 }
 
@@ -731,28 +784,40 @@ template <typename T, int L>
 hipError_t dgrad_t(const Geo& g, const void* dho, const void* dlo, const uint8_t* mask, const void* w, int C_in,
                    int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws, hipStream_t st) {
     (void)mask;
-    const DgradLayout D = dgrad_layout(sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2), g, C_in, C_out,
-                                       hi_cap, lo_cap);
+    constexpr int dt = sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2);
+    const DgradLayout D = dgrad_layout(dt, L, g, C_in, C_out, hi_cap, lo_cap);
     if (ws.bytes < D.total || !ws.p) return hipErrorInvalidValue;
     char* base = (char*)ws.p;
     T* qh = (T*)base;
     T* ql = (T*)(base + D.qh);
     T* wt = (T*)(base + D.qh + D.ql);
     uint8_t* ones = (uint8_t*)(base + D.qh + D.ql + D.wt);
-    uint8_t* zeros = ones + g.B;
+    const long long nm = std::max<long long>({g.B, (long long)hi_cap, (long long)lo_cap});
+    uint8_t* zeros = ones + nm;
+    void* igws = base + D.qh + D.ql + D.wt + D.masks;
     const int lb = g.bs / 2;
     const int grid = device_cus() * 4;
-    hipLaunchKernelGGL((k_fill8), dim3(grid), dim3(WG), 0, st, ones, g.B, (uint8_t)1);
-    hipLaunchKernelGGL((k_fill8), dim3(grid), dim3(WG), 0, st, zeros, g.B, (uint8_t)0);
-    hipLaunchKernelGGL((k_wflip<T, L>), dim3((C_in * C_out * 9 + WG - 1) / WG), dim3(WG), 0, st, (const T*)w, C_out,
-                       C_in, wt);
-    if (hi_cap > 0)
-        hipLaunchKernelGGL((k_pad2<T, L>), dim3(grid), dim3(WG), 0, st, (const T*)dho, hi_cap, C_out, g.bs, qh);
-    if (lo_cap > 0)
-        hipLaunchKernelGGL((k_pad2<T, L>), dim3(grid), dim3(WG), 0, st, (const T*)dlo, lo_cap, C_out, lb, ql);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int dt = sizeof(T) == 4 ? 0 : (std::is_same<T, f16>::value ? 1 : 2);
+    hipError_t e;
+    // the implicit GEMM when both calls take it (shapes and alignment)
+    DgradCall h = dgrad_call(g, g.bs, hi_cap, C_in, C_out), l = dgrad_call(g, lb, lo_cap, C_in, C_out);
+    h.a.in_hi = qh;
+    h.a.weight = wt;
+    h.a.out_hi = dhp;
+    l.a.in_hi = ql;
+    l.a.weight = wt;
+    l.a.out_hi = dlp;
+    const bool ig = D.ig_shape && (hi_cap == 0 || igemm_fits(dt, L, h.g, h.a)) &&
+                    (lo_cap == 0 || igemm_fits(dt, L, l.g, l.a));
+    const int pad = ig ? 1 : 2;
+    hipLaunchKernelGGL((k_dgrad_prep<T, L>), dim3(grid), dim3(WG), 0, st, (const T*)w, C_out, C_in, wt, ones, zeros,
+                       nm, (const T*)dho, hi_cap, qh, (const T*)dlo, lo_cap, ql, g.bs, pad);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ig) {
+        const Ws w2{igws, D.ig};
+        if (hi_cap > 0 && (e = launch_igemm(dt, h.g, ones, h.a, 3, 1, w2, st)) != hipSuccess) return e;
+        if (lo_cap > 0 && (e = launch_igemm(dt, l.g, ones, l.a, 3, 1, w2, st)) != hipSuccess) return e;
+        return hipSuccess;
+    }
     // the high stack: every block of the grid taken as high, extent bs + 2 (the padded gradient)
     if (hi_cap > 0) {
         Geo gh = g;
@@ -825,8 +890,8 @@ hipError_t launch_pad_bwd(int dtype, int layout, const Geo& g, const void* dhp, 
     }
 }
 
-size_t dgrad_ws_bytes(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
-    return dgrad_layout(dtype, g, C_in, C_out, hi_cap, lo_cap).total;
+size_t dgrad_ws_bytes(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap) {
+    return dgrad_layout(dtype, layout, g, C_in, C_out, hi_cap, lo_cap).total;
 }
 
 hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, const void* dlo, const uint8_t* mask,

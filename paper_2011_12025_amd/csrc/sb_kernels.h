@@ -99,7 +99,7 @@ hipError_t launch_maxpool(int dtype, const void* x, int N, int C, int H, int W, 
 // are launch_split / launch_combine with bwd.
 hipError_t launch_pad_bwd(int dtype, int layout, const Geo& g, const void* dhp, const void* dlp, const uint8_t* mask,
                           void* dhi, void* dlo, int hi_cap, int lo_cap, int pm, hipStream_t st);
-size_t dgrad_ws_bytes(int dtype, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap);
+size_t dgrad_ws_bytes(int dtype, int layout, const Geo& g, int C_in, int C_out, int hi_cap, int lo_cap);
 hipError_t launch_dgrad(int dtype, int layout, const Geo& g, const void* dho, const void* dlo, const uint8_t* mask,
                         const void* w, int C_in, int C_out, void* dhp, void* dlp, int hi_cap, int lo_cap, Ws ws,
                         hipStream_t st);
