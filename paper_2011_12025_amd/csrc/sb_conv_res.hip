@@ -4,15 +4,15 @@
 //
 // One 8-wave workgroup per CU computes a 64-output-channel slice and walks a
 // static list of tiles.  A tile is a group of rows of one block: R rows of a
-// high block (R = 8 for blocks of 32, 4 for blocks of 64) or, from packed
-// stacks, 2R rows of a low block, so every tile has the same number of
-// output pixels and a low block has a quarter of a high block's tiles (from
-// the dense map, R/2 low rows; see res_tile).  The list holds the high
-// blocks' tiles, then the low blocks', in slot order; its length follows the
-// class counts of the mask, so the work of a launch falls with the
-// low-resolution fraction.  The padded input
-// tile (all input channels, 128 bytes per pixel) is triple-buffered in LDS
-// and the waves are specialised:
+// high block (R = 8 for blocks of 32, 4 for blocks of 64) or, from packed or
+// padded stacks, 2R rows of a low block, so every tile has the same number
+// of output pixels and a low block has a quarter of a high block's tiles;
+// that list holds the high blocks' tiles, then the low blocks', in slot
+// order, and its length follows the class counts of the mask, so the work
+// of a launch falls with the low-resolution fraction.  From the dense map a
+// low tile is R/2 low rows and the list is block-major (see res_tile).  The
+// padded input tile (all input channels, 128 bytes per pixel) is
+// triple-buffered in LDS and the waves are specialised:
 //
 //   waves 0-3  (consumers): wave c owns output channels co0 + 32 * (c & 1)
 //              + [0, 32) and half (c >> 1) of the tile; its 32 x 9 x C_in
@@ -113,23 +113,36 @@ struct RTile {
     float inv_pe;
 };
 
-// Tile `tile` of the class-major list: first the high blocks' tiles (Gh per
-// block, R image rows each), then the low blocks' (Gl per block, RL low rows
-// each), in slot order.  nth = high tiles in the list.  From packed or padded
-// stacks RL = 2R (the same pixels as a high tile, so a low block costs a
-// quarter of a high one); from the dense map RL = R/2 (a low tile's pixels
-// are 2x2 averages of image pixels, staged through registers, and 2R rows of
-// them take three rounds of loads where R/2 rows take one).
+// Tile `tile` of the list.  From packed or padded stacks the list is
+// class-major: first the high blocks' tiles (Gh per block, R image rows
+// each), then the low blocks' (Gl per block, RL = 2R low rows each: the same
+// pixels as a high tile, so a low block costs a quarter of a high one), in
+// slot order; nth = high tiles in the list.  From the dense map the list is
+// block-major with RL = R/2 (Gh = Gl): a low tile's pixels are 2x2 averages
+// of image pixels, staged through registers, and 2R rows of them take three
+// rounds of loads where R/2 rows take one; the block of a tile is then its
+// index over Gh, with no search for the n-th block of a class.
 template <int SRC, int DST, bool ONE>
 __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const WaveMaskT<ONE>& wm, int R, int RL,
                                          int Gh, int Gl, int nth, int tile, RTile& t, Neigh& nb) {
-    const bool high = tile < nth;
-    const int G = high ? Gh : Gl;
-    const int q = high ? tile : tile - nth;
-    const int slot = q / G;
-    const int grp = q - slot * G;
-    const int k = wm.find_nth(slot, high);
-    if (k < 0) return false;
+    bool high;
+    int slot, grp, k;
+    if constexpr (SRC == SRC_DENSE) {
+        // block-major: Gh == Gl tiles per block of either class, and no
+        // search for the n-th block of a class
+        k = tile / Gh;
+        grp = tile - k * Gh;
+        high = wm.high(k);
+        slot = 0;
+    } else {
+        high = tile < nth;
+        const int G = high ? Gh : Gl;
+        const int q = high ? tile : tile - nth;
+        slot = q / G;
+        grp = q - slot * G;
+        k = wm.find_nth(slot, high);
+        if (k < 0) return false;
+    }
     const int per = g.GH * g.GW;
     t.n = k / per;
     const int rem = k - t.n * per;
@@ -138,7 +151,7 @@ __device__ __forceinline__ bool res_tile(const Geo& g, const ConvArgs& a, const 
     constexpr bool NEED_SLOTS = !(SRC == SRC_DENSE && DST == DST_DENSE);
     nb = wave_neighbourhood<NEED_SLOTS>(wm, g.GH, g.GW, t.n, t.gy, t.gx);
     t.high = high ? 1 : 0;
-    t.slot = slot;
+    t.slot = SRC == SRC_DENSE ? (NEED_SLOTS ? nb.slot[4] : 0) : slot;
     t.e = high ? g.bs : (g.bs >> 1);
     const int rr = high ? R : RL;
     t.r0 = grp * rr;
@@ -636,11 +649,14 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     // one block (which share halo rows) run on one XCD and share its L2.
     // The tile list by class (the class counts come from the mask; slots past
     // a stack's capacity are skipped).
-    const int nh_all = wm.count_high((int)g.B);
-    constexpr bool CAPS = !(SRC == SRC_DENSE && DST == DST_DENSE);
-    const int nh = CAPS ? min(nh_all, a.hi_cap) : nh_all;
-    const int nl = CAPS ? min((int)g.B - nh_all, a.lo_cap) : (int)g.B - nh_all;
-    const int nth = nh * Gh, ntiles = nth + nl * Gl;
+    int nth = 0, ntiles = (int)g.B * Gh;  // the dense map: every block, block-major
+    if constexpr (SRC != SRC_DENSE) {
+        const int nh_all = wm.count_high((int)g.B);
+        const int nh = min(nh_all, a.hi_cap);
+        const int nl = min((int)g.B - nh_all, a.lo_cap);
+        nth = nh * Gh;
+        ntiles = nth + nl * Gl;
+    }
     const int nwg = (int)gridDim.x;
     const int pos = (nwg & 7) ? (int)blockIdx.x : (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
     int tile = pos;
