@@ -396,6 +396,25 @@ def extra_measurements(args, torch, np, sb, B, inputs, sets, wd, bd, x_first, ti
     t = time_batch_fn(torch, lambda i: sb.policy_heuristic(img, 128, 0.4, out=(mk, sc)), it)
     out["policy_heuristic_us"] = {"us": round(t * 1e3, 2), "image": "1x3x1024x2048 f16, 128-px blocks, tau 0.4",
                                   "GB/s": round(img.numel() * 2 / (t * 1e-3) / 1e9, 1)}
+    # -- a policy network forward for overhead timing (random weights): four
+    # 3x3 stride-2 layers of 64 features with ReLU on a 256x512 low-resolution
+    # image, then a 1x1 stride-2 layer to one logit per 128-px block (8x16)
+    pin = inputs.feature_map(2, 1, 3, 256, 512, "f16").to(dev).contiguous(memory_format=cl)
+    pws = [inputs.conv_weight(10 + i, co, ci, k, "f16").to(dev).contiguous(memory_format=cl)
+           for i, (co, ci, k) in enumerate([(64, 3, 3), (64, 64, 3), (64, 64, 3), (64, 64, 3), (1, 64, 1)])]
+    pbs = [inputs.conv_bias(10 + i, w_.shape[0], w_.shape[1] * w_.shape[2] ** 2, "f16").to(dev) for i, w_ in enumerate(pws)]
+
+    def policy_net(i):
+        h = pin
+        for li, (w_, b_) in enumerate(zip(pws, pbs)):
+            k = w_.shape[2]
+            h = sb.conv2d(h, w_, b_, stride=2, padding=k // 2, relu=li < 4)
+        return h
+    t = time_batch_fn(torch, policy_net, it)
+    macs = (128 * 256 * 64 * 27 + 64 * 128 * 64 * 576 + 32 * 64 * 64 * 576 + 16 * 32 * 64 * 576 + 8 * 16 * 64)
+    out["policy_net_us"] = {"us": round(t * 1e3, 2), "GMAC": round(macs / 1e9, 3),
+                            "net": "3x3/2 convs 3-64-64-64-64 with ReLU on 1x3x256x512 f16, then 1x1/2 to 1 channel "
+                                   "(8x16 logits); random weights, timing only"}
     # -- backward pass of the benchmark layer (counts known, every call queued)
     dy = inputs.feature_map(1, N, C, H, W, "f16").to(dev).contiguous(memory_format=cl)
     hp, lp = sb.pad(hi, lo, md, bs, H, W)
