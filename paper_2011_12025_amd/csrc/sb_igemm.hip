@@ -11,21 +11,21 @@
 // the block plan in LDS (for every block the number of high blocks before
 // it, by a workgroup-wide scan of the mask) and then, for each of its tile
 // pixels and taps, a source descriptor: a pixel of the high or the low stack
-// (own block, same-resolution neighbour, or the low neighbour's pixel
-// nearest-upsampled), the 2x2 cell of a high neighbour to average, or zero
-// (outside the image, or a neighbour past its stack's capacity).  Stride-2
-// and 1x1 convolutions only change which padded pixel a tap reads.
+// (own block, same-resolution neighbour, the low neighbour's pixel
+// nearest-upsampled, the top-left pixel of a high neighbour's cell with
+// strided sampling), or zero (outside the image, a neighbour past its
+// stack's capacity, zero padding).  A low block's halo across a resolution
+// change with average sampling (the 2x2 average of a high neighbour's cell)
+// comes from the low stack padded beforehand by the pad kernel, so every
+// source is a plain copy.  Stride-2 and 1x1 convolutions only change which
+// padded pixel a tap reads.
 //
 // Pipeline (three LDS stages): weights and pixels of step s+2 go global ->
 // LDS by DMA (global_load_lds, 16 bytes per lane) while the MFMAs of step s
 // run, so every wave issues the same number of DMAs per step and waits for
-// step s+1 with a constant count.  A pixel that is a 2x2 average gets its
-// top-left source by that DMA; its three other sources are copied into a side
-// buffer of LDS (issued one step ahead, before the next step's DMAs, so the
-// same wait covers them), then averaged in fp32 in the library's fixed order
-// over the top-left value.  Rows of 128
-// bytes carry an XOR swizzle of their 16-byte chunks so that the 16 rows
-// read by one MFMA operand hit distinct banks.
+// step s+1 with a constant count.  Rows of 128 bytes carry an XOR swizzle of
+// their 16-byte chunks so that the 16 rows read by one MFMA operand hit
+// distinct banks.
 //
 // Split K: when the tiles alone do not fill the chip, the K steps of a tile
 // are divided among grid.z workgroups that write fp32 partial tiles to a
@@ -75,13 +75,12 @@ constexpr int GNST = 3;        // LDS stages
 constexpr int GMAXB = 8192;    // blocks whose plan fits the LDS table
 constexpr int GMAXC = 4096;    // input channels the zero row covers
 
-// A row of zeros that pixels outside the image (and 2x2-average pixels before
-// their average is written) are copied from; device globals start zeroed and
-// this one is never written.
+// A row of zeros that pixels outside the image are copied from; device
+// globals start zeroed and this one is never written.
 __device__ __align__(16) uint4 g_zero_row[GMAXC * 2 / 16];
 
 // source descriptor: kind in bits 30..31, pixel index (in its stack) below
-constexpr uint32_t GK_HI = 0u, GK_LO = 1u, GK_AVG = 2u, GK_ZERO = 3u;
+constexpr uint32_t GK_HI = 0u, GK_LO = 1u, GK_ZERO = 3u;
 __device__ __forceinline__ uint32_t gdesc(uint32_t kind, int pix) { return (kind << 30) | (uint32_t)pix; }
 
 // byte offset of 16-byte chunk q of LDS row r (XOR swizzle, see above)
@@ -108,34 +107,8 @@ __device__ __forceinline__ void gbarrier() {
     asm volatile("" ::: "memory");
 }
 
-// 16-byte LDS read and write that complete before returning.  Written as
-// inline assembly so that the compiler, which cannot tell the step that just
-// landed from the DMAs still in flight, does not wait for all of them first.
-typedef unsigned int gu32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 glds_read16(const void* p) {
-    gu32x4 r;
-    const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)p;
-    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(a) : "memory");
-    return uint4{r.x, r.y, r.z, r.w};
-}
-__device__ __forceinline__ void glds_write16(void* p, uint4 v) {
-    const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)p;
-    const gu32x4 w = {v.x, v.y, v.z, v.w};
-    asm volatile("ds_write_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" ::"v"(a), "v"(w) : "memory");
-}
-
 __device__ __forceinline__ void gdma16(const void* g, unsigned char* window) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr)window, 16, 0, 0);
-}
-
-// ((a + b) + (c + d)) * 0.25 per element of four 16-byte vectors of T
-template <typename T>
-__device__ __forceinline__ uint4 gavg(uint4 a, uint4 b, uint4 c, uint4 d) {
-    Vec<T, 8> va, vb, vc, vd, r;
-    va.raw = a; vb.raw = b; vc.raw = c; vd.raw = d;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r.e[i] = avg4(va.e[i], vb.e[i], vc.e[i], vd.e[i]);
-    return r.raw;
 }
 
 // Smallest block k whose class-c count through k exceeds s (the block of
@@ -160,19 +133,16 @@ __device__ __forceinline__ void gissue_a(const T* const (&wrow)[AR], unsigned ch
 }
 
 // This lane's pixel-row sources of one tap, decoded once per tap: a pointer
-// to chunk pq of the source row (the top-left pixel of a 2x2-average cell,
-// the zero row for pixels outside the image) and a bit per row that is a
-// 2x2 average.  A step then only adds its channel offset.
+// to chunk pq of the source row (the zero row for pixels outside the
+// image).  A step then only adds its channel offset.
 template <typename T, int BR>
 struct GRows {
     const T* p[BR];
-    uint32_t avg;
 };
 
 template <typename T, int BR>
 __device__ __forceinline__ void gdecode(const uint32_t (&dsc)[BR], const int (&pq)[BR], const T* __restrict__ in_hi,
                                         const T* __restrict__ in_lo, const T* zrow, int C_in, GRows<T, BR>& r) {
-    r.avg = 0;
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
         const uint32_t d = dsc[j];
@@ -180,7 +150,6 @@ __device__ __forceinline__ void gdecode(const uint32_t (&dsc)[BR], const int (&p
         const T* base = kind == GK_LO ? in_lo : (kind == GK_ZERO ? zrow : in_hi);
         const size_t pix = kind != GK_ZERO ? (size_t)(d & 0x3FFFFFFFu) : 0;
         r.p[j] = base + pix * C_in + pq[j];
-        r.avg |= (kind == GK_AVG ? 1u : 0u) << j;
     }
 }
 
@@ -205,41 +174,6 @@ template <typename T, int N>
 __device__ __forceinline__ void gissue_pad(const T* zrow, unsigned char* st, int wave, int lane) {
 #pragma unroll
     for (int j = 0; j < N; ++j) gdma16(zrow + (lane & 7) * 8, st + (wave * N + j) * 1024);
-}
-
-// The three other sources (right, below, below-right) of this lane's
-// 2x2-average pixels of one step, copied into the side buffer: window
-// (wave * BR + j) * 3 + t, this lane's slot at lane * 16.
-template <typename T, int BR>
-__device__ __forceinline__ void gissue_side(const GRows<T, BR>& r, int c, int C_in, int bs, unsigned char* side,
-                                            int wave) {
-#pragma unroll
-    for (int j = 0; j < BR; ++j) {
-        if ((r.avg >> j) & 1u) {
-            const T* p0 = r.p[j] + c;
-            unsigned char* w = side + (wave * BR + j) * 3 * 1024;
-            gdma16(p0 + C_in, w);
-            gdma16(p0 + (size_t)bs * C_in, w + 1024);
-            gdma16(p0 + (size_t)(bs + 1) * C_in, w + 2048);
-        }
-    }
-}
-
-// Replaces the top-left value of every 2x2-average pixel of a landed step
-// (st: the step's pixel tile) by the average of its four sources.
-template <typename T, int BR>
-__device__ __forceinline__ void gcommit_side(uint32_t avg, unsigned char* st, const unsigned char* side, int wave,
-                                             int lane) {
-#pragma unroll
-    for (int j = 0; j < BR; ++j) {
-        if ((avg >> j) & 1u) {
-            unsigned char* slot = st + (wave * BR + j) * 1024 + lane * 16;
-            const unsigned char* w = side + (wave * BR + j) * 3 * 1024 + lane * 16;
-            const uint4 va = glds_read16(slot), vb = glds_read16(w), vc = glds_read16(w + 1024),
-                        vd = glds_read16(w + 2048);
-            glds_write16(slot, gavg<T>(va, vb, vc, vd));
-        }
-    }
 }
 
 struct GParams {
@@ -318,8 +252,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     uint32_t* s_desc = reinterpret_cast<uint32_t*>(smem + GNST * STAGE);
     int* s_pk = reinterpret_cast<int*>(smem + GNST * STAGE + TM * KT * 4);
     int* s_pij = s_pk + TM;
-    unsigned char* s_side = smem + GNST * STAGE + TM * KT * 4 + 2 * TM * 4;
-    uint16_t* s_hb = reinterpret_cast<uint16_t*>(s_side + GWAVES * BR * 3 * 1024);
+    uint16_t* s_hb = reinterpret_cast<uint16_t*>(smem + GNST * STAGE + TM * KT * 4 + 2 * TM * 4);
     __shared__ int s_wsum[GWAVES];
 
     const int tid = (int)threadIdx.x, lane = tid & 63;
@@ -447,7 +380,10 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                     if (s2 < (h2 ? a.hi_cap : a.lo_cap)) {
                         if (h2 == high) ds = gdesc(high ? GK_HI : GK_LO, (s2 * e_in + u2) * e_in + v2);
                         else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
-                        else ds = gdesc(pm == PM_STRIDED ? GK_HI : GK_AVG, (s2 * bs + 2 * u2) * bs + 2 * v2);
+                        // a low block beside a high one: strided sampling reads the
+                        // cell's top-left pixel; average sampling never gets here (the
+                        // low stack is then padded beforehand, see igemm_plan)
+                        else ds = gdesc(GK_HI, (s2 * bs + 2 * u2) * bs + 2 * v2);
                     }
                 }
             }
@@ -456,7 +392,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     }
     __syncthreads();
 
-    // ---- prologue: step 0 (2x2 averages, pixels), step 1 (weights, pixels)
+    // ---- prologue: step 0 (pixels), step 1 (weights, pixels)
     int tap1 = tap0, c1 = c0 + 1;
     if (c1 == cpt) { c1 = 0; ++tap1; }
     uint32_t dsc[BR];
@@ -465,7 +401,6 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, r0);
     gload_desc<BR>(s_desc, prow, KT, tap1 < KT ? tap1 : tap0, dsc);
     gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, rA);
-    gissue_side<T, BR>(r0, c0 * GKC, C_in, bs, s_side, wave);
     gissue_b<T, BR>(r0, c0 * GKC, s_stage + A_BYTES, wave);
     if (n > 1) {
         gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
@@ -474,7 +409,6 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         gissue_pad<T, AR + BR>(zrow, s_stage + STAGE, wave, lane);
     }
     __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-    gcommit_side<T, BR>(r0.avg, s_stage + A_BYTES, s_side, wave, lane);
     gbarrier();
 
     floatx4 acc[MS][NS];
@@ -485,8 +419,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
 
     const int wm = wave % WM, wn = wave / WM;
     const int l16 = lane & 15, kg = lane >> 4;
-    // (tap, chunk) of step s + 1 and s + 2
-    int ca = c1;
+    // (tap, chunk) of step s + 2
     int tb = tap1, cb = c1 + 1;
     if (cb == cpt) { cb = 0; ++tb; }
     gload_desc<BR>(s_desc, prow, KT, tb < KT ? tb : tap0, dsc);
@@ -511,7 +444,6 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                     *reinterpret_cast<const frag*>(cur + A_BYTES + gsw(wm * MS * 16 + ms * 16 + l16, ks * 4 + kg));
         }
         __builtin_amdgcn_sched_barrier(0);
-        if (s + 1 < n) gissue_side<T, BR>(rA, ca * GKC, C_in, bs, s_side, wave);
         if (s + 2 < n) {
             gissue_a<T, AR>(wrow, s_stage + b2 * STAGE, tb * C_in + cb * GKC, wave);
             gissue_b<T, BR>(rB, cb * GKC, s_stage + b2 * STAGE + A_BYTES, wave);
@@ -528,10 +460,8 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         __builtin_amdgcn_sched_barrier(0);
         // step s + 1 has landed once only step s + 2's DMAs can be outstanding
         __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
-        if (s + 1 < n) gcommit_side<T, BR>(rA.avg, s_stage + b1 * STAGE + A_BYTES, s_side, wave, lane);
         gbarrier();
         b_cur = b1;
-        ca = cb;
         rA = rB;
         if (++cb == cpt) {  // a new tap: its sources (read a step before they are used)
             cb = 0;
@@ -632,7 +562,18 @@ inline size_t ground256(size_t b) { return (b + 255) / 256 * 256; }
 
 template <int TM, int TN, int KT>
 constexpr int igemm_smem_fixed() {
-    return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4 + GWAVES * (TM / (8 * GWAVES)) * 3 * 1024;
+    return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4;
+}
+
+inline int igemm_hb_bytes(const Geo& g) { return (((int)g.B + 1) * 2 + 15) / 16 * 16; }
+
+// Widest workgroup tile for these shapes: 64 output channels for narrow
+// layers, 256 from 256 channels on (eight 64 x 64 wave tiles: a third fewer
+// LDS reads per MAC than 128) when its LDS fits, else 128.
+inline int igemm_tn(const Geo& g, const ConvArgs& a) {
+    if (a.C_out <= 64) return 64;
+    if (a.C_out >= 256 && igemm_smem_fixed<128, 256, 9>() + igemm_hb_bytes(g) + GWAVES * 4 <= 160 * 1024) return 256;
+    return 128;
 }
 
 // Everything about a launch that the host decides from the shapes alone:
@@ -647,42 +588,47 @@ struct IgPlan {
 IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     IgPlan p;
     p.TM = 128;
-    p.TN = a.C_out <= 64 ? 64 : 128;
     const int eo_h = g.bs / stride, eo_l = (g.bs / 2) / stride;
     p.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + p.TM - 1) / p.TM);
     p.tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + p.TM - 1) / p.TM);
-    p.tiles_n = (a.C_out + p.TN - 1) / p.TN;
     const int tiles = p.tiles_h + p.tiles_l;
-    // Split K: one workgroup per CU at a time (LDS), each taking about the
-    // same time per K step, so a launch costs about rounds x (steps per split
-    // + start-up); a split costs the partial-sum pass on top, which grows with
-    // the number of splits.  Take the cheapest split that keeps at least four
-    // steps per workgroup.
+    // Tile width and split K by a cost model in units of one 128 x 128 K step
+    // (about 1 us): one workgroup per CU at a time (LDS), so a launch costs
+    // about rounds x (steps per split x step cost + start-up); a 128 x 256
+    // step does twice the MACs at about 1.3 times the cost; a split adds the
+    // partial-sum pass, which grows with the partial tiles it reads.  Take the
+    // cheapest choice that keeps at least four steps per workgroup.
     const int cus = device_cus();
     const int nsteps = ks * ks * (a.C_in / GKC);
-    int S = 1;
-    {
-        const long long wgs = (long long)tiles * p.tiles_n;
-        long long best = 0;
+    const int tn_max = igemm_tn(g, a);
+    double best = -1.0;
+    p.TN = tn_max;
+    p.splits = 1;
+    for (int tn = tn_max; tn >= 128 || tn == tn_max; tn /= 2) {
+        const int tiles_n = (a.C_out + tn - 1) / tn;
+        const double w = tn == 256 ? 1.3 : 1.0, wr = tn == 256 ? 2.0 : 1.0;
+        const long long wgs = (long long)tiles * tiles_n;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
             const long long rounds = (wgs * c + cus - 1) / cus;
-            const long long cost = rounds * ((nsteps + c - 1) / c + GSTART_COST) + (c > 1 ? GSPLIT_COST + c : 0);
-            if (c == 1 || cost < best) {
+            const double cost = (double)rounds * ((nsteps + c - 1) / c * w + GSTART_COST) +
+                                (c > 1 ? GSPLIT_COST + c * wr : 0.0);
+            if (best < 0.0 || cost < best) {
                 best = cost;
-                S = c;
+                p.TN = tn;
+                p.splits = c;
             }
         }
+        if (tn <= 128) break;
     }
-    p.splits = tiles > 0 ? S : 1;
-    // A low block's halo pixels across a resolution boundary are 2x2 averages
-    // of the high neighbour: four loads per element in every K step, which make
-    // the low tiles the last to finish.  A 3 x 3 convolution with both classes
-    // pads the low stack once instead (BlockPad of the low blocks, one extra
-    // launch), so that every low-tile source is a plain copy.  Measured at the
-    // ResNet-18 stage shapes of a 1024x2048 image (128, 256 and 512 channels,
-    // 25-75 % low blocks), the extra pass is 6-12 us faster than the averages
-    // in the K loop at 25 % low blocks and at 128 channels, and within 3 us
-    // either way elsewhere.
+    p.tiles_n = (a.C_out + p.TN - 1) / p.TN;
+    if (tiles == 0) p.splits = 1;
+    // A low block's halo across a resolution change, with average sampling, is
+    // the 2x2 average of a high neighbour's cell: a 3 x 3 convolution with
+    // both classes pads the low stack once beforehand (BlockPad of the low
+    // blocks, one extra launch), so that every source of the K loop is a plain
+    // copy.  (Averaging in the K loop instead measured 6-12 us slower at the
+    // ResNet-18 stage shapes with 25 % low blocks or 128 channels, within
+    // 3 us either way elsewhere.)
     p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG;
     p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 4)
                                 : 0;
@@ -704,7 +650,7 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
     gp.eo_l = (g.bs / 2) / ST;
     gp.cpt = a.C_in / GKC;
     gp.tiles_h = pl.tiles_h;
-    const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
+    const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + igemm_hb_bytes(g);
     hipError_t e = ensure_dyn_lds((const void*)k_igemm<T, KS, ST, WM, MS, NS>, smem);
     if (e != hipSuccess) return e;
     const int tiles_n = pl.tiles_n;
@@ -740,7 +686,9 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
 
 template <typename T, int KS, int ST>
 hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
-    if (a.C_out <= 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st);
+    const int tn = igemm_plan(g, a, KS, ST).TN;
+    if (tn == 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st);
+    if (tn == 256) return igemm_run<T, KS, ST, 2, 4, 4>(g, mask, a, ws, st);
     return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, ws, st);
 }
 
@@ -761,7 +709,7 @@ bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     const long long lb = g.bs / 2;
     if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * (lb + 2) * (lb + 2) >= (1LL << 30))
         return false;
-    const int smem = igemm_smem_fixed<128, 128, 9>() + (((int)g.B + 1) * 2 + 15) / 16 * 16;
+    const int smem = igemm_smem_fixed<128, 128, 9>() + igemm_hb_bytes(g);
     return smem + GWAVES * 4 <= 160 * 1024;
 }
 
