@@ -61,7 +61,8 @@ def parse():
                    help="what --profile-run launches: layer, split, pad, combine, conv3x3, block_conv3x3 (the "
                         "headline workload), or bconv:<stage>:<low fraction> / layer:<stage>:<low fraction> (the "
                         "packed block convolution / fused layer at ResNet-18 stage 1-4 of a 1024x2048 image, "
-                        "exact-fraction mask)")
+                        "exact-fraction mask), or encoder:<low fraction> (20 replays of the N=1 1024x2048 block "
+                        "encoder graph, 128-px blocks, Bernoulli mask)")
     return p.parse_args()
 
 
@@ -398,23 +399,31 @@ def extra_measurements(args, torch, np, sb, B, inputs, sets, wd, bd, x_first, ti
                                   "GB/s": round(img.numel() * 2 / (t * 1e-3) / 1e9, 1)}
     # -- a policy network forward for overhead timing (random weights): four
     # 3x3 stride-2 layers of 64 features with ReLU on a 256x512 low-resolution
-    # image, then a 1x1 stride-2 layer to one logit per 128-px block (8x16)
+    # image, then a 1x1 stride-2 layer to eight channels, one pixel per
+    # 128-px block of the full image (8x16).  The first layer is the dense
+    # small-channel convolution; the others run as block convolutions of two
+    # 128-px blocks, all high, whose BlockPad equals zero padding.
     pin = inputs.feature_map(2, 1, 3, 256, 512, "f16").to(dev).contiguous(memory_format=cl)
     pws = [inputs.conv_weight(10 + i, co, ci, k, "f16").to(dev).contiguous(memory_format=cl)
-           for i, (co, ci, k) in enumerate([(64, 3, 3), (64, 64, 3), (64, 64, 3), (64, 64, 3), (1, 64, 1)])]
-    pbs = [inputs.conv_bias(10 + i, w_.shape[0], w_.shape[1] * w_.shape[2] ** 2, "f16").to(dev) for i, w_ in enumerate(pws)]
+           for i, (co, ci, k) in enumerate([(64, 3, 3), (64, 64, 3), (64, 64, 3), (64, 64, 3), (8, 64, 1)])]
+    pbs = [inputs.conv_bias(10 + i, w_.shape[0], w_.shape[1] * w_.shape[2] ** 2, "f16").to(dev)
+           for i, w_ in enumerate(pws)]
+    ones2 = torch.ones((1, 1, 2), dtype=torch.uint8, device=dev)
+    empty_lo = torch.empty((0, 64, 64, 64), dtype=torch.float16, device=dev).contiguous(memory_format=cl)
 
     def policy_net(i):
-        h = pin
-        for li, (w_, b_) in enumerate(zip(pws, pbs)):
-            k = w_.shape[2]
-            h = sb.conv2d(h, w_, b_, stride=2, padding=k // 2, relu=li < 4)
-        return h
+        h = sb.conv2d(pin, pws[0], pbs[0], stride=2, padding=1, relu=True)  # 64 x 128 x 256
+        hi, lo = sb.split(h, ones2, 128, counts=(2, 0))
+        bsz, Hh, Wh = 128, 128, 256
+        for li in range(1, 5):
+            hi, lo = sb.block_conv_ex(hi, lo, ones2, bsz, Hh, Wh, pws[li], pbs[li], stride=2, relu=li < 4)
+            bsz, Hh, Wh = bsz // 2, Hh // 2, Wh // 2
+        return hi
     t = time_batch_fn(torch, policy_net, it)
-    macs = (128 * 256 * 64 * 27 + 64 * 128 * 64 * 576 + 32 * 64 * 64 * 576 + 16 * 32 * 64 * 576 + 8 * 16 * 64)
+    macs = (128 * 256 * 64 * 27 + 64 * 128 * 64 * 576 + 32 * 64 * 64 * 576 + 16 * 32 * 64 * 576 + 8 * 16 * 64 * 8)
     out["policy_net_us"] = {"us": round(t * 1e3, 2), "GMAC": round(macs / 1e9, 3),
-                            "net": "3x3/2 convs 3-64-64-64-64 with ReLU on 1x3x256x512 f16, then 1x1/2 to 1 channel "
-                                   "(8x16 logits); random weights, timing only"}
+                            "net": "3x3/2 convs 3-64-64-64-64 with ReLU on 1x3x256x512 f16, then 1x1/2 to 8 channels "
+                                   "(8x16 per block); random weights, timing only"}
     # -- backward pass of the benchmark layer (counts known, every call queued)
     dy = inputs.feature_map(1, N, C, H, W, "f16").to(dev).contiguous(memory_format=cl)
     hp, lp = sb.pad(hi, lo, md, bs, H, W)
@@ -704,6 +713,8 @@ def profile_stage(args):
     import paper_2011_12025_amd as sb
     import paper_2011_12025_amd._binding as B
     from paper_2011_12025_amd import inputs
+    if args.profile_op.startswith("encoder:"):
+        return profile_encoder(args)
     kind, stage, f = args.profile_op.split(":")
     C, H, W, bs = SWEEP_LAYERS[int(stage) - 1]
     f = float(f)
@@ -728,6 +739,33 @@ def profile_stage(args):
     torch.cuda.synchronize()
     print(json.dumps({"profile_run": True, "copy_bytes": a.numel(), "op": args.profile_op, "launches": 10,
                       "n_high": nh, "n_low": nl}))
+
+
+def profile_encoder(args):
+    """--profile-run for the N=1 block encoder: a 256 MiB copy of known size,
+    then 20 replays of the captured graph (1024x2048x3 fp16, 128-px blocks,
+    Bernoulli mask with the given low fraction)."""
+    import torch
+
+    from paper_2011_12025_amd import inputs
+    from paper_2011_12025_amd.encoder import BlockEncoder
+    q = float(args.profile_op.split(":")[1])
+    dev, cl = torch.device("cuda:0"), torch.channels_last
+    torch.cuda.set_device(dev)
+    x = inputs.feature_map(0, 1, 3, 1024, 2048, "f16").to(dev).contiguous(memory_format=cl)
+    enc = BlockEncoder(inputs.encoder_weights(0, "f16"), 128)
+    m = inputs.mask_bernoulli(0, 1, 8, 16, q)
+    nh = int(m.sum())
+    g, y = enc.capture(x, torch.from_numpy(m).to(dev), (nh, m.size - nh))
+    a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    bcp = torch.empty_like(a)
+    for _ in range(3):
+        bcp.copy_(a)
+    for _ in range(20):
+        g.replay()
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_run": True, "copy_bytes": a.numel(), "op": args.profile_op, "replays": 20,
+                      "n_high": nh, "n_low": int(m.size - nh)}))
 
 
 def bench_suite(args):
