@@ -73,6 +73,12 @@ BCASES = [
     # 128 input channels with both classes: the low stack is padded once before the GEMM
     BCase("ig_lowpad_k3s2_c128_bf16", "bf16", 2, 128, 128, 32, 64, 8, 3, 2, relu=True, seed=83),
     BCase("ig_lowpad_k3s1_c128_bs16_f16", "f16", 2, 128, 64, 64, 96, 16, 3, 1, p_low=0.75, residual=True, seed=84),
+    # 256 and more output channels: the 128x256 workgroup tile (split K, and a
+    # partial second N tile at 320 channels), padded low stack at 256 / 512 channels
+    BCase("ig_tn256_k3s1_c256_bs8_f16", "f16", 1, 256, 256, 64, 128, 8, 3, 1, relu=True, residual=True, seed=85),
+    BCase("ig_tn256_k3s1_c64_co320_bf16", "bf16", 1, 64, 320, 32, 64, 8, 3, 1, seed=86),
+    BCase("ig_tn256_k3s2_c256_co256_f16", "f16", 2, 256, 256, 32, 64, 8, 3, 2, p_low=0.25, seed=87),
+    BCase("ig_tn256_k3s1_c512_bs4_bf16", "bf16", 1, 512, 512, 32, 64, 4, 3, 1, p_low=0.75, residual=True, seed=88),
 ]
 
 
