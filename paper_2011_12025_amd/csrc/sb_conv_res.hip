@@ -426,19 +426,20 @@ __device__ __forceinline__ void rw_issue(const Geo& g, const ConvArgs& a, const 
     const int lane = lane_id(), pwave = ptid >> 6, i = lane >> 3;
     const int C = a.C_in;
     const int wpr = t.e >> 3;  // windows per row interior
-    const int nwin = (t.rows + 2) * wpr;
-    for (int w = pwave; w < nwin; w += NPW) {
-        const int u = w / wpr, k = w - u * wpr;
+    // a wave takes whole rows (their source is found once per row)
+    for (int u = pwave; u < t.rows + 2; u += NPW) {
         const RowSrc S = row_src<SRC>(g, a, nb, t, u);
         if (S.kind == ROW_ITEMS) continue;
-        const int v0 = 1 + 8 * k;                           // the window's first tile column
-        const int q = (lane & 7) ^ (((v0 + i) >> 1) & 7);   // the sub-chunk this lane's slot holds
-        unsigned char* win = buf + (u * t.pe + v0) * RROW;
-        if (S.kind != ROW_ZERO && q * 8 < C) {
-            const int px = S.kind == ROW_COPY ? 8 * k + i : ((8 * k + i) >> 1);
-            dma16((S.which ? b1 : b0) + S.off + px * C + q * 8, win);
-        } else {
-            lds_zero16(win + lane * 16);
+        for (int k = 0; k < wpr; ++k) {
+            const int v0 = 1 + 8 * k;                           // the window's first tile column
+            const int q = (lane & 7) ^ (((v0 + i) >> 1) & 7);   // the sub-chunk this lane's slot holds
+            unsigned char* win = buf + (u * t.pe + v0) * RROW;
+            if (S.kind != ROW_ZERO && q * 8 < C) {
+                const int px = S.kind == ROW_COPY ? 8 * k + i : ((8 * k + i) >> 1);
+                dma16((S.which ? b1 : b0) + S.off + px * C + q * 8, win);
+            } else {
+                lds_zero16(win + lane * 16);
+            }
         }
     }
     const typename ResAvg<T, SRC>::Plan P = ResAvg<T, SRC>::plan(g, a, nb, t);
