@@ -111,19 +111,6 @@ __device__ __forceinline__ void gdma16(const void* g, unsigned char* window) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr)window, 16, 0, 0);
 }
 
-// Smallest block k whose class-c count through k exceeds s (the block of
-// slot s of class c); hb[k] = high blocks before block k.
-__device__ __forceinline__ int gblock_of(const uint16_t* hb, int B, int c, int s) {
-    int lo = 0, hi = B - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        const int cnt = c ? (int)hb[mid + 1] : (mid + 1 - (int)hb[mid + 1]);
-        if (cnt > s) hi = mid;
-        else lo = mid + 1;
-    }
-    return lo;
-}
-
 // DMA of one step's weight rows: wrow[j] points at this lane's chunk of its
 // weight row, off selects the tap and the 64 channels.
 template <typename T, int AR>
@@ -250,63 +237,31 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* s_stage = smem;
     uint32_t* s_desc = reinterpret_cast<uint32_t*>(smem + GNST * STAGE);
-    int* s_pk = reinterpret_cast<int*>(smem + GNST * STAGE + TM * KT * 4);
-    int* s_pij = s_pk + TM;
-    uint16_t* s_hb = reinterpret_cast<uint16_t*>(smem + GNST * STAGE + TM * KT * 4 + 2 * TM * 4);
+    int* s_pij = reinterpret_cast<int*>(smem + GNST * STAGE + TM * KT * 4);
+    uint16_t* s_hb = reinterpret_cast<uint16_t*>(smem + GNST * STAGE + TM * KT * 4 + TM * 4);
+    // Start-up tables in the third stage, which no DMA touches before the
+    // main loop: the block of each slot of this workgroup's class (uint16),
+    // then for each block of the tile its nine neighbour sources (uint32).
+    unsigned char* s_tmp = s_stage + 2 * STAGE;
     __shared__ int s_wsum[GWAVES];
 
     const int tid = (int)threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS windows are scalar addresses
     const int B = (int)g.B;
-
-    // ---- block plan: s_hb[k] = high blocks before k (k = 0..B)
-    {
-        const int per = (B + GWG - 1) / GWG;
-        const int k0 = tid * per;
-        int c = 0;
-        for (int i = 0; i < per; ++i) {
-            const int k = k0 + i;
-            if (k < B) c += mask[k] != 0;
-        }
-        int x = c;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int y = __shfl_up(x, d, 64);
-            if (lane >= d) x += y;
-        }
-        if (lane == 63) s_wsum[wave] = x;
-        __syncthreads();
-        int run = x - c;
-        for (int w = 0; w < wave; ++w) run += s_wsum[w];
-        for (int i = 0; i < per; ++i) {
-            const int k = k0 + i;
-            if (k < B) {
-                s_hb[k] = (uint16_t)run;
-                run += mask[k] != 0;
-            }
-        }
-        if (tid == GWG - 1) s_hb[B] = (uint16_t)run;
-        __syncthreads();
-    }
-    const int n_high = s_hb[B];
     const int high = (int)blockIdx.x < gp.tiles_h;
-    const int mt = high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h;
-    const int eo = high ? gp.eo_h : gp.eo_l;
-    const int eo2 = eo * eo;
-    const int count = min(high ? n_high : B - n_high, high ? a.hi_cap : a.lo_cap);
-    const int rows_valid = count * eo2;
-    const int m0 = mt * TM;
-    if (gp.splits > 1 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0) gp.rows[blockIdx.x] = rows_valid;
-    if (m0 >= rows_valid) return;  // uniform over the workgroup
     const int co0 = (int)blockIdx.y * TN;
-    const int bs = g.bs, lb = bs >> 1;
-    const int e_in = high ? bs : lb;
     const int C_in = a.C_in, C_out = a.C_out;
     const int cpt = gp.cpt;
     const int nsteps = KT * cpt;
     const int z = (int)blockIdx.z;
     const int s_first = z * nsteps / gp.splits;
     const int n = (z + 1) * nsteps / gp.splits - s_first;  // steps of this workgroup (>= 1)
+    const T* zrow = reinterpret_cast<const T*>(g_zero_row);
+
+    // the mask byte of the thread's first block
+    const int per = (B + GWG - 1) / GWG;
+    const int k0 = tid * per;
+    const uint8_t mv0 = mask[min(k0, B - 1)];  // the thread's first block (in bounds for every thread)
 
     // this lane's DMA rows and chunks: LDS slot (lane & 7) of row r holds global chunk (lane & 7) ^ ((r >> 1) & 7)
     const T* wrow[AR];
@@ -316,6 +271,60 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         const int co = min(co0 + gperm(r), C_out - 1);
         wrow[j] = (const T*)a.weight + (size_t)co * KT * C_in + (((lane & 7) ^ ((r >> 1) & 7)) * 8);
     }
+    const int tap0 = s_first / cpt, c0 = s_first - (s_first / cpt) * cpt;
+    int tap1 = tap0, c1 = c0 + 1;
+    if (c1 == cpt) { c1 = 0; ++tap1; }
+    const int hk0 = k0 < B && mv0 != 0;
+    // The weights of steps 0 and 1 do not depend on the mask: they land while
+    // the plan and the descriptors are built.  (Issued after the mask byte is
+    // in: a wait for it would otherwise wait for them too.)
+    gissue_a<T, AR>(wrow, s_stage, tap0 * C_in + c0 * GKC, wave);
+    if (n > 1) gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
+    else gissue_pad<T, AR>(zrow, s_stage + STAGE, wave, lane);
+
+    // ---- block plan: s_hb[k] = high blocks before k (k = 0..B), and the
+    // block of every slot of this workgroup's class
+    uint16_t* s_inv = reinterpret_cast<uint16_t*>(s_tmp);
+    {
+        int c = hk0;
+        for (int i = 1; i < per; ++i) c += k0 + i < B && mask[k0 + i] != 0;
+        int x = c;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int y = __shfl_up(x, d, 64);
+            if (lane >= d) x += y;
+        }
+        if (lane == 63) s_wsum[wave] = x;
+        gbarrier();
+        int run = x - c;
+        for (int w = 0; w < wave; ++w) run += s_wsum[w];
+        for (int i = 0; i < per; ++i) {
+            const int k = k0 + i;
+            if (k < B) {
+                const bool hk = i == 0 ? hk0 != 0 : mask[k] != 0;
+                s_hb[k] = (uint16_t)run;
+                if (hk == (high != 0)) s_inv[hk ? run : k - run] = (uint16_t)k;
+                run += hk;
+            }
+        }
+        if (tid == GWG - 1) s_hb[B] = (uint16_t)run;
+        gbarrier();
+    }
+    const int n_high = s_hb[B];
+    const int mt = high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h;
+    const int eo = high ? gp.eo_h : gp.eo_l;
+    const int eo2 = eo * eo;
+    const int count = min(high ? n_high : B - n_high, high ? a.hi_cap : a.lo_cap);
+    const int rows_valid = count * eo2;
+    const int m0 = mt * TM;
+    if (gp.splits > 1 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0) gp.rows[blockIdx.x] = rows_valid;
+    if (m0 >= rows_valid) {  // uniform over the workgroup; no DMA may still be writing LDS at exit
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
+    }
+    const int bs = g.bs, lb = bs >> 1;
+    const int e_in = high ? bs : lb;
+
     int prow[BR], pq[BR];
 #pragma unroll
     for (int j = 0; j < BR; ++j) {
@@ -326,75 +335,104 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     // a low tile reads the padded low stack when there is one (uniform)
     const bool lpad = !high && gp.lo_pad != nullptr;
     const T* __restrict__ in_lo = lpad ? (const T*)gp.lo_pad : (const T*)a.in_lo;
-    const T* zrow = reinterpret_cast<const T*>(g_zero_row);
 
-    // the first step's weights are in flight while the descriptors are built
-    int tap0 = s_first / cpt, c0 = s_first - (s_first / cpt) * cpt;
-    gissue_a<T, AR>(wrow, s_stage, tap0 * C_in + c0 * GKC, wave);
-
-    // ---- source descriptors: first the block and position of each tile pixel,
-    // then (pixel, tap) pairs over the whole workgroup
-    if (tid < TM) {
+    // ---- source descriptors.  First, at once: the position of each tile pixel
+    // (one thread each), and the nine neighbour sources of each block of the
+    // tile (kind and slot: own block, neighbour block of either class, or
+    // zero; one (block, direction) per thread beyond the first TM).
+    const int slot0 = m0 / eo2;
+    const int nblk = (min(m0 + TM, rows_valid) - 1) / eo2 - slot0 + 1;  // blocks the tile touches (<= TM + 1)
+    uint32_t* s_nb = reinterpret_cast<uint32_t*>(s_tmp + ((2 * B + 15) & ~15));
+    const int pm = pad_mode(a.flags);
+    if (tid < TM) {  // each tile pixel: its block among the tile's blocks, row, column
         const int m = m0 + tid;
-        int k = -1, ij = 0;
+        int pij = -1;
         if (m < rows_valid) {
             const int slot = m / eo2;
             const int rem = m - slot * eo2;
             const int i = rem / eo;
-            ij = (i << 16) | (rem - i * eo);
-            k = gblock_of(s_hb, B, high, slot);
+            pij = ((slot - slot0) << 22) | (i << 11) | (rem - i * eo);
         }
-        s_pk[tid] = k;
-        s_pij[tid] = ij;
+        s_pij[tid] = pij;
+    } else if (!lpad) {
+        const int per_img = g.GH * g.GW;
+        for (int e = tid - TM; e < nblk * 9; e += GWG - TM) {
+            const int b = e / 9, d = e - (e / 9) * 9;
+            const int dy = d / 3 - 1, dx = d - (d / 3) * 3 - 1;
+            const int slot = slot0 + b;
+            const int k = s_inv[slot];
+            const int nn = k / per_img;
+            const int r = k - nn * per_img;
+            const int gy = r / g.GW, gx = r - (r / g.GW) * g.GW;
+            const int ny = gy + dy, nx = gx + dx;
+            const bool inside = ny >= 0 && ny < g.GH && nx >= 0 && nx < g.GW;
+            const int k2 = inside ? (nn * g.GH + ny) * g.GW + nx : k;  // both reads in bounds, no branch
+            const int before = s_hb[k2];
+            const int h2 = (int)s_hb[k2 + 1] - before;
+            const int s2 = h2 ? before : k2 - before;
+            uint32_t ent = gdesc(GK_ZERO, 0);
+            if (d == 4) ent = gdesc(high ? GK_HI : GK_LO, slot);
+            else if (pm != PM_ZERO && inside && s2 < (h2 ? a.hi_cap : a.lo_cap))  // zero padding: halo stays zero
+                ent = gdesc(h2 ? GK_HI : GK_LO, s2);
+            s_nb[e] = ent;
+        }
     }
-    __syncthreads();
-    const int per_img = g.GH * g.GW;
-    const int pm = pad_mode(a.flags);
-    for (int idx = tid; idx < TM * KT; idx += GWG) {
-        const int p = idx / KT, t = idx - (idx / KT) * KT;
-        const int k = s_pk[p];
+    gbarrier();
+    // Then a descriptor per (tile pixel, tap), spread over the workgroup; a
+    // thread reads the records of all its entries before it uses any.
+    constexpr int NIT = (TM * KT + GWG - 1) / GWG;
+    int pijv[NIT];
+    uint32_t nbv[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int idx = tid + it * GWG;
+        pijv[it] = idx < TM * KT ? s_pij[idx / KT] : -1;
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int idx = tid + it * GWG, t = idx - (idx / KT) * KT;
+        const int pij = pijv[it];
+        const int b = pij >> 22, i = (pij >> 11) & 2047, j = pij & 2047;
+        const int uu = ST * i + t / KS - KS / 2, vv = ST * j + (t - (t / KS) * KS) - KS / 2;
+        const int dy = uu < 0 ? -1 : (uu >= e_in ? 1 : 0);
+        const int dx = vv < 0 ? -1 : (vv >= e_in ? 1 : 0);
+        nbv[it] = (pij >= 0 && !lpad) ? s_nb[b * 9 + (dy + 1) * 3 + dx + 1] : gdesc(GK_ZERO, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int idx = tid + it * GWG;
+        if (idx >= TM * KT) break;
+        const int t = idx - (idx / KT) * KT;
+        const int pij = pijv[it];
         uint32_t ds = gdesc(GK_ZERO, 0);
-        if (k >= 0) {
-            const int i = s_pij[p] >> 16, j = s_pij[p] & 0xFFFF;
-            const int kbefore = s_hb[k];
-            const int slot = high ? kbefore : k - kbefore;
+        if (pij >= 0) {
+            const int b = pij >> 22, i = (pij >> 11) & 2047, j = pij & 2047;
             const int ky = t / KS, kx = t - (t / KS) * KS;
             const int uu = ST * i + ky - KS / 2, vv = ST * j + kx - KS / 2;
-            const int dy = uu < 0 ? -1 : (uu >= e_in ? 1 : 0);
-            const int dx = vv < 0 ? -1 : (vv >= e_in ? 1 : 0);
             if (lpad) {  // a low tile over the padded low stack: every source is a copy
-                ds = gdesc(GK_LO, (slot * (lb + 2) + uu + 1) * (lb + 2) + vv + 1);
-            } else if (dy == 0 && dx == 0) {
-                ds = gdesc(high ? GK_HI : GK_LO, (slot * e_in + uu) * e_in + vv);
-            } else if (pm != PM_ZERO) {  // zero padding leaves the halo at zero
-                const int nn = k / per_img;
-                const int r = k - nn * per_img;
-                const int gy = r / g.GW, gx = r - (r / g.GW) * g.GW;
-                const int ny = gy + dy, nx = gx + dx;
-                if (ny >= 0 && ny < g.GH && nx >= 0 && nx < g.GW) {
-                    const int k2 = (nn * g.GH + ny) * g.GW + nx;
-                    const int before = s_hb[k2];
-                    const int h2 = (int)s_hb[k2 + 1] - before;
-                    const int s2 = h2 ? before : k2 - before;
-                    const int u2 = uu - dy * e_in, v2 = vv - dx * e_in;
-                    if (s2 < (h2 ? a.hi_cap : a.lo_cap)) {
-                        if (h2 == high) ds = gdesc(high ? GK_HI : GK_LO, (s2 * e_in + u2) * e_in + v2);
-                        else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
-                        // a low block beside a high one: strided sampling reads the
-                        // cell's top-left pixel; average sampling never gets here (the
-                        // low stack is then padded beforehand, see igemm_plan)
-                        else ds = gdesc(GK_HI, (s2 * bs + 2 * u2) * bs + 2 * v2);
-                    }
+                ds = gdesc(GK_LO, ((slot0 + b) * (lb + 2) + uu + 1) * (lb + 2) + vv + 1);
+            } else {
+                const int dy = uu < 0 ? -1 : (uu >= e_in ? 1 : 0);
+                const int dx = vv < 0 ? -1 : (vv >= e_in ? 1 : 0);
+                const uint32_t e = nbv[it];
+                const uint32_t kind = e >> 30;
+                const int s2 = (int)(e & 0x3FFFFFFFu);
+                const int u2 = uu - dy * e_in, v2 = vv - dx * e_in;
+                if (kind != GK_ZERO) {
+                    if ((kind == GK_HI) == (high != 0)) ds = gdesc(kind, (s2 * e_in + u2) * e_in + v2);
+                    else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
+                    // a low block beside a high one: strided sampling reads the
+                    // cell's top-left pixel; average sampling never gets here (the
+                    // low stack is then padded beforehand, see igemm_plan)
+                    else ds = gdesc(GK_HI, (s2 * bs + 2 * u2) * bs + 2 * v2);
                 }
             }
         }
         s_desc[idx] = ds;
     }
-    __syncthreads();
+    gbarrier();
 
-    // ---- prologue: step 0 (pixels), step 1 (weights, pixels)
-    int tap1 = tap0, c1 = c0 + 1;
-    if (c1 == cpt) { c1 = 0; ++tap1; }
+    // ---- prologue: pixels of steps 0 and 1 (their weights went out at entry)
     uint32_t dsc[BR];
     GRows<T, BR> r0, rA, rB;  // pixel-row sources of steps 0 / s + 1 / s + 2
     gload_desc<BR>(s_desc, prow, KT, tap0, dsc);
@@ -402,13 +440,10 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     gload_desc<BR>(s_desc, prow, KT, tap1 < KT ? tap1 : tap0, dsc);
     gdecode<T, BR>(dsc, pq, in_hi, in_lo, zrow, C_in, rA);
     gissue_b<T, BR>(r0, c0 * GKC, s_stage + A_BYTES, wave);
-    if (n > 1) {
-        gissue_a<T, AR>(wrow, s_stage + STAGE, tap1 * C_in + c1 * GKC, wave);
-        gissue_b<T, BR>(rA, c1 * GKC, s_stage + STAGE + A_BYTES, wave);
-    } else {
-        gissue_pad<T, AR + BR>(zrow, s_stage + STAGE, wave, lane);
-    }
-    __builtin_amdgcn_s_waitcnt(gvm_wait(AR + BR));
+    if (n > 1) gissue_b<T, BR>(rA, c1 * GKC, s_stage + STAGE + A_BYTES, wave);
+    else gissue_pad<T, BR>(zrow, s_stage + STAGE + A_BYTES, wave, lane);
+    // step 0 has landed once only step 1's pixels can be outstanding
+    __builtin_amdgcn_s_waitcnt(gvm_wait(BR));
     gbarrier();
 
     floatx4 acc[MS][NS];
@@ -562,7 +597,7 @@ inline size_t ground256(size_t b) { return (b + 255) / 256 * 256; }
 
 template <int TM, int TN, int KT>
 constexpr int igemm_smem_fixed() {
-    return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4;
+    return GNST * (TM + TN) * GROWB + TM * KT * 4 + TM * 4;
 }
 
 inline int igemm_hb_bytes(const Geo& g) { return (((int)g.B + 1) * 2 + 15) / 16 * 16; }
@@ -704,7 +739,7 @@ hipError_t igemm_t(const Geo& g, const uint8_t* mask, const ConvArgs& a, int ks,
 
 bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (layout != NHWC || (dtype != 1 && dtype != 2)) return false;
-    if (a.C_in % GKC || a.C_in > GMAXC || a.C_out % 8 || g.B > GMAXB) return false;
+    if (a.C_in % GKC || a.C_in > GMAXC || a.C_out % 8 || g.B > GMAXB || g.bs > 2048) return false;
     // pixel indices of the stacks fit the 30 bits of a descriptor
     const long long lb = g.bs / 2;
     if ((long long)a.hi_cap * g.bs * g.bs >= (1LL << 30) || (long long)a.lo_cap * (lb + 2) * (lb + 2) >= (1LL << 30))
