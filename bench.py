@@ -54,6 +54,9 @@ def parse():
                    help="layer: the headline single layer (one JSON line); sweep: the four ResNet-18 stage shapes "
                         "over low-res fractions; encoder: the N=1 ResNet-18 encoder; encoder-batched: N=4 encoders "
                         "over mask quantiles, image block sizes and fp16/bf16 (one JSON line per point)")
+    p.add_argument("--batch", type=int, default=1,
+                   help="sweep: images per layer (each with its own 8x16 block grid, one exact-fraction mask "
+                        "over all of them)")
     p.add_argument("--profile-run", action="store_true",
                    help="short run for rocprofv3 counters: a 256 MiB copy of known size, then 10 launches of "
                         "--profile-op")
@@ -529,33 +532,34 @@ def bench_sweep(args, torch, np, sb, B, inputs):
     stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
     P = lambda t: ctypes.c_void_p(t.data_ptr())
     it = args.breakdown_iters
+    N = args.batch
     for li, (C, H, W, bs) in enumerate(SWEEP_LAYERS):
         lb, es = bs // 2, 2
         # one workspace per call site, sized for the largest need over the fractions
-        B_ = (H // bs) * (W // bs)
-        ws_layer = sb.layer_workspace_size(torch.float16, B.SB_NHWC, 1, C, H, W, bs, C)
-        ws_bc = max(sb.block_conv3x3_workspace_size(torch.float16, B.SB_NHWC, 1, C, H, W, bs, C, h, B_ - h)
-                    for h in range(B_ + 1))
-        ws_ex = max(sb.block_conv_ex_workspace_size(torch.float16, 1, C, H, W, bs, C, 3, 1, h, B_ - h)
-                    for h in range(B_ + 1))
+        B_ = N * (H // bs) * (W // bs)
+        ws_layer = sb.layer_workspace_size(torch.float16, B.SB_NHWC, N, C, H, W, bs, C)
+        ws_bc = max(sb.block_conv3x3_workspace_size(torch.float16, B.SB_NHWC, N, C, H, W, bs, C, h, B_ - h)
+                    for h in range(0, B_ + 1, N))
+        ws_ex = max(sb.block_conv_ex_workspace_size(torch.float16, N, C, H, W, bs, C, 3, 1, h, B_ - h)
+                    for h in range(0, B_ + 1, N))
         wsl, wsb, wse = [None if n == 0 else torch.empty(n + 256, dtype=torch.uint8, device=dev)
                          for n in (ws_layer, ws_bc, ws_ex)]
 
         def wsp(t):
             return (None, 0) if t is None else (ctypes.c_void_p(t.data_ptr() + (-t.data_ptr()) % 256),
                                                 t.numel() - (-t.data_ptr()) % 256)
-        x0 = inputs.feature_map(0, 1, C, H, W, "f16")
+        x0 = inputs.feature_map(0, N, C, H, W, "f16")
         w = inputs.conv_weight(0, C, C, 3, "f16").to(dev).contiguous(memory_format=cl)
         b = inputs.conv_bias(0, C, 9 * C, "f16").to(dev)
-        map_bytes = C * H * W * es
+        map_bytes = N * C * H * W * es
         R = max(2, -(-2 * MALL_BYTES // (2 * map_bytes)))
         xs = [x0.to(dev).contiguous(memory_format=cl) for _ in range(R)]
         ys = [torch.empty_like(xs[0]) for _ in range(R)]
-        dense_flop = 2.0 * 9 * C * C * H * W
+        dense_flop = 2.0 * 9 * C * C * N * H * W
         miopen_ms = _gpu_ms(torch, lambda i: F.conv2d(xs[i % R], w, b, padding=1), it)
         t_f0 = None
         for f in SWEEP_FRACTIONS:
-            mask_np = inputs.mask_exact_fraction(0, 1, H // bs, W // bs, f)
+            mask_np = inputs.mask_exact_fraction(0, N, H // bs, W // bs, f)
             nh = int(mask_np.sum()); nl = mask_np.size - nh
             mask = torch.from_numpy(mask_np).to(dev)
             his = [torch.empty((nh, C, bs, bs), dtype=torch.float16, device=dev, memory_format=cl) for _ in range(R)]
@@ -566,14 +570,14 @@ def bench_sweep(args, torch, np, sb, B, inputs):
                 sb.split(xs[r], mask, bs, counts=(nh, nl), out=(his[r], los[r]))
 
             def layer(i):
-                rc = lib.segblocks_layer(P(xs[i % R]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs, P(w), P(b), C,
+                rc = lib.segblocks_layer(P(xs[i % R]), B.SB_F16, B.SB_NHWC, N, C, H, W, P(mask), bs, P(w), P(b), C,
                                          0, P(ys[i % R]), *wsp(wsl), stream)
                 if rc:
                     raise RuntimeError(lib.segblocks_last_error().decode())
 
             def bconv(i):
                 r = i % R
-                rc = lib.segblocks_block_conv3x3(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
+                rc = lib.segblocks_block_conv3x3(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, N, C, H, W, P(mask), bs,
                                                  P(w), P(b), C, 0, None, None, P(hos[r]), P(loos[r]), nh, nl,
                                                  *wsp(wsb), stream)
                 if rc:
@@ -581,7 +585,7 @@ def bench_sweep(args, torch, np, sb, B, inputs):
 
             def bconv_ex(i):
                 r = i % R
-                rc = lib.segblocks_block_conv_ex(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, 1, C, H, W, P(mask), bs,
+                rc = lib.segblocks_block_conv_ex(P(his[r]), P(los[r]), B.SB_F16, B.SB_NHWC, N, C, H, W, P(mask), bs,
                                                  P(w), P(b), C, 3, 1, 0, None, None, P(hos[r]), P(loos[r]), nh, nl,
                                                  *wsp(wse), stream)
                 if rc:
@@ -593,7 +597,7 @@ def bench_sweep(args, torch, np, sb, B, inputs):
             if t_f0 is None:
                 t_f0 = t_layer
             block_flop = 2.0 * 9 * C * C * (nh * bs * bs + nl * lb * lb)
-            _emit({"workload": "sweep", "layer": li + 1, "C": C, "H": H, "W": W, "bs": bs, "low_fraction": f,
+            _emit({"workload": "sweep", "N": N, "layer": li + 1, "C": C, "H": H, "W": W, "bs": bs, "low_fraction": f,
                    "n_high": nh, "n_low": nl, "layer_us": round(t_layer * 1e3, 2),
                    "block_conv_us": round(t_bconv * 1e3, 2), "block_conv_ex_us": round(t_ex * 1e3, 2),
                    "miopen_conv2d_us": round(miopen_ms * 1e3, 2),

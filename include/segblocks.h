@@ -183,7 +183,8 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
  * x [N,C_in,H,W] -> y [N,C_out,H,W]; weight/bias as in segblocks_conv3x3.
  * Channels-last fp16/bf16 with C_in <= 64 and blocks of 32 or 64 run as one
  * kernel (the packed stacks never reach memory); channels-last fp16/bf16
- * with C_in % 64 == 0 and 64 < C_in <= 128 or C_in > 256 run as three
+ * with C_in % 64 == 0 and C_in > 64 (for 128 < C_in <= 256 only above
+ * 8192 pixels, N * H * W) run as three
  * (split, the block convolution of segblocks_block_conv3x3, combine) over
  * packed stacks in the workspace; everything else runs as one general
  * kernel.  Intermediate values are rounded to `dtype` exactly where the

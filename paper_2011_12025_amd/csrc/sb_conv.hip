@@ -485,10 +485,13 @@ inline size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 
 bool layer_packed_route(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     // Measured on the stage shapes of a 1024x2048 image (8x16 blocks): at 128
-    // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us;
-    // at 256 the general kernel is faster (40-44 against 46-69 us) and stays.
-    if (!((a.C_in > 64 && a.C_in <= 128) || a.C_in > 256) || layout != NHWC || (dtype != 1 && dtype != 2))
-        return false;
+    // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us.
+    // At 256 channels the general kernel is faster on one 64x128 map (40 / 43
+    // against 43 / 45 us at 0 / 50 % low blocks) and scales with the pixels,
+    // the packed route much less (two maps 77 / 82 against 56 / 57 us, four
+    // 148 / 165 against 103 / 80 us): it takes the layer from 8192 pixels on.
+    if (a.C_in <= 64 || layout != NHWC || (dtype != 1 && dtype != 2)) return false;
+    if (a.C_in > 128 && a.C_in <= 256 && (long long)g.N * g.H * g.W <= 8192) return false;
     Geo gi = g, go = g;
     gi.C = a.C_in;
     go.C = a.C_out;

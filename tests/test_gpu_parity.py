@@ -181,9 +181,12 @@ def test_full_size_layer_stage1_config():
     assert torch.equal(sb.combine(ho, lo_o, md, c.bs, c.H, c.W), y)
 
 
-# Fused layers with 128 or more than 256 input channels run as split, the
-# implicit GEMM's block convolution and combine over library workspace stacks.
+# Fused layers with 128 or more than 256 input channels, and with 129-256
+# above 8192 pixels, run as split, the implicit GEMM's block convolution and
+# combine over library workspace stacks.
 DEEP_CASES = [Case("deep512_f16", "f16", 1, 512, 64, 32, 64, 8, seed=21),
+              Case("c256_n2_packed_route_f16", "f16", 2, 256, 64, 48, 96, 8, p_low=0.5, seed=26),
+              Case("c192_n3_packed_route_bf16", "bf16", 3, 192, 64, 32, 96, 4, p_low=0.3, seed=27),
               Case("c128_layer_f16", "f16", 2, 128, 128, 32, 64, 8, seed=24),
               Case("c128_layer_alllow_bf16", "bf16", 1, 128, 64, 32, 32, 16, mask_kind="low", seed=25),
               Case("deep384_bf16", "bf16", 2, 384, 128, 16, 32, 4, p_low=0.6, seed=22),
