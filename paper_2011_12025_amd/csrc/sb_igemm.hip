@@ -28,9 +28,16 @@
 // distinct banks.
 //
 // Split K: when the tiles alone do not fill the chip, the K steps of a tile
-// are divided among grid.z workgroups that write fp32 partial tiles to a
-// workspace owned by the library; a second kernel sums them in split order
+// are divided among several workgroups that write fp32 partial tiles to the
+// caller's workspace; a second kernel sums them in split order
 // (deterministic) and runs the epilogue.
+//
+// The grid has room for every slot below the stacks' capacities; the class
+// counts are only known in the kernel, so each workgroup numbers the tiles
+// that hold pixels (the high class's, then the low class's) from them and
+// takes its M tile in that order; with room for surplus tiles the tile
+// number is the slowest grid index, so the surplus workgroups are dispatched
+// last and leave after the plan.
 //
 // MFMA: v_mfma_f32_16x16x32_{f16,bf16}, weights as A (16 output channels),
 // pixels as B (16 pixels).  Eight waves (two per SIMD, so that one wave's
@@ -38,6 +45,7 @@
 // 16 x MS pixel and 16 x NS channel fragments.  The weight rows of each 32-channel group
 // are permuted in LDS so that a lane ends with 8 consecutive output channels
 // of one pixel and stores them as one 16-byte write.
+#include <algorithm>
 #include <type_traits>
 
 #include "sb_common.h"
@@ -164,12 +172,15 @@ __device__ __forceinline__ void gissue_pad(const T* zrow, unsigned char* st, int
 }
 
 struct GParams {
-    int tiles_h;    // M tiles of the high class (the low class's follow)
     int eo_h, eo_l; // output extents
     int cpt;        // K steps per tap (C_in / 64)
-    int splits;     // workgroups sharing the K steps of a tile (grid.z)
+    int tiles;      // M tiles of the grid (both classes)
+    int tiles_n;    // output-channel tiles
+    int tile_major; // grid order: 1 = M tile slowest, 0 = M tile fastest
+    int splits;     // workgroups sharing the K steps of a tile
     float* part;    // fp32 partial tiles [tile][n tile][split][TM * TN] when splits > 1
-    int* rows;      // valid output rows of each M tile, written when splits > 1
+    int* rows;      // per M tile, written when splits > 1: valid output rows of its class's stack and its
+                    // tile number in that class (-1 - number for the low class)
     const void* lo_pad;  // the low stack with its 1-pixel halo [lo_cap][lb+2][lb+2][C_in], or nullptr
 };
 
@@ -248,12 +259,27 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     const int tid = (int)threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS windows are scalar addresses
     const int B = (int)g.B;
-    const int high = (int)blockIdx.x < gp.tiles_h;
-    const int co0 = (int)blockIdx.y * TN;
+    // Workgroup lin = (M tile, channel tile, split).  When the stacks have
+    // room for more blocks than the mask can fill, the M tile is the slowest
+    // index, so that the surplus workgroups are dispatched last; otherwise
+    // the fastest, so that the channel tiles and splits of a tile, which
+    // share its pixels, run on one XCD when the tile count is a multiple of 8
+    // (workgroups go to the XCDs round-robin).
+    const int lin = (int)blockIdx.x, per_tile = gp.tiles_n * gp.splits;
+    int tx, rq;
+    if (gp.tile_major) {
+        tx = lin / per_tile;
+        rq = lin - tx * per_tile;
+    } else {
+        rq = lin / gp.tiles;
+        tx = lin - rq * gp.tiles;
+    }
+    const int ny = gp.tile_major ? rq / gp.splits : rq - (rq / gp.tiles_n) * gp.tiles_n;
+    const int co0 = ny * TN;
     const int C_in = a.C_in, C_out = a.C_out;
     const int cpt = gp.cpt;
     const int nsteps = KT * cpt;
-    const int z = (int)blockIdx.z;
+    const int z = gp.tile_major ? rq - ny * gp.splits : rq / gp.tiles_n;
     const int s_first = z * nsteps / gp.splits;
     const int n = (z + 1) * nsteps / gp.splits - s_first;  // steps of this workgroup (>= 1)
     const T* zrow = reinterpret_cast<const T*>(g_zero_row);
@@ -285,6 +311,8 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     // ---- block plan: s_hb[k] = high blocks before k (k = 0..B), and the
     // block of every slot of this workgroup's class
     uint16_t* s_inv = reinterpret_cast<uint16_t*>(s_tmp);
+    int high, mt, nh_eff, nl_eff;
+    bool surplus;
     {
         int c = hk0;
         for (int i = 1; i < per; ++i) c += k0 + i < B && mask[k0 + i] != 0;
@@ -296,8 +324,21 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         }
         if (lane == 63) s_wsum[wave] = x;
         gbarrier();
-        int run = x - c;
-        for (int w = 0; w < wave; ++w) run += s_wsum[w];
+        int run = x - c, nh_all = 0;
+        for (int w = 0; w < GWAVES; ++w) {
+            if (w < wave) run += s_wsum[w];
+            nh_all += s_wsum[w];
+        }
+        // This workgroup's tile, from the class counts: the filled tiles of
+        // the high class come first, then those of the low class, and the
+        // grid's surplus (room for blocks that the mask does not have) last.
+        nh_eff = min(nh_all, a.hi_cap);
+        nl_eff = min(B - nh_all, a.lo_cap);
+        const int real_h = (int)(((long long)nh_eff * gp.eo_h * gp.eo_h + TM - 1) / TM);
+        const int real_l = (int)(((long long)nl_eff * gp.eo_l * gp.eo_l + TM - 1) / TM);
+        high = tx < real_h;
+        mt = high ? tx : tx - real_h;
+        surplus = !high && mt >= real_l;
         for (int i = 0; i < per; ++i) {
             const int k = k0 + i;
             if (k < B) {
@@ -310,14 +351,14 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         if (tid == GWG - 1) s_hb[B] = (uint16_t)run;
         gbarrier();
     }
-    const int n_high = s_hb[B];
-    const int mt = high ? (int)blockIdx.x : (int)blockIdx.x - gp.tiles_h;
     const int eo = high ? gp.eo_h : gp.eo_l;
     const int eo2 = eo * eo;
-    const int count = min(high ? n_high : B - n_high, high ? a.hi_cap : a.lo_cap);
-    const int rows_valid = count * eo2;
+    const int rows_valid = surplus ? 0 : (high ? nh_eff : nl_eff) * eo2;
     const int m0 = mt * TM;
-    if (gp.splits > 1 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0) gp.rows[blockIdx.x] = rows_valid;
+    if (gp.splits > 1 && ny == 0 && z == 0 && tid == 0) {
+        gp.rows[2 * tx] = rows_valid;
+        gp.rows[2 * tx + 1] = high ? mt : -1 - mt;
+    }
     if (m0 >= rows_valid) {  // uniform over the workgroup; no DMA may still be writing LDS at exit
         __builtin_amdgcn_s_waitcnt(0);
         return;
@@ -512,7 +553,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     if (gp.splits == 1) {
         gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0);
     } else {
-        const int tile_lin = (int)blockIdx.x * (int)gridDim.y + (int)blockIdx.y;
+        const int tile_lin = tx * gp.tiles_n + ny;
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -542,9 +583,10 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
     const int ms = r % MS;
     const int wave = r / MS;
     const int tx = tile_lin / tiles_n, ty = tile_lin - tx * tiles_n;
-    const int rows_valid = gp.rows[tx];
-    const int high = tx < gp.tiles_h;
-    const int m0 = (high ? tx : tx - gp.tiles_h) * TM;
+    const int rows_valid = gp.rows[2 * tx];
+    const int code = gp.rows[2 * tx + 1];
+    const int high = code >= 0;
+    const int m0 = (high ? code : -1 - code) * TM;
     const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
     const int m = m0 + wm * MS * 16 + ms * 16 + l16;
     const int co = ty * TN + wn * NS * 16 + jj * 32 + kg * 8;
@@ -627,6 +669,17 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     p.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + p.TM - 1) / p.TM);
     p.tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + p.TM - 1) / p.TM);
     const int tiles = p.tiles_h + p.tiles_l;
+    // The work the cost model sees: the tiles that hold pixels under the
+    // worst mask.  With room for every block in both classes (the fused
+    // layer's packed route) the grid has twice the tiles any mask fills; the
+    // surplus workgroups leave after the plan.
+    auto filled = [&](long long nh) {
+        const long long nl = std::min<long long>(g.B - nh, a.lo_cap);
+        return (nh * eo_h * eo_h + p.TM - 1) / p.TM + (nl * eo_l * eo_l + p.TM - 1) / p.TM;
+    };
+    const long long nh_max = std::min<long long>(a.hi_cap, g.B);
+    const long long nh_min = std::max<long long>(0, g.B - a.lo_cap);
+    const long long work = std::min<long long>(tiles, std::max(filled(nh_max), filled(std::min(nh_min, nh_max))));
     // Tile width and split K by a cost model in units of one 128 x 128 K step
     // (about 1 us): one workgroup per CU at a time (LDS), so a launch costs
     // about rounds x (steps per split x step cost + start-up); a 128 x 256
@@ -642,7 +695,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     for (int tn = tn_max; tn >= 128 || tn == tn_max; tn /= 2) {
         const int tiles_n = (a.C_out + tn - 1) / tn;
         const double w = tn == 256 ? 1.3 : 1.0, wr = tn == 256 ? 2.0 : 1.0;
-        const long long wgs = (long long)tiles * tiles_n;
+        const long long wgs = work * tiles_n;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
             const long long rounds = (wgs * c + cus - 1) / cus;
             const double cost = (double)rounds * ((nsteps + c - 1) / c * w + GSTART_COST) +
@@ -665,7 +718,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     // ResNet-18 stage shapes with 25 % low blocks or 128 channels, within
     // 3 us either way elsewhere.)
     p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG;
-    p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 4)
+    p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 8)
                                 : 0;
     p.pad_bytes = p.pad_low ? ground256((size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * 2) : 0;
     return p;
@@ -684,19 +737,21 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
     gp.eo_h = g.bs / ST;
     gp.eo_l = (g.bs / 2) / ST;
     gp.cpt = a.C_in / GKC;
-    gp.tiles_h = pl.tiles_h;
     const int smem = igemm_smem_fixed<TM, TN, KS * KS>() + igemm_hb_bytes(g);
     hipError_t e = ensure_dyn_lds((const void*)k_igemm<T, KS, ST, WM, MS, NS>, smem);
     if (e != hipSuccess) return e;
     const int tiles_n = pl.tiles_n;
     const int S = pl.splits;
     gp.splits = S;
+    gp.tiles = tiles;
+    gp.tiles_n = tiles_n;
+    gp.tile_major = (long long)a.hi_cap + a.lo_cap > g.B;  // room for surplus tiles
     gp.part = nullptr;
     gp.rows = nullptr;
     gp.lo_pad = nullptr;
     if (S > 1) {
         gp.part = (float*)ws.p;
-        gp.rows = (int*)((char*)ws.p + (size_t)tiles * tiles_n * S * TM * TN * 4);
+        gp.rows = (int*)((char*)ws.p + (size_t)tiles * tiles_n * S * TM * TN * 4);  // 2 ints per tile
     }
     if (pl.pad_low) {
         void* lp = (char*)ws.p + pl.part_bytes;
@@ -707,7 +762,7 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
         if (e != hipSuccess) return e;
         gp.lo_pad = lp;
     }
-    const dim3 grid((unsigned)tiles, (unsigned)tiles_n, (unsigned)S);
+    const dim3 grid((unsigned)((long long)tiles * tiles_n * S));
     hipLaunchKernelGGL((k_igemm<T, KS, ST, WM, MS, NS>), grid, dim3(GWG), smem, st, g, mask, a, gp);
     if (S > 1) {
         e = hipGetLastError();
