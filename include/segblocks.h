@@ -183,11 +183,13 @@ int segblocks_block_conv3x3(const void* hi, const void* lo, int dtype, int layou
  * x [N,C_in,H,W] -> y [N,C_out,H,W]; weight/bias as in segblocks_conv3x3.
  * Channels-last fp16/bf16 with C_in <= 64 and blocks of 32 or 64 run as one
  * kernel (the packed stacks never reach memory); channels-last fp16/bf16
- * with C_in % 64 == 0 and C_in > 64 (for 128 < C_in <= 256 only above
- * 8192 pixels, N * H * W) run as three
- * (split, the block convolution of segblocks_block_conv3x3, combine) over
- * packed stacks in the workspace; everything else runs as one general
- * kernel.  Intermediate values are rounded to `dtype` exactly where the
+ * with C_in % 64 == 0 and C_in > 64 run on the implicit GEMM of
+ * segblocks_block_conv3x3: with average sampling as two kernels (the padded
+ * low stack straight from x into the workspace, then the GEMM reading the
+ * high blocks from x and writing y), with the other samplings as split, the
+ * block convolution and combine over packed stacks in the workspace (for
+ * 128 < C_in <= 256 only above 8192 pixels, N * H * W); everything else runs
+ * as one general kernel.  Intermediate values are rounded to `dtype` exactly where the
  * four-call chain stores them, so the result equals that chain's up to the
  * order of the fp32 accumulation.  flags: SB_FLAG_RELU (after the bias) and
  * the BlockPad alternatives, as for segblocks_block_conv3x3. */

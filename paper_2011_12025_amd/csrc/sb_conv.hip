@@ -474,24 +474,31 @@ hipError_t conv_t(int layout, ConvSrc src, ConvDst dst, const Geo& g, const uint
 
 }  // namespace
 
-// A fused layer (dense map in and out) with many channels runs as split, the
-// GEMM's block convolution (BlockPad fused) and combine over packed stacks
-// in the caller's workspace, with room for every block in either class (the
-// counts are only known on the device).  The values equal the one-kernel
-// layer's up to the order of the fp32 accumulation.
+// A fused layer (dense map in and out) with many channels runs on the GEMM:
+// with average sampling and blocks that tile the map, as the padded low
+// stack (straight from the map) and the GEMM reading the high blocks from
+// the map and writing the dense output; otherwise as split, the GEMM's block
+// convolution (BlockPad fused) and combine over packed stacks in the
+// caller's workspace, with room for every block in either class (the counts
+// are only known on the device).  The values equal the one-kernel layer's up
+// to the order of the fp32 accumulation.
 namespace {
 
 inline size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 
 bool layer_packed_route(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     // Measured on the stage shapes of a 1024x2048 image (8x16 blocks): at 128
-    // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us.
-    // At 256 channels the general kernel is faster on one 64x128 map (40 / 43
-    // against 43 / 45 us at 0 / 50 % low blocks) and scales with the pixels,
-    // the packed route much less (two maps 77 / 82 against 56 / 57 us, four
-    // 148 / 165 against 103 / 80 us): it takes the layer from 8192 pixels on.
+    // channels 44-50 -> 38-43 us (all-low 29 -> 38), at 512 105-116 -> 37-62 us
+    // with split + GEMM + combine; the dense GEMM route (the padded low stack
+    // from the map, high pixels read from it, the output written to it) takes
+    // 8-10 us more off (128 channels 34 / 37 -> 24 / 27 us at 0 / 50 % low,
+    // 512 channels 41 -> 33 us) and beats the general kernel at 256 channels as
+    // well (40 / 43 -> 34 / 35 us on one 64x128 map).  Without the dense route
+    // the general kernel stays faster at 129-256 channels on up to 8192 pixels
+    // (two maps: 77 / 82 against 56 / 57 us with split + GEMM + combine).
     if (a.C_in <= 64 || layout != NHWC || (dtype != 1 && dtype != 2)) return false;
-    if (a.C_in > 128 && a.C_in <= 256 && (long long)g.N * g.H * g.W <= 8192) return false;
+    if (a.C_in > 128 && a.C_in <= 256 && (long long)g.N * g.H * g.W <= 8192 && !igemm_dense_fits(dtype, layout, g, a))
+        return false;
     Geo gi = g, go = g;
     gi.C = a.C_in;
     go.C = a.C_out;
@@ -544,7 +551,7 @@ size_t conv_ws_bytes(int dtype, int layout, ConvSrc src, ConvDst dst, const Geo&
     if (src == SRC_PACKED && dst == DST_PACKED && igemm_fits_shape(dtype, layout, g, a))
         return igemm_ws_bytes(g, a, 3, 1);
     if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a))
-        return packed_layout(g, a).total;
+        return igemm_dense_fits(dtype, layout, g, a) ? igemm_dense_ws_bytes(g, a) : packed_layout(g, a).total;
     return 0;
 }
 
@@ -555,8 +562,13 @@ hipError_t launch_conv(int dtype, int layout, ConvSrc src, ConvDst dst, const Ge
         return launch_igemm(dtype, g, mask, a, 3, 1, ws, st);
     if (src == SRC_DENSE && dst == DST_DENSE && layer_packed_route(dtype, layout, g, a) &&
         reinterpret_cast<uintptr_t>(a.in_hi) % 16 == 0 && reinterpret_cast<uintptr_t>(a.out_hi) % 16 == 0 &&
-        reinterpret_cast<uintptr_t>(a.weight) % 16 == 0)
+        reinterpret_cast<uintptr_t>(a.weight) % 16 == 0) {
+        if (igemm_dense_fits(dtype, layout, g, a)) {
+            if (ws.bytes < igemm_dense_ws_bytes(g, a)) return hipErrorInvalidValue;
+            return launch_igemm_dense(dtype, g, mask, a, ws, st);
+        }
         return layer_via_packed(dtype, g, mask, a, ws, st);
+    }
     switch (dtype) {
     case 0: return conv_t<float>(layout, src, dst, g, mask, a, st);
     case 1: return conv_t<f16>(layout, src, dst, g, mask, a, st);

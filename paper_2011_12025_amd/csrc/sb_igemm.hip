@@ -182,13 +182,40 @@ struct GParams {
     int* rows;      // per M tile, written when splits > 1: valid output rows of its class's stack and its
                     // tile number in that class (-1 - number for the low class)
     const void* lo_pad;  // the low stack with its 1-pixel halo [lo_cap][lb+2][lb+2][C_in], or nullptr
+    // Dense mode (a whole layer): the high blocks' pixels come from the dense
+    // map a.in_hi [N][H][W][C_in] (the low neighbours' from lo_pad, which the
+    // low tiles read too), and the results go to the dense map a.out_hi
+    // [N][H][W][C_out], a low pixel to its 2 x 2 cell (BlockCombine).
+    int dense;
+    int W;          // dense mode: width of the map
+    int* dout;      // per M tile, TM dense output pixels (-1: none), written when splits > 1
 };
+
+// The store of 8 finished channels of one output pixel: row m of the class's
+// output stack, or (dense mode, dpix >= 0) pixel dpix of the dense output
+// map, a low pixel to its 2 x 2 cell (map width W).
+template <typename T>
+__device__ __forceinline__ void gstore8(T* out, int m, int dpix, int W, int high, int C_out, int co,
+                                        const uint4& v) {
+    if (dpix < 0) {
+        *reinterpret_cast<uint4*>(out + (size_t)m * C_out + co) = v;
+        return;
+    }
+    T* q = out + (size_t)dpix * C_out + co;
+    *reinterpret_cast<uint4*>(q) = v;
+    if (!high) {
+        *reinterpret_cast<uint4*>(q + C_out) = v;
+        *reinterpret_cast<uint4*>(q + (size_t)W * C_out) = v;
+        *reinterpret_cast<uint4*>(q + (size_t)(W + 1) * C_out) = v;
+    }
+}
 
 // Bias, residual, ReLU and the store of a finished tile: lane holds channels
 // co0 + wn*NS*16 + jj*32 + kg*8 + 0..7 of pixel row m0 + wm*MS*16 + ms*16 + l16.
+// dout: dense mode, the dense output pixel of each tile pixel (else nullptr).
 template <typename T, int WM, int MS, int NS>
 __device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const ConvArgs& a, int high, int m0,
-                                          int rows_valid, int co0) {
+                                          int rows_valid, int co0, const int* dout, int W) {
     const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
     const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
     const int C_out = a.C_out;
@@ -223,7 +250,7 @@ __device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const Co
             Vec<T, 8> o;
 #pragma unroll
             for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
-            *reinterpret_cast<uint4*>(out + off) = o.raw;
+            gstore8<T>(out, m, dout ? dout[m - m0] : -1, W, high, C_out, co, o.raw);
         }
     }
 }
@@ -249,7 +276,8 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     unsigned char* s_stage = smem;
     uint32_t* s_desc = reinterpret_cast<uint32_t*>(smem + GNST * STAGE);
     int* s_pij = reinterpret_cast<int*>(smem + GNST * STAGE + TM * KT * 4);
-    uint16_t* s_hb = reinterpret_cast<uint16_t*>(smem + GNST * STAGE + TM * KT * 4 + TM * 4);
+    int* s_dout = s_pij + TM;  // dense mode: output pixel of each tile pixel
+    uint16_t* s_hb = reinterpret_cast<uint16_t*>(smem + GNST * STAGE + TM * KT * 4 + 2 * TM * 4);
     // Start-up tables in the third stage, which no DMA touches before the
     // main loop: the block of each slot of this workgroup's class (uint16),
     // then for each block of the tile its nine neighbour sources (uint32).
@@ -373,9 +401,11 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         pq[j] = ((lane & 7) ^ ((prow[j] >> 1) & 7)) * 8;
     }
     const T* __restrict__ in_hi = (const T*)a.in_hi;
-    // a low tile reads the padded low stack when there is one (uniform)
+    // a low tile reads the padded low stack when there is one (uniform); in
+    // dense mode the high tiles' low neighbours come from it too
     const bool lpad = !high && gp.lo_pad != nullptr;
-    const T* __restrict__ in_lo = lpad ? (const T*)gp.lo_pad : (const T*)a.in_lo;
+    const bool dense = gp.dense != 0;
+    const T* __restrict__ in_lo = (lpad || dense) ? (const T*)gp.lo_pad : (const T*)a.in_lo;
 
     // ---- source descriptors.  First, at once: the position of each tile pixel
     // (one thread each), and the nine neighbour sources of each block of the
@@ -384,6 +414,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     const int slot0 = m0 / eo2;
     const int nblk = (min(m0 + TM, rows_valid) - 1) / eo2 - slot0 + 1;  // blocks the tile touches (<= TM + 1)
     uint32_t* s_nb = reinterpret_cast<uint32_t*>(s_tmp + ((2 * B + 15) & ~15));
+    int* s_nbase = reinterpret_cast<int*>(s_nb + nblk * 9);  // dense mode: top-left pixel of each block of the tile
     const int pm = pad_mode(a.flags);
     if (tid < TM) {  // each tile pixel: its block among the tile's blocks, row, column
         const int m = m0 + tid;
@@ -395,7 +426,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
             pij = ((slot - slot0) << 22) | (i << 11) | (rem - i * eo);
         }
         s_pij[tid] = pij;
-    } else if (!lpad) {
+    } else if (!lpad || dense) {
         const int per_img = g.GH * g.GW;
         for (int e = tid - TM; e < nblk * 9; e += GWG - TM) {
             const int b = e / 9, d = e - (e / 9) * 9;
@@ -412,6 +443,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
             const int h2 = (int)s_hb[k2 + 1] - before;
             const int s2 = h2 ? before : k2 - before;
             uint32_t ent = gdesc(GK_ZERO, 0);
+            if (d == 4 && dense) s_nbase[b] = (nn * g.H + gy * bs) * g.W + gx * bs;
             if (d == 4) ent = gdesc(high ? GK_HI : GK_LO, slot);
             else if (pm != PM_ZERO && inside && s2 < (h2 ? a.hi_cap : a.lo_cap))  // zero padding: halo stays zero
                 ent = gdesc(h2 ? GK_HI : GK_LO, s2);
@@ -459,7 +491,10 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                 const uint32_t kind = e >> 30;
                 const int s2 = (int)(e & 0x3FFFFFFFu);
                 const int u2 = uu - dy * e_in, v2 = vv - dx * e_in;
-                if (kind != GK_ZERO) {
+                if (kind != GK_ZERO && dense) {  // a high tile: dense pixels, or a low neighbour's padded pixel
+                    if (kind == GK_HI) ds = gdesc(GK_HI, s_nbase[b] + uu * g.W + vv);
+                    else ds = gdesc(GK_LO, (s2 * (lb + 2) + (u2 >> 1) + 1) * (lb + 2) + (v2 >> 1) + 1);
+                } else if (kind != GK_ZERO) {
                     if ((kind == GK_HI) == (high != 0)) ds = gdesc(kind, (s2 * e_in + u2) * e_in + v2);
                     else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
                     // a low block beside a high one: strided sampling reads the
@@ -470,6 +505,16 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
             }
         }
         s_desc[idx] = ds;
+    }
+    if (dense && tid < TM) {  // the dense output pixel of each tile pixel (a low one: its cell's top left)
+        const int pij = s_pij[tid];
+        int o = -1;
+        if (pij >= 0) {
+            const int b = pij >> 22, i = (pij >> 11) & 2047, j = pij & 2047;
+            o = s_nbase[b] + (high ? i * g.W + j : 2 * i * g.W + 2 * j);
+        }
+        s_dout[tid] = o;
+        if (gp.splits > 1 && ny == 0 && z == 0) gp.dout[tx * TM + tid] = o;
     }
     gbarrier();
 
@@ -551,7 +596,7 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     __builtin_amdgcn_s_waitcnt(0);  // the padding DMAs
 
     if (gp.splits == 1) {
-        gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0);
+        gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0, dense ? s_dout : nullptr, g.W);
     } else {
         const int tile_lin = tx * gp.tiles_n + ny;
 #pragma unroll
@@ -621,7 +666,7 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
     Vec<T, 8> o;
 #pragma unroll
     for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
-    *reinterpret_cast<uint4*>(out + off) = o.raw;
+    gstore8<T>(out, m, gp.dense ? gp.dout[tx * TM + (m - m0)] : -1, gp.W, high, a.C_out, co, o.raw);
 }
 
 }  // namespace
@@ -639,7 +684,7 @@ inline size_t ground256(size_t b) { return (b + 255) / 256 * 256; }
 
 template <int TM, int TN, int KT>
 constexpr int igemm_smem_fixed() {
-    return GNST * (TM + TN) * GROWB + TM * KT * 4 + TM * 4;
+    return GNST * (TM + TN) * GROWB + TM * KT * 4 + 2 * TM * 4;
 }
 
 inline int igemm_hb_bytes(const Geo& g) { return (((int)g.B + 1) * 2 + 15) / 16 * 16; }
@@ -662,7 +707,7 @@ struct IgPlan {
     size_t part_bytes, pad_bytes;
 };
 
-IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
+IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dense = false) {
     IgPlan p;
     p.TM = 128;
     const int eo_h = g.bs / stride, eo_l = (g.bs / 2) / stride;
@@ -717,17 +762,20 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride) {
     // copy.  (Averaging in the K loop instead measured 6-12 us slower at the
     // ResNet-18 stage shapes with 25 % low blocks or 128 channels, within
     // 3 us either way elsewhere.)
-    p.pad_low = ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG;
-    p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 8)
+    // In dense mode the padded low stack comes straight from the dense map and
+    // the high tiles read their low neighbours from it as well.
+    p.pad_low = dense || (ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG);
+    p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 8 +
+                                            (dense ? (size_t)tiles * p.TM * 4 : 0))
                                 : 0;
     p.pad_bytes = p.pad_low ? ground256((size_t)a.lo_cap * (g.bs / 2 + 2) * (g.bs / 2 + 2) * a.C_in * 2) : 0;
     return p;
 }
 
 template <typename T, int KS, int ST, int WM, int MS, int NS>
-hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
+hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st, bool dense) {
     constexpr int TM = WM * MS * 16, TN = (GWAVES / WM) * NS * 16;
-    const IgPlan pl = igemm_plan(g, a, KS, ST);
+    const IgPlan pl = igemm_plan(g, a, KS, ST, dense);
     if (pl.TM != TM || pl.TN != TN) return hipErrorInvalidValue;
     const int tiles = pl.tiles_h + pl.tiles_l;
     if (tiles == 0) return hipSuccess;
@@ -749,16 +797,21 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
     gp.part = nullptr;
     gp.rows = nullptr;
     gp.lo_pad = nullptr;
+    gp.dense = dense ? 1 : 0;
+    gp.W = g.W;
+    gp.dout = nullptr;
     if (S > 1) {
         gp.part = (float*)ws.p;
         gp.rows = (int*)((char*)ws.p + (size_t)tiles * tiles_n * S * TM * TN * 4);  // 2 ints per tile
+        gp.dout = gp.rows + 2 * tiles;                                              // dense mode: TM per tile
     }
     if (pl.pad_low) {
         void* lp = (char*)ws.p + pl.part_bytes;
         Geo pg = g;
         pg.C = a.C_in;
-        e = launch_pad_rows(std::is_same<T, f16>::value ? 1 : 2, pg, a.in_hi, a.in_lo, mask, nullptr, lp, a.hi_cap,
-                            a.lo_cap, PM_AVG, st);
+        const int dt = std::is_same<T, f16>::value ? 1 : 2;
+        e = dense ? launch_pad_low_dense(dt, pg, a.in_hi, mask, lp, a.lo_cap, st)
+                  : launch_pad_rows(dt, pg, a.in_hi, a.in_lo, mask, nullptr, lp, a.hi_cap, a.lo_cap, PM_AVG, st);
         if (e != hipSuccess) return e;
         gp.lo_pad = lp;
     }
@@ -775,11 +828,12 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
 }
 
 template <typename T, int KS, int ST>
-hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
-    const int tn = igemm_plan(g, a, KS, ST).TN;
-    if (tn == 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st);
-    if (tn == 256) return igemm_run<T, KS, ST, 2, 4, 4>(g, mask, a, ws, st);
-    return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, ws, st);
+hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st,
+                      bool dense = false) {
+    const int tn = igemm_plan(g, a, KS, ST, dense).TN;
+    if (tn == 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st, dense);
+    if (tn == 256) return igemm_run<T, KS, ST, 2, 4, 4>(g, mask, a, ws, st, dense);
+    return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, ws, st, dense);
 }
 
 template <typename T>
@@ -819,6 +873,33 @@ hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const Conv
                         hipStream_t st) {
     if (dtype == 1) return igemm_t<f16>(g, mask, a, ksize, stride, ws, st);
     return igemm_t<bf16>(g, mask, a, ksize, stride, ws, st);
+}
+
+bool igemm_dense_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
+    // the dense pixel indices fit a descriptor; blocks tile the map exactly;
+    // average sampling (the padded low stack is then the dense map's 2x2 averages)
+    if (g.H % g.bs || g.W % g.bs || (long long)g.N * g.H * g.W >= (1LL << 30) || pad_mode(a.flags) != PM_AVG)
+        return false;
+    ConvArgs p = a;
+    p.hi_cap = p.lo_cap = (int)g.B;
+    return igemm_fits_shape(dtype, layout, g, p);
+}
+
+size_t igemm_dense_ws_bytes(const Geo& g, const ConvArgs& a) {
+    ConvArgs p = a;
+    p.hi_cap = p.lo_cap = (int)g.B;
+    const IgPlan pl = igemm_plan(g, p, 3, 1, true);
+    return pl.part_bytes + pl.pad_bytes;
+}
+
+hipError_t launch_igemm_dense(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st) {
+    ConvArgs p = a;
+    p.in_lo = nullptr;
+    p.out_lo = a.out_hi;  // one dense output map for both classes
+    p.res_hi = p.res_lo = nullptr;
+    p.hi_cap = p.lo_cap = (int)g.B;
+    if (dtype == 1) return igemm_tile<f16, 3, 1>(g, mask, p, ws, st, true);
+    return igemm_tile<bf16, 3, 1>(g, mask, p, ws, st, true);
 }
 
 }  // namespace sb

@@ -71,6 +71,10 @@ hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* 
                            void* lp, int hi_cap, int lo_cap, int pm, hipStream_t st);
 hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask,
                                int hi_cap, int lo_cap, void* y, hipStream_t st, bool bwd = false);
+// The padded low stack (1-pixel halo, average sampling) straight from the
+// dense map, for fp16 / bf16 maps whose sides are multiples of the block size.
+hipError_t launch_pad_low_dense(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* lp, int lo_cap,
+                                hipStream_t st);
 
 // Encoder kernels (channels-last fp16/bf16): block convolution K x K
 // (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
@@ -85,6 +89,13 @@ hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const Conv
                         Ws ws, hipStream_t st);
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         hipStream_t st);
+// A whole 3x3 layer on the implicit GEMM (dense map a.in_hi in, dense map
+// a.out_hi out, average sampling): the padded low stack straight from the
+// map, then the GEMM with the high blocks' pixels read from the map and the
+// results written to the map (BlockCombine fused).
+bool igemm_dense_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
+size_t igemm_dense_ws_bytes(const Geo& g, const ConvArgs& a);
+hipError_t launch_igemm_dense(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st);
 int conv2d_lds_bytes(int dtype, int C_in, int K, int S);
 int stem_lds_bytes(int K, int S);
 hipError_t launch_conv2d(int dtype, const void* x, int N, int C_in, int H, int W, const void* w, const void* bias,

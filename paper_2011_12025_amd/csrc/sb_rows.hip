@@ -192,6 +192,75 @@ __global__ __launch_bounds__(WG) void k_split_rows(const T* __restrict__ x, int 
 }
 
 // ---------------------------------------------------------------------------
+// low blocks of a dense map, sampled and padded in one pass: x -> lp
+// ---------------------------------------------------------------------------
+// Row u of the padded tile of low block (n, gy, gx) is the 2x2 average of
+// the image cells at twice its coordinates, zero outside the image: that is
+// BlockSample of the block and of its neighbours, and so, with average
+// sampling, BlockPad of the low stack (a high neighbour's halo cell is the
+// same average).  Maps whose sides are multiples of the block size (cells
+// never straddle the border).  A job is (block, padded row); the jobs of
+// high blocks end at the plan, before any load.
+template <typename T, bool ONE>
+__global__ __launch_bounds__(WG) void k_pad_low_dense(const T* __restrict__ x, int C, int H, int W,
+                                                      const uint8_t* __restrict__ mask, int bs, int B, int GH, int GW,
+                                                      T* __restrict__ lp, int lo_cap) {
+    constexpr int V = 16 / (int)sizeof(T);
+    const int lane = lane_id();
+    const int CV = C / V, lb = bs >> 1, pe = lb + 2, cells = pe * CV;
+    const int njobs = B * pe;
+    const int nw = (int)gridDim.x * RW_WAVES;
+    ROWS_PLAN_PREAMBLE();
+    int job = (int)blockIdx.x * RW_WAVES + wave_id();
+    if (job >= njobs) return;
+    RPlan<ONE> wm;
+    wm.init(mask, B, s_mask, &s_pt);
+    for (; job < njobs; job += nw) {
+        const int k = job / pe, u = job - k * pe;
+        if (wm.high(k)) continue;
+        const int s = wm.slot(k, false);
+        if (s >= lo_cap) continue;
+        int n, gy, gx;
+        coords(k, GH, GW, n, gy, gx);
+        const int Y = gy * bs + 2 * (u - 1);
+        const bool yin = Y >= 0 && Y + 1 < H;
+        const T* r0 = x + ((size_t)n * H + (yin ? Y : 0)) * W * C;
+        const T* r1 = r0 + (size_t)W * C;
+        T* d = lp + ((size_t)(s * pe + u) * pe) * C;
+        for (int cb = 0; cb < cells; cb += 64 * MAXM) {
+            uint4 v[MAXM][4];
+            bool in[MAXM];
+#pragma unroll
+            for (int m = 0; m < MAXM; ++m) {
+                const int cell = cb + lane + 64 * m;
+                in[m] = false;
+                if (cell < cells) {
+                    const int j = cell / CV, c = (cell - j * CV) * V;
+                    const int X = gx * bs + 2 * (j - 1);
+                    if (yin && X >= 0 && X + 1 < W) {
+                        const int o = X * C + c;
+                        in[m] = true;
+                        v[m][0] = ld_nt16(r0 + o);
+                        v[m][1] = ld_nt16(r0 + o + C);
+                        v[m][2] = ld_nt16(r1 + o);
+                        v[m][3] = ld_nt16(r1 + o + C);
+                    }
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < MAXM; ++m) {
+                const int cell = cb + lane + 64 * m;
+                if (cell < cells) {
+                    const int j = cell / CV, c = (cell - j * CV) * V;
+                    st_nt16(d + j * C + c, in[m] ? avg_raw<T>(v[m][0], v[m][1], v[m][2], v[m][3])
+                                                 : uint4{0u, 0u, 0u, 0u});
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // combine: hi, lo -> y (blocks past a stack's capacity are written as zeros)
 // ---------------------------------------------------------------------------
 // BWD: the transpose of BlockSample instead (a low value is spread as quarters)
@@ -447,6 +516,14 @@ hipError_t combine_rows(const Geo& g, const void* hi, const void* lo, const uint
 }
 
 template <typename T, bool ONE>
+hipError_t pad_low_dense(const Geo& g, const void* x, const uint8_t* mask, void* lp, int lo_cap, hipStream_t st) {
+    const long long jobs = g.B * (g.bs / 2 + 2);
+    hipLaunchKernelGGL((k_pad_low_dense<T, ONE>), dim3(rows_grid(jobs)), dim3(WG), 0, st, (const T*)x, g.C, g.H, g.W,
+                       mask, g.bs, (int)g.B, g.GH, g.GW, (T*)lp, lo_cap);
+    return hipGetLastError();
+}
+
+template <typename T, bool ONE>
 hipError_t pad_rows(const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp, void* lp,
                     int hi_cap, int lo_cap, int pm, hipStream_t st) {
     const long long jobs = g.B * (g.bs / 2 + 2) + (hp ? (long long)hi_cap * (g.bs - g.bs / 2) : 0LL);
@@ -512,6 +589,15 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
     case 1: return combine_rows_t<f16>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
     default: return combine_rows_t<bf16>(g, hi, lo, mask, hi_cap, lo_cap, y, bwd, st);
     }
+}
+
+hipError_t launch_pad_low_dense(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* lp, int lo_cap,
+                                hipStream_t st) {
+    const bool one = g.B <= 1024;
+    if (dtype == 1) return one ? pad_low_dense<f16, true>(g, x, mask, lp, lo_cap, st)
+                               : pad_low_dense<f16, false>(g, x, mask, lp, lo_cap, st);
+    return one ? pad_low_dense<bf16, true>(g, x, mask, lp, lo_cap, st)
+               : pad_low_dense<bf16, false>(g, x, mask, lp, lo_cap, st);
 }
 
 hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* lo, const uint8_t* mask, void* hp,
