@@ -13,15 +13,16 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Pointers are DEVICE pointers unless stated otherwise.  The caller owns
- *    every buffer; the library allocates no device memory.  Three calls may
+ *    every buffer; the library allocates no device memory.  Four calls may
  *    need scratch memory beyond their inputs and outputs (fp32 partial tiles
  *    of a reduction split over several workgroups, a padded copy of the low
  *    stack, the packed stacks of a fused layer with many channels):
- *    segblocks_block_conv3x3, segblocks_block_conv_ex and segblocks_layer
- *    take it as a `workspace` pointer with its size `ws_bytes`.  The size a
+ *    segblocks_block_conv3x3, segblocks_block_conv_ex,
+ *    segblocks_block_conv_chain and segblocks_layer take it as a `workspace` pointer with its size `ws_bytes`.  The size a
  *    call needs depends only on its shapes, capacities and device, and is
  *    given by segblocks_block_conv3x3_workspace_size,
- *    segblocks_block_conv_ex_workspace_size and
+ *    segblocks_block_conv_ex_workspace_size,
+ *    segblocks_block_conv_chain_workspace_size and
  *    segblocks_layer_workspace_size (0 = none needed; NULL is then fine).  A
  *    workspace must be 256-byte aligned and must not overlap any argument;
  *    a smaller one (or NULL when one is needed) fails with SB_ENOMEM before
@@ -241,8 +242,48 @@ int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, i
                                     void* hi_out, void* lo_out, int hi_cap, int lo_cap,
                                     hipStream_t stream);
 
+/* A block convolution for chains of them (paper: Method > Block modules >
+ * BlockPad -- with average sampling a low block's halo cell facing a high
+ * neighbour is the 2x2 average of that neighbour's cell, i.e. a pixel of the
+ * high block at half resolution).  The arguments and results of
+ * segblocks_block_conv_ex (3x3 at stride 1 takes the routes of
+ * segblocks_block_conv3x3), plus:
+ *   hi_half [nh, C_in, bs/2, bs/2] (input, or NULL): the high input blocks at
+ *     half resolution, hi_half[s,c,u,v] = the 2x2 average of
+ *     hi[s,c,2u..2u+1,2v..2v+1] rounded to dtype, as hi_out_half of the call
+ *     that wrote `hi` gives it.  With average sampling the implicit GEMM then
+ *     takes those halo cells from it instead of padding the low stack in a
+ *     launch of its own; the other routes ignore it.  The result is the same
+ *     bit for bit either way; a hi_half that is not those averages gives
+ *     wrong results.
+ *   hi_out_half [nh, C_out, bo/2, bo/2] (output, or NULL; bo = bs/stride must
+ *     be even and C_out % 8 == 0): receives hi_out at half resolution, from
+ *     the GEMM's epilogue where its tile layout allows, else from one extra
+ *     launch after the convolution.
+ * hi_half and hi_out_half are 16-byte aligned (with hi_out_half, hi_out as
+ * well); they hold hi_cap blocks (slots past the mask's high count are
+ * written with don't-care values).  Workspace:
+ * segblocks_block_conv_chain_workspace_size (enough with or without
+ * hi_half). */
+int segblocks_block_conv_chain(const void* hi, const void* lo, const void* hi_half, int dtype,
+                               int layout, int N, int C_in, int H, int W, const uint8_t* mask,
+                               int bs, const void* weight, const void* bias, int C_out,
+                               int ksize, int stride, int flags,
+                               const void* residual_hi, const void* residual_lo,
+                               void* hi_out, void* lo_out, void* hi_out_half, int hi_cap,
+                               int lo_cap, void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Whether segblocks_block_conv_chain with these shapes, flags and
+ * capacities (16-byte aligned buffers) reads hi_half, so that the call
+ * producing its input knows whether to ask for hi_out_half: *reads (HOST
+ * pointer) = 1 or 0.  Pure host function; arguments are validated as in
+ * the workspace queries. */
+int segblocks_block_conv_chain_reads_half(int dtype, int layout, int N, int C_in, int H, int W,
+                                          int bs, int C_out, int ksize, int stride, int flags,
+                                          int hi_cap, int lo_cap, int* reads);
+
 /* Workspace sizes (bytes, HOST out-parameter) of segblocks_block_conv3x3,
- * segblocks_block_conv_ex and segblocks_layer for the given shapes and
+ * segblocks_block_conv_ex, segblocks_block_conv_chain and segblocks_layer for the given shapes and
  * stack capacities on the current device; the arguments mean what they mean
  * in those calls and are validated the same way.  The size covers every
  * flag combination (a call checks only what its own route needs) and assumes
@@ -253,6 +294,9 @@ int segblocks_block_conv3x3_workspace_size(int dtype, int layout, int N, int C_i
 int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
                                            int bs, int C_out, int ksize, int stride,
                                            int hi_cap, int lo_cap, size_t* bytes);
+int segblocks_block_conv_chain_workspace_size(int dtype, int layout, int N, int C_in, int H, int W,
+                                              int bs, int C_out, int ksize, int stride,
+                                              int hi_cap, int lo_cap, size_t* bytes);
 int segblocks_layer_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
                                    int C_out, size_t* bytes);
 

@@ -22,7 +22,7 @@ __all__ = ["count", "split", "pad", "conv3x3", "combine", "block_conv3x3", "bloc
            "maxpool", "layout_of", "block_conv3x3_workspace_size", "block_conv_ex_workspace_size",
            "layer_workspace_size", "policy_heuristic", "combine_backward", "split_backward", "pad_backward",
            "conv3x3_backward_data", "conv3x3_backward_weight", "layer_backward", "pad_halo", "conv_halo",
-           "maxpool_halo"]
+           "maxpool_halo", "block_conv_chain", "block_conv_chain_workspace_size", "block_conv_chain_reads_half"]
 
 _DT = {torch.float32: _b.SB_F32, torch.float16: _b.SB_F16, torch.bfloat16: _b.SB_BF16}
 
@@ -113,6 +113,13 @@ def block_conv_ex_workspace_size(dtype: torch.dtype, N: int, C_in: int, H: int, 
                                  k: int, stride: int, hi_cap: int, lo_cap: int) -> int:
     """Bytes of workspace that block_conv_ex needs for these shapes (0 = none)."""
     return _query("segblocks_block_conv_ex_workspace_size", _DT[dtype], _b.SB_NHWC, N, C_in, H, W, bs, C_out, k,
+                  stride, hi_cap, lo_cap)
+
+
+def block_conv_chain_workspace_size(dtype: torch.dtype, N: int, C_in: int, H: int, W: int, bs: int, C_out: int,
+                                    k: int, stride: int, hi_cap: int, lo_cap: int) -> int:
+    """Bytes of workspace that block_conv_chain needs for these shapes (0 = none)."""
+    return _query("segblocks_block_conv_chain_workspace_size", _DT[dtype], _b.SB_NHWC, N, C_in, H, W, bs, C_out, k,
                   stride, hi_cap, lo_cap)
 
 
@@ -297,6 +304,50 @@ def block_conv_ex(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: in
             _ptr(weight), _ptr(bias), C_out, k, stride, _flags(relu, sampling), _ptr(rh), _ptr(rl),
             _ptr(ho), _ptr(lo_o), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
     return ho, lo_o
+
+
+def block_conv_chain_reads_half(dtype: torch.dtype, N: int, C_in: int, H: int, W: int, bs: int, C_out: int, k: int,
+                                stride: int, hi_cap: int, lo_cap: int, sampling: str = "avg") -> bool:
+    """Whether block_conv_chain with these shapes reads ``hi_half`` (so that
+    the call producing its input knows whether to ask for it)."""
+    r = ctypes.c_int(0)
+    _b.call("segblocks_block_conv_chain_reads_half", _DT[dtype], _b.SB_NHWC, N, C_in, H, W, bs, C_out, k, stride,
+            _flags(False, sampling), hi_cap, lo_cap, ctypes.byref(r))
+    return bool(r.value)
+
+
+def block_conv_chain(hi: torch.Tensor, lo: torch.Tensor, mask: torch.Tensor, bs: int, H: int, W: int,
+                     weight: torch.Tensor, bias=None, stride: int = 1, relu: bool = False, residual=None,
+                     hi_half=None, want_half: bool = False, out=None, workspace=None, sampling: str = "avg"):
+    """block_conv_ex for chains of block convolutions: ``hi_half`` (or None)
+    is ``hi`` at half resolution (each block's 2x2 averages, as a previous
+    call's third result), from which the implicit GEMM takes a low block's
+    halo cells beside a high neighbour instead of padding the low stack in a
+    launch of its own; with ``want_half`` the call also returns the high
+    output at half resolution.  3x3 at stride 1 takes the routes of
+    block_conv3x3.  Returns (hi_out, lo_out, hi_out_half or None)."""
+    mask = _mask(mask)
+    ref = hi if hi.shape[0] else lo
+    layout = _b.SB_NHWC
+    _check_layout(layout, hi, lo)
+    k = weight.shape[2]
+    C_in, C_out, N = ref.shape[1], weight.shape[0], mask.shape[0]
+    weight = _weight(weight, layout, k)
+    bias = None if bias is None else bias.contiguous()
+    bo, lo_e = bs // stride, bs // 2 // stride
+    if out is None:
+        ho = _empty((hi.shape[0], C_out, bo, bo), ref, layout)
+        lo_o = _empty((lo.shape[0], C_out, lo_e, lo_e), ref, layout)
+        hh = _empty((hi.shape[0], C_out, bo // 2, bo // 2), ref, layout) if want_half else None
+    else:
+        ho, lo_o, hh = out
+    rh, rl = (None, None) if residual is None else residual
+    need = block_conv_chain_workspace_size(ref.dtype, N, C_in, H, W, bs, C_out, k, stride, hi.shape[0], lo.shape[0])
+    wp, wn, _keep = _ws(need, ref.device, workspace)
+    _b.call("segblocks_block_conv_chain", _ptr(hi), _ptr(lo), _ptr(hi_half), _dt(ref), layout, N, C_in, H, W,
+            _ptr(mask), bs, _ptr(weight), _ptr(bias), C_out, k, stride, _flags(relu, sampling), _ptr(rh), _ptr(rl),
+            _ptr(ho), _ptr(lo_o), _ptr(hh), hi.shape[0], lo.shape[0], wp, wn, _stream(ref))
+    return ho, lo_o, hh
 
 
 def conv2d(x: torch.Tensor, weight: torch.Tensor, bias=None, stride: int = 1, padding: int = 0,

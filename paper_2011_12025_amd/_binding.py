@@ -23,7 +23,9 @@ SB_PAD_AVG, SB_PAD_STRIDED, SB_PAD_ZERO = 0, 1, 2
 EXPORTS = ["segblocks_count", "segblocks_split", "segblocks_pad", "segblocks_pad_ex", "segblocks_conv3x3", "segblocks_combine",
            "segblocks_block_conv3x3", "segblocks_layer", "segblocks_block_conv_ex", "segblocks_conv2d",
            "segblocks_maxpool", "segblocks_block_conv3x3_workspace_size", "segblocks_block_conv_ex_workspace_size",
-           "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_policy_heuristic",
+           "segblocks_layer_workspace_size", "segblocks_block_conv_ex_noalloc", "segblocks_block_conv_chain",
+           "segblocks_block_conv_chain_workspace_size", "segblocks_block_conv_chain_reads_half",
+           "segblocks_policy_heuristic",
            "segblocks_combine_backward", "segblocks_split_backward", "segblocks_pad_backward",
            "segblocks_conv3x3_backward_data", "segblocks_conv3x3_backward_data_workspace_size",
            "segblocks_conv3x3_backward_weight", "segblocks_conv3x3_backward_weight_workspace_size",
@@ -49,6 +51,10 @@ _SIGS = {
                                 _I, _I, _P, _Z, _P],
     "segblocks_block_conv_ex_noalloc": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P,
                                         _P, _I, _I, _P],
+    "segblocks_block_conv_chain": [_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _P,
+                                   _P, _P, _I, _I, _P, _Z, _P],
+    "segblocks_block_conv_chain_workspace_size": [_I] * 12 + [_ZP],
+    "segblocks_block_conv_chain_reads_half": [_I] * 13 + [ctypes.POINTER(_I)],
     "segblocks_policy_heuristic": [_P, _I, _I, _I, _I, _I, _I, _I, ctypes.c_double, _P, _P, _P],
     "segblocks_combine_backward": [_P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _I, _P],
     "segblocks_split_backward": [_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P],

@@ -412,6 +412,68 @@ int segblocks_block_conv_ex_noalloc(const void* hi, const void* lo, int dtype, i
                               hi_cap, lo_cap, nullptr, 0, stream);
 }
 
+int segblocks_block_conv_chain(const void* hi, const void* lo, const void* hi_half, int dtype, int layout, int N,
+                               int C_in, int H, int W, const uint8_t* mask, int bs, const void* weight,
+                               const void* bias, int C_out, int ksize, int stride, int flags, const void* residual_hi,
+                               const void* residual_lo, void* hi_out, void* lo_out, void* hi_out_half, int hi_cap,
+                               int lo_cap, void* workspace, size_t ws_bytes, hipStream_t stream) {
+    const char* fn = "segblocks_block_conv_chain";
+    sb::Geo g;
+    int s;
+    if ((s = check_geo(fn, dtype, layout, N, C_in, H, W, mask, bs, g))) return s;
+    if ((s = check_conv_shape(fn, C_in, C_out, bs, weight))) return s;
+    if ((s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride))) return s;
+    if ((s = check_conv_flags(fn, flags))) return s;
+    if ((residual_hi == nullptr) != (residual_lo == nullptr) && hi_cap > 0 && lo_cap > 0)
+        return fail(SB_EINVAL, fn, "residual_hi and residual_lo must both be given or both be NULL");
+    if ((s = check_caps(fn, hi_cap, lo_cap)) || (s = check_stack(fn, "hi", hi, hi_cap)) ||
+        (s = check_stack(fn, "lo", lo, lo_cap)) || (s = check_stack(fn, "hi_out", hi_out, hi_cap)) ||
+        (s = check_stack(fn, "lo_out", lo_out, lo_cap)))
+        return s;
+    const long long es = esize(dtype), lb = bs / 2, bo = bs / stride, lo_e = lb / stride;
+    if (hi_out_half && (bo % 2 || C_out % 8))
+        return fail(SB_ESHAPE, fn, "hi_out_half needs an even output block side and C_out %% 8 == 0 (got %lld, %d)",
+                    bo, C_out);
+    if ((reinterpret_cast<uintptr_t>(hi_half) | reinterpret_cast<uintptr_t>(hi_out_half)) % 16 ||
+        (hi_out_half && reinterpret_cast<uintptr_t>(hi_out) % 16))
+        return fail(SB_EINVAL, fn, "hi_half, hi_out_half and (with hi_out_half) hi_out must be 16-byte aligned");
+    sb::ConvArgs a{hi, lo, weight, bias, residual_hi, residual_lo, hi_out, lo_out, C_in, C_out, flags, hi_cap, lo_cap};
+    a.in_hs = hi_half;
+    a.out_hs = hi_out_half;
+    // 3x3 at stride 1 takes the routes of segblocks_block_conv3x3, the rest
+    // those of segblocks_block_conv_ex; only the implicit GEMM reads hi_half
+    // and writes hi_out_half itself
+    const bool k33 = ksize == 3 && stride == 1;
+    const size_t need = k33 ? sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a)
+                            : (sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0);
+    if ((s = check_ws(fn, need, workspace, ws_bytes))) return s;
+    const Range rh{hi, hi_cap * (long long)C_in * bs * bs * es}, rl{lo, lo_cap * (long long)C_in * lb * lb * es};
+    const Range rhh{hi_half, hi_half ? hi_cap * (long long)C_in * (lb * lb) * es : 0};
+    const Range rw{weight, (long long)C_out * C_in * ksize * ksize * es}, rb{bias, bias ? C_out * es : 0};
+    const Range rho{hi_out, hi_cap * (long long)C_out * bo * bo * es};
+    const Range rlo{lo_out, lo_cap * (long long)C_out * lo_e * lo_e * es};
+    const Range rhoh{hi_out_half, hi_out_half ? hi_cap * (long long)C_out * (bo / 2) * (bo / 2) * es : 0};
+    const Range rrh{residual_hi, hi_cap * (long long)C_out * bo * bo * es};
+    const Range rrl{residual_lo, lo_cap * (long long)C_out * lo_e * lo_e * es};
+    const Range rws{workspace, (long long)need};
+    if (any_overlap({rho, rlo, rhoh, rws}, {rh, rl, rhh, rw, rb, rrh, rrl, Range{mask, g.B}}))
+        return fail(SB_EINVAL, fn, "output buffers or the workspace overlap inputs or each other");
+    const sb::Ws ws{workspace, ws_bytes};
+    bool gemm;
+    hipError_t e;
+    if (k33) {
+        gemm = !sb::conv_res_fits(dtype, layout, g, a) && sb::igemm_fits(dtype, layout, g, a);
+        e = sb::launch_conv(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, mask, a, ws, stream);
+    } else {
+        gemm = sb::igemm_fits(dtype, layout, g, a);
+        e = gemm ? sb::launch_igemm(dtype, g, mask, a, ksize, stride, ws, stream)
+                 : sb::launch_bconv(dtype, g, mask, a, ksize, stride, stream);
+    }
+    if (e == hipSuccess && hi_out_half && !gemm)
+        e = sb::launch_sample_hs(dtype, hi_out, hi_cap, (int)bo, C_out, hi_out_half, stream);
+    return hip_status(fn, e);
+}
+
 namespace {
 
 // Geometry of a workspace query: the checks of check_geo without a mask.
@@ -458,6 +520,53 @@ int segblocks_block_conv_ex_workspace_size(int dtype, int layout, int N, int C_i
     sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, hi_cap,
                    lo_cap};
     *bytes = sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0;
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_block_conv_chain_workspace_size(int dtype, int layout, int N, int C_in, int H, int W, int bs,
+                                              int C_out, int ksize, int stride, int hi_cap, int lo_cap,
+                                              size_t* bytes) {
+    const char* fn = "segblocks_block_conv_chain_workspace_size";
+    sb::Geo g;
+    int s;
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, bytes, g)) ||
+        (s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride)) || (s = check_caps(fn, hi_cap, lo_cap)))
+        return s;
+    // the most any flags need without hi_half (with it a call needs no more)
+    sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, 0, hi_cap,
+                   lo_cap};
+    size_t n = 0;
+    for (int f : {0, (int)SB_FLAG_PAD_STRIDED}) {
+        a.flags = f;
+        const size_t k = ksize == 3 && stride == 1
+                             ? sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a)
+                             : (sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0);
+        n = k > n ? k : n;
+    }
+    *bytes = n;
+    g_err.clear();
+    return SB_OK;
+}
+
+int segblocks_block_conv_chain_reads_half(int dtype, int layout, int N, int C_in, int H, int W, int bs, int C_out,
+                                          int ksize, int stride, int flags, int hi_cap, int lo_cap, int* reads) {
+    const char* fn = "segblocks_block_conv_chain_reads_half";
+    sb::Geo g;
+    size_t unused = 0;
+    int s;
+    if (!reads) return fail(SB_EINVAL, fn, "reads is NULL");
+    if ((s = check_query(fn, dtype, layout, N, C_in, H, W, bs, C_out, &unused, g)) ||
+        (s = check_conv_ex_shape(fn, dtype, layout, C_in, bs, ksize, stride)) || (s = check_caps(fn, hi_cap, lo_cap)) ||
+        (s = check_conv_flags(fn, flags)))
+        return s;
+    sb::ConvArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, C_in, C_out, flags, hi_cap,
+                   lo_cap};
+    // the implicit GEMM's route (16-byte aligned buffers), average sampling,
+    // a 3x3 kernel and blocks of both classes
+    const bool gemm = sb::igemm_fits_shape(dtype, layout, g, a) &&
+                      !(ksize == 3 && stride == 1 && sb::conv_res_fits_shape(dtype, layout, g, a));
+    *reads = gemm && ksize == 3 && (flags & (SB_FLAG_PAD_STRIDED | SB_FLAG_PAD_ZERO)) == 0 && hi_cap > 0 && lo_cap > 0;
     g_err.clear();
     return SB_OK;
 }

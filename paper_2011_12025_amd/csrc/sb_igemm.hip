@@ -46,6 +46,7 @@
 // are permuted in LDS so that a lane ends with 8 consecutive output channels
 // of one pixel and stores them as one 16-byte write.
 #include <algorithm>
+#include <utility>
 #include <type_traits>
 
 #include "sb_common.h"
@@ -87,7 +88,10 @@ constexpr int GMAXC = 4096;    // input channels the zero row covers
 // globals start zeroed and this one is never written.
 __device__ __align__(16) uint4 g_zero_row[GMAXC * 2 / 16];
 
-// source descriptor: kind in bits 30..31, pixel index (in its stack) below
+// source descriptor: kind in bits 30..31, pixel index (in its stack) below.
+// A low tile that reads the input's high stack at half resolution
+// (ConvArgs::in_hs) has no full-resolution high source: GK_HI then indexes
+// that stack.
 constexpr uint32_t GK_HI = 0u, GK_LO = 1u, GK_ZERO = 3u;
 __device__ __forceinline__ uint32_t gdesc(uint32_t kind, int pix) { return (kind << 30) | (uint32_t)pix; }
 
@@ -189,6 +193,7 @@ struct GParams {
     int dense;
     int W;          // dense mode: width of the map
     int* dout;      // per M tile, TM dense output pixels (-1: none), written when splits > 1
+    int hs_lg;      // log2 of the high output extent when the epilogue writes a.out_hs, else -1
 };
 
 // The store of 8 finished channels of one output pixel: row m of the class's
@@ -210,12 +215,75 @@ __device__ __forceinline__ void gstore8(T* out, int m, int dpix, int W, int high
     }
 }
 
+template <typename T>
+__device__ __forceinline__ Vec<T, 8> gshfl_xor(const Vec<T, 8>& v, int mask) {
+    Vec<T, 8> r;
+    r.raw.x = (uint32_t)__shfl_xor((int)v.raw.x, mask, 64);
+    r.raw.y = (uint32_t)__shfl_xor((int)v.raw.y, mask, 64);
+    r.raw.z = (uint32_t)__shfl_xor((int)v.raw.z, mask, 64);
+    r.raw.w = (uint32_t)__shfl_xor((int)v.raw.w, mask, 64);
+    return r;
+}
+
+template <typename T>
+__device__ __forceinline__ Vec<T, 8> gsel(bool c, const Vec<T, 8>& x, const Vec<T, 8>& y) {
+    Vec<T, 8> r;
+    r.raw.x = c ? x.raw.x : y.raw.x;
+    r.raw.y = c ? x.raw.y : y.raw.y;
+    r.raw.z = c ? x.raw.z : y.raw.z;
+    r.raw.w = c ? x.raw.w : y.raw.w;
+    return r;
+}
+
+template <typename T, int MS, int ms>
+__device__ __forceinline__ void gsample_one(const Vec<T, 8> (&o)[MS], int mbase, int rows_valid, int l16, int lg,
+                                            T* hs, int C_out, int co) {
+    const int eo = 1 << lg, eh = eo >> 1;
+    const int vstep = eo >> 4;  // fragment step of the row below (eo >= 16)
+    // values selected per component, fragments by fixed index (a select
+    // between array elements would put the array in scratch memory)
+    const Vec<T, 8> down = gsel(eo == 16, o[ms ^ 1], o[(ms ^ 2) % MS]);
+    const Vec<T, 8> right = gshfl_xor(o[ms], 1);
+    const Vec<T, 8> below = gsel(eo <= 8, gshfl_xor(o[ms], eo), down);
+    const Vec<T, 8> diag = gshfl_xor(gsel(eo <= 8, o[ms], down), eo <= 8 ? (eo | 1) : 1);
+    const int m = mbase + ms * 16 + l16;
+    const bool top = eo <= 8 ? (l16 & eo) == 0 : (ms & vstep) == 0;
+    if (m < rows_valid && (l16 & 1) == 0 && top) {
+        const int slot = m >> (2 * lg), rem = m & (eo * eo - 1);
+        const int i = rem >> lg, j = rem & (eo - 1);
+        const size_t idx = ((size_t)slot * eh + (i >> 1)) * eh + (j >> 1);
+        *reinterpret_cast<uint4*>(hs + idx * C_out + co) = vavg4<T, 8>(o[ms], right, below, diag).raw;
+    }
+}
+
+template <typename T, int MS, int... I>
+__device__ __forceinline__ void gsample_seq(std::integer_sequence<int, I...>, const Vec<T, 8> (&o)[MS], int mbase,
+                                            int rows_valid, int l16, int lg, T* hs, int C_out, int co) {
+    (gsample_one<T, MS, I>(o, mbase, rows_valid, l16, lg, hs, C_out, co), ...);
+}
+
+// The 2x2 averages of a finished high tile (its blocks at half resolution,
+// ConvArgs::out_hs), from the rounded results o[ms] of 8 channels (co..) of
+// pixel rows mbase + 16 ms + l16.  Rows of a block of extent eo = 2^lg are
+// row-major, and a 16-row group starts a block row, so the cell of a pixel
+// at even (i, j) has its right partner in lane ^ 1 and the row below in
+// lane ^ eo for eo <= 8, in fragment ms ^ 1 for eo = 16 and in ms ^ 2 for
+// eo = 32 (MS = 4).  Every lane takes part in every shuffle (partners lie in
+// the lane's own group of 16, all valid or all past rows_valid together).
+template <typename T, int MS>
+__device__ __forceinline__ void gsample(const Vec<T, 8> (&o)[MS], int mbase, int rows_valid, int l16, int lg, T* hs,
+                                        int C_out, int co) {
+    gsample_seq<T, MS>(std::make_integer_sequence<int, MS>{}, o, mbase, rows_valid, l16, lg, hs, C_out, co);
+}
+
 // Bias, residual, ReLU and the store of a finished tile: lane holds channels
 // co0 + wn*NS*16 + jj*32 + kg*8 + 0..7 of pixel row m0 + wm*MS*16 + ms*16 + l16.
 // dout: dense mode, the dense output pixel of each tile pixel (else nullptr).
+// hs: a high tile's half-resolution output (gsample; lg = log2 of the block
+// extent), or nullptr.
 template <typename T, int WM, int MS, int NS>
 __device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const ConvArgs& a, int high, int m0,
-                                          int rows_valid, int co0, const int* dout, int W) {
+                                          int rows_valid, int co0, const int* dout, int W, T* hs, int lg) {
     const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
     const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
     const int C_out = a.C_out;
@@ -230,10 +298,38 @@ __device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const Co
         float bv[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) bv[i] = bias ? to_f32(bias[co + i]) : 0.0f;
+        if (!hs) {  // (uniform) the plain stores
+#pragma unroll
+            for (int ms = 0; ms < MS; ++ms) {
+                const int m = m0 + wm * MS * 16 + ms * 16 + l16;
+                if (m >= rows_valid) continue;
+                float f[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    f[i] = acc[ms][2 * jj][i] + bv[i];
+                    f[4 + i] = acc[ms][2 * jj + 1][i] + bv[4 + i];
+                }
+                const size_t off = (size_t)m * C_out + co;
+                if (res) {
+                    Vec<T, 8> rv;
+                    rv.raw = *reinterpret_cast<const uint4*>(res + off);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
+                }
+                Vec<T, 8> o;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
+                gstore8<T>(out, m, dout ? dout[m - m0] : -1, W, high, C_out, co, o.raw);
+            }
+            continue;
+        }
+        // with the half-resolution output: every lane computes every fragment
+        // (the cell's partners are taken by shuffles), stores where valid
+        Vec<T, 8> o[MS];
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms) {
             const int m = m0 + wm * MS * 16 + ms * 16 + l16;
-            if (m >= rows_valid) continue;
+            const bool valid = m < rows_valid;
             float f[8];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -241,17 +337,17 @@ __device__ __forceinline__ void gepilogue(const floatx4 (&acc)[MS][NS], const Co
                 f[4 + i] = acc[ms][2 * jj + 1][i] + bv[4 + i];
             }
             const size_t off = (size_t)m * C_out + co;
-            if (res) {
+            if (res && valid) {
                 Vec<T, 8> rv;
                 rv.raw = *reinterpret_cast<const uint4*>(res + off);
 #pragma unroll
                 for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
             }
-            Vec<T, 8> o;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
-            gstore8<T>(out, m, dout ? dout[m - m0] : -1, W, high, C_out, co, o.raw);
+            for (int i = 0; i < 8; ++i) o[ms].e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
+            if (valid) gstore8<T>(out, m, dout ? dout[m - m0] : -1, W, high, C_out, co, o[ms].raw);
         }
+        gsample<T, MS>(o, m0 + wm * MS * 16, rows_valid, l16, lg, hs, C_out, co);
     }
 }
 
@@ -400,12 +496,17 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
         prow[j] = (wave * BR + j) * 8 + (lane >> 3);
         pq[j] = ((lane & 7) ^ ((prow[j] >> 1) & 7)) * 8;
     }
-    const T* __restrict__ in_hi = (const T*)a.in_hi;
     // a low tile reads the padded low stack when there is one (uniform); in
     // dense mode the high tiles' low neighbours come from it too
     const bool lpad = !high && gp.lo_pad != nullptr;
     const bool dense = gp.dense != 0;
     const T* __restrict__ in_lo = (lpad || dense) ? (const T*)gp.lo_pad : (const T*)a.in_lo;
+    // a low tile takes a high neighbour's halo cells (average sampling) from
+    // the input's high stack at half resolution when the caller gives it, and
+    // then reads nothing else of the high stack: its GK_HI sources index that
+    const int pm = pad_mode(a.flags);
+    const bool hsrc = !high && a.in_hs != nullptr && pm == PM_AVG;
+    const T* __restrict__ in_hi = (const T*)(hsrc ? a.in_hs : a.in_hi);
 
     // ---- source descriptors.  First, at once: the position of each tile pixel
     // (one thread each), and the nine neighbour sources of each block of the
@@ -415,7 +516,6 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     const int nblk = (min(m0 + TM, rows_valid) - 1) / eo2 - slot0 + 1;  // blocks the tile touches (<= TM + 1)
     uint32_t* s_nb = reinterpret_cast<uint32_t*>(s_tmp + ((2 * B + 15) & ~15));
     int* s_nbase = reinterpret_cast<int*>(s_nb + nblk * 9);  // dense mode: top-left pixel of each block of the tile
-    const int pm = pad_mode(a.flags);
     if (tid < TM) {  // each tile pixel: its block among the tile's blocks, row, column
         const int m = m0 + tid;
         int pij = -1;
@@ -497,9 +597,11 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
                 } else if (kind != GK_ZERO) {
                     if ((kind == GK_HI) == (high != 0)) ds = gdesc(kind, (s2 * e_in + u2) * e_in + v2);
                     else if (high) ds = gdesc(GK_LO, (s2 * lb + (u2 >> 1)) * lb + (v2 >> 1));
-                    // a low block beside a high one: strided sampling reads the
-                    // cell's top-left pixel; average sampling never gets here (the
-                    // low stack is then padded beforehand, see igemm_plan)
+                    // a low block beside a high one: average sampling reads the
+                    // cell's average from the half-resolution high stack (without
+                    // it the low stack is padded beforehand, see igemm_plan),
+                    // strided sampling the cell's top-left pixel
+                    else if (hsrc) ds = gdesc(GK_HI, (s2 * lb + u2) * lb + v2);
                     else ds = gdesc(GK_HI, (s2 * bs + 2 * u2) * bs + 2 * v2);
                 }
             }
@@ -596,7 +698,8 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
     __builtin_amdgcn_s_waitcnt(0);  // the padding DMAs
 
     if (gp.splits == 1) {
-        gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0, dense ? s_dout : nullptr, g.W);
+        gepilogue<T, WM, MS, NS>(acc, a, high, m0, rows_valid, co0, dense ? s_dout : nullptr, g.W,
+                                 high && gp.hs_lg >= 0 ? (T*)a.out_hs : nullptr, gp.hs_lg);
     } else {
         const int tile_lin = tx * gp.tiles_n + ny;
 #pragma unroll
@@ -611,22 +714,40 @@ __global__ __launch_bounds__(GWG, 1) void k_igemm(Geo g, const uint8_t* __restri
 // Sums the split partial tiles in split order and runs the epilogue.  One
 // thread per (tile, wave, ms, ns pair, lane) of the multiply kernel, so the
 // whole grid shares the work; a thread holds 8 consecutive output channels
-// of one pixel, exactly as the multiply kernel's lane does.
+// of one pixel, exactly as the multiply kernel's lane does.  Consecutive
+// waves take the ns pairs of a fragment (their stores fill whole lines),
+// except with the half-resolution output (a.out_hs): the MS fragments of a
+// (wave, ns pair) are then consecutive waves of one workgroup, so that a
+// 2x2 cell's four pixels can come from LDS: the right neighbour is thread
+// ^ 1, the row below thread ^ eo for eo <= 8, the next fragment's wave
+// (thread ^ 64) for eo = 16 and the one after (thread ^ 128) for eo = 32
+// (MS = 4).
 template <typename T, int WM, int MS, int NS>
 __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, int tiles, int tiles_n) {
     constexpr int WN = GWAVES / WM;
     constexpr int TM = WM * MS * 16, TN = WN * NS * 16;
     constexpr int PER_TILE = GWAVES * MS * (NS / 2) * 64;
+    static_assert(PER_TILE % 256 == 0, "a workgroup stays in one tile");
+    __shared__ uint4 s_o[256];
     const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (gid >= (long long)tiles * tiles_n * PER_TILE) return;
+    if (gid >= (long long)tiles * tiles_n * PER_TILE) return;  // whole workgroups
     const int tile_lin = (int)(gid / PER_TILE);
     int r = (int)(gid - (long long)tile_lin * PER_TILE);
     const int lane = r & 63;
     r >>= 6;
-    const int jj = r % (NS / 2);
-    r /= (NS / 2);
-    const int ms = r % MS;
-    const int wave = r / MS;
+    int ms, jj;
+    if (gp.hs_lg >= 0) {
+        ms = r % MS;
+        r /= MS;
+        jj = r % (NS / 2);
+        r /= (NS / 2);
+    } else {
+        jj = r % (NS / 2);
+        r /= (NS / 2);
+        ms = r % MS;
+        r /= MS;
+    }
+    const int wave = r;
     const int tx = tile_lin / tiles_n, ty = tile_lin - tx * tiles_n;
     const int rows_valid = gp.rows[2 * tx];
     const int code = gp.rows[2 * tx + 1];
@@ -635,38 +756,58 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
     const int wm = wave % WM, wn = wave / WM, l16 = lane & 15, kg = lane >> 4;
     const int m = m0 + wm * MS * 16 + ms * 16 + l16;
     const int co = ty * TN + wn * NS * 16 + jj * 32 + kg * 8;
-    if (m >= rows_valid || co >= a.C_out) return;
-    floatx4 lo = *reinterpret_cast<const floatx4*>(
-        gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj, lane));
-    floatx4 hi = *reinterpret_cast<const floatx4*>(
-        gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj + 1, lane));
-    for (int z = 1; z < gp.splits; ++z) {
-        lo += *reinterpret_cast<const floatx4*>(
-            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj, lane));
-        hi += *reinterpret_cast<const floatx4*>(
-            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj + 1, lane));
-    }
-    const T* __restrict__ bias = (const T*)a.bias;
-    const T* __restrict__ res = (const T*)(high ? a.res_hi : a.res_lo);
-    T* __restrict__ out = (T*)(high ? a.out_hi : a.out_lo);
-    const bool relu = (a.flags & 1) != 0;
-    float f[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        f[i] = lo[i] + (bias ? to_f32(bias[co + i]) : 0.0f);
-        f[4 + i] = hi[i] + (bias ? to_f32(bias[co + 4 + i]) : 0.0f);
-    }
-    const size_t off = (size_t)m * a.C_out + co;
-    if (res) {
-        Vec<T, 8> rv;
-        rv.raw = *reinterpret_cast<const uint4*>(res + off);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
-    }
     Vec<T, 8> o;
+    o.raw = uint4{0u, 0u, 0u, 0u};
+    if (m < rows_valid && co < a.C_out) {
+        floatx4 lo = *reinterpret_cast<const floatx4*>(
+            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj, lane));
+        floatx4 hi = *reinterpret_cast<const floatx4*>(
+            gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, 0, gp.splits, wave, ms, 2 * jj + 1, lane));
+        for (int z = 1; z < gp.splits; ++z) {
+            lo += *reinterpret_cast<const floatx4*>(
+                gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj, lane));
+            hi += *reinterpret_cast<const floatx4*>(
+                gp.part + gpart_off<TM * TN, MS, NS>(tile_lin, z, gp.splits, wave, ms, 2 * jj + 1, lane));
+        }
+        const T* __restrict__ bias = (const T*)a.bias;
+        const T* __restrict__ res = (const T*)(high ? a.res_hi : a.res_lo);
+        T* __restrict__ out = (T*)(high ? a.out_hi : a.out_lo);
+        const bool relu = (a.flags & 1) != 0;
+        float f[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
-    gstore8<T>(out, m, gp.dense ? gp.dout[tx * TM + (m - m0)] : -1, gp.W, high, a.C_out, co, o.raw);
+        for (int i = 0; i < 4; ++i) {
+            f[i] = lo[i] + (bias ? to_f32(bias[co + i]) : 0.0f);
+            f[4 + i] = hi[i] + (bias ? to_f32(bias[co + 4 + i]) : 0.0f);
+        }
+        const size_t off = (size_t)m * a.C_out + co;
+        if (res) {
+            Vec<T, 8> rv;
+            rv.raw = *reinterpret_cast<const uint4*>(res + off);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) f[i] += to_f32(rv.e[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o.e[i] = from_f32<T>(relu ? fmaxf(f[i], 0.0f) : f[i]);
+        gstore8<T>(out, m, gp.dense ? gp.dout[tx * TM + (m - m0)] : -1, gp.W, high, a.C_out, co, o.raw);
+    }
+    if (gp.hs_lg >= 0 && high) {  // uniform over the workgroup (one tile)
+        const int lg = gp.hs_lg, eo = 1 << lg, eh = eo >> 1;
+        const int t = (int)threadIdx.x;
+        s_o[t] = o.raw;
+        __syncthreads();
+        const int tb = eo <= 8 ? t ^ eo : t ^ (64 * (eo >> 4));  // the row below
+        const bool top = eo <= 8 ? (l16 & eo) == 0 : (ms & (eo >> 4)) == 0;
+        if (m < rows_valid && co < a.C_out && (l16 & 1) == 0 && top) {
+            Vec<T, 8> rt, bl, dg;
+            rt.raw = s_o[t ^ 1];
+            bl.raw = s_o[tb];
+            dg.raw = s_o[tb ^ 1];
+            const int slot = m >> (2 * lg), rem = m & (eo * eo - 1);
+            const int i = rem >> lg, j = rem & (eo - 1);
+            const size_t idx = ((size_t)slot * eh + (i >> 1)) * eh + (j >> 1);
+            *reinterpret_cast<uint4*>((T*)a.out_hs + idx * a.C_out + co) = vavg4<T, 8>(o, rt, bl, dg).raw;
+        }
+    }
 }
 
 }  // namespace
@@ -764,7 +905,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dens
     // 3 us either way elsewhere.)
     // In dense mode the padded low stack comes straight from the dense map and
     // the high tiles read their low neighbours from it as well.
-    p.pad_low = dense || (ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG);
+    p.pad_low = dense || (ks == 3 && p.tiles_l > 0 && a.hi_cap > 0 && pad_mode(a.flags) == PM_AVG && !a.in_hs);
     p.part_bytes = p.splits > 1 ? ground256((size_t)tiles * p.tiles_n * p.splits * p.TM * p.TN * 4 + (size_t)tiles * 8 +
                                             (dense ? (size_t)tiles * p.TM * 4 : 0))
                                 : 0;
@@ -800,6 +941,12 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
     gp.dense = dense ? 1 : 0;
     gp.W = g.W;
     gp.dout = nullptr;
+    // the half-resolution output from the epilogue when a 2x2 cell's pixels
+    // lie in one wave (see gsample), else from launch_sample_hs afterwards
+    const int eo_h = gp.eo_h;
+    const bool hs_epi = a.out_hs != nullptr && !dense && eo_h >= 2 && (eo_h & (eo_h - 1)) == 0 &&
+                        (eo_h <= 16 || (eo_h == 32 && MS == 4));
+    gp.hs_lg = hs_epi ? __builtin_ctz((unsigned)eo_h) : -1;
     if (S > 1) {
         gp.part = (float*)ws.p;
         gp.rows = (int*)((char*)ws.p + (size_t)tiles * tiles_n * S * TM * TN * 4);  // 2 ints per tile
@@ -823,6 +970,11 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
         const long long threads = (long long)tiles * tiles_n * GWAVES * MS * (NS / 2) * 64;
         hipLaunchKernelGGL((k_igemm_reduce<T, WM, MS, NS>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, a,
                            gp, tiles, tiles_n);
+    }
+    if (a.out_hs && !hs_epi && !dense) {
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_sample_hs(std::is_same<T, f16>::value ? 1 : 2, a.out_hi, a.hi_cap, eo_h, a.C_out, a.out_hs, st);
     }
     return hipGetLastError();
 }
@@ -859,7 +1011,8 @@ bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a) {
 
 bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a) {
     if (!galigned(a.in_hi) || !galigned(a.in_lo) || !galigned(a.weight) || !galigned(a.out_hi) ||
-        !galigned(a.out_lo) || !galigned(a.res_hi) || !galigned(a.res_lo))
+        !galigned(a.out_lo) || !galigned(a.res_hi) || !galigned(a.res_lo) || !galigned(a.in_hs) ||
+        !galigned(a.out_hs))
         return false;
     return igemm_fits_shape(dtype, layout, g, a);
 }

@@ -32,6 +32,14 @@ struct ConvArgs {
     void* out_hi;        // packed output stacks, or the dense output map
     void* out_lo;
     int C_in, C_out, flags, hi_cap, lo_cap;
+    // The high stacks at half resolution (each block's 2x2 averages, the
+    // values BlockPad with average sampling gives a low neighbour's halo):
+    // in_hs [hi_cap][bs/2][bs/2][C_in] of the input, read by the implicit
+    // GEMM instead of padding the low stack beforehand; out_hs
+    // [hi_cap][bo/2][bo/2][C_out] of the output (bo = bs / stride), written
+    // from the results.  nullptr = not given / not wanted.
+    const void* in_hs = nullptr;
+    void* out_hs = nullptr;
 };
 
 // bwd: the transposes for the backward pass instead: split of a gradient map
@@ -75,6 +83,10 @@ hipError_t launch_combine_rows(int dtype, const Geo& g, const void* hi, const vo
 // dense map, for fp16 / bf16 maps whose sides are multiples of the block size.
 hipError_t launch_pad_low_dense(int dtype, const Geo& g, const void* x, const uint8_t* mask, void* lp, int lo_cap,
                                 hipStream_t st);
+// The high stack at half resolution: hs[s][u][v] = the 2x2 average of cell
+// (2u, 2v) of block s of hi [hi_cap][e][e][C] (e even), for every slot below
+// hi_cap (fp16 / bf16, channels-last, 16-byte aligned, C % 8 == 0).
+hipError_t launch_sample_hs(int dtype, const void* hi, int hi_cap, int e, int C, void* hs, hipStream_t st);
 
 // Encoder kernels (channels-last fp16/bf16): block convolution K x K
 // (K = 1, 3) at stride 1 or 2 on packed stacks, dense convolution, and
@@ -85,6 +97,8 @@ hipError_t launch_pad_low_dense(int dtype, const Geo& g, const void* x, const ui
 bool igemm_fits_shape(int dtype, int layout, const Geo& g, const ConvArgs& a);
 bool igemm_fits(int dtype, int layout, const Geo& g, const ConvArgs& a);
 size_t igemm_ws_bytes(const Geo& g, const ConvArgs& a, int ksize, int stride);
+// launch_igemm writes a.out_hs (when given) from its epilogue where the tile
+// layout keeps every 2x2 cell within a wave, else with launch_sample_hs after.
 hipError_t launch_igemm(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,
                         Ws ws, hipStream_t st);
 hipError_t launch_bconv(int dtype, const Geo& g, const uint8_t* mask, const ConvArgs& a, int ksize, int stride,

@@ -562,6 +562,25 @@ hipError_t pad_rows_t(const Geo& g, const void* hi, const void* lo, const uint8_
 
 inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// The high stack at half resolution: one thread per (slot, cell, 8
+// channels); the cell's four pixels are read as 16-byte vectors and averaged
+// in the library's association (vavg4).
+template <typename T>
+__global__ __launch_bounds__(256) void k_sample_hs(const T* __restrict__ hi, long long items, int e, int C,
+                                                   T* __restrict__ hs) {
+    const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (t >= items) return;
+    const int c8 = C >> 3, eh = e >> 1;
+    const long long cell = t / c8;
+    const int c = (int)(t - cell * c8) * 8;
+    const long long s = cell / (eh * eh);
+    const int r = (int)(cell - s * eh * eh), u = r / eh, v = r - (r / eh) * eh;
+    const T* p = hi + (((size_t)s * e + 2 * u) * e + 2 * v) * C + c;
+    const Vec<T, 8> a = vload<T, 8>(p), b = vload<T, 8>(p + C), cc = vload<T, 8>(p + (size_t)e * C),
+                    d = vload<T, 8>(p + (size_t)e * C + C);
+    *reinterpret_cast<uint4*>(hs + (size_t)cell * C + c) = vavg4<T, 8>(a, b, cc, d).raw;
+}
+
 }  // namespace
 
 bool rows_fit(int dtype, int layout, const Geo& g, std::initializer_list<const void*> ptrs) {
@@ -607,6 +626,20 @@ hipError_t launch_pad_rows(int dtype, const Geo& g, const void* hi, const void* 
     case 1: return pad_rows_t<f16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     default: return pad_rows_t<bf16>(g, hi, lo, mask, hp, lp, hi_cap, lo_cap, pm, st);
     }
+}
+
+hipError_t launch_sample_hs(int dtype, const void* hi, int hi_cap, int e, int C, void* hs, hipStream_t st) {
+    if (hi_cap <= 0 || e < 2) return hipSuccess;
+    if ((e & 1) || C % 8 || (dtype != 1 && dtype != 2) || (reinterpret_cast<uintptr_t>(hi) & 15) ||
+        (reinterpret_cast<uintptr_t>(hs) & 15))
+        return hipErrorInvalidValue;
+    const long long items = (long long)hi_cap * (e / 2) * (e / 2) * (C / 8);
+    const unsigned grid = (unsigned)((items + 255) / 256);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_sample_hs<f16>, dim3(grid), dim3(256), 0, st, (const f16*)hi, items, e, C, (f16*)hs);
+    else
+        hipLaunchKernelGGL(k_sample_hs<bf16>, dim3(grid), dim3(256), 0, st, (const bf16*)hi, items, e, C, (bf16*)hs);
+    return hipGetLastError();
 }
 
 }  // namespace sb

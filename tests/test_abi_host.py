@@ -175,3 +175,52 @@ def test_calls_reject_missing_or_small_workspace(lib):
     bargs = [P(base), P(base + 0x1000000), 1, 1, 1, 512, 32, 64, P(base + 0x2000000), 4, P(base + 0x3000000), NULL,
              512, 0, NULL, NULL, P(base + 0x4000000), P(base + 0x5000000), 128, 128]
     assert lib.segblocks_block_conv3x3(*bargs, NULL, 0, None) == b.SB_ENOMEM
+
+
+def test_chain_queries_and_validation(lib):
+    """segblocks_block_conv_chain: its workspace is what block_conv_ex /
+    block_conv3x3 need for the same shapes; the host query tells whether a
+    call reads hi_half (the implicit GEMM with average sampling and blocks of
+    both classes); a channel count the half-resolution output cannot be
+    stored in, or misaligned half stacks, are rejected before anything is launched."""
+    _, ex = _ws_query(lib, "segblocks_block_conv_ex_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 2, 128, 128)
+    r, ch = _ws_query(lib, "segblocks_block_conv_chain_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 2, 128, 128)
+    assert r == 0 and ch == ex
+    _, b3 = _ws_query(lib, "segblocks_block_conv3x3_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 128, 128)
+    r, ch = _ws_query(lib, "segblocks_block_conv_chain_workspace_size", 1, 1, 1, 512, 32, 64, 4, 512, 3, 1, 128, 128)
+    assert r == 0 and ch == b3
+
+    def reads(*a):
+        v = ctypes.c_int(7)
+        assert lib.segblocks_block_conv_chain_reads_half(*a, ctypes.byref(v)) == 0
+        return v.value
+
+    # dtype, layout, N, C_in, H, W, bs, C_out, k, stride, flags, hi_cap, lo_cap
+    assert reads(1, 1, 1, 128, 64, 128, 16, 128, 3, 1, 0, 10, 22) == 1
+    assert reads(1, 1, 1, 64, 256, 512, 32, 128, 3, 2, 0, 70, 58) == 1      # stride 2: the GEMM
+    assert reads(1, 1, 1, 64, 256, 512, 32, 64, 3, 1, 0, 70, 58) == 0       # the resident kernel pads itself
+    assert reads(1, 1, 1, 128, 64, 128, 16, 128, 3, 1, 0, 32, 0) == 0       # no low blocks
+    assert reads(1, 1, 1, 128, 64, 128, 16, 128, 3, 1, b.SB_FLAG_PAD_STRIDED, 10, 22) == 0
+    assert reads(1, 1, 1, 128, 64, 128, 16, 256, 1, 2, 0, 10, 22) == 0      # 1x1: no halo
+    v = ctypes.c_int(0)
+    assert lib.segblocks_block_conv_chain_reads_half(1, 1, 1, 128, 64, 128, 16, 128, 5, 1, 0, 10, 22,
+                                                     ctypes.byref(v)) == b.SB_EINVAL
+
+    P = ctypes.c_void_p
+    base = 0x100000000
+
+    _, need = _ws_query(lib, "segblocks_block_conv_chain_workspace_size", 1, 1, 1, 128, 64, 128, 16, 128, 3, 1, 16,
+                        16)
+
+    def call(hi_half, hi_out_half, bs=16, stride=1, C_out=128):
+        return lib.segblocks_block_conv_chain(P(base), P(base + 0x1000000), hi_half, 1, 1, 1, 128, 64, 128,
+                                              P(base + 0x2000000), bs, P(base + 0x3000000), NULL, C_out, 3, stride, 0,
+                                              NULL, NULL, P(base + 0x4000000), P(base + 0x5000000), hi_out_half,
+                                              16, 16, P(base + 0x10000000), need, None)
+    # the half-resolution output is stored 8 channels at a time
+    assert call(NULL, P(base + 0x6000000), C_out=12) == b.SB_ESHAPE
+    assert "C_out % 8" in lib.segblocks_last_error().decode()
+    assert call(P(base + 0x6000008), NULL) == b.SB_EINVAL
+    assert "aligned" in lib.segblocks_last_error().decode()
+    assert call(NULL, P(base + 0x4000000)) == b.SB_EINVAL        # hi_out_half = hi_out
+    assert "overlap" in lib.segblocks_last_error().decode()
