@@ -107,6 +107,17 @@ __device__ __forceinline__ Vec<T, V> vzero() {
     return v;
 }
 
+// The 16-byte vector of lane (lane ^ mask) of the wave.
+template <typename T>
+__device__ __forceinline__ Vec<T, 8> vshfl_xor(const Vec<T, 8>& v, int mask) {
+    Vec<T, 8> r;
+    r.raw.x = (uint32_t)__shfl_xor((int)v.raw.x, mask, 64);
+    r.raw.y = (uint32_t)__shfl_xor((int)v.raw.y, mask, 64);
+    r.raw.z = (uint32_t)__shfl_xor((int)v.raw.z, mask, 64);
+    r.raw.w = (uint32_t)__shfl_xor((int)v.raw.w, mask, 64);
+    return r;
+}
+
 template <typename T, int V>
 __device__ __forceinline__ Vec<T, V> vavg4(const Vec<T, V>& a, const Vec<T, V>& b,
                                            const Vec<T, V>& c, const Vec<T, V>& d) {

@@ -216,16 +216,6 @@ __device__ __forceinline__ void gstore8(T* out, int m, int dpix, int W, int high
 }
 
 template <typename T>
-__device__ __forceinline__ Vec<T, 8> gshfl_xor(const Vec<T, 8>& v, int mask) {
-    Vec<T, 8> r;
-    r.raw.x = (uint32_t)__shfl_xor((int)v.raw.x, mask, 64);
-    r.raw.y = (uint32_t)__shfl_xor((int)v.raw.y, mask, 64);
-    r.raw.z = (uint32_t)__shfl_xor((int)v.raw.z, mask, 64);
-    r.raw.w = (uint32_t)__shfl_xor((int)v.raw.w, mask, 64);
-    return r;
-}
-
-template <typename T>
 __device__ __forceinline__ Vec<T, 8> gsel(bool c, const Vec<T, 8>& x, const Vec<T, 8>& y) {
     Vec<T, 8> r;
     r.raw.x = c ? x.raw.x : y.raw.x;
@@ -243,9 +233,9 @@ __device__ __forceinline__ void gsample_one(const Vec<T, 8> (&o)[MS], int mbase,
     // values selected per component, fragments by fixed index (a select
     // between array elements would put the array in scratch memory)
     const Vec<T, 8> down = gsel(eo == 16, o[ms ^ 1], o[(ms ^ 2) % MS]);
-    const Vec<T, 8> right = gshfl_xor(o[ms], 1);
-    const Vec<T, 8> below = gsel(eo <= 8, gshfl_xor(o[ms], eo), down);
-    const Vec<T, 8> diag = gshfl_xor(gsel(eo <= 8, o[ms], down), eo <= 8 ? (eo | 1) : 1);
+    const Vec<T, 8> right = vshfl_xor(o[ms], 1);
+    const Vec<T, 8> below = gsel(eo <= 8, vshfl_xor(o[ms], eo), down);
+    const Vec<T, 8> diag = vshfl_xor(gsel(eo <= 8, o[ms], down), eo <= 8 ? (eo | 1) : 1);
     const int m = mbase + ms * 16 + l16;
     const bool top = eo <= 8 ? (l16 & eo) == 0 : (ms & vstep) == 0;
     if (m < rows_valid && (l16 & 1) == 0 && top) {
