@@ -441,8 +441,9 @@ int segblocks_block_conv_chain(const void* hi, const void* lo, const void* hi_ha
     a.in_hs = hi_half;
     a.out_hs = hi_out_half;
     // 3x3 at stride 1 takes the routes of segblocks_block_conv3x3, the rest
-    // those of segblocks_block_conv_ex; only the implicit GEMM reads hi_half,
-    // it and the resident kernel write hi_out_half themselves
+    // those of segblocks_block_conv_ex; only the implicit GEMM reads hi_half
+    // and writes hi_out_half itself (in the resident kernel the extra
+    // registers cost more than the launch after it)
     const bool k33 = ksize == 3 && stride == 1;
     const size_t need = k33 ? sb::conv_ws_bytes(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, a)
                             : (sb::igemm_fits_shape(dtype, layout, g, a) ? sb::igemm_ws_bytes(g, a, ksize, stride) : 0);
@@ -462,7 +463,7 @@ int segblocks_block_conv_chain(const void* hi, const void* lo, const void* hi_ha
     bool gemm;
     hipError_t e;
     if (k33) {
-        gemm = sb::conv_res_fits(dtype, layout, g, a) || sb::igemm_fits(dtype, layout, g, a);
+        gemm = !sb::conv_res_fits(dtype, layout, g, a) && sb::igemm_fits(dtype, layout, g, a);
         e = sb::launch_conv(dtype, layout, sb::SRC_PACKED, sb::DST_PACKED, g, mask, a, ws, stream);
     } else {
         gemm = sb::igemm_fits(dtype, layout, g, a);

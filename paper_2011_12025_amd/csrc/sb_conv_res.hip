@@ -50,8 +50,6 @@
 // a pixel's position does not depend on its row.  The weights never pass
 // through LDS: each consumer lane loads its A fragments (16 bytes each)
 // directly.
-#include <type_traits>
-
 #include "sb_common.h"
 #include "sb_kernels.h"
 #include "sb_pixel.h"
@@ -86,10 +84,6 @@ constexpr int NPW = 4;            // producer waves
 constexpr int RWG = 64 * (NCW + NPW);
 constexpr int PT = 64 * NPW;      // producer threads
 constexpr int NBUF = 3;           // tile buffers
-// Packed output that also writes the high blocks at half resolution
-// (ConvArgs::out_hs) from the epilogue: a variant of its own, so that the
-// plain packed kernel keeps its registers.
-constexpr int DST_PACKED_HS = 2;
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -540,7 +534,7 @@ __device__ __forceinline__ void rw_compute(const Geo& g, const ConvArgs& a, cons
     const bool full = vec_out && co + 8 <= Co;
     T* obase;  // the tile's block in its output stack, or the tile's image
     const T* rbase = nullptr;
-    if constexpr (DST != DST_DENSE) {
+    if constexpr (DST == DST_PACKED) {
         const size_t blk = (size_t)t.slot * E * E * Co;
         obase = (T*)(t.high ? a.out_hi : a.out_lo) + blk;
         const T* rb = (const T*)(t.high ? a.res_hi : a.res_lo);
@@ -548,12 +542,11 @@ __device__ __forceinline__ void rw_compute(const Geo& g, const ConvArgs& a, cons
     } else {
         obase = (T*)a.out_hi + (size_t)t.n * g.H * g.W * Co;
     }
-    Vec<T, 8> ovs[M];  // the rounded results, for the half-resolution output (DST_PACKED_HS)
 #pragma unroll
     for (int o = 0; o < M; ++o) {
         const int i = t.r0 + row0 + o, jx = strip * 16 + l16;  // block-local output pixel
         int off, down = 0;  // element offset of channel 0 of the pixel (the first of 2x2 for a low block)
-        if constexpr (DST != DST_DENSE) {
+        if constexpr (DST == DST_PACKED) {
             off = (i * E + jx) * Co;
         } else {
             const int Y = t.gy * g.bs + (t.high ? i : 2 * i), X = t.gx * g.bs + (t.high ? jx : 2 * jx);
@@ -579,7 +572,6 @@ __device__ __forceinline__ void rw_compute(const Geo& g, const ConvArgs& a, cons
         Vec<T, 8> ov;
 #pragma unroll
         for (int e = 0; e < 8; ++e) ov.e[e] = from_f32<T>(relu ? fmaxf(f[e], 0.0f) : f[e]);
-        ovs[o] = ov;
         const int reps = (DST == DST_DENSE && !t.high) ? 2 : 1;
         for (int dy = 0; dy < reps; ++dy)
             for (int dx = 0; dx < reps; ++dx) {
@@ -592,20 +584,6 @@ __device__ __forceinline__ void rw_compute(const Geo& g, const ConvArgs& a, cons
                         if (co + e < Co) q[e] = ov.e[e];
                 }
             }
-    }
-    // A high block's half-resolution output (ConvArgs::out_hs; this variant
-    // runs only with whole 16-byte stores): the unit's two rows start at an
-    // even block row, so a 2x2 cell is (lane, lane ^ 1) of both rows.
-    if constexpr (DST == DST_PACKED_HS && M == 2) {
-        if (t.high) {  // uniform over the tile
-            const Vec<T, 8> rt = vshfl_xor(ovs[0], 1), dg = vshfl_xor(ovs[1], 1);
-            if ((l16 & 1) == 0) {
-                constexpr int EH = E / 2;
-                const int i = t.r0 + row0, jx = strip * 16 + l16;
-                T* q = (T*)a.out_hs + (((size_t)t.slot * EH + (i >> 1)) * EH + (jx >> 1)) * Co + co;
-                *reinterpret_cast<uint4*>(q) = vavg4<T, 8>(ovs[0], rt, ovs[1], dg).raw;
-            }
-        }
     }
 }
 
@@ -813,26 +791,13 @@ hipError_t run_res(const Geo& g, const uint8_t* mask, const ConvArgs& a, int R, 
     const int ob = 16;
     const int vec_out = (a.C_out % 8 == 0) && aligned_to(a.out_hi, ob) && aligned_to(a.out_lo, ob) &&
                         aligned_to(a.res_hi, ob) && aligned_to(a.res_lo, ob);
-    // the high output at half resolution from the epilogue (packed stacks in,
-    // whole 16-byte stores), else from one launch after
-    if constexpr (DST == DST_PACKED && SRC == SRC_PACKED) {
-        if (a.out_hs && vec_out && aligned_to(a.out_hs, ob))
-            return run_res<T, SRC, DST_PACKED_HS, ONE, NKS>(g, mask, a, R, st);
-    }
     hipError_t e = ensure_dyn_lds((const void*)k_conv_res<T, SRC, DST, ONE, NKS>, smem);
     if (e != hipSuccess) return e;
     const int cus = device_cus();
     const int nwg = (int)(ntiles < cus ? ntiles : cus);
     const dim3 grid((unsigned)nwg, (unsigned)((a.C_out + RNT - 1) / RNT));
-    ConvArgs ka = a;
-    if (DST == DST_PACKED) ka.out_hs = nullptr;
-    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, ka, R, RL, Gh, Gl,
+    hipLaunchKernelGGL((k_conv_res<T, SRC, DST, ONE, NKS>), grid, dim3(RWG), smem, st, g, mask, a, R, RL, Gh, Gl,
                        buf_bytes, vec_out);
-    if (DST == DST_PACKED && a.out_hs) {
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        return launch_sample_hs(std::is_same<T, f16>::value ? 1 : 2, a.out_hi, a.hi_cap, g.bs, a.C_out, a.out_hs, st);
-    }
     return hipGetLastError();
 }
 

@@ -79,10 +79,10 @@ CASES = [
     # stride 2 (a stage transition) and 1x1 at stride 2
     CCase("k3s2_c128_co256_f16", "f16", 2, 128, 256, 64, 96, 16, stride=2, seed=308),
     CCase("k1s2_c128_co256_bf16", "bf16", 1, 128, 256, 64, 64, 16, k=1, stride=2, relu=False, seed=309),
-    # the resident kernel's route (64 channels, blocks of 32 and 64): averages from its epilogue
+    # the resident kernel's route (64 channels, blocks of 32 and 64): averages from the extra launch
     CCase("resident_c64_bs32_f16", "f16", 1, 64, 64, 64, 128, 32, residual=True, seed=310),
     CCase("resident_c64_bs64_bf16", "bf16", 2, 64, 64, 128, 256, 64, p_low=0.4, seed=314),
-    # 48 output channels: the resident kernel without whole 16-byte stores, averages from the extra launch
+    # 48 output channels on the resident kernel
     CCase("resident_c64_co48_f16", "f16", 1, 64, 48, 64, 128, 32, seed=315),
     # one class only, and more than 1024 blocks
     CCase("allhigh_eo8_f16", "f16", 1, 128, 128, 32, 64, 8, mask_kind="high", seed=311),
