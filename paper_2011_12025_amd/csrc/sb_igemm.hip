@@ -829,6 +829,13 @@ inline int igemm_tn(const Geo& g, const ConvArgs& a) {
     return 128;
 }
 
+// The 256 x 128 workgroup tile (eight 64 x 64 wave tiles over 256 pixel rows)
+// when its LDS fits: three 48 KB stages and a descriptor table twice as long.
+inline bool igemm_tm256_fits(const Geo& g, int ks) {
+    const int fixed = ks == 3 ? igemm_smem_fixed<256, 128, 9>() : igemm_smem_fixed<256, 128, 1>();
+    return fixed + igemm_hb_bytes(g) + GWAVES * 4 <= 160 * 1024;
+}
+
 // Everything about a launch that the host decides from the shapes alone:
 // tile counts (from the stack capacities), the K split, the padded low stack,
 // and the caller's workspace that they take.
@@ -840,50 +847,66 @@ struct IgPlan {
 
 IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dense = false) {
     IgPlan p;
-    p.TM = 128;
     const int eo_h = g.bs / stride, eo_l = (g.bs / 2) / stride;
-    p.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + p.TM - 1) / p.TM);
-    p.tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + p.TM - 1) / p.TM);
-    const int tiles = p.tiles_h + p.tiles_l;
+    auto tiles_of = [&](int TM, long long nh, long long nl) {
+        return (nh * eo_h * eo_h + TM - 1) / TM + (nl * eo_l * eo_l + TM - 1) / TM;
+    };
     // The work the cost model sees: the tiles that hold pixels under the
     // worst mask.  With room for every block in both classes (the fused
     // layer's packed route) the grid has twice the tiles any mask fills; the
     // surplus workgroups leave after the plan.
-    auto filled = [&](long long nh) {
-        const long long nl = std::min<long long>(g.B - nh, a.lo_cap);
-        return (nh * eo_h * eo_h + p.TM - 1) / p.TM + (nl * eo_l * eo_l + p.TM - 1) / p.TM;
-    };
     const long long nh_max = std::min<long long>(a.hi_cap, g.B);
     const long long nh_min = std::max<long long>(0, g.B - a.lo_cap);
-    const long long work = std::min<long long>(tiles, std::max(filled(nh_max), filled(std::min(nh_min, nh_max))));
-    // Tile width and split K by a cost model in units of one 128 x 128 K step
-    // (about 1 us): one workgroup per CU at a time (LDS), so a launch costs
-    // about rounds x (steps per split x step cost + start-up); a 128 x 256
-    // step does twice the MACs at about 1.3 times the cost; a split adds the
-    // partial-sum pass, which grows with the partial tiles it reads.  Take the
-    // cheapest choice that keeps at least four steps per workgroup.
+    auto work_of = [&](int TM) {
+        auto filled = [&](long long nh) { return tiles_of(TM, nh, std::min<long long>(g.B - nh, a.lo_cap)); };
+        return std::min<long long>(tiles_of(TM, a.hi_cap, a.lo_cap),
+                                   std::max(filled(nh_max), filled(std::min(nh_min, nh_max))));
+    };
+    // Workgroup tile and split K by a cost model in units of one 128 x 128 K
+    // step (about 1 us): one workgroup per CU at a time (LDS), so a launch
+    // costs about rounds x (steps per split x step cost + start-up); a 128 x
+    // 256 or 256 x 128 step (eight 64 x 64 wave tiles) does twice the MACs at
+    // about 1.3 times the cost; a split adds the partial-sum pass, which grows
+    // with the partial tiles it reads.  Take the cheapest choice that keeps at
+    // least four steps per workgroup (ties: the first of 128 x 256, 128 x 128,
+    // 256 x 128).
     const int cus = device_cus();
     const int nsteps = ks * ks * (a.C_in / GKC);
     const int tn_max = igemm_tn(g, a);
+    const bool tm256 = !dense && a.C_out >= 128 && igemm_tm256_fits(g, ks);
     double best = -1.0;
+    p.TM = 128;
     p.TN = tn_max;
     p.splits = 1;
-    for (int tn = tn_max; tn >= 128 || tn == tn_max; tn /= 2) {
+    for (int cand = 0; cand < 4; ++cand) {
+        int TM = 128, tn;
+        if (cand < 3) {
+            tn = tn_max >> cand;
+            if (cand > 0 && (tn < 128 || tn_max <= 128)) continue;
+        } else {
+            if (!tm256) continue;
+            TM = 256;
+            tn = 128;
+        }
         const int tiles_n = (a.C_out + tn - 1) / tn;
-        const double w = tn == 256 ? 1.3 : 1.0, wr = tn == 256 ? 2.0 : 1.0;
-        const long long wgs = work * tiles_n;
+        const bool wide = tn == 256 || TM == 256;
+        const double w = wide ? 1.3 : 1.0, wr = wide ? 2.0 : 1.0;
+        const long long wgs = work_of(TM) * tiles_n;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
             const long long rounds = (wgs * c + cus - 1) / cus;
             const double cost = (double)rounds * ((nsteps + c - 1) / c * w + GSTART_COST) +
                                 (c > 1 ? GSPLIT_COST + c * wr : 0.0);
             if (best < 0.0 || cost < best) {
                 best = cost;
+                p.TM = TM;
                 p.TN = tn;
                 p.splits = c;
             }
         }
-        if (tn <= 128) break;
     }
+    p.tiles_h = (int)(((long long)a.hi_cap * eo_h * eo_h + p.TM - 1) / p.TM);
+    p.tiles_l = (int)(((long long)a.lo_cap * eo_l * eo_l + p.TM - 1) / p.TM);
+    const int tiles = p.tiles_h + p.tiles_l;
     p.tiles_n = (a.C_out + p.TN - 1) / p.TN;
     if (tiles == 0) p.splits = 1;
     // A low block's halo across a resolution change, with average sampling, is
@@ -972,7 +995,9 @@ hipError_t igemm_run(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws
 template <typename T, int KS, int ST>
 hipError_t igemm_tile(const Geo& g, const uint8_t* mask, const ConvArgs& a, Ws ws, hipStream_t st,
                       bool dense = false) {
-    const int tn = igemm_plan(g, a, KS, ST, dense).TN;
+    const IgPlan pl = igemm_plan(g, a, KS, ST, dense);
+    const int tn = pl.TN;
+    if (pl.TM == 256) return igemm_run<T, KS, ST, 4, 4, 4>(g, mask, a, ws, st, dense);
     if (tn == 64) return igemm_run<T, KS, ST, 4, 2, 2>(g, mask, a, ws, st, dense);
     if (tn == 256) return igemm_run<T, KS, ST, 2, 4, 4>(g, mask, a, ws, st, dense);
     return igemm_run<T, KS, ST, 2, 4, 2>(g, mask, a, ws, st, dense);

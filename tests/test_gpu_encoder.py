@@ -79,6 +79,9 @@ BCASES = [
     BCase("ig_tn256_k3s1_c64_co320_bf16", "bf16", 1, 64, 320, 32, 64, 8, 3, 1, seed=86),
     BCase("ig_tn256_k3s2_c256_co256_f16", "f16", 2, 256, 256, 32, 64, 8, 3, 2, p_low=0.25, seed=87),
     BCase("ig_tn256_k3s1_c512_bs4_bf16", "bf16", 1, 512, 512, 32, 64, 4, 3, 1, p_low=0.75, residual=True, seed=88),
+    # enough pixel rows for the 256 x 128 workgroup tile (eight 64 x 64 wave tiles)
+    BCase("ig_tm256_k3s1_c64_co128_f16", "f16", 1, 64, 128, 256, 256, 16, 3, 1, relu=True, residual=True, seed=89),
+    BCase("ig_tm256_k3s1_c64_co128_bs8_bf16", "bf16", 2, 64, 128, 128, 256, 8, 3, 1, p_low=0.3, seed=90),
 ]
 
 
