@@ -873,6 +873,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dens
     const int cus = device_cus();
     const int nsteps = ks * ks * (a.C_in / GKC);
     const int tn_max = igemm_tn(g, a);
+    // (not in dense mode: there the wider tile measured slower at half low)
     const bool tm256 = !dense && a.C_out >= 128 && igemm_tm256_fits(g, ks);
     double best = -1.0;
     p.TM = 128;

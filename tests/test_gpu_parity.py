@@ -188,6 +188,8 @@ DEEP_CASES = [Case("deep512_f16", "f16", 1, 512, 64, 32, 64, 8, seed=21),
               Case("c256_n2_packed_route_f16", "f16", 2, 256, 64, 48, 96, 8, p_low=0.5, seed=26),
               Case("c192_n3_packed_route_bf16", "bf16", 3, 192, 64, 32, 96, 4, p_low=0.3, seed=27),
               Case("c128_layer_f16", "f16", 2, 128, 128, 32, 64, 8, seed=24),
+              # a larger dense-route layer: more workgroups than CUs
+              Case("c128_layer_2rounds_f16", "f16", 2, 128, 128, 128, 256, 16, seed=28),
               Case("c128_layer_alllow_bf16", "bf16", 1, 128, 64, 32, 32, 16, mask_kind="low", seed=25),
               Case("deep384_bf16", "bf16", 2, 384, 128, 16, 32, 4, p_low=0.6, seed=22),
               Case("deep512_allhigh_f16", "f16", 1, 512, 32, 16, 32, 4, mask_kind="high", seed=23)]
