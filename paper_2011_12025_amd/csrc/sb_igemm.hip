@@ -804,11 +804,12 @@ __global__ __launch_bounds__(256) void k_igemm_reduce(ConvArgs a, GParams gp, in
 
 namespace {
 
-// Launch cost model, in K steps (about 1 us each): a workgroup's start-up
-// (mask plan, descriptors, first stages), and the partial-sum pass, which
-// reads every split's partial tiles.
-constexpr int GSTART_COST = 5;
-constexpr int GSPLIT_COST = 10;  // plus one per split
+// Launch cost model, in 128 x 128 K steps (about 0.65 us each, measured):
+// a workgroup's start-up (launch spread, mask plan, descriptors, first
+// stages: about 6.5 us), and the partial-sum pass, which reads every split's
+// partial tiles.
+constexpr int GSTART_COST = 10;
+constexpr int GSPLIT_COST = 12;  // plus one per split
 
 inline bool galigned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 inline size_t ground256(size_t b) { return (b + 255) / 256 * 256; }
@@ -863,10 +864,10 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dens
                                    std::max(filled(nh_max), filled(std::min(nh_min, nh_max))));
     };
     // Workgroup tile and split K by a cost model in units of one 128 x 128 K
-    // step (about 1 us): one workgroup per CU at a time (LDS), so a launch
-    // costs about rounds x (steps per split x step cost + start-up); a 128 x
-    // 256 or 256 x 128 step (eight 64 x 64 wave tiles) does twice the MACs at
-    // about 1.3 times the cost; a split adds the partial-sum pass, which grows
+    // step: one workgroup per CU at a time (LDS), so a launch costs about
+    // rounds x (steps per split x step cost + start-up); a 128 x 256 or
+    // 256 x 128 step (eight 64 x 64 wave tiles) does twice the MACs at about
+    // 1.5 times the cost; a split adds the partial-sum pass, which grows
     // with the partial tiles it reads.  Take the cheapest choice that keeps at
     // least four steps per workgroup (ties: the first of 128 x 256, 128 x 128,
     // 256 x 128).
@@ -891,7 +892,7 @@ IgPlan igemm_plan(const Geo& g, const ConvArgs& a, int ks, int stride, bool dens
         }
         const int tiles_n = (a.C_out + tn - 1) / tn;
         const bool wide = tn == 256 || TM == 256;
-        const double w = wide ? 1.3 : 1.0, wr = wide ? 2.0 : 1.0;
+        const double w = wide ? 1.5 : 1.0, wr = wide ? 2.0 : 1.0;
         const long long wgs = work_of(TM) * tiles_n;
         for (int c = 1; c <= 16 && (c == 1 || nsteps / c >= 4); ++c) {
             const long long rounds = (wgs * c + cus - 1) / cus;
