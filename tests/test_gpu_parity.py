@@ -181,6 +181,36 @@ def test_full_size_layer_stage1_config():
     assert torch.equal(sb.combine(ho, lo_o, md, c.bs, c.H, c.W), y)
 
 
+# Fused layers on the resident-weight kernel over several images: tile lists
+# of more than two rounds of workgroups, blocks of 32 and 64, one class only,
+# fewer output channels than a workgroup's 64, and more than 1024 blocks (the
+# mask is then read in strides of 1024 blocks).
+ROUNDS_CASES = [Case("res_n3_bs32_f16", "f16", 3, 64, 64, 256, 512, 32, seed=60),
+                Case("res_n2_bs64_bf16", "bf16", 2, 64, 64, 256, 512, 64, p_low=0.6, seed=61),
+                Case("res_n2_bs32_alllow_f16", "f16", 2, 64, 64, 256, 512, 32, mask_kind="low", seed=62),
+                Case("res_n2_bs32_co48_bf16", "bf16", 2, 64, 48, 256, 512, 32, p_low=0.3, seed=63),
+                # more than 1024 blocks
+                Case("res_n9_c16_f16", "f16", 9, 16, 16, 256, 512, 32, seed=64)]
+
+
+@pytest.mark.parametrize("c", ROUNDS_CASES, ids=_ids(ROUNDS_CASES))
+def test_resident_layer_many_rounds(c):
+    import paper_2011_12025_amd as sb
+    log(f"[layer, many rounds] {c.name}: oracle ...")
+    mask, x, w, b, ref = prepared(c)
+    log(f"[layer, many rounds] {c.name}: gpu")
+    md = torch.from_numpy(mask).cuda()
+    xd = to_dev(x, "nhwc")
+    y = sb.layer(xd, md, c.bs, w.cuda(), None if b is None else b.cuda())
+    assert_conv_close(y, y64_from_stacks(c, mask, ref["ho64"], ref["lo64"]), c.dtype, 9 * c.C, "layer")
+    # the unfused chain computes every output pixel with the same MFMA schedule
+    hi, lo = sb.split(xd, md, c.bs)
+    hp, lp = sb.pad(hi, lo, md, c.bs, c.H, c.W)
+    ho, lo_o = sb.conv3x3(hp, lp, md, c.bs, c.H, c.W, w.cuda(), None if b is None else b.cuda())
+    assert torch.equal(sb.combine(ho, lo_o, md, c.bs, c.H, c.W), y)
+    torch.cuda.synchronize()
+
+
 # Fused layers with 128 or more than 256 input channels, and with 129-256
 # above 8192 pixels, run as split, the implicit GEMM's block convolution and
 # combine over library workspace stacks.
