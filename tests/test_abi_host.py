@@ -224,3 +224,14 @@ def test_chain_queries_and_validation(lib):
     assert "aligned" in lib.segblocks_last_error().decode()
     assert call(NULL, P(base + 0x4000000)) == b.SB_EINVAL        # hi_out_half = hi_out
     assert "overlap" in lib.segblocks_last_error().decode()
+
+
+def test_bench_runs_on_one_gpu_only():
+    """bench.py measures one GPU; asked for more it exits with a message, before
+    anything touches a device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=600, cwd=ROOT)
+    assert r.returncode != 0
+    assert "one GPU only" in r.stdout + r.stderr
