@@ -116,8 +116,9 @@ struct RTile {
 // Tile `tile` of the list.  From packed or padded stacks the list is
 // class-major: first the high blocks' tiles (Gh per block, R image rows
 // each), then the low blocks' (Gl per block, RL = 2R low rows each: the same
-// pixels as a high tile, so a low block costs a quarter of a high one), in
-// slot order; nth = high tiles in the list.  From the dense map the list is
+// pixels as a high tile, so a low block costs a quarter of a high one; R/2
+// rows when that spreads a second round over every workgroup, see the
+// kernel), in slot order; nth = high tiles in the list.  From the dense map the list is
 // block-major with RL = R/2 (Gh = Gl): a low tile's pixels are 2x2 averages
 // of image pixels, staged through registers, and 2R rows of them take three
 // rounds of loads where R/2 rows take one; the block of a tile is then its
@@ -650,20 +651,30 @@ __global__ __launch_bounds__(RWG, 1) void k_conv_res(Geo g, const uint8_t* __res
     // one block (which share halo rows) run on one XCD and share its L2.
     // The tile list by class (the class counts come from the mask; slots past
     // a stack's capacity are skipped).
+    const int nwg = (int)gridDim.x;
     int nth = 0, ntiles = (int)g.B * Gh;  // the dense map: every block, block-major
+    int rl = RL, gl = Gl;                 // rows and tiles of a low block
     if constexpr (SRC != SRC_DENSE) {
         const int nh_all = wm.count_high((int)g.B);
         const int nh = min(nh_all, a.hi_cap);
         const int nl = min((int)g.B - nh_all, a.lo_cap);
         nth = nh * Gh;
-        ntiles = nth + nl * Gl;
+        ntiles = nth + nl * gl;
+        // When the high tiles fit in one round and whole-block low tiles would
+        // make a second round on a few workgroups, low tiles of R/2 rows (a
+        // quarter of the work each) spread that round over every workgroup.
+        const int gq = (g.bs >> 1) / (R >> 1);
+        if (nl > 0 && nth <= nwg && ntiles > nwg && nth + nl * gq <= 2 * nwg) {
+            rl = R >> 1;
+            gl = gq;
+            ntiles = nth + nl * gl;
+        }
     }
-    const int nwg = (int)gridDim.x;
     const int pos = (nwg & 7) ? (int)blockIdx.x : (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
     int tile = pos;
     auto next_tile = [&](RTile& t, Neigh& nb) -> bool {
         while (tile < ntiles) {
-            const bool ok = res_tile<SRC, DST, ONE>(g, a, wm, R, RL, Gh, Gl, nth, tile, t, nb);
+            const bool ok = res_tile<SRC, DST, ONE>(g, a, wm, R, rl, Gh, gl, nth, tile, t, nb);
             tile += nwg;
             if (ok) return true;
         }

@@ -72,6 +72,46 @@ def test_layer_at_stage_shapes(stage, f_low, dtype):
     assert_conv_close(flo, lo64, dtype, 9 * C, c.name + " block_conv3x3 lo")
 
 
+@pytest.mark.parametrize("bs,f_low,dtype,relu", [(32, 0.5, "f16", False), (64, 0.5, "bf16", True),
+                                                 (32, 0.55, "f16", False), (32, 0.75, "bf16", True)])
+def test_resident_conv_low_tile_sizes(bs, f_low, dtype, relu):
+    """The resident-weight convolutions at the stage-1 shape (C=64, 256x512)
+    with exact-fraction masks: at half low the high tiles fill one round of
+    workgroups and the low blocks are cut into quarter-block tiles spread over
+    every workgroup; at 0.55 and 0.75 they stay whole.  Padded and packed
+    sources against the oracle, and bit for bit against each other and the
+    fused layer (one MFMA schedule per output pixel)."""
+    import paper_2011_12025_amd as sb
+    C, H, W = 64, 256, 512
+    c = Case(f"res_bs{bs}_f{f_low}", dtype, 1, C, C, H, W, bs, seed=70)
+    mask = inputs.mask_exact_fraction(c.seed, 1, H // bs, W // bs, f_low)
+    x = inputs.feature_map(c.seed, 1, C, H, W, dtype)
+    w = inputs.conv_weight(c.seed, C, C, 3, dtype)
+    b = inputs.conv_bias(c.seed, C, 9 * C, dtype)
+    log(f"[resident low tiles] {c.name}: oracle ...")
+    hi, lo = oracle.split(x.float().numpy(), mask, bs, dtype)
+    hp, lp = oracle.pad(hi, lo, mask, bs, H, W, dtype)
+    ho64 = oracle.conv3x3_valid(hp, w.float().numpy(), b.float().numpy())
+    lo64 = oracle.conv3x3_valid(lp, w.float().numpy(), b.float().numpy())
+    if relu:
+        ho64, lo64 = np.maximum(ho64, 0), np.maximum(lo64, 0)
+    log(f"[resident low tiles] {c.name}: gpu")
+    t = TDT[dtype]
+    md = torch.from_numpy(mask).cuda()
+    wd, bd = w.cuda(), b.cuda()
+    fho, flo = sb.block_conv3x3(_cl(torch.from_numpy(hi).to(t)), _cl(torch.from_numpy(lo).to(t)), md, bs, H, W,
+                                wd, bd, relu=relu)
+    pho, plo = sb.conv3x3(_cl(torch.from_numpy(hp).to(t)), _cl(torch.from_numpy(lp).to(t)), md, bs, H, W, wd, bd)
+    if relu:  # rounding and ReLU commute
+        pho, plo = pho.clamp(min=0), plo.clamp(min=0)
+    y = sb.layer(to_dev(x, "nhwc"), md, bs, wd, bd, relu=relu)
+    torch.cuda.synchronize()
+    assert_conv_close(fho, ho64, dtype, 9 * C, c.name + " block_conv3x3 hi")
+    assert_conv_close(flo, lo64, dtype, 9 * C, c.name + " block_conv3x3 lo")
+    assert torch.equal(fho, pho) and torch.equal(flo, plo)
+    assert torch.equal(sb.combine(fho, flo, md, bs, H, W), y)
+
+
 # stride-2 block convolutions with input blocks of 32 and 64 pixels: the
 # implicit GEMM's 128-pixel tiles lie inside one output block
 @pytest.mark.parametrize("name,dtype,N,C,Co,H,W,bs,k,p_low,seed", [
