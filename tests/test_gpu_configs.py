@@ -76,9 +76,10 @@ def test_layer_at_stage_shapes(stage, f_low, dtype):
                                                  (32, 0.55, "f16", False), (32, 0.75, "bf16", True)])
 def test_resident_conv_low_tile_sizes(bs, f_low, dtype, relu):
     """The resident-weight convolutions at the stage-1 shape (C=64, 256x512)
-    with exact-fraction masks: at half low the high tiles fill one round of
-    workgroups and the low blocks are cut into quarter-block tiles spread over
-    every workgroup; at 0.55 and 0.75 they stay whole.  Padded and packed
+    with exact-fraction masks: at 0.5 and 0.55 low the high tiles fit in one
+    round of workgroups and the low blocks are cut into quarter-block tiles
+    spread over every workgroup in the second; at 0.75 the whole low tiles
+    fit beside the high ones in one round and stay whole.  Padded and packed
     sources against the oracle, and bit for bit against each other and the
     fused layer (one MFMA schedule per output pixel)."""
     import paper_2011_12025_amd as sb
